@@ -1,0 +1,220 @@
+/*
+ * pariskv.h -- C ABI of the ParisKV decode-step retrieval library for AMD
+ * Instinct MI355X (gfx950).
+ *
+ * Method: ParisKV, "Fast and Drift-Robust KV-Cache Retrieval for Long-Context
+ * LLMs" (arXiv 2602.07721).  The library implements, per decode step and per
+ * query head, the path of Alg. 1: key summarisation (encode / append), the
+ * query transform, tier-weighted collision scores (Eq. collision_score),
+ * top-beta candidate selection, RSQ-IP reranking (Eq. rsqip_raw_weighted),
+ * the final top-k, and attention restricted to the selected keys
+ * (Eqs. approx_weight, approx_output).
+ *
+ * General rules for every entry point
+ *   - Device pointers are caller-owned memory on the current HIP device
+ *     (for example torch tensors).  The library allocates no device memory,
+ *     keeps no per-index state, and never synchronises a stream: every call
+ *     validates its arguments on the host, enqueues kernels on `stream`
+ *     (a hipStream_t; NULL = the default stream) and returns.
+ *   - Validation happens before any launch.  On error nothing is enqueued
+ *     and a negative PARISKV_ERR_* code is returned; pariskv_last_error()
+ *     gives a thread-local message.  No C++ exception crosses the ABI.
+ *   - Calls on one stream are ordered.  Calls on different streams that touch
+ *     the same index or workspace must be ordered by the caller.
+ *   - Inputs must be finite float16 values; codes computed from non-finite
+ *     keys are unspecified (no fault).
+ *
+ * Shapes used below: D = head_dim = 128, B = n_subspaces = 16, m = D/B = 8
+ * (2^m = 256 centroids per subspace), Hkv KV heads, G query heads per KV
+ * head, Hq = Hkv * G; query head h reads KV head h / G.
+ */
+#ifndef PARISKV_H
+#define PARISKV_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+/* ---------------------------------------------------------------- codes */
+#define PARISKV_OK 0
+#define PARISKV_ERR_INVALID (-1)     /* bad shape, budget, pointer or alignment  */
+#define PARISKV_ERR_CAPACITY (-2)    /* keys would not fit in the index arrays  */
+#define PARISKV_ERR_WORKSPACE (-3)   /* workspace missing or too small           */
+#define PARISKV_ERR_HIP (-4)         /* a HIP runtime call or launch failed      */
+#define PARISKV_ERR_UNSUPPORTED (-5) /* valid but outside what this build serves */
+
+#define PARISKV_HEAD_DIM 128
+#define PARISKV_SUBSPACES 16
+#define PARISKV_SUBDIM 8
+#define PARISKV_CENTROIDS 256
+#define PARISKV_REC_BYTES 128
+#define PARISKV_MAX_SCORE 96        /* 6 * B: largest collision score        */
+#define PARISKV_MAX_CAND 65536      /* largest candidate budget C served     */
+#define PARISKV_MAX_TOPK 2048       /* largest final k served                */
+
+/* ---------------------------------------------------------------- types */
+
+/* Shape of one layer's KV cache and the shared rotation.
+ *   rot_signs: HOST pointer to D int8 values, each +1 or -1: the diagonal s
+ *   of the rotation R = H_D diag(s) / sqrt(D) (Sec. "Preprocessing" step (1),
+ *   "implemented by SRHT"; H_D is the Sylvester Walsh-Hadamard matrix).  The
+ *   library copies the signs at every call; the caller keeps ownership. */
+typedef struct pariskv_config {
+    int32_t head_dim;        /* D; must be 128                                  */
+    int32_t n_subspaces;     /* B; must be 16 (m = 8)                           */
+    int32_t n_kv_heads;      /* Hkv >= 1                                        */
+    int32_t q_per_kv;        /* G, 1..16                                        */
+    int64_t capacity;        /* key slots per (sequence, KV head), 1..2^31-1    */
+    const int8_t* rot_signs; /* host, [D], each +1 or -1                        */
+} pariskv_config;
+
+/* Per-key metadata kept on the GPU (Sec. "Low-Bit Rerank Metadata": centroid
+ * ids, 4-bit codes and weights w).  All three arrays are device memory owned
+ * by the caller, 16-byte aligned (128-byte alignment of rec is recommended).
+ *
+ *   ids    uint8 [batch][Hkv][capacity][B]: centroid id of subspace b (Eq.
+ *          dir_assign).  Bit j is set when coordinate j of the rotated
+ *          subspace is negative (a zero coordinate counts as positive).
+ *   rec    [batch][Hkv][capacity][128] bytes, the rerank record of one key,
+ *          eight 16-byte chunks; chunk c = 0..7 holds subspaces 2c and 2c+1:
+ *            bytes 16c+0..3   uint32 code word of subspace 2c
+ *            bytes 16c+4..7   uint32 code word of subspace 2c+1
+ *            bytes 16c+8..11  float  W_{2c}
+ *            bytes 16c+12..15 float  W_{2c+1}
+ *          A code word holds the 4-bit code of coordinate j in bits 4j..4j+3:
+ *          (sign << 3) | t with sign = 1 for negative and t the 3-bit magnitude
+ *          bin of Eq. rsqip_sign_mag_code.  W_b = sqrt(D) * w_b with w_b the
+ *          weight of Eq. scaling_factor.
+ *   counts uint32 [batch][Hkv][B][256]: number of indexed keys in each
+ *          centroid cluster (needed for "top clusters covering ratio rho"). */
+typedef struct pariskv_index {
+    uint8_t* ids;
+    uint8_t* rec;
+    uint32_t* counts;
+} pariskv_index;
+
+/* Retrieval budgets of Alg. 1: C = ceil(beta n), C_rho = ceil(rho n), k. */
+typedef struct pariskv_budget {
+    int64_t n_cand;    /* C, 1..PARISKV_MAX_CAND; clamped to n at run time    */
+    int64_t n_collide; /* C_rho >= 1: keys covered by the admitted clusters   */
+    int32_t top_k;     /* k, 1..min(C, PARISKV_MAX_TOPK)                      */
+} pariskv_budget;
+
+/* Byte offsets of the intermediate arrays inside a retrieve workspace.  They
+ * are stable for given (config, batch, n, budget), so a caller may inspect
+ * them after pariskv_retrieve (the parity tests do). */
+typedef struct pariskv_ws_layout {
+    size_t total;       /* bytes needed                                         */
+    size_t zq;          /* float [batch][Hq][D]: H(s*q)/D, rounded to float     */
+    size_t lut;         /* uint32 [batch][Hkv][quads][B][256]: tier bonus, byte
+                           h%4 of the word is query head 4*quad + h%4 of the group */
+    size_t score8;      /* uint8 [batch][Hq][n_pad]: collision scores S_i        */
+    size_t chunk_hist;  /* uint32 [batch][Hq][n_chunks][97]: S histogram per chunk */
+    size_t chunk_base;  /* int32 [batch][Hq][n_chunks][2]: selected keys (S>theta,
+                           S==theta) in earlier chunks                          */
+    size_t thresh;      /* int32 [batch][Hq][4]: theta, #(S>theta), quota, C_eff */
+    size_t cand;        /* int32 [batch][Hq][n_cand]: candidates, ascending      */
+    size_t cand_score;  /* float [batch][Hq][n_cand]: RSQ-IP estimates           */
+    int64_t n_pad;      /* row length of score8 (n rounded up to 64)             */
+    int64_t n_chunks;   /* ceil(n / chunk_keys)                                  */
+    int64_t chunk_keys; /* keys per selection chunk                              */
+    int64_t c_eff;      /* min(n_cand, n)                                        */
+    int32_t quads;      /* ceil(G / 4)                                           */
+    int32_t reserved;
+} pariskv_ws_layout;
+
+/* ------------------------------------------------------------ encoding */
+
+/* Prefill key summarisation (Sec. "Prefill Phase"; Alg. 1 encode loop).
+ * keys: device float16 [batch][Hkv][n][D], contiguous.  For every key writes
+ * ids and rec at rows [0, n) of each (sequence, KV head) and recomputes
+ * counts from those n keys (counts are cleared first).
+ * Errors: INVALID (shapes, pointers, n < 0), CAPACITY (n > capacity), HIP. */
+int pariskv_encode(const pariskv_config* cfg, const pariskv_index* index,
+                   const void* keys, int64_t n, int32_t batch, void* stream);
+
+/* Streaming update (Sec. "Buffer Update": newly evicted keys are encoded and
+ * indexed).  keys: device float16 [batch][Hkv][t][D]; writes rows
+ * [n_cur, n_cur + t) and adds them to counts.  t may be 1 (per-step append)
+ * or a whole update buffer.
+ * Errors: INVALID, CAPACITY (n_cur + t > capacity), HIP. */
+int pariskv_append(const pariskv_config* cfg, const pariskv_index* index,
+                   const void* keys, int64_t n_cur, int64_t t, int32_t batch,
+                   void* stream);
+
+/* ------------------------------------------------------------ retrieval */
+
+/* Workspace bytes pariskv_retrieve needs for these shapes (0 on invalid input). */
+size_t pariskv_retrieve_workspace(const pariskv_config* cfg, int32_t batch, int64_t n,
+                                  const pariskv_budget* budget);
+
+/* Offsets of the intermediates inside that workspace.  Errors: INVALID. */
+int pariskv_workspace_layout(const pariskv_config* cfg, int32_t batch, int64_t n,
+                             const pariskv_budget* budget, pariskv_ws_layout* out);
+
+/* Two-stage retrieval for every query head (Sec. "Retrieval"; Alg. 1 decode).
+ *   q          device float16 [batch][Hq][D]
+ *   n          keys indexed per (sequence, KV head), 0..capacity
+ *   out_idx    device int32 [batch][Hq][k]: selected key indices ordered by
+ *              (RSQ-IP estimate descending, index ascending); -1 pads when
+ *              fewer than k keys exist
+ *   out_score  device float [batch][Hq][k] or NULL: the matching estimates of
+ *              <k_i, q> (-inf on padding)
+ *   workspace  device, >= pariskv_retrieve_workspace(...) bytes, 256-byte
+ *              aligned; overwritten
+ * Stage I ranks clusters per subspace by <q_tilde_b, omega_c> (ties: lower
+ * centroid id), admits whole clusters while fewer than C_rho keys precede
+ * them, gives tier weights 6..1 at cuts ceil({5,15,30,50,75,100}% * C_rho)
+ * by the number of keys preceding the cluster, and sums over subspaces.
+ * Selection keeps the min(C, n) best scores, ties at the threshold in
+ * ascending key index.  Stage II estimates <k_i, q> for those candidates.
+ * Errors: INVALID, UNSUPPORTED (C or k above the served maximum), WORKSPACE, HIP. */
+int pariskv_retrieve(const pariskv_config* cfg, const pariskv_index* index,
+                     const void* q, int64_t n, int32_t batch,
+                     const pariskv_budget* budget, int32_t* out_idx, float* out_score,
+                     void* workspace, size_t ws_bytes, void* stream);
+
+/* Attention over the fetched keys only (Eqs. approx_weight, approx_output):
+ *   o = sum_{i in idx} softmax_i(scale * <k_i, q>) v_i,
+ * float16 inputs, float32 accumulation.
+ *   q     device float16 [batch][Hq][D]
+ *   K, V  float16 [batch][Hkv][kv_capacity][D]; device memory when
+ *         kv_host_mapped == 0; pinned host memory (hipHostMalloc) when 1, read
+ *         directly by the kernel over the host link (the paper's UVA fetch)
+ *   idx   device int32 [batch][Hq][k], entries in [0, kv_capacity) or -1 (skipped)
+ *   out   device float [batch][Hq][D]; zero when no valid index
+ * scale = 1 reproduces the paper's raw score; models use 1/sqrt(D).
+ * Errors: INVALID, HIP. */
+int pariskv_sparse_attend(const pariskv_config* cfg, const void* q, const void* K,
+                          const void* V, int32_t kv_host_mapped, int64_t kv_capacity,
+                          const int32_t* idx, int32_t k, int32_t batch, float scale,
+                          float* out, void* stream);
+
+/* ------------------------------------------------------------ utilities */
+
+/* The offline magnitude quantizer (Appendix "Coordinate-Magnitude Quantizer"):
+ * Lloyd-Max thresholds tau[0..6] (= tau_1..tau_7) and levels a[0..7] for
+ * X = |u_j| with X^2 ~ Beta(1/2, (m-1)/2), rounded to double.  Host only.
+ * Errors: UNSUPPORTED for m != 8. */
+int pariskv_quantizer_table(int32_t m, double* tau, double* a);
+
+/* Per-kernel timing with HIP events recorded on the launch stream. */
+int pariskv_profile_enable(int32_t on);
+int pariskv_profile_reset(void);
+/* Waits for the recorded events; fills at most max_entries rows. Returns the
+ * number of distinct kernels seen, or a negative error code. */
+int pariskv_profile_read(int32_t max_entries, const char** names, int64_t* launches,
+                         double* total_ms);
+
+const char* pariskv_strerror(int code);
+const char* pariskv_last_error(void);
+int32_t pariskv_abi_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* PARISKV_H */

@@ -1,0 +1,257 @@
+"""ParisKV decode-step KV retrieval for AMD MI355X (gfx950).
+
+Python binding of ``libpariskv.so`` (declared in ``include/pariskv.h``).  It
+only marshals arguments: torch tensors provide device memory and streams,
+every step of the path runs in the library's HIP kernels, and a missing
+library raises instead of falling back to anything.
+
+Method: ParisKV (arXiv 2602.07721), Alg. 1 -- encode keys into centroid ids,
+4-bit codes and weights; per decode step rank clusters, score collisions,
+select top-beta candidates, rerank them with the RSQ-IP estimator, keep the
+top-k; then attend over the fetched K/V rows only.
+"""
+
+import ctypes
+import os
+from dataclasses import dataclass
+
+import numpy as np
+
+__all__ = [
+    "PariskvError", "Config", "Budget", "Index", "lib", "encode", "append", "retrieve",
+    "retrieve_workspace_size", "workspace_layout", "sparse_attend", "quantizer_table",
+    "profile_enable", "profile_reset", "profile_read",
+]
+
+LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libpariskv.so")
+
+OK, ERR_INVALID, ERR_CAPACITY, ERR_WORKSPACE, ERR_HIP, ERR_UNSUPPORTED = 0, -1, -2, -3, -4, -5
+HEAD_DIM, SUBSPACES, CENTROIDS, REC_BYTES = 128, 16, 256, 128
+
+
+class PariskvError(RuntimeError):
+    def __init__(self, code, message):
+        super().__init__(f"pariskv error {code}: {message}")
+        self.code = code
+
+
+class _Config(ctypes.Structure):
+    _fields_ = [("head_dim", ctypes.c_int32), ("n_subspaces", ctypes.c_int32),
+                ("n_kv_heads", ctypes.c_int32), ("q_per_kv", ctypes.c_int32),
+                ("capacity", ctypes.c_int64), ("rot_signs", ctypes.POINTER(ctypes.c_int8))]
+
+
+class _Index(ctypes.Structure):
+    _fields_ = [("ids", ctypes.c_void_p), ("rec", ctypes.c_void_p), ("counts", ctypes.c_void_p)]
+
+
+class _Budget(ctypes.Structure):
+    _fields_ = [("n_cand", ctypes.c_int64), ("n_collide", ctypes.c_int64), ("top_k", ctypes.c_int32)]
+
+
+class _Layout(ctypes.Structure):
+    _fields_ = [(name, ctypes.c_size_t) for name in
+                ("total", "zq", "lut", "score8", "chunk_hist", "chunk_base", "thresh", "cand",
+                 "cand_score")] + \
+               [(name, ctypes.c_int64) for name in ("n_pad", "n_chunks", "chunk_keys", "c_eff")] + \
+               [("quads", ctypes.c_int32), ("reserved", ctypes.c_int32)]
+
+
+_lib = None
+
+
+def lib():
+    """The loaded library; raises ImportError when it has not been built."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            raise ImportError(f"{LIB_PATH} is not built; run `python -m paper_2602_07721_amd.build`")
+        L = ctypes.CDLL(LIB_PATH)
+        P, VP, I32, I64, SZ = ctypes.POINTER, ctypes.c_void_p, ctypes.c_int32, ctypes.c_int64, ctypes.c_size_t
+        L.pariskv_encode.argtypes = [P(_Config), P(_Index), VP, I64, I32, VP]
+        L.pariskv_append.argtypes = [P(_Config), P(_Index), VP, I64, I64, I32, VP]
+        L.pariskv_retrieve_workspace.argtypes = [P(_Config), I32, I64, P(_Budget)]
+        L.pariskv_retrieve_workspace.restype = SZ
+        L.pariskv_workspace_layout.argtypes = [P(_Config), I32, I64, P(_Budget), P(_Layout)]
+        L.pariskv_retrieve.argtypes = [P(_Config), P(_Index), VP, I64, I32, P(_Budget), VP, VP, VP,
+                                       SZ, VP]
+        L.pariskv_sparse_attend.argtypes = [P(_Config), VP, VP, VP, I32, I64, VP, I32, I32,
+                                            ctypes.c_float, VP, VP]
+        L.pariskv_quantizer_table.argtypes = [I32, P(ctypes.c_double), P(ctypes.c_double)]
+        L.pariskv_profile_enable.argtypes = [I32]
+        L.pariskv_profile_read.argtypes = [I32, P(ctypes.c_char_p), P(I64), P(ctypes.c_double)]
+        L.pariskv_strerror.restype = ctypes.c_char_p
+        L.pariskv_strerror.argtypes = [ctypes.c_int]
+        L.pariskv_last_error.restype = ctypes.c_char_p
+        L.pariskv_abi_version.restype = I32
+        _lib = L
+    return _lib
+
+
+def _check(rc):
+    if rc != OK:
+        msg = lib().pariskv_last_error().decode()
+        raise PariskvError(rc, msg or lib().pariskv_strerror(rc).decode())
+    return rc
+
+
+@dataclass
+class Config:
+    """Layer shape and rotation signs (see ``pariskv_config``)."""
+    n_kv_heads: int
+    q_per_kv: int
+    capacity: int
+    rot_signs: np.ndarray
+    head_dim: int = HEAD_DIM
+    n_subspaces: int = SUBSPACES
+
+    def __post_init__(self):
+        self._signs = np.ascontiguousarray(np.asarray(self.rot_signs, dtype=np.int8))
+        self._c = _Config(self.head_dim, self.n_subspaces, self.n_kv_heads, self.q_per_kv,
+                          self.capacity, self._signs.ctypes.data_as(ctypes.POINTER(ctypes.c_int8)))
+
+    @property
+    def n_q_heads(self):
+        return self.n_kv_heads * self.q_per_kv
+
+    def c(self):
+        return ctypes.byref(self._c)
+
+
+@dataclass
+class Budget:
+    """C = n_cand, C_rho = n_collide, k = top_k (see ``pariskv_budget``)."""
+    n_cand: int
+    n_collide: int
+    top_k: int
+
+    def c(self):
+        self._c = _Budget(self.n_cand, self.n_collide, self.top_k)
+        return ctypes.byref(self._c)
+
+
+def _ptr(t, name, device=True):
+    if t is None:
+        return None
+    import torch
+    if not isinstance(t, torch.Tensor):
+        raise TypeError(f"{name} must be a torch tensor")
+    if device and not t.is_cuda:
+        raise ValueError(f"{name} must be a GPU tensor")
+    if not t.is_contiguous():
+        raise ValueError(f"{name} must be contiguous")
+    return ctypes.c_void_p(t.data_ptr())
+
+
+def _stream(stream):
+    import torch
+    s = torch.cuda.current_stream() if stream is None else stream
+    return ctypes.c_void_p(s.cuda_stream)
+
+
+class Index:
+    """Device arrays of the per-key metadata (see ``pariskv_index``)."""
+
+    def __init__(self, ids, rec, counts):
+        self.ids, self.rec, self.counts = ids, rec, counts
+
+    @classmethod
+    def empty(cls, cfg, batch, device="cuda"):
+        import torch
+        ids = torch.empty((batch, cfg.n_kv_heads, cfg.capacity, SUBSPACES), dtype=torch.uint8, device=device)
+        rec = torch.empty((batch, cfg.n_kv_heads, cfg.capacity, REC_BYTES), dtype=torch.uint8, device=device)
+        counts = torch.zeros((batch, cfg.n_kv_heads, SUBSPACES, CENTROIDS), dtype=torch.int32, device=device)
+        return cls(ids, rec, counts)
+
+    @property
+    def batch(self):
+        return int(self.ids.shape[0])
+
+    def c(self):
+        self._c = _Index(_ptr(self.ids, "ids"), _ptr(self.rec, "rec"), _ptr(self.counts, "counts"))
+        return ctypes.byref(self._c)
+
+
+def encode(cfg, index, keys, stream=None):
+    """Prefill: encode keys [batch][Hkv][n][D] float16 into rows [0, n); resets counts."""
+    n = int(keys.shape[2])
+    _check(lib().pariskv_encode(cfg.c(), index.c(), _ptr(keys, "keys"), n, int(keys.shape[0]),
+                                _stream(stream)))
+
+
+def append(cfg, index, keys, n_cur, stream=None):
+    """Streaming update: encode keys [batch][Hkv][t][D] into rows [n_cur, n_cur + t)."""
+    _check(lib().pariskv_append(cfg.c(), index.c(), _ptr(keys, "keys"), int(n_cur), int(keys.shape[2]),
+                                int(keys.shape[0]), _stream(stream)))
+
+
+def retrieve_workspace_size(cfg, batch, n, budget):
+    return int(lib().pariskv_retrieve_workspace(cfg.c(), batch, n, budget.c()))
+
+
+def workspace_layout(cfg, batch, n, budget):
+    L = _Layout()
+    _check(lib().pariskv_workspace_layout(cfg.c(), batch, n, budget.c(), ctypes.byref(L)))
+    return {name: getattr(L, name) for name, _ in _Layout._fields_}
+
+
+def retrieve(cfg, index, q, n, budget, out_idx=None, out_score=None, workspace=None, stream=None):
+    """Alg. 1 decode for all query heads; returns (idx, score, workspace) tensors."""
+    import torch
+    batch = int(q.shape[0])
+    rows = batch * cfg.n_q_heads
+    if out_idx is None:
+        out_idx = torch.empty((batch, cfg.n_q_heads, budget.top_k), dtype=torch.int32, device=q.device)
+    if workspace is None:
+        workspace = torch.empty(max(256, retrieve_workspace_size(cfg, batch, n, budget)),
+                                dtype=torch.uint8, device=q.device)
+    assert out_idx.numel() == rows * budget.top_k
+    _check(lib().pariskv_retrieve(cfg.c(), index.c(), _ptr(q, "q"), int(n), batch, budget.c(),
+                                  _ptr(out_idx, "out_idx"), _ptr(out_score, "out_score"),
+                                  _ptr(workspace, "workspace"), workspace.numel(), _stream(stream)))
+    return out_idx, out_score, workspace
+
+
+def sparse_attend(cfg, q, K, V, idx, scale, out=None, kv_host_mapped=False, stream=None):
+    """Attention over idx only; K, V [batch][Hkv][kv_capacity][D] float16 (device or pinned host)."""
+    import torch
+    batch = int(q.shape[0])
+    if out is None:
+        out = torch.empty((batch, cfg.n_q_heads, HEAD_DIM), dtype=torch.float32, device=q.device)
+    if kv_host_mapped:
+        for t, nm in ((K, "K"), (V, "V")):
+            if t.is_cuda or not t.is_pinned():
+                raise ValueError(f"{nm} must be pinned host memory when kv_host_mapped")
+    k = int(idx.shape[-1])
+    _check(lib().pariskv_sparse_attend(cfg.c(), _ptr(q, "q"), _ptr(K, "K", not kv_host_mapped),
+                                       _ptr(V, "V", not kv_host_mapped), int(bool(kv_host_mapped)),
+                                       int(K.shape[2]), _ptr(idx, "idx"), k, batch, float(scale),
+                                       _ptr(out, "out"), _stream(stream)))
+    return out
+
+
+def quantizer_table(m=8):
+    """(tau[7], a[8]) float64 of the library's offline Lloyd-Max quantizer."""
+    tau = (ctypes.c_double * 7)()
+    a = (ctypes.c_double * 8)()
+    _check(lib().pariskv_quantizer_table(m, tau, a))
+    return np.array(tau[:]), np.array(a[:])
+
+
+def profile_enable(on=True):
+    _check(lib().pariskv_profile_enable(1 if on else 0))
+
+
+def profile_reset():
+    _check(lib().pariskv_profile_reset())
+
+
+def profile_read(max_entries=64):
+    """{kernel name: (launches, total ms)} from events recorded since the last reset."""
+    names = (ctypes.c_char_p * max_entries)()
+    launches = (ctypes.c_int64 * max_entries)()
+    ms = (ctypes.c_double * max_entries)()
+    n = lib().pariskv_profile_read(max_entries, names, launches, ms)
+    if n < 0:
+        _check(n)
+    return {names[i].decode(): (launches[i], ms[i]) for i in range(min(n, max_entries))}

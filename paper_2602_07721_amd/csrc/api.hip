@@ -1,0 +1,435 @@
+// Host side of the C ABI declared in include/pariskv.h: argument validation,
+// workspace layout, kernel sequencing and per-kernel event timing.  No
+// device memory is allocated here; every HIP call happens after validation.
+
+#include <hip/hip_runtime.h>
+
+#include <cmath>
+#include <cstdarg>
+#include <cstdio>
+#include <cstring>
+#include <map>
+#include <mutex>
+#include <string>
+#include <vector>
+
+#include "../../include/pariskv.h"
+#include "internal.hpp"
+
+namespace pariskv {
+
+namespace {
+
+thread_local std::string t_last_error;
+
+int fail(int code, const char* fmt, ...) {
+    char buf[512];
+    va_list ap;
+    va_start(ap, fmt);
+    vsnprintf(buf, sizeof buf, fmt, ap);
+    va_end(ap);
+    t_last_error = buf;
+    return code;
+}
+
+int hip_fail(hipError_t e, const char* where) {
+    return fail(PARISKV_ERR_HIP, "%s: %s", where, hipGetErrorString(e));
+}
+
+bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+
+constexpr int64_t kMaxGridY = 65535;
+
+// Multiply non-negative int64 values, false on overflow past 2^62.
+bool mul_ok(int64_t a, int64_t b, int64_t* out) {
+    if (a < 0 || b < 0) return false;
+    if (a != 0 && b > (int64_t(1) << 62) / a) return false;
+    *out = a * b;
+    return true;
+}
+
+int check_config(const pariskv_config* cfg, int32_t batch) {
+    if (!cfg) return fail(PARISKV_ERR_INVALID, "config is NULL");
+    const int32_t D = cfg->head_dim, B = cfg->n_subspaces;
+    if (D <= 0 || (D & (D - 1)) != 0)
+        return fail(PARISKV_ERR_INVALID, "head_dim %d is not a positive power of two", D);
+    if (B <= 0 || D % B != 0)
+        return fail(PARISKV_ERR_INVALID, "n_subspaces %d does not divide head_dim %d", B, D);
+    if (D != kD || B != kB)
+        return fail(PARISKV_ERR_UNSUPPORTED, "only head_dim 128 with 16 subspaces (m = 8) is built");
+    if (cfg->n_kv_heads < 1) return fail(PARISKV_ERR_INVALID, "n_kv_heads %d < 1", cfg->n_kv_heads);
+    if (cfg->q_per_kv < 1 || cfg->q_per_kv > 16)
+        return fail(PARISKV_ERR_INVALID, "q_per_kv %d outside 1..16", cfg->q_per_kv);
+    if (cfg->capacity < 1 || cfg->capacity > INT32_MAX)
+        return fail(PARISKV_ERR_INVALID, "capacity %lld outside 1..2^31-1", (long long)cfg->capacity);
+    if (!cfg->rot_signs) return fail(PARISKV_ERR_INVALID, "rot_signs is NULL");
+    for (int j = 0; j < D; ++j)
+        if (cfg->rot_signs[j] != 1 && cfg->rot_signs[j] != -1)
+            return fail(PARISKV_ERR_INVALID, "rot_signs[%d] = %d is not +1 or -1", j, cfg->rot_signs[j]);
+    if (batch < 1) return fail(PARISKV_ERR_INVALID, "batch %d < 1", batch);
+    int64_t t;
+    if (!mul_ok((int64_t)batch * cfg->n_kv_heads, cfg->capacity, &t) || !mul_ok(t, kRec, &t))
+        return fail(PARISKV_ERR_INVALID, "batch * n_kv_heads * capacity overflows");
+    if ((int64_t)batch * cfg->n_kv_heads * cfg->q_per_kv > kMaxGridY)
+        return fail(PARISKV_ERR_UNSUPPORTED, "batch * query heads above %lld", (long long)kMaxGridY);
+    return PARISKV_OK;
+}
+
+int check_index(const pariskv_index* ix) {
+    if (!ix) return fail(PARISKV_ERR_INVALID, "index is NULL");
+    if (!ix->ids || !ix->rec || !ix->counts)
+        return fail(PARISKV_ERR_INVALID, "index arrays must be non-NULL");
+    if (!aligned16(ix->ids) || !aligned16(ix->rec) || !aligned16(ix->counts))
+        return fail(PARISKV_ERR_INVALID, "index arrays must be 16-byte aligned");
+    return PARISKV_OK;
+}
+
+SignBits pack_signs(const int8_t* s) {
+    SignBits b{};
+    for (int j = 0; j < kD; ++j)
+        if (s[j] < 0) b.w[j >> 5] |= 1u << (j & 31);
+    return b;
+}
+
+const QuantConsts& quant_consts() {
+    static QuantConsts qc;
+    static std::once_flag once;
+    std::call_once(once, [] {
+        double tau[7], a[8];
+        quantizer_table_m8(tau, a);
+        for (int t = 0; t < 8; ++t) {
+            qc.a[t] = a[t];
+            qc.a32[t] = (float)a[t];
+        }
+        for (int t = 0; t < 7; ++t) qc.tau2[t] = tau[t] * tau[t];
+    });
+    return qc;
+}
+
+int layout(const pariskv_config* cfg, int32_t batch, int64_t n, const pariskv_budget* bud,
+           pariskv_ws_layout* L) {
+    int rc = check_config(cfg, batch);
+    if (rc) return rc;
+    if (!bud) return fail(PARISKV_ERR_INVALID, "budget is NULL");
+    if (n < 0) return fail(PARISKV_ERR_INVALID, "n %lld < 0", (long long)n);
+    if (n > cfg->capacity)
+        return fail(PARISKV_ERR_INVALID, "n %lld exceeds capacity %lld", (long long)n,
+                    (long long)cfg->capacity);
+    if (bud->n_cand < 1) return fail(PARISKV_ERR_INVALID, "n_cand %lld < 1", (long long)bud->n_cand);
+    if (bud->n_cand > PARISKV_MAX_CAND)
+        return fail(PARISKV_ERR_UNSUPPORTED, "n_cand %lld above %d", (long long)bud->n_cand,
+                    PARISKV_MAX_CAND);
+    if (bud->n_collide < 1)
+        return fail(PARISKV_ERR_INVALID, "n_collide %lld < 1", (long long)bud->n_collide);
+    if (bud->top_k < 1 || bud->top_k > bud->n_cand)
+        return fail(PARISKV_ERR_INVALID, "top_k %d outside 1..n_cand", bud->top_k);
+    if (bud->top_k > PARISKV_MAX_TOPK)
+        return fail(PARISKV_ERR_UNSUPPORTED, "top_k %d above %d", bud->top_k, PARISKV_MAX_TOPK);
+
+    const int64_t hkv = cfg->n_kv_heads, g = cfg->q_per_kv, hq = hkv * g;
+    const int64_t quads = (g + 3) / 4;
+    const int64_t rows = (int64_t)batch * hq;
+    std::memset(L, 0, sizeof *L);
+    L->n_pad = ((n > 0 ? n : 1) + 63) / 64 * 64;
+    L->chunk_keys = kChunk;
+    L->n_chunks = (n + kChunk - 1) / kChunk;
+    L->c_eff = bud->n_cand < n ? bud->n_cand : n;
+    L->quads = (int32_t)quads;
+    size_t off = 0;
+    auto take = [&](size_t bytes) {
+        const size_t at = off;
+        off += (bytes + 255) / 256 * 256;
+        return at;
+    };
+    L->zq = take((size_t)rows * kD * 4);
+    L->lut = take((size_t)batch * hkv * quads * kB * kCentroids * 4);
+    L->score8 = take((size_t)rows * L->n_pad);
+    L->chunk_hist = take((size_t)rows * L->n_chunks * kBins * 4);
+    L->chunk_base = take((size_t)rows * L->n_chunks * 2 * 4);
+    L->thresh = take((size_t)rows * 4 * 4);
+    L->cand = take((size_t)rows * bud->n_cand * 4);
+    L->cand_score = take((size_t)rows * bud->n_cand * 4);
+    L->total = off;
+    return PARISKV_OK;
+}
+
+// ---------------------------------------------------------------- profiler
+
+struct Pending {
+    std::string name;
+    hipEvent_t start, stop;
+};
+struct Acc {
+    int64_t launches = 0;
+    double ms = 0.0;
+};
+
+std::mutex g_prof_mu;
+bool g_prof_on = false;
+std::vector<Pending> g_pending;
+std::vector<hipEvent_t> g_pool;
+std::map<std::string, Acc> g_acc;
+thread_local Pending t_open;
+thread_local bool t_has_open = false;
+
+hipEvent_t pool_get() {
+    if (!g_pool.empty()) {
+        hipEvent_t e = g_pool.back();
+        g_pool.pop_back();
+        return e;
+    }
+    hipEvent_t e = nullptr;
+    if (hipEventCreate(&e) != hipSuccess) return nullptr;
+    return e;
+}
+
+int collect_locked() {
+    for (auto& p : g_pending) {
+        float ms = 0.f;
+        if (hipEventSynchronize(p.stop) != hipSuccess) return hip_fail(hipGetLastError(), "hipEventSynchronize");
+        if (hipEventElapsedTime(&ms, p.start, p.stop) == hipSuccess) {
+            Acc& a = g_acc[p.name];
+            a.launches += 1;
+            a.ms += ms;
+        }
+        g_pool.push_back(p.start);
+        g_pool.push_back(p.stop);
+    }
+    g_pending.clear();
+    return PARISKV_OK;
+}
+
+}  // namespace
+
+void prof_begin(const char* name, hipStream_t s) {
+    std::lock_guard<std::mutex> lk(g_prof_mu);
+    if (!g_prof_on) return;
+    hipEvent_t a = pool_get(), b = pool_get();
+    if (!a || !b) return;
+    t_open = Pending{name, a, b};
+    t_has_open = true;
+    hipEventRecord(a, s);
+}
+
+void prof_end(hipStream_t s) {
+    std::lock_guard<std::mutex> lk(g_prof_mu);
+    if (!t_has_open) return;
+    t_has_open = false;
+    hipEventRecord(t_open.stop, s);
+    g_pending.push_back(t_open);
+}
+
+}  // namespace pariskv
+
+using namespace pariskv;
+
+extern "C" {
+
+int32_t pariskv_abi_version(void) { return 1; }
+
+const char* pariskv_strerror(int code) {
+    switch (code) {
+        case PARISKV_OK: return "ok";
+        case PARISKV_ERR_INVALID: return "invalid argument";
+        case PARISKV_ERR_CAPACITY: return "index capacity exceeded";
+        case PARISKV_ERR_WORKSPACE: return "workspace missing or too small";
+        case PARISKV_ERR_HIP: return "HIP runtime error";
+        case PARISKV_ERR_UNSUPPORTED: return "unsupported configuration";
+        default: return "unknown error";
+    }
+}
+
+const char* pariskv_last_error(void) { return t_last_error.c_str(); }
+
+int pariskv_quantizer_table(int32_t m, double* tau, double* a) {
+    if (!tau || !a) return fail(PARISKV_ERR_INVALID, "NULL output");
+    if (m != kM) return fail(PARISKV_ERR_UNSUPPORTED, "only m = 8 is built");
+    quantizer_table_m8(tau, a);
+    return PARISKV_OK;
+}
+
+static int encode_common(const pariskv_config* cfg, const pariskv_index* index, const void* keys,
+                         int64_t row0, int64_t t, int32_t batch, bool reset_counts, void* stream) {
+    int rc = check_config(cfg, batch);
+    if (rc) return rc;
+    rc = check_index(index);
+    if (rc) return rc;
+    if (row0 < 0 || t < 0) return fail(PARISKV_ERR_INVALID, "negative key range");
+    if (t > 0 && (!keys || !aligned16(keys)))
+        return fail(PARISKV_ERR_INVALID, "keys must be non-NULL and 16-byte aligned");
+    if (row0 + t > cfg->capacity)
+        return fail(PARISKV_ERR_CAPACITY, "rows [%lld, %lld) exceed capacity %lld", (long long)row0,
+                    (long long)(row0 + t), (long long)cfg->capacity);
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    const int64_t groups = (int64_t)batch * cfg->n_kv_heads;
+    hipError_t e;
+    if (reset_counts) {
+        e = launch_zero_u32(index->counts, groups * kB * kCentroids, s);
+        if (e != hipSuccess) return hip_fail(e, "zero counts");
+    }
+    e = launch_encode(keys, t, groups, row0, cfg->capacity, index->ids, index->rec, index->counts,
+                      pack_signs(cfg->rot_signs), quant_consts(), s);
+    if (e != hipSuccess) return hip_fail(e, "encode launch");
+    return PARISKV_OK;
+}
+
+int pariskv_encode(const pariskv_config* cfg, const pariskv_index* index, const void* keys,
+                   int64_t n, int32_t batch, void* stream) {
+    if (n < 0) return fail(PARISKV_ERR_INVALID, "n %lld < 0", (long long)n);
+    return encode_common(cfg, index, keys, 0, n, batch, true, stream);
+}
+
+int pariskv_append(const pariskv_config* cfg, const pariskv_index* index, const void* keys,
+                   int64_t n_cur, int64_t t, int32_t batch, void* stream) {
+    return encode_common(cfg, index, keys, n_cur, t, batch, false, stream);
+}
+
+size_t pariskv_retrieve_workspace(const pariskv_config* cfg, int32_t batch, int64_t n,
+                                  const pariskv_budget* budget) {
+    pariskv_ws_layout L;
+    if (layout(cfg, batch, n, budget, &L) != PARISKV_OK) return 0;
+    return L.total;
+}
+
+int pariskv_workspace_layout(const pariskv_config* cfg, int32_t batch, int64_t n,
+                             const pariskv_budget* budget, pariskv_ws_layout* out) {
+    if (!out) return fail(PARISKV_ERR_INVALID, "layout output is NULL");
+    return layout(cfg, batch, n, budget, out);
+}
+
+int pariskv_retrieve(const pariskv_config* cfg, const pariskv_index* index, const void* q,
+                     int64_t n, int32_t batch, const pariskv_budget* budget, int32_t* out_idx,
+                     float* out_score, void* workspace, size_t ws_bytes, void* stream) {
+    pariskv_ws_layout L;
+    int rc = layout(cfg, batch, n, budget, &L);
+    if (rc) return rc;
+    rc = check_index(index);
+    if (rc) return rc;
+    if (!q || !aligned16(q)) return fail(PARISKV_ERR_INVALID, "q must be non-NULL and 16-byte aligned");
+    if (!out_idx || !aligned16(out_idx))
+        return fail(PARISKV_ERR_INVALID, "out_idx must be non-NULL and 16-byte aligned");
+    if (out_score && !aligned16(out_score))
+        return fail(PARISKV_ERR_INVALID, "out_score must be 16-byte aligned");
+    if (!workspace || (reinterpret_cast<uintptr_t>(workspace) & 255u) != 0)
+        return fail(PARISKV_ERR_WORKSPACE, "workspace must be non-NULL and 256-byte aligned");
+    if (ws_bytes < L.total)
+        return fail(PARISKV_ERR_WORKSPACE, "workspace has %zu bytes, needs %zu", ws_bytes, L.total);
+
+    RetrieveArgs a{};
+    a.batch = batch;
+    a.hkv = cfg->n_kv_heads;
+    a.g = cfg->q_per_kv;
+    a.quads = L.quads;
+    a.hq = a.hkv * a.g;
+    a.n = n;
+    a.n_pad = L.n_pad;
+    a.n_chunks = L.n_chunks;
+    a.capacity = cfg->capacity;
+    a.n_cand = budget->n_cand;
+    a.c_eff = L.c_eff;
+    a.top_k = budget->top_k;
+    for (int l = 0; l < kTierCount; ++l) {
+        static const int64_t pct[kTierCount] = {5, 15, 30, 50, 75, 100};
+        // ceil(pct * C_rho / 100) in integers; start ranks never exceed 2^31.
+        const int64_t c = budget->n_collide > (int64_t(1) << 40)
+                              ? (int64_t(1) << 40)
+                              : (pct[l] * budget->n_collide + 99) / 100;
+        a.cuts[l] = c > 0xffffffffLL ? 0xffffffffu : (uint32_t)c;
+    }
+    a.q = q;
+    a.ids = index->ids;
+    a.rec = index->rec;
+    a.counts = index->counts;
+    char* ws = static_cast<char*>(workspace);
+    a.zq = reinterpret_cast<float*>(ws + L.zq);
+    a.lut = reinterpret_cast<uint32_t*>(ws + L.lut);
+    a.score8 = reinterpret_cast<uint8_t*>(ws + L.score8);
+    a.chunk_hist = reinterpret_cast<uint32_t*>(ws + L.chunk_hist);
+    a.chunk_base = reinterpret_cast<int32_t*>(ws + L.chunk_base);
+    a.thresh = reinterpret_cast<int32_t*>(ws + L.thresh);
+    a.cand = reinterpret_cast<int32_t*>(ws + L.cand);
+    a.cand_score = reinterpret_cast<float*>(ws + L.cand_score);
+    a.out_idx = out_idx;
+    a.out_score = out_score;
+    a.sb = pack_signs(cfg->rot_signs);
+    a.qc = quant_consts();
+
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    hipError_t e;
+    if (n == 0) {
+        e = launch_pad_outputs(a, s);
+        return e == hipSuccess ? PARISKV_OK : hip_fail(e, "pad outputs");
+    }
+    if ((e = launch_query_lut(a, s)) != hipSuccess) return hip_fail(e, "query_lut launch");
+    if ((e = launch_collide(a, s)) != hipSuccess) return hip_fail(e, "collide launch");
+    if ((e = launch_threshold(a, s)) != hipSuccess) return hip_fail(e, "threshold launch");
+    if ((e = launch_compact(a, s)) != hipSuccess) return hip_fail(e, "compact launch");
+    if ((e = launch_rerank(a, s)) != hipSuccess) return hip_fail(e, "rerank launch");
+    if ((e = launch_topk(a, s)) != hipSuccess) return hip_fail(e, "topk launch");
+    return PARISKV_OK;
+}
+
+int pariskv_sparse_attend(const pariskv_config* cfg, const void* q, const void* K, const void* V,
+                          int32_t kv_host_mapped, int64_t kv_capacity, const int32_t* idx, int32_t k,
+                          int32_t batch, float scale, float* out, void* stream) {
+    int rc = check_config(cfg, batch);
+    if (rc) return rc;
+    if (!q || !K || !V || !idx || !out)
+        return fail(PARISKV_ERR_INVALID, "q, K, V, idx and out must be non-NULL");
+    if (!aligned16(q) || !aligned16(K) || !aligned16(V) || !aligned16(out) ||
+        (reinterpret_cast<uintptr_t>(idx) & 3u) != 0)
+        return fail(PARISKV_ERR_INVALID, "q, K, V, out must be 16-byte aligned, idx 4-byte aligned");
+    if (k < 1) return fail(PARISKV_ERR_INVALID, "k %d < 1", k);
+    if (kv_capacity < 1 || kv_capacity > INT32_MAX)
+        return fail(PARISKV_ERR_INVALID, "kv_capacity %lld outside 1..2^31-1", (long long)kv_capacity);
+    if (kv_host_mapped != 0 && kv_host_mapped != 1)
+        return fail(PARISKV_ERR_INVALID, "kv_host_mapped must be 0 or 1");
+    if (!std::isfinite(scale)) return fail(PARISKV_ERR_INVALID, "scale is not finite");
+    const void* Kd = K;
+    const void* Vd = V;
+    if (kv_host_mapped) {
+        void* p = nullptr;
+        hipError_t e = hipHostGetDevicePointer(&p, const_cast<void*>(K), 0);
+        if (e != hipSuccess) return hip_fail(e, "hipHostGetDevicePointer(K)");
+        Kd = p;
+        e = hipHostGetDevicePointer(&p, const_cast<void*>(V), 0);
+        if (e != hipSuccess) return hip_fail(e, "hipHostGetDevicePointer(V)");
+        Vd = p;
+    }
+    hipError_t e = launch_attend(q, Kd, Vd, kv_capacity, idx, k, batch, cfg->n_kv_heads,
+                                 cfg->q_per_kv, scale, out, static_cast<hipStream_t>(stream));
+    if (e != hipSuccess) return hip_fail(e, "attend launch");
+    return PARISKV_OK;
+}
+
+int pariskv_profile_enable(int32_t on) {
+    std::lock_guard<std::mutex> lk(g_prof_mu);
+    g_prof_on = on != 0;
+    return PARISKV_OK;
+}
+
+int pariskv_profile_reset(void) {
+    std::lock_guard<std::mutex> lk(g_prof_mu);
+    int rc = collect_locked();
+    g_acc.clear();
+    return rc;
+}
+
+int pariskv_profile_read(int32_t max_entries, const char** names, int64_t* launches,
+                         double* total_ms) {
+    std::lock_guard<std::mutex> lk(g_prof_mu);
+    int rc = collect_locked();
+    if (rc) return rc;
+    int i = 0;
+    for (auto& kv : g_acc) {
+        if (i < max_entries) {
+            if (names) names[i] = kv.first.c_str();
+            if (launches) launches[i] = kv.second.launches;
+            if (total_ms) total_ms[i] = kv.second.ms;
+        }
+        ++i;
+    }
+    return i;
+}
+
+}  // extern "C"

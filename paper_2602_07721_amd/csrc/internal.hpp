@@ -1,0 +1,88 @@
+// Library-internal declarations shared by the host API and the kernel files.
+#pragma once
+
+#include <hip/hip_runtime.h>
+
+#include <cstddef>
+#include <cstdint>
+
+namespace pariskv {
+
+constexpr int kD = 128;           // head dimension
+constexpr int kB = 16;            // subspaces
+constexpr int kM = 8;             // coordinates per subspace
+constexpr int kCentroids = 256;   // 2^m
+constexpr int kRec = 128;         // bytes per rerank record
+constexpr int kMaxScore = 96;     // 6 * B
+constexpr int kBins = kMaxScore + 1;
+constexpr int kChunk = 4096;      // keys per collision / selection chunk
+constexpr int kTierCount = 6;
+
+// 128 rotation signs packed as bits: bit j of word j/32 set <=> s_j = -1.
+struct SignBits {
+    uint32_t w[4];
+};
+
+// Offline quantizer constants as the kernels consume them.
+struct QuantConsts {
+    double a[8];    // reconstruction levels a[0..7]
+    double tau2[7]; // fl(tau_t * tau_t), t = 1..7
+    float a32[8];   // a rounded to float, for the float32 rerank
+};
+
+bool quantizer_table_m8(double* tau, double* a);
+
+// ---- launchers (each lives next to its kernel) --------------------------
+
+hipError_t launch_zero_u32(uint32_t* p, int64_t count, hipStream_t s);
+
+// Encode keys [groups][n_src][D] into rows [row0, row0 + n_src) of each group.
+hipError_t launch_encode(const void* keys, int64_t n_src, int64_t groups, int64_t row0,
+                         int64_t capacity, uint8_t* ids, uint8_t* rec, uint32_t* counts,
+                         const SignBits& sb, const QuantConsts& qc, hipStream_t s);
+
+struct RetrieveArgs {
+    // shapes
+    int32_t batch, hkv, g, quads, hq;
+    int64_t n, n_pad, n_chunks, capacity;
+    int64_t n_cand, c_eff;   // row stride of cand / cand_score, and min(C, n)
+    int32_t top_k;
+    uint32_t cuts[kTierCount];
+    // inputs
+    const void* q;
+    const uint8_t* ids;
+    const uint8_t* rec;
+    const uint32_t* counts;
+    // workspace
+    float* zq;
+    uint32_t* lut;
+    uint8_t* score8;
+    uint32_t* chunk_hist;
+    int32_t* chunk_base;
+    int32_t* thresh;
+    int32_t* cand;
+    float* cand_score;
+    // outputs
+    int32_t* out_idx;
+    float* out_score;
+    SignBits sb;
+    QuantConsts qc;
+};
+
+hipError_t launch_query_lut(const RetrieveArgs& a, hipStream_t s);
+hipError_t launch_collide(const RetrieveArgs& a, hipStream_t s);
+hipError_t launch_threshold(const RetrieveArgs& a, hipStream_t s);
+hipError_t launch_compact(const RetrieveArgs& a, hipStream_t s);
+hipError_t launch_rerank(const RetrieveArgs& a, hipStream_t s);
+hipError_t launch_topk(const RetrieveArgs& a, hipStream_t s);
+hipError_t launch_pad_outputs(const RetrieveArgs& a, hipStream_t s);
+
+hipError_t launch_attend(const void* q, const void* K, const void* V, int64_t kv_capacity,
+                         const int32_t* idx, int32_t k, int32_t batch, int32_t hkv, int32_t g,
+                         float scale, float* out, hipStream_t s);
+
+// Kernel-level profiling hooks (no-ops unless enabled).
+void prof_begin(const char* name, hipStream_t s);
+void prof_end(hipStream_t s);
+
+}  // namespace pariskv

@@ -1,0 +1,169 @@
+"""Host-side checks of the C ABI: the library loads, exports every declared
+symbol, and rejects bad arguments before touching the GPU.  No kernel is
+launched here, so these run without a GPU."""
+
+import ctypes
+import os
+import re
+
+import numpy as np
+import pytest
+
+import paper_2602_07721_amd as pk
+import workloads
+from oracle import quantizer
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "pariskv.h")
+
+pytestmark = pytest.mark.skipif(not os.path.exists(pk.LIB_PATH), reason="library not built")
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(pariskv_[a-z_0-9]+)\s*\(", text)))
+
+
+def test_every_declared_symbol_is_exported():
+    names = declared_functions()
+    assert len(names) >= 12
+    L = pk.lib()
+    for n in names:
+        assert hasattr(L, n), n
+    assert L.pariskv_abi_version() == 1
+
+
+def test_error_strings():
+    L = pk.lib()
+    for code in (0, -1, -2, -3, -4, -5):
+        assert L.pariskv_strerror(code)
+
+
+def test_quantizer_table_is_bit_identical_to_the_oracle():
+    # The library derives the table in closed form with binary128 arithmetic,
+    # the oracle through Beta incomplete integrals in mpmath; both round the
+    # same fixed point to double.
+    tau_l, a_l = pk.quantizer_table(8)
+    tau_o, a_o, _ = quantizer.lloyd_max(8)
+    assert [x.hex() for x in tau_l] == [float(x).hex() for x in tau_o]
+    assert [x.hex() for x in a_l] == [float(x).hex() for x in a_o]
+    with pytest.raises(pk.PariskvError) as e:
+        pk.quantizer_table(4)
+    assert e.value.code == pk.ERR_UNSUPPORTED
+
+
+def _cfg(**kw):
+    base = dict(n_kv_heads=8, q_per_kv=4, capacity=4096, rot_signs=workloads.rotation_signs(0))
+    base.update(kw)
+    return pk.Config(**base)
+
+
+FAKE = 1 << 20  # an aligned address that is never dereferenced: validation fails first
+
+
+def _index(ids=FAKE, rec=FAKE, counts=FAKE):
+    return pk._Index(ids, rec, counts)
+
+
+def _encode(cfg, idx, keys=FAKE, n=16, batch=1):
+    L = pk.lib()
+    return L.pariskv_encode(cfg.c(), ctypes.byref(idx), ctypes.c_void_p(keys), n, batch, None)
+
+
+@pytest.mark.parametrize("kw,code", [
+    (dict(head_dim=100), pk.ERR_INVALID),
+    (dict(head_dim=64, n_subspaces=8), pk.ERR_UNSUPPORTED),
+    (dict(n_subspaces=32), pk.ERR_UNSUPPORTED),
+    (dict(n_kv_heads=0), pk.ERR_INVALID),
+    (dict(q_per_kv=0), pk.ERR_INVALID),
+    (dict(q_per_kv=17), pk.ERR_INVALID),
+    (dict(capacity=0), pk.ERR_INVALID),
+    (dict(capacity=1 << 31), pk.ERR_INVALID),
+])
+def test_config_validation(kw, code):
+    assert _encode(_cfg(**kw), _index()) == code
+
+
+def test_sign_validation():
+    s = workloads.rotation_signs(0).copy()
+    s[5] = 0
+    assert _encode(_cfg(rot_signs=s), _index()) == pk.ERR_INVALID
+    assert b"rot_signs[5]" in pk.lib().pariskv_last_error()
+
+
+def test_encode_pointer_and_capacity_validation():
+    cfg = _cfg()
+    assert _encode(cfg, _index(ids=0)) == pk.ERR_INVALID
+    assert _encode(cfg, _index(rec=FAKE + 8)) == pk.ERR_INVALID
+    assert _encode(cfg, _index(), keys=0) == pk.ERR_INVALID
+    assert _encode(cfg, _index(), keys=FAKE + 2) == pk.ERR_INVALID
+    assert _encode(cfg, _index(), n=-1) == pk.ERR_INVALID
+    assert _encode(cfg, _index(), n=4097) == pk.ERR_CAPACITY
+    assert _encode(cfg, _index(), batch=0) == pk.ERR_INVALID
+    L = pk.lib()
+    rc = L.pariskv_append(cfg.c(), ctypes.byref(_index()), ctypes.c_void_p(FAKE), 4000, 97, 1, None)
+    assert rc == pk.ERR_CAPACITY
+
+
+def test_workspace_layout_is_consistent():
+    cfg = _cfg()
+    b = pk.Budget(512, 1024, 64)
+    lay = pk.workspace_layout(cfg, 2, 4000, b)
+    assert lay["total"] == pk.retrieve_workspace_size(cfg, 2, 4000, b)
+    assert lay["n_pad"] == 4032 and lay["n_chunks"] == 1 and lay["c_eff"] == 512 and lay["quads"] == 1
+    offs = [lay[k] for k in ("zq", "lut", "score8", "chunk_hist", "chunk_base", "thresh", "cand",
+                             "cand_score")]
+    assert offs == sorted(offs) and all(o % 256 == 0 for o in offs) and lay["total"] > offs[-1]
+    assert lay["score8"] - lay["lut"] >= 2 * 8 * 1 * 16 * 256 * 4
+    lay2 = pk.workspace_layout(_cfg(q_per_kv=6), 1, 100, pk.Budget(512, 1024, 64))
+    assert lay2["quads"] == 2 and lay2["c_eff"] == 100
+    assert pk.workspace_layout(cfg, 1, 0, b)["n_chunks"] == 0
+
+
+@pytest.mark.parametrize("budget,n,code", [
+    ((0, 10, 1), 100, pk.ERR_INVALID),
+    ((10, 0, 1), 100, pk.ERR_INVALID),
+    ((10, 10, 11), 100, pk.ERR_INVALID),
+    ((10, 10, 0), 100, pk.ERR_INVALID),
+    ((70000, 10, 5), 100, pk.ERR_UNSUPPORTED),
+    ((4000, 4000, 3000), 100, pk.ERR_UNSUPPORTED),
+    ((10, 10, 5), 5000, pk.ERR_INVALID),     # n > capacity
+    ((10, 10, 5), -1, pk.ERR_INVALID),
+])
+def test_retrieve_budget_validation(budget, n, code):
+    cfg = _cfg()
+    b = pk.Budget(*budget)
+    L = pk.lib()
+    rc = L.pariskv_retrieve(cfg.c(), ctypes.byref(_index()), ctypes.c_void_p(FAKE), n, 1, b.c(),
+                            ctypes.c_void_p(FAKE), None, ctypes.c_void_p(FAKE), 1 << 40, None)
+    assert rc == code
+    assert L.pariskv_retrieve_workspace(cfg.c(), 1, n, b.c()) == 0
+
+
+def test_retrieve_workspace_validation():
+    cfg = _cfg()
+    b = pk.Budget(512, 1024, 64)
+    need = pk.retrieve_workspace_size(cfg, 1, 4000, b)
+    L = pk.lib()
+    args = lambda ws, size: (cfg.c(), ctypes.byref(_index()), ctypes.c_void_p(FAKE), 4000, 1, b.c(),
+                             ctypes.c_void_p(FAKE), None, ctypes.c_void_p(ws), size, None)
+    assert L.pariskv_retrieve(*args(FAKE, need - 1)) == pk.ERR_WORKSPACE
+    assert L.pariskv_retrieve(*args(FAKE + 128, need)) == pk.ERR_WORKSPACE
+    assert L.pariskv_retrieve(*args(0, need)) == pk.ERR_WORKSPACE
+
+
+def test_sparse_attend_validation():
+    cfg = _cfg()
+    L = pk.lib()
+
+    def call(k=8, host=0, cap=4096, scale=0.1, idx=FAKE, out=FAKE):
+        return L.pariskv_sparse_attend(cfg.c(), ctypes.c_void_p(FAKE), ctypes.c_void_p(FAKE),
+                                       ctypes.c_void_p(FAKE), host, cap, ctypes.c_void_p(idx), k, 1,
+                                       ctypes.c_float(scale), ctypes.c_void_p(out), None)
+    assert call(k=0) == pk.ERR_INVALID
+    assert call(host=2) == pk.ERR_INVALID
+    assert call(cap=0) == pk.ERR_INVALID
+    assert call(scale=float("nan")) == pk.ERR_INVALID
+    assert call(idx=FAKE + 2) == pk.ERR_INVALID
+    assert call(out=0) == pk.ERR_INVALID

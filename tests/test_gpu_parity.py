@@ -1,0 +1,249 @@
+"""GPU parity of the HIP path (through the C ABI) with the CPU oracle.
+
+Bit-exact: centroid ids, 4-bit codes, W, cluster counts, the query transform
+rounded to float, the bonus tables, collision scores, the selection threshold
+and the candidate lists.  Within the stated tolerances: RSQ-IP estimates,
+the top-k sets and the attention output (see tests/parity.py)."""
+
+import numpy as np
+import pytest
+import torch
+
+import paper_2602_07721_amd as pk
+import workloads
+from oracle import attention as oatt
+from oracle import retrieve as oret
+
+from parity import (GpuRun, check_attention, check_head, check_index, decode_rec, oracle_group)
+
+pytestmark = pytest.mark.gpu
+SCALE = 1.0 / np.sqrt(128.0)
+
+
+def _inputs(cfg, n=None, batch=None, step=0):
+    n = cfg.n if n is None else n
+    wc = workloads.Config(**{**cfg.__dict__, "n": n, "batch": batch or cfg.batch})
+    K, V = workloads.layer_kv(wc)
+    Q, needles = workloads.layer_queries(wc, K, step=step)
+    return wc, K, V, Q, needles, workloads.rotation_signs(cfg.seed)
+
+
+def _full_check(wc, K, V, Q, signs, budget, capacity=None, attention=True):
+    run = GpuRun(K, V, Q, signs, wc.q_per_kv, budget, SCALE, capacity=capacity).retrieve()
+    inter = run.intermediates()
+    o_gpu = run.attend() if attention else None
+    gids, grec, gcnt = run.host_index()
+    b, hkv, n, _ = K.shape
+    results = {}
+    for s in range(b):
+        for h in range(hkv):
+            orc = oracle_group(K[s, h], signs)
+            check_index(gids[s, h], grec[s, h], gcnt[s, h], orc)
+            for g in range(wc.q_per_kv):
+                hq = h * wc.q_per_kv + g
+                r = check_head(inter, s, h, g, wc.q_per_kv, Q[s, hq], orc, signs, budget, n)
+                if attention:
+                    check_attention(o_gpu[s, hq], Q[s, hq], K[s, h], V[s, h], inter["idx"][s, hq], SCALE)
+                results[(s, hq)] = r
+    return run, inter, results
+
+
+def test_tiny_single_head_full_pipeline():
+    cfg = workloads.CONFIGS["tiny"]
+    wc, K, V, Q, needles, signs = _inputs(cfg)
+    print(f"case tiny n={wc.n}", flush=True)
+    budget = pk.Budget(cfg.n_cand, cfg.n_collide, cfg.top_k)
+    run, inter, res = _full_check(wc, K, V, Q, signs, budget)
+    hits = sum(int(needles[0, h]) in set(inter["idx"][0, h].tolist()) for h in range(wc.n_q_heads))
+    assert hits == wc.n_q_heads
+
+
+def test_layer32k_all_heads():
+    cfg = workloads.CONFIGS["layer32k"]
+    wc, K, V, Q, needles, signs = _inputs(cfg)
+    print(f"case layer32k n={wc.n}", flush=True)
+    budget = pk.Budget(cfg.n_cand, cfg.n_collide, cfg.top_k)
+    _full_check(wc, K, V, Q, signs, budget)
+
+
+EDGE = [
+    # name, batch, hkv, G, n, (C, C_rho, k)
+    ("n1", 1, 1, 4, 1, (512, 1024, 64)),
+    ("n_below_C", 1, 2, 4, 100, (512, 1024, 64)),
+    ("k_eq_C_eq_n", 1, 1, 4, 64, (64, 64, 64)),
+    ("ragged_two_chunks", 1, 1, 4, 4099, (512, 1024, 64)),
+    ("g3_batch2", 2, 2, 3, 9000, (700, 1500, 100)),
+    ("g6_two_quads", 1, 2, 6, 5000, (400, 800, 50)),
+    ("g1", 1, 3, 1, 3001, (300, 300, 30)),
+    ("tiny_collide_budget", 1, 1, 4, 2000, (200, 1, 20)),
+    ("collide_budget_above_n", 1, 1, 4, 2000, (200, 100000, 20)),
+    ("k_odd_ragged", 1, 1, 2, 777, (333, 555, 77)),
+]
+
+
+@pytest.mark.parametrize("name,batch,hkv,G,n,bud", EDGE, ids=[e[0] for e in EDGE])
+def test_edge_shapes(name, batch, hkv, G, n, bud):
+    print(f"case {name} batch={batch} hkv={hkv} G={G} n={n} budget={bud}", flush=True)
+    wc = workloads.Config(name, batch=batch, n_kv_heads=hkv, q_per_kv=G, n=n, n_cand=bud[0],
+                          n_collide=bud[1], top_k=bud[2], seed=101 + len(name))
+    K, V = workloads.layer_kv(wc)
+    Q, _ = workloads.layer_queries(wc, K)
+    signs = workloads.rotation_signs(wc.seed)
+    _full_check(wc, K, V, Q, signs, pk.Budget(*bud), capacity=n + 37)
+
+
+def test_degenerate_keys_and_queries():
+    # duplicates (ties in S and in the estimates), zero keys, a zero query,
+    # and one giant cluster (positive multiples of one key).
+    wc = workloads.Config("degenerate", batch=1, n_kv_heads=2, q_per_kv=4, n=3000, n_cand=300,
+                          n_collide=600, top_k=40, seed=77)
+    K, V = workloads.layer_kv(wc)
+    K[0, 0, 1000:1500] = K[0, 0, 10]                 # 500 identical keys
+    K[0, 0, 1500:1520] = 0                            # zero keys
+    base = K[0, 1, 5].astype(np.float32)
+    K[0, 1] = (base[None, :] * np.linspace(0.5, 2.0, 3000, dtype=np.float32)[:, None]).astype(np.float16)
+    Q, _ = workloads.layer_queries(wc, K)
+    Q[0, 1] = 0                                       # zero query
+    Q[0, 2] = K[0, 0, 10]                             # query equal to the duplicated key
+    signs = workloads.rotation_signs(wc.seed)
+    print("case degenerate", flush=True)
+    _full_check(wc, K, V, Q, signs, pk.Budget(300, 600, 40))
+
+
+def test_full_budget_reproduces_full_attention():
+    # C = n and k = n: every key is selected, so the sparse output is full attention.
+    wc = workloads.Config("full", batch=1, n_kv_heads=2, q_per_kv=4, n=512, n_cand=512,
+                          n_collide=512, top_k=512, seed=9)
+    K, V = workloads.layer_kv(wc)
+    Q, _ = workloads.layer_queries(wc, K)
+    signs = workloads.rotation_signs(wc.seed)
+    print("case full-budget", flush=True)
+    run = GpuRun(K, V, Q, signs, 4, pk.Budget(512, 512, 512), SCALE).retrieve()
+    o = run.attend()
+    idx = run.out_idx.cpu().numpy()
+    for hq in range(8):
+        assert sorted(idx[0, hq].tolist()) == list(range(512))
+        ref = oatt.full_attention(Q[0, hq], K[0, hq // 4], V[0, hq // 4], scale=SCALE)
+        d = np.abs(o[0, hq] - ref)
+        assert d.max() <= 2e-3 * np.abs(ref).max()
+
+
+def test_repeat_runs_are_bit_identical():
+    cfg = workloads.CONFIGS["layer32k"]
+    wc, K, V, Q, _, signs = _inputs(cfg, n=20000)
+    print("case determinism", flush=True)
+    budget = pk.Budget(cfg.n_cand, cfg.n_collide, cfg.top_k)
+    run = GpuRun(K, V, Q, signs, wc.q_per_kv, budget, SCALE).retrieve()
+    a = run.intermediates()
+    oa = run.attend()
+    ids_a, rec_a, cnt_a = run.host_index()
+    pk.encode(run.cfg, run.index, run.K)
+    run.retrieve()
+    b = run.intermediates()
+    ob = run.attend()
+    ids_b, rec_b, cnt_b = run.host_index()
+    # S rows are padded to a multiple of 64; only the first n entries are defined.
+    np.testing.assert_array_equal(a["S"][..., :run.n], b["S"][..., :run.n])
+    for k in ("lut", "thresh", "cand", "cand_score", "idx", "score"):
+        np.testing.assert_array_equal(a[k], b[k])
+    np.testing.assert_array_equal(oa, ob)
+    np.testing.assert_array_equal(ids_a, ids_b)
+    np.testing.assert_array_equal(rec_a, rec_b)
+    np.testing.assert_array_equal(cnt_a, cnt_b)
+
+
+def test_append_equals_bulk_encode():
+    wc = workloads.Config("append", batch=2, n_kv_heads=2, q_per_kv=4, n=3000, n_cand=256,
+                          n_collide=512, top_k=32, seed=55)
+    K, V = workloads.layer_kv(wc)
+    Q, _ = workloads.layer_queries(wc, K)
+    signs = workloads.rotation_signs(wc.seed)
+    print("case append", flush=True)
+    budget = pk.Budget(256, 512, 32)
+    bulk = GpuRun(K, V, Q, signs, 4, budget, SCALE).retrieve()
+    inc = GpuRun(K[:, :, :2000].copy(), V, Q, signs, 4, budget, SCALE, capacity=3000)
+    n_cur = 2000
+    for t in (1, 1, 5, 300, 693):
+        chunk = torch.from_numpy(np.ascontiguousarray(K[:, :, n_cur:n_cur + t])).cuda()
+        pk.append(inc.cfg, inc.index, chunk, n_cur)
+        n_cur += t
+    assert n_cur == 3000
+    inc.n = 3000
+    inc.retrieve()
+    for x, y in zip(bulk.host_index(), inc.host_index()):
+        np.testing.assert_array_equal(x, y)
+    a, b = bulk.intermediates(), inc.intermediates()
+    np.testing.assert_array_equal(a["S"][..., :3000], b["S"][..., :3000])
+    for k in ("lut", "cand", "idx", "score"):
+        np.testing.assert_array_equal(a[k], b[k])
+
+
+def test_host_mapped_attention_matches_hbm():
+    cfg = workloads.CONFIGS["layer32k"]
+    wc, K, V, Q, _, signs = _inputs(cfg, n=8192)
+    print("case host-mapped", flush=True)
+    budget = pk.Budget(1024, 2048, 256)
+    run = GpuRun(K, V, Q, signs, wc.q_per_kv, budget, SCALE).retrieve()
+    o_hbm = run.attend()
+    o_host = run.attend(host_mapped=True)
+    np.testing.assert_array_equal(o_hbm, o_host)
+    idx = run.out_idx.cpu().numpy()
+    for hq in (0, 13, 31):
+        check_attention(o_host[0, hq], Q[0, hq], K[0, hq // 4], V[0, hq // 4], idx[0, hq], SCALE)
+
+
+@pytest.mark.timeout(400)
+def test_batch8_128k_sampled_at_full_size():
+    # The bench workload in its launch configuration: every output that the
+    # oracle can recompute in seconds is checked (two whole (sequence, KV head)
+    # groups with their 8 query heads, plus encode of 4096 sampled keys from
+    # every group), the rest through properties that hold at any size.
+    cfg = workloads.CONFIGS["batch8_128k"]
+    wc, K, V, Q, needles, signs = _inputs(cfg)
+    print("case batch8_128k", flush=True)
+    budget = pk.Budget(cfg.n_cand, cfg.n_collide, cfg.top_k)
+    run = GpuRun(K, V, Q, signs, wc.q_per_kv, budget, SCALE).retrieve()
+    inter = run.intermediates()
+    o_gpu = run.attend()
+    torch.cuda.synchronize()
+    rng = np.random.default_rng(0)
+    # encode, sampled keys of every group
+    for s in range(wc.batch):
+        for h in range(wc.n_kv_heads):
+            rows = np.sort(rng.choice(wc.n, size=512, replace=False))
+            gids = run.index.ids[s, h, rows].cpu().numpy()
+            grec = run.index.rec[s, h, rows].cpu().numpy()
+            from oracle import encode as oenc
+            from parity import A, TAU
+            ids, codes, W = oenc.encode(K[s, h, rows], signs, TAU, A, 16)
+            np.testing.assert_array_equal(gids, ids)
+            gc, gW = decode_rec(grec)
+            np.testing.assert_array_equal(gc, codes)
+            np.testing.assert_array_equal(gW.view(np.uint32), W.view(np.uint32))
+    # properties of every head: counts sum, candidate count, sortedness, scores
+    cnt = run.index.counts.cpu().numpy()
+    assert np.all(cnt.sum(axis=-1) == wc.n)
+    C, k = budget.n_cand, budget.top_k
+    cand = inter["cand"][:, :, :C]
+    assert np.all(np.diff(cand, axis=-1) > 0) and cand.min() >= 0 and cand.max() < wc.n
+    S = inter["S"][:, :, :wc.n]
+    th = inter["thresh"]
+    for s in range(wc.batch):
+        for hq in range(wc.n_q_heads):
+            sel = S[s, hq, cand[s, hq]]
+            assert sel.min() >= th[s, hq, 0]
+            assert np.sum(S[s, hq] > th[s, hq, 0]) == th[s, hq, 1]
+    assert np.all(np.diff(inter["score"], axis=-1) <= 0)
+    # two whole groups through the oracle
+    for s, h in ((0, 0), (5, 3)):
+        orc = oracle_group(K[s, h], signs)
+        check_index(run.index.ids[s, h].cpu().numpy(), run.index.rec[s, h].cpu().numpy(),
+                    cnt[s, h].view(np.uint32), orc)
+        for g in range(wc.q_per_kv):
+            hq = h * wc.q_per_kv + g
+            check_head(inter, s, h, g, wc.q_per_kv, Q[s, hq], orc, signs, budget, wc.n)
+            check_attention(o_gpu[s, hq], Q[s, hq], K[s, h], V[s, h], inter["idx"][s, hq], SCALE)
+    hits = np.mean([needles[s, hq] in set(inter["idx"][s, hq].tolist())
+                    for s in range(wc.batch) for hq in range(wc.n_q_heads)])
+    print(f"needle hit rate {hits:.3f}", flush=True)
+    assert hits > 0.9

@@ -69,7 +69,9 @@ def head_keys(seed, seq, kvh, n, D=D_DEFAULT):
     law = head_law(seed, seq, kvh, D)
     r = _rng(_TAG_KEYS, seed, seq, kvh, 1)
     eps = r.standard_normal(size=(n, D), dtype=np.float32)
-    return (law.mu[None, :] + law.scale[None, :] * eps).astype(np.float16)
+    eps *= law.scale.astype(np.float32)[None, :]
+    eps += law.mu.astype(np.float32)[None, :]
+    return eps.astype(np.float16)
 
 
 def head_values(seed, seq, kvh, n, D=D_DEFAULT):
@@ -157,13 +159,26 @@ CONFIGS = {
 }
 
 
-def layer_kv(cfg, seqs=None, heads=None, n=None):
-    """K, V float16 arrays [len(seqs)][len(heads)][n][D] for a config."""
-    seqs = range(cfg.batch) if seqs is None else seqs
-    heads = range(cfg.n_kv_heads) if heads is None else heads
+def layer_kv(cfg, seqs=None, heads=None, n=None, values=True, threads=8):
+    """K, V float16 arrays [len(seqs)][len(heads)][n][D] for a config (V None if not values)."""
+    from concurrent.futures import ThreadPoolExecutor
+
+    seqs = list(range(cfg.batch) if seqs is None else seqs)
+    heads = list(range(cfg.n_kv_heads) if heads is None else heads)
     n = cfg.n if n is None else n
-    K = np.stack([np.stack([head_keys(cfg.seed, s, h, n, cfg.head_dim) for h in heads]) for s in seqs])
-    V = np.stack([np.stack([head_values(cfg.seed, s, h, n, cfg.head_dim) for h in heads]) for s in seqs])
+    D = cfg.head_dim
+    K = np.empty((len(seqs), len(heads), n, D), dtype=np.float16)
+    V = np.empty((len(seqs), len(heads), n, D), dtype=np.float16) if values else None
+
+    def fill(job):
+        i, j = job
+        K[i, j] = head_keys(cfg.seed, seqs[i], heads[j], n, D)
+        if values:
+            V[i, j] = head_values(cfg.seed, seqs[i], heads[j], n, D)
+
+    jobs = [(i, j) for i in range(len(seqs)) for j in range(len(heads))]
+    with ThreadPoolExecutor(max(1, threads)) as ex:
+        list(ex.map(fill, jobs))
     return K, V
 
 

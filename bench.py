@@ -1,0 +1,282 @@
+#!/usr/bin/env python3
+"""Decode-step benchmark of the ParisKV retrieval path on one MI355X.
+
+Workload (default): one Llama-3-8B-shaped layer at 128K context in the
+throughput regime -- 8 independent sequences x 8 KV heads x 4 query heads,
+N = 131072 keys per sequence, D = 128, candidate budget C = 8192, collision
+budget C_rho = 16384, top-k = 512, synthetic keys (outlier-channel Gaussian,
+see workloads/) and fresh planted-needle queries at every step.
+
+One step = the whole hot path for the whole batch: pariskv_retrieve (query
+transform + bonus tables, collision scan, selection, RSQ-IP rerank, top-k)
+followed by pariskv_sparse_attend over the selected K/V rows.  Keys are
+encoded once before timing (reported separately).  K, V, the index and all
+queries are resident in HBM before the timed region starts.
+
+Between timed steps the 256 MB Infinity Cache and the L2s are flushed by
+writing a 1 GiB buffer (outside the step's events): in a real model the other
+layers' weights and KV evict this layer's codes between two of its steps.
+The per-step time is the HIP-event interval around each step on the launch
+stream; per-kernel times come from the library's own event profiler on the
+same stream during the same timed steps.
+
+Prints one JSON line (see the roofline and cpu_baseline fields).
+"""
+
+import argparse
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBS = 8000.0  # MI355X HBM3E, vendor figure
+
+
+def parse():
+    ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=64)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--workload", default="batch8_128k")
+    ap.add_argument("--no-flush", action="store_true", help="keep caches warm between steps")
+    ap.add_argument("--no-profile", action="store_true", help="no per-kernel events in the timed steps")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-groups", type=int, default=4)
+    ap.add_argument("--cpu-steps", type=int, default=5)
+    ap.add_argument("--copy-calibration", action="store_true",
+                    help="also run one plain 1 GiB device copy (for scaling HBM counters)")
+    return ap.parse_args()
+
+
+def algorithmic_bytes(wc, c_eff):
+    """Bytes each kernel must move per launch (whole batch), by its definition."""
+    b, hkv, G, n, k = wc.batch, wc.n_kv_heads, wc.q_per_kv, wc.n, wc.top_k
+    hq = hkv * G
+    quads = (G + 3) // 4
+    return {
+        # 16 id bytes per key and KV head (once per quad of query heads) + 1 score byte per key and query head
+        "collide": b * hkv * quads * n * 16 + b * hq * n,
+        # score bytes read + 4-byte candidate index written
+        "compact": b * hq * n + b * hq * c_eff * 4,
+        # 128-byte record + 4-byte index read + 4-byte estimate written per candidate
+        "rerank": b * hq * c_eff * (128 + 4 + 4),
+        # 256-byte K row + 256-byte V row + 4-byte index per selected key
+        "attend": b * hq * k * (512 + 4),
+    }
+
+
+def cpu_baseline(wc, K, V, Qs, signs, budget, scale, groups, steps):
+    """Time the oracle's retrieve + attend on a bounded sample, scaled to a whole step."""
+    import numpy as np
+    from threadpoolctl import threadpool_limits
+
+    from oracle import attention as oatt
+    from oracle import encode as oenc
+    from oracle import quantizer as oq
+    from oracle import retrieve as oret
+
+    tau, a, _ = oq.lloyd_max(8)
+    picks = [(s % wc.batch, (s * 3) % wc.n_kv_heads) for s in range(groups)]
+    index = {}
+    for (s, h) in picks:  # prefill, not part of a decode step: untimed
+        ids, codes, W = oenc.encode(K[s, h], signs, tau, a, 16)
+        index[(s, h)] = (ids, codes, W, oenc.cluster_counts(ids, 8))
+    with threadpool_limits(limits=1):
+        t0 = time.perf_counter()
+        for st in range(steps):
+            Q = Qs[st]
+            for (s, h) in picks:
+                ids, codes, W, cnt = index[(s, h)]
+                for g in range(wc.q_per_kv):
+                    q = Q[s, h * wc.q_per_kv + g]
+                    r = oret.retrieve_head(q, ids, codes, W, cnt, signs, a, 16, budget.n_cand,
+                                           budget.n_collide, budget.top_k)
+                    oatt.sparse_attention(q, K[s, h], V[s, h], r["idx"], scale=scale)
+        el = time.perf_counter() - t0
+    per_group_step = el / (groups * steps)
+    return {
+        "value": per_group_step * wc.batch * wc.n_kv_heads * 1e6,
+        "unit": "us/step/layer",
+        "cores": 1,
+        "kind": "oracle",
+        "sample": (f"{groups} of {wc.batch * wc.n_kv_heads} (sequence, KV head) groups x "
+                   f"{wc.q_per_kv} query heads x {steps} steps of retrieve+attend "
+                   f"({el:.1f} s single-threaded NumPy float64), scaled x"
+                   f"{wc.batch * wc.n_kv_heads} to one whole step; host has "
+                   f"{len(os.sched_getaffinity(0))} cores available"),
+    }
+
+
+def main():
+    args = parse()
+    world = int(os.environ.get("WORLD_SIZE", "1"))
+    if args.gpus != 1 or world != 1:
+        print(f"bench.py: this build runs on exactly one GPU (asked for --gpus {args.gpus}, "
+              f"WORLD_SIZE {world}); the retrieval path shards by (sequence, KV head) with no "
+              f"exchange, so a multi-GPU figure would add no information here.", file=sys.stderr)
+        sys.exit(2)
+
+    import numpy as np
+    import torch
+
+    import paper_2602_07721_amd as pk
+    import workloads
+
+    if not torch.cuda.is_available():
+        print("bench.py needs a GPU", file=sys.stderr)
+        sys.exit(1)
+    pk.lib()
+    wc = workloads.CONFIGS[args.workload]
+    signs = workloads.rotation_signs(wc.seed)
+    budget = pk.Budget(wc.n_cand, wc.n_collide, wc.top_k)
+    scale = 1.0 / np.sqrt(wc.head_dim)
+    total_steps = args.warmup + args.steps
+
+    t_gen = time.perf_counter()
+    K, V = workloads.layer_kv(wc, threads=16)
+    Qs = [workloads.layer_queries(wc, K, step=s)[0] for s in range(total_steps)]
+    print(f"[bench] generated {wc.name} inputs in {time.perf_counter() - t_gen:.1f} s", file=sys.stderr,
+          flush=True)
+
+    dev = torch.device("cuda:0")
+    Kd = torch.from_numpy(K).to(dev)
+    Vd = torch.from_numpy(V).to(dev)
+    Qd = torch.from_numpy(np.stack(Qs)).to(dev)
+    cfg = pk.Config(wc.n_kv_heads, wc.q_per_kv, wc.n, signs)
+    index = pk.Index.empty(cfg, wc.batch, dev)
+    hq = cfg.n_q_heads
+    out_idx = torch.empty((wc.batch, hq, wc.top_k), dtype=torch.int32, device=dev)
+    out_score = torch.empty((wc.batch, hq, wc.top_k), dtype=torch.float32, device=dev)
+    out = torch.empty((wc.batch, hq, wc.head_dim), dtype=torch.float32, device=dev)
+    lay = pk.workspace_layout(cfg, wc.batch, wc.n, budget)
+    ws = torch.empty(lay["total"], dtype=torch.uint8, device=dev)
+    flush = torch.empty(1 << 30, dtype=torch.uint8, device=dev)
+
+    # Prefill encode (timed on its own).
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    pk.encode(cfg, index, Kd)
+    e1.record()
+    torch.cuda.synchronize()
+    enc_ms = e0.elapsed_time(e1)
+    n_keys = wc.batch * wc.n_kv_heads * wc.n
+
+    def step(s):
+        pk.retrieve(cfg, index, Qd[s], wc.n, budget, out_idx=out_idx, out_score=out_score, workspace=ws)
+        pk.sparse_attend(cfg, Qd[s], Kd, Vd, out_idx, scale, out=out)
+
+    for s in range(args.warmup):
+        if not args.no_flush:
+            flush.fill_(s & 255)
+        step(s)
+    torch.cuda.synchronize()
+
+    starts = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps)]
+    ends = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps)]
+    pk.profile_reset()
+    pk.profile_enable(not args.no_profile)
+    torch.cuda.synchronize()
+    w0 = time.perf_counter()
+    for i in range(args.steps):
+        if not args.no_flush:
+            flush.fill_(i & 255)
+        starts[i].record()
+        step(args.warmup + i)
+        ends[i].record()
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - w0
+    pk.profile_enable(False)
+    prof = pk.profile_read()
+    step_ms = np.array([starts[i].elapsed_time(ends[i]) for i in range(args.steps)])
+
+    # Needle hit rate on the last step (a sanity figure, not a parity check).
+    _, needles = workloads.layer_queries(wc, K, step=total_steps - 1)
+    idx_h = out_idx.cpu().numpy()
+    hits = float(np.mean([needles[s, h] in set(idx_h[s, h].tolist())
+                          for s in range(wc.batch) for h in range(hq)]))
+
+    c_eff = min(wc.n_cand, wc.n)
+    algo = algorithmic_bytes(wc, c_eff)
+    kernels = {}
+    for name, (launches, ms) in prof.items():
+        avg_ms = ms / max(1, launches)
+        row = {"launches": int(launches), "avg_us": avg_ms * 1e3}
+        if name in algo:
+            row["bytes_per_launch"] = algo[name]
+            row["GBps"] = algo[name] / (avg_ms * 1e-3) / 1e9
+            row["frac_hbm_peak"] = row["GBps"] / HBM_PEAK_GBS
+        kernels[name] = row
+    dominant = max((k for k in ("collide", "rerank") if k in kernels), key=lambda k: kernels[k]["avg_us"],
+                   default=None)
+    roofline = None
+    if dominant:
+        kr = kernels[dominant]
+        roofline = {"bound": "hbm", "kernel": dominant, "achieved": round(kr["GBps"], 1),
+                    "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": round(kr["frac_hbm_peak"], 4),
+                    "traffic": None}
+    collide_gbs = kernels.get("collide", {}).get("GBps")
+
+    if args.copy_calibration:
+        src = torch.empty(1 << 30, dtype=torch.uint8, device=dev)
+        dst = torch.empty_like(src)
+        src.fill_(1)
+        torch.cuda.synchronize()
+        c0, c1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        c0.record()
+        dst.copy_(src)
+        c1.record()
+        torch.cuda.synchronize()
+        copy_gbs = 2 * src.numel() / (c0.elapsed_time(c1) * 1e-3) / 1e9
+        del src, dst
+    else:
+        copy_gbs = None
+
+    cpu = None
+    if not args.no_cpu_baseline:
+        cpu = cpu_baseline(wc, K, V, Qs, signs, budget, scale, args.cpu_groups,
+                           min(args.cpu_steps, total_steps))
+
+    mean_us = float(step_ms.mean() * 1e3)
+    result = {
+        "metric": "retrieve+attend us/step/layer at 128K ctx; code-scan HBM GB/s vs peak",
+        "value": round(mean_us, 2),
+        "unit": "us/step/layer",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(float(step_ms.mean()), 5),
+        "higher_is_better": False,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f32",
+        "data": "synthetic",
+        "config": {
+            "workload": (f"{wc.name}: {wc.batch} seqs x {wc.n_kv_heads} KV heads x {wc.q_per_kv} query "
+                         f"heads, N={wc.n}, D={wc.head_dim}, B=16, C={wc.n_cand}, C_rho={wc.n_collide}, "
+                         f"k={wc.top_k}, float16 K/V/Q in HBM"),
+            "caches": "flushed between steps" if not args.no_flush else "warm",
+        },
+        "p10_us": round(float(np.percentile(step_ms, 10) * 1e3), 2),
+        "p50_us": round(float(np.percentile(step_ms, 50) * 1e3), 2),
+        "p90_us": round(float(np.percentile(step_ms, 90) * 1e3), 2),
+        "wall_ms_per_step_incl_flush": round(wall / args.steps * 1e3, 4),
+        "code_scan_GBps": round(collide_gbs, 1) if collide_gbs else None,
+        "code_scan_frac_hbm_peak": round(collide_gbs / HBM_PEAK_GBS, 4) if collide_gbs else None,
+        "roofline": roofline,
+        "kernels": {k: {kk: (round(vv, 3) if isinstance(vv, float) else vv) for kk, vv in v.items()}
+                    for k, v in sorted(kernels.items())},
+        "encode": {"ms": round(enc_ms, 3), "keys_per_s": round(n_keys / (enc_ms * 1e-3), 1),
+                   "GBps": round(n_keys * (256 + 144) / (enc_ms * 1e-3) / 1e9, 1)},
+        "needle_hit_rate": round(hits, 4),
+        "copy_GBps": round(copy_gbs, 1) if copy_gbs else None,
+        "cpu_baseline": cpu,
+    }
+    print(json.dumps(result), flush=True)
+
+
+if __name__ == "__main__":
+    main()

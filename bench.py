@@ -14,8 +14,10 @@ encoded once before timing (reported separately).  K, V, the index and all
 queries are resident in HBM before the timed region starts.
 
 Between timed steps the 256 MB Infinity Cache and the L2s are flushed by
-writing a 1 GiB buffer (outside the step's events): in a real model the other
-layers' weights and KV evict this layer's codes between two of its steps.
+reading a 1 GiB buffer (outside the step's events): in a real model the other
+layers' weights evict this layer's codes between two of its steps.  The
+flush reads rather than writes so that no dirty lines are left for the timed
+step to write back.
 The per-step time is the HIP-event interval around each step on the launch
 stream; per-kernel times come from the library's own event profiler on the
 same stream during the same timed steps.
@@ -153,7 +155,8 @@ def main():
     out = torch.empty((wc.batch, hq, wc.head_dim), dtype=torch.float32, device=dev)
     lay = pk.workspace_layout(cfg, wc.batch, wc.n, budget)
     ws = torch.empty(lay["total"], dtype=torch.uint8, device=dev)
-    flush = torch.empty(1 << 30, dtype=torch.uint8, device=dev)
+    flush = torch.zeros((1 << 30) // 4, dtype=torch.int32, device=dev)
+    flush_sink = torch.zeros((), dtype=torch.int32, device=dev)
 
     # Prefill encode (timed on its own).
     torch.cuda.synchronize()
@@ -171,7 +174,7 @@ def main():
 
     for s in range(args.warmup):
         if not args.no_flush:
-            flush.fill_(s & 255)
+            flush_sink.copy_(flush.amax())
         step(s)
     torch.cuda.synchronize()
 
@@ -183,7 +186,7 @@ def main():
     w0 = time.perf_counter()
     for i in range(args.steps):
         if not args.no_flush:
-            flush.fill_(i & 255)
+            flush_sink.copy_(flush.amax())
         starts[i].record()
         step(args.warmup + i)
         ends[i].record()

@@ -112,7 +112,8 @@ typedef struct pariskv_ws_layout {
     size_t lut;         /* uint32 [batch][Hkv][quads][B][256]: tier bonus, byte
                            h%4 of the word is query head 4*quad + h%4 of the group */
     size_t score8;      /* uint8 [batch][Hq][n_pad]: collision scores S_i        */
-    size_t chunk_hist;  /* uint32 [batch][Hq][n_chunks][97]: S histogram per chunk */
+    size_t chunk_sfx;   /* uint32 [batch][Hq][n_chunks][98]: per chunk, #{S >= v}
+                           for v = 0..97                                        */
     size_t chunk_base;  /* int32 [batch][Hq][n_chunks][2]: selected keys (S>theta,
                            S==theta) in earlier chunks                          */
     size_t thresh;      /* int32 [batch][Hq][4]: theta, #(S>theta), quota, C_eff */
@@ -158,9 +159,10 @@ int pariskv_workspace_layout(const pariskv_config* cfg, int32_t batch, int64_t n
 /* Two-stage retrieval for every query head (Sec. "Retrieval"; Alg. 1 decode).
  *   q          device float16 [batch][Hq][D]
  *   n          keys indexed per (sequence, KV head), 0..capacity
- *   out_idx    device int32 [batch][Hq][k]: selected key indices ordered by
- *              (RSQ-IP estimate descending, index ascending); -1 pads when
- *              fewer than k keys exist
+ *   out_idx    device int32 [batch][Hq][k]: the k keys with the largest
+ *              RSQ-IP estimates (ties at the k-th estimate: lower key index
+ *              first), listed in ascending key index; -1 pads when fewer than
+ *              k keys exist
  *   out_score  device float [batch][Hq][k] or NULL: the matching estimates of
  *              <k_i, q> (-inf on padding)
  *   workspace  device, >= pariskv_retrieve_workspace(...) bytes, 256-byte
@@ -184,10 +186,11 @@ int pariskv_retrieve(const pariskv_config* cfg, const pariskv_index* index,
  *   K, V  float16 [batch][Hkv][kv_capacity][D]; device memory when
  *         kv_host_mapped == 0; pinned host memory (hipHostMalloc) when 1, read
  *         directly by the kernel over the host link (the paper's UVA fetch)
- *   idx   device int32 [batch][Hq][k], entries in [0, kv_capacity) or -1 (skipped)
+ *   idx   device int32 [batch][Hq][k], k <= 4096; entries outside
+ *         [0, kv_capacity) (for example -1 padding) are skipped
  *   out   device float [batch][Hq][D]; zero when no valid index
  * scale = 1 reproduces the paper's raw score; models use 1/sqrt(D).
- * Errors: INVALID, HIP. */
+ * Errors: INVALID, UNSUPPORTED (k > 4096), HIP. */
 int pariskv_sparse_attend(const pariskv_config* cfg, const void* q, const void* K,
                           const void* V, int32_t kv_host_mapped, int64_t kv_capacity,
                           const int32_t* idx, int32_t k, int32_t batch, float scale,

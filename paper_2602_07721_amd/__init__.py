@@ -51,7 +51,7 @@ class _Budget(ctypes.Structure):
 
 class _Layout(ctypes.Structure):
     _fields_ = [(name, ctypes.c_size_t) for name in
-                ("total", "zq", "lut", "score8", "chunk_hist", "chunk_base", "thresh", "cand",
+                ("total", "zq", "lut", "score8", "chunk_sfx", "chunk_base", "thresh", "cand",
                  "cand_score")] + \
                [(name, ctypes.c_int64) for name in ("n_pad", "n_chunks", "chunk_keys", "c_eff")] + \
                [("quads", ctypes.c_int32), ("reserved", ctypes.c_int32)]

@@ -144,7 +144,7 @@ int layout(const pariskv_config* cfg, int32_t batch, int64_t n, const pariskv_bu
     L->zq = take((size_t)rows * kD * 4);
     L->lut = take((size_t)batch * hkv * quads * kB * kCentroids * 4);
     L->score8 = take((size_t)rows * L->n_pad);
-    L->chunk_hist = take((size_t)rows * L->n_chunks * kBins * 4);
+    L->chunk_sfx = take((size_t)rows * L->n_chunks * kSfx * 4);
     L->chunk_base = take((size_t)rows * L->n_chunks * 2 * 4);
     L->thresh = take((size_t)rows * 4 * 4);
     L->cand = take((size_t)rows * bud->n_cand * 4);
@@ -344,7 +344,7 @@ int pariskv_retrieve(const pariskv_config* cfg, const pariskv_index* index, cons
     a.zq = reinterpret_cast<float*>(ws + L.zq);
     a.lut = reinterpret_cast<uint32_t*>(ws + L.lut);
     a.score8 = reinterpret_cast<uint8_t*>(ws + L.score8);
-    a.chunk_hist = reinterpret_cast<uint32_t*>(ws + L.chunk_hist);
+    a.chunk_sfx = reinterpret_cast<uint32_t*>(ws + L.chunk_sfx);
     a.chunk_base = reinterpret_cast<int32_t*>(ws + L.chunk_base);
     a.thresh = reinterpret_cast<int32_t*>(ws + L.thresh);
     a.cand = reinterpret_cast<int32_t*>(ws + L.cand);
@@ -380,6 +380,7 @@ int pariskv_sparse_attend(const pariskv_config* cfg, const void* q, const void* 
         (reinterpret_cast<uintptr_t>(idx) & 3u) != 0)
         return fail(PARISKV_ERR_INVALID, "q, K, V, out must be 16-byte aligned, idx 4-byte aligned");
     if (k < 1) return fail(PARISKV_ERR_INVALID, "k %d < 1", k);
+    if (k > 4096) return fail(PARISKV_ERR_UNSUPPORTED, "k %d above 4096", k);
     if (kv_capacity < 1 || kv_capacity > INT32_MAX)
         return fail(PARISKV_ERR_INVALID, "kv_capacity %lld outside 1..2^31-1", (long long)kv_capacity);
     if (kv_host_mapped != 0 && kv_host_mapped != 1)

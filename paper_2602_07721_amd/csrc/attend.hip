@@ -10,7 +10,8 @@
 // one 256-byte contiguous read by 16 lanes.  Indices outside
 // [0, kv_capacity) are skipped like -1.  Every (wave, key slot) keeps an
 // online-softmax state (running max, sum, 8 accumulators per lane); the 16
-// states are merged in LDS at the end.
+// states are merged in LDS at the end.  The row's indices are staged in LDS
+// first and every lane keeps 4 K and 4 V row segments in flight.
 
 #include <hip/hip_fp16.h>
 
@@ -22,6 +23,8 @@ namespace {
 
 constexpr int kAtThreads = 256;
 constexpr int kAtGroups = kAtThreads / 16;  // concurrent key slots per block
+constexpr int kAtUnroll = 4;                // K/V rows in flight per lane
+constexpr int kAtMaxK = 4096;               // largest k a block stages in LDS
 
 __device__ __forceinline__ void unpack8(const uint4 v, float* f) {
     const uint32_t w[4] = {v.x, v.y, v.z, v.w};
@@ -42,6 +45,7 @@ __global__ __launch_bounds__(kAtThreads) void attend_kernel(const __half* __rest
                                                             float* __restrict__ out) {
     __shared__ float s_m[kAtGroups], s_l[kAtGroups];
     __shared__ float s_acc[kAtGroups][kD];
+    __shared__ int32_t s_idx[kAtMaxK];
 
     const int tid = threadIdx.x;
     const int grp16 = tid >> 4;      // key slot 0..15
@@ -51,44 +55,75 @@ __global__ __launch_bounds__(kAtThreads) void attend_kernel(const __half* __rest
     const int h = (int)(row % hq);
     const int64_t kvrow0 = ((int64_t)seq * hkv + h / g) * kv_capacity;
 
+    // Stage the row's indices (invalid ones as -1) so the row loads never wait on them.
+    const int32_t* ir = idx + row * k;
+    for (int r = tid; r < k; r += kAtThreads) {
+        const int32_t key = ir[r];
+        s_idx[r] = (key >= 0 && key < kv_capacity) ? key : -1;
+    }
+
     float qf[8];
     unpack8(reinterpret_cast<const uint4*>(q + row * kD)[l16], qf);
 #pragma unroll
     for (int d = 0; d < 8; ++d) qf[d] *= scale;
+    __syncthreads();
 
     float m = -__builtin_huge_valf(), lsum = 0.f;
     float acc[8];
 #pragma unroll
     for (int d = 0; d < 8; ++d) acc[d] = 0.f;
 
-    const int32_t* ir = idx + row * k;
-    for (int base = 0; base < k; base += kAtGroups) {
-        const int r = base + grp16;
-        int32_t key = r < k ? ir[r] : -1;
-        if (key >= kv_capacity) key = -1;  // never read outside the K/V rows
-        uint4 kc = make_uint4(0, 0, 0, 0), vc = make_uint4(0, 0, 0, 0);
-        if (key >= 0) {
-            const int64_t off = (kvrow0 + key) * kD;
-            kc = reinterpret_cast<const uint4*>(K + off)[l16];
-            vc = reinterpret_cast<const uint4*>(V + off)[l16];
+    // Slot grp16 takes keys grp16, grp16 + 16, ...; kAtUnroll rows in flight per lane.
+    for (int base = 0; base < k; base += kAtGroups * kAtUnroll) {
+        int32_t key[kAtUnroll];
+        uint4 kc[kAtUnroll], vc[kAtUnroll];
+#pragma unroll
+        for (int u = 0; u < kAtUnroll; ++u) {
+            const int r = base + grp16 + kAtGroups * u;
+            key[u] = r < k ? s_idx[r] : -1;
+            kc[u] = make_uint4(0, 0, 0, 0);
+            vc[u] = make_uint4(0, 0, 0, 0);
+            if (key[u] >= 0) {
+                const int64_t off = (kvrow0 + key[u]) * kD;
+                kc[u] = reinterpret_cast<const uint4*>(K + off)[l16];
+                vc[u] = reinterpret_cast<const uint4*>(V + off)[l16];
+            }
         }
-        float kf[8], vf[8];
-        unpack8(kc, kf);
-        unpack8(vc, vf);
-        float dot = 0.f;
+        float dot[kAtUnroll];
 #pragma unroll
-        for (int d = 0; d < 8; ++d) dot += qf[d] * kf[d];
-        dot += __shfl_xor(dot, 1, 64);
-        dot += __shfl_xor(dot, 2, 64);
-        dot += __shfl_xor(dot, 4, 64);
-        dot += __shfl_xor(dot, 8, 64);
-        if (key >= 0) {
-            const float mn = fmaxf(m, dot);
+        for (int u = 0; u < kAtUnroll; ++u) {
+            float kf[8];
+            unpack8(kc[u], kf);
+            float d0 = 0.f;
+#pragma unroll
+            for (int d = 0; d < 8; ++d) d0 += qf[d] * kf[d];
+            dot[u] = d0;
+        }
+#pragma unroll
+        for (int st = 1; st < 16; st <<= 1) {
+#pragma unroll
+            for (int u = 0; u < kAtUnroll; ++u) dot[u] += __shfl_xor(dot[u], st, 64);
+        }
+        float mn = m;
+#pragma unroll
+        for (int u = 0; u < kAtUnroll; ++u)
+            if (key[u] >= 0) mn = fmaxf(mn, dot[u]);
+        if (mn > -__builtin_huge_valf()) {
             const float corr = __expf(m - mn);
-            const float p = __expf(dot - mn);
-            lsum = lsum * corr + p;
+            lsum *= corr;
 #pragma unroll
-            for (int d = 0; d < 8; ++d) acc[d] = acc[d] * corr + p * vf[d];
+            for (int d = 0; d < 8; ++d) acc[d] *= corr;
+#pragma unroll
+            for (int u = 0; u < kAtUnroll; ++u) {
+                if (key[u] >= 0) {
+                    const float p = __expf(dot[u] - mn);
+                    float vf[8];
+                    unpack8(vc[u], vf);
+                    lsum += p;
+#pragma unroll
+                    for (int d = 0; d < 8; ++d) acc[d] += p * vf[d];
+                }
+            }
             m = mn;
         }
     }

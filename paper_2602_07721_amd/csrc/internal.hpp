@@ -15,6 +15,7 @@ constexpr int kCentroids = 256;   // 2^m
 constexpr int kRec = 128;         // bytes per rerank record
 constexpr int kMaxScore = 96;     // 6 * B
 constexpr int kBins = kMaxScore + 1;
+constexpr int kSfx = kBins + 1;     // suffix histogram entries v = 0..97 (entry 97 is 0)
 constexpr int kChunk = 4096;      // keys per collision / selection chunk
 constexpr int kTierCount = 6;
 
@@ -57,7 +58,7 @@ struct RetrieveArgs {
     float* zq;
     uint32_t* lut;
     uint8_t* score8;
-    uint32_t* chunk_hist;
+    uint32_t* chunk_sfx;
     int32_t* chunk_base;
     int32_t* thresh;
     int32_t* cand;

@@ -5,22 +5,23 @@
 // "Top-beta selection with small-range integer scores"; Alg. 1 Stage I).
 //
 // Kernels, in launch order:
-//   query_lut_kernel   one block per (sequence, KV head, quad, slot): z = H(s q)
-//                      in exact float64, writes z/D as float for the rerank,
-//                      ranks the 256 centroids of every subspace by the exact
-//                      proxy sum_j +-z_j (ties: lower id), prefix-sums the
-//                      cluster counts in that order and writes the tier bonus
-//                      of each cluster into byte `slot` of a packed table
-//                      (4 query heads of a KV head share one uint32 entry).
+//   query_lut_kernel   one block per (sequence, KV head, quad, 4 subspaces), one
+//                      wave per (head slot, subspace): z = H(s q) in exact
+//                      float64 (written as z/D float for the rerank), the 256
+//                      centroids ranked by the exact proxy sum_j +-z_j (ties:
+//                      lower id), cluster counts prefix-summed in that order, and
+//                      the tier bonus of each cluster placed in byte `slot` of a
+//                      packed word (4 query heads of a KV head share one uint32),
+//                      assembled in LDS and stored whole.
 //   collide_kernel     streams the 16 id bytes of every key once per quad of
-//                      query heads, sums 16 packed LDS lookups (the 4 head
-//                      scores ride in the 4 bytes of one uint32; each is at
-//                      most 96, so no carries), writes S as bytes per head and
-//                      a 97-bin histogram per head and chunk (no atomics in
-//                      global memory).
-//   threshold_kernel   one block per query head: theta = largest v with
-//                      #{S >= v} >= C_eff, quota of S == theta keys, and for
-//                      every chunk the number of S > theta / S == theta keys in
+//                      query heads, sums 16 packed LDS lookups (4 head scores in
+//                      the 4 bytes of one uint32; each is at most 96, so no
+//                      carries), writes S as bytes per head and a suffix
+//                      histogram #{S >= v} per head and 4096-key chunk (frequent
+//                      low scores counted by wave ballots, the rest by LDS atomics).
+//   threshold_kernel   one wave per query head: theta = largest v with
+//                      #{S >= v} >= C_eff, the quota of S == theta keys, and per
+//                      chunk the number of S > theta / S == theta keys in
 //                      earlier chunks.
 //   compact_kernel     writes candidate indices in ascending key order: all
 //                      S > theta and the first `quota` S == theta keys.
@@ -48,56 +49,59 @@ __device__ __forceinline__ uint32_t wave_incl_scan_u32(uint32_t v, int lane) {
 
 // ---------------------------------------------------------------- query + LUT
 
-constexpr int kLutThreads = 256;
+constexpr int kLutThreads = 1024;  // 16 waves: 4 head slots x 4 subspaces
 
 __global__ __launch_bounds__(kLutThreads) void query_lut_kernel(RetrieveArgs a) {
-    __shared__ double s_z[kD];
+    __shared__ double s_z[4][kD];
+    __shared__ uint32_t s_cnt[4][kCentroids];
+    __shared__ uint32_t s_lut[4][kCentroids];  // packed bonus words of the 4 subspaces
     const int tid = threadIdx.x;
     const int lane = tid & 63;
     const int wave = tid >> 6;
+    const int slot = wave >> 2;          // head of the quad
+    const int sub = wave & 3;
 
-    // blockIdx.x = ((seq * hkv + kvh) * quads + quad) * 4 + slot
-    const int slot = blockIdx.x & 3;
-    const int quad = (blockIdx.x >> 2) % a.quads;
-    const int64_t grp = (blockIdx.x >> 2) / a.quads;  // seq * hkv + kvh
+    // blockIdx.x = ((seq * hkv + kvh) * quads + quad) * 4 + subspace group
+    const int sg = blockIdx.x & 3;
+    const int64_t gq = blockIdx.x >> 2;  // (seq * hkv + kvh) * quads + quad
+    const int quad = (int)(gq % a.quads);
+    const int64_t grp = gq / a.quads;    // seq * hkv + kvh
     const int seq = (int)(grp / a.hkv);
     const int kvh = (int)(grp % a.hkv);
-    const int hg = quad * 4 + slot;  // head within the KV group
-    uint8_t* lut_bytes = reinterpret_cast<uint8_t*>(a.lut + (grp * a.quads + quad) * (kB * kCentroids));
+    const int b = 4 * sg + sub;          // this wave's subspace
+    const int hg = quad * 4 + slot;      // head within the KV group
+    const bool live = hg < a.g;
+    const int64_t row = (int64_t)seq * a.hq + kvh * a.g + hg;
 
-    if (hg >= a.g) {
-        // Unused slot of the last quad: zero bonus everywhere.
-        for (int i = tid; i < kB * kCentroids; i += kLutThreads) lut_bytes[4 * i + slot] = 0;
-        return;
-    }
-    const int hq = kvh * a.g + hg;
-    const int64_t row = (int64_t)seq * a.hq + hq;
-
-    // z = H (s (.) q), exact in float64 (butterflies in LDS).
-    if (tid < kD) {
-        const __half* qp = static_cast<const __half*>(a.q) + row * kD;
-        double v = (double)__half2float(qp[tid]);
-        if ((a.sb.w[tid >> 5] >> (tid & 31)) & 1u) v = -v;
-        s_z[tid] = v;
+    // Cluster counts of the 4 subspaces; z = H (s (.) q) of the 4 heads, exactly in float64.
+    const uint32_t* cnt = a.counts + grp * (kB * kCentroids) + (4 * sg) * kCentroids;
+    (&s_cnt[0][0])[tid] = cnt[tid];
+    (&s_lut[0][0])[tid] = 0u;
+    const int zh = tid >> 7, zi = tid & (kD - 1);  // threads < 512: 4 heads x 128 coordinates
+    const bool zlive = zh < 4 && quad * 4 + zh < a.g;
+    if (zlive) {
+        const __half* qp = static_cast<const __half*>(a.q) + (row + (zh - slot)) * kD;
+        double v = (double)__half2float(qp[zi]);
+        if ((a.sb.w[zi >> 5] >> (zi & 31)) & 1u) v = -v;
+        s_z[zh][zi] = v;
     }
     __syncthreads();
     for (int h = 1; h < kD; h <<= 1) {
-        if (tid < kD / 2) {
-            const int i = ((tid / h) * 2 * h) + (tid % h);
-            const double x0 = s_z[i], x1 = s_z[i + h];
-            s_z[i] = __dadd_rn(x0, x1);
-            s_z[i + h] = __dsub_rn(x0, x1);
+        if (zi < kD / 2 && zlive) {
+            const int i = ((zi / h) * 2 * h) + (zi % h);
+            const double x0 = s_z[zh][i], x1 = s_z[zh][i + h];
+            s_z[zh][i] = __dadd_rn(x0, x1);
+            s_z[zh][i + h] = __dsub_rn(x0, x1);
         }
         __syncthreads();
     }
-    if (tid < kD) a.zq[row * kD + tid] = (float)(s_z[tid] * (1.0 / kD));
+    if (sg == 0 && zlive)
+        a.zq[(row + (zh - slot)) * kD + zi] = (float)(s_z[zh][zi] * (1.0 / kD));
 
-    const uint32_t* cnt = a.counts + grp * (kB * kCentroids);
-    // One wave per subspace; lane L holds ranks 4L..4L+3 after the sort.
-    for (int b = wave; b < kB; b += kLutThreads / 64) {
+    if (live) {
         double zb[8];
 #pragma unroll
-        for (int j = 0; j < 8; ++j) zb[j] = s_z[8 * b + j];
+        for (int j = 0; j < 8; ++j) zb[j] = s_z[slot][8 * b + j];
         int64_t key[4];
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
@@ -148,7 +152,7 @@ __global__ __launch_bounds__(kLutThreads) void query_lut_kernel(RetrieveArgs a) 
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
             cid[r] = 255 - (int)(key[r] & 255);
-            cc[r] = cnt[b * kCentroids + cid[r]];
+            cc[r] = s_cnt[sub][cid[r]];
         }
         const uint32_t tot = cc[0] + cc[1] + cc[2] + cc[3];
         const uint32_t incl = wave_incl_scan_u32(tot, lane);
@@ -159,151 +163,211 @@ __global__ __launch_bounds__(kLutThreads) void query_lut_kernel(RetrieveArgs a) 
 #pragma unroll
             for (int l = kTierCount - 1; l >= 0; --l)
                 if (start < a.cuts[l]) bonus = (uint32_t)(kTierCount - l);
-            lut_bytes[4 * (b * kCentroids + cid[r]) + slot] = (uint8_t)bonus;
+            if (bonus) atomicOr(&s_lut[sub][cid[r]], bonus << (8 * slot));
             start += cc[r];
         }
     }
+    __syncthreads();
+    // Unused slots of the last quad keep bonus 0.
+    a.lut[gq * (kB * kCentroids) + (4 * sg) * kCentroids + tid] = (&s_lut[0][0])[tid];
 }
 
 // ---------------------------------------------------------------- collision scan
 
 constexpr int kColThreads = 256;
 constexpr int kColWaves = kColThreads / 64;
+constexpr int kColKeysPerIter = 4 * kColThreads;  // 4 keys per thread per iteration
+constexpr int kLowCut = 4;  // scores below this are counted by ballot, not by LDS atomics
+
+// Suffix sums of a 97-bin histogram held as (lo = bins 0..63 by lane, hi = bins
+// 64..96 by lane < 33): returns (sfx_lo, sfx_hi) with sfx[v] = sum_{u >= v} h[u].
+__device__ __forceinline__ void wave_suffix97(uint32_t lo, uint32_t hi, int lane, uint32_t* s_lo,
+                                              uint32_t* s_hi) {
+#pragma unroll
+    for (int d = 1; d < 64; d <<= 1) {
+        const uint32_t o = __shfl_down(hi, d, 64);
+        if (lane + d < 64) hi += o;
+    }
+    const uint32_t tot_hi = __shfl(hi, 0, 64);
+#pragma unroll
+    for (int d = 1; d < 64; d <<= 1) {
+        const uint32_t o = __shfl_down(lo, d, 64);
+        if (lane + d < 64) lo += o;
+    }
+    *s_lo = lo + tot_hi;
+    *s_hi = hi;
+}
 
 __global__ __launch_bounds__(kColThreads) void collide_kernel(RetrieveArgs a) {
     __shared__ uint32_t s_lut[kB * kCentroids];
-    __shared__ uint32_t s_hist[kColWaves][4][kBins];
+    __shared__ uint32_t s_hist[kColWaves][4][kBins + 3];
+    __shared__ uint32_t s_pack[kColKeysPerIter];
+    __shared__ uint32_t s_low[kColWaves][kLowCut - 1][4];
 
     const int tid = threadIdx.x;
+    const int lane = tid & 63;
     const int wave = tid >> 6;
     const int64_t chunk = blockIdx.x;
-    const int quad = blockIdx.y % a.quads;
-    const int64_t grp = blockIdx.y / a.quads;  // seq * hkv + kvh
+    const int64_t gq = blockIdx.y;             // (seq * hkv + kvh) * quads + quad
+    const int quad = (int)(gq % a.quads);
+    const int64_t grp = gq / a.quads;          // seq * hkv + kvh
     const int seq = (int)(grp / a.hkv);
     const int kvh = (int)(grp % a.hkv);
     const int nh = min(4, a.g - 4 * quad);     // heads in this quad
+    const int64_t row0 = (int64_t)seq * a.hq + kvh * a.g + 4 * quad;  // row of head 0 of the quad
 
-    const uint4* lsrc = reinterpret_cast<const uint4*>(a.lut + (grp * a.quads + quad) * (kB * kCentroids));
+    const uint4* lsrc = reinterpret_cast<const uint4*>(a.lut + gq * (kB * kCentroids));
     for (int i = tid; i < kB * kCentroids / 4; i += kColThreads)
         reinterpret_cast<uint4*>(s_lut)[i] = lsrc[i];
-    for (int i = tid; i < kColWaves * 4 * kBins; i += kColThreads) (&s_hist[0][0][0])[i] = 0;
+    for (int i = tid; i < kColWaves * 4 * (kBins + 3); i += kColThreads) (&s_hist[0][0][0])[i] = 0;
     __syncthreads();
 
     const uint8_t* ids = a.ids + grp * a.capacity * kB;
     const int64_t c0 = chunk * kChunk;
-    const int64_t c1 = min(c0 + kChunk, a.n);
-    uint8_t* srow[4];
+    const int64_t c1 = min(c0 + (int64_t)kChunk, a.n);
+    uint32_t low[kLowCut - 1][4];  // wave-uniform: #{S >= v} for v = 1 .. kLowCut-1, per head
 #pragma unroll
-    for (int h = 0; h < 4; ++h) {
-        const int hq = kvh * a.g + 4 * quad + min(h, nh - 1);
-        srow[h] = a.score8 + ((int64_t)seq * a.hq + hq) * a.n_pad;
-    }
+    for (int v = 0; v < kLowCut - 1; ++v)
+#pragma unroll
+        for (int h = 0; h < 4; ++h) low[v][h] = 0;
 
-    for (int64_t base = c0 + 4 * tid; base < c1; base += 4 * kColThreads) {
-        uint32_t s[4];
+    for (int64_t base = c0; base < c1; base += kColKeysPerIter) {
+        // Key base + tid + 256 j: one 16-byte id row per lane, a wave reads 1 KiB contiguous.
+        uint4 w[4];
 #pragma unroll
-        for (int kk = 0; kk < 4; ++kk) {
-            const int64_t i = base + kk;
+        for (int j = 0; j < 4; ++j) {
+            const int64_t i = base + tid + kColThreads * j;
+            w[j] = i < c1 ? *reinterpret_cast<const uint4*>(ids + i * kB) : make_uint4(0, 0, 0, 0);
+        }
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+            const int64_t i = base + tid + kColThreads * j;
+            const uint32_t ww[4] = {w[j].x, w[j].y, w[j].z, w[j].w};
             uint32_t acc = 0;
-            if (i < c1) {
-                const uint4 w = *reinterpret_cast<const uint4*>(ids + i * kB);
-                const uint32_t ww[4] = {w.x, w.y, w.z, w.w};
 #pragma unroll
-                for (int b = 0; b < kB; ++b)
-                    acc += s_lut[b * kCentroids + ((ww[b >> 2] >> (8 * (b & 3))) & 0xffu)];
+            for (int b = 0; b < kB; ++b)
+                acc += s_lut[b * kCentroids + ((ww[b >> 2] >> (8 * (b & 3))) & 0xffu)];
+            const bool live = i < c1;
+            acc = live ? acc : 0u;
+            // Low scores are frequent: #{S >= v} for v < kLowCut is counted for all 4
+            // heads at once with a byte-wise compare ((x | 0x80) - v has its top bit set
+            // iff x >= v, for bytes below 128) and one wave ballot per head.
+#pragma unroll
+            for (int v = 1; v < kLowCut; ++v) {
+                const uint32_t ge = ((acc | 0x80808080u) - (uint32_t)v * 0x01010101u) & 0x80808080u;
 #pragma unroll
                 for (int h = 0; h < 4; ++h)
-                    if (h < nh) atomicAdd(&s_hist[wave][h][(acc >> (8 * h)) & 0xffu], 1u);
+                    low[v - 1][h] += (uint32_t)__popcll(__ballot(live && ((ge >> (8 * h + 7)) & 1u)));
             }
-            s[kk] = acc;
-        }
-        // Transpose 4 keys x 4 heads of bytes into one word per head.
-        const uint32_t lo01 = __builtin_amdgcn_perm(s[1], s[0], 0x05010400u);
-        const uint32_t hi01 = __builtin_amdgcn_perm(s[1], s[0], 0x07030602u);
-        const uint32_t lo23 = __builtin_amdgcn_perm(s[3], s[2], 0x05010400u);
-        const uint32_t hi23 = __builtin_amdgcn_perm(s[3], s[2], 0x07030602u);
-        uint32_t o[4];
-        o[0] = __builtin_amdgcn_perm(lo23, lo01, 0x05040100u);
-        o[1] = __builtin_amdgcn_perm(lo23, lo01, 0x07060302u);
-        o[2] = __builtin_amdgcn_perm(hi23, hi01, 0x05040100u);
-        o[3] = __builtin_amdgcn_perm(hi23, hi01, 0x07060302u);
+            // Higher scores are rare and spread out: exact per-value LDS histogram.
 #pragma unroll
-        for (int h = 0; h < 4; ++h)
-            if (h < nh) *reinterpret_cast<uint32_t*>(srow[h] + base) = o[h];
+            for (int h = 0; h < 4; ++h) {
+                const uint32_t sh = (acc >> (8 * h)) & 0xffu;
+                if (h < nh && live && sh >= (uint32_t)kLowCut) atomicAdd(&s_hist[wave][h][sh], 1u);
+            }
+            s_pack[tid + kColThreads * j] = acc;
+        }
+        __syncthreads();
+        // Thread t now writes keys base + 4t .. 4t+3 for every head: transpose 4 keys x 4
+        // heads of bytes into one word per head.
+        const int64_t k4 = base + 4 * tid;
+        if (k4 < c1) {
+            const uint4 sp = reinterpret_cast<const uint4*>(s_pack)[tid];
+            const uint32_t lo01 = __builtin_amdgcn_perm(sp.y, sp.x, 0x05010400u);
+            const uint32_t hi01 = __builtin_amdgcn_perm(sp.y, sp.x, 0x07030602u);
+            const uint32_t lo23 = __builtin_amdgcn_perm(sp.w, sp.z, 0x05010400u);
+            const uint32_t hi23 = __builtin_amdgcn_perm(sp.w, sp.z, 0x07030602u);
+            uint32_t o[4];
+            o[0] = __builtin_amdgcn_perm(lo23, lo01, 0x05040100u);
+            o[1] = __builtin_amdgcn_perm(lo23, lo01, 0x07060302u);
+            o[2] = __builtin_amdgcn_perm(hi23, hi01, 0x05040100u);
+            o[3] = __builtin_amdgcn_perm(hi23, hi01, 0x07060302u);
+#pragma unroll
+            for (int h = 0; h < 4; ++h)
+                if (h < nh) *reinterpret_cast<uint32_t*>(a.score8 + (row0 + h) * a.n_pad + k4) = o[h];
+        }
+        __syncthreads();
+    }
+
+    if (lane == 0) {
+#pragma unroll
+        for (int v = 0; v < kLowCut - 1; ++v)
+#pragma unroll
+            for (int h = 0; h < 4; ++h) s_low[wave][v][h] = low[v][h];
     }
     __syncthreads();
 
-    for (int i = tid; i < nh * kBins; i += kColThreads) {
-        const int h = i / kBins, v = i % kBins;
-        uint32_t t = 0;
+    // Per-chunk suffix histogram of every head: sfx[v] = #{keys in chunk : S >= v}, v = 0..97.
+    if (wave < nh) {
+        const int h = wave;
+        uint32_t lo = 0, hi = 0;
 #pragma unroll
-        for (int w = 0; w < kColWaves; ++w) t += s_hist[w][h][v];
-        const int hq = kvh * a.g + 4 * quad + h;
-        const int64_t row = (int64_t)seq * a.hq + hq;
-        a.chunk_hist[(row * a.n_chunks + chunk) * kBins + v] = t;
+        for (int w2 = 0; w2 < kColWaves; ++w2) {
+            lo += s_hist[w2][h][lane];
+            hi += lane < kBins - 64 ? s_hist[w2][h][64 + lane] : 0u;
+        }
+        uint32_t sl, sh;
+        wave_suffix97(lo, hi, lane, &sl, &sh);  // exact for v >= kLowCut
+        if (lane == 0) sl = (uint32_t)(c1 - c0);
+        if (lane >= 1 && lane < kLowCut) {
+            uint32_t t = 0;
+#pragma unroll
+            for (int w2 = 0; w2 < kColWaves; ++w2) t += s_low[w2][lane - 1][h];
+            sl = t;
+        }
+        uint32_t* dst = a.chunk_sfx + ((row0 + h) * a.n_chunks + chunk) * kSfx;
+        dst[lane] = sl;
+        if (lane < kSfx - 64) dst[64 + lane] = lane < kBins - 64 ? sh : 0u;
     }
+
 }
 
 // ---------------------------------------------------------------- threshold
 
-constexpr int kThrThreads = 256;
+constexpr int kThrThreads = 256;  // one wave per query head
 
 __global__ __launch_bounds__(kThrThreads) void threshold_kernel(RetrieveArgs a) {
-    __shared__ uint32_t s_hist[kBins];
-    __shared__ int s_theta;
-    __shared__ uint32_t s_wsum[kThrThreads / 64][2];
-    const int tid = threadIdx.x;
-    const int lane = tid & 63, wave = tid >> 6;
-    const int64_t row = blockIdx.x;
-    const uint32_t* ch = a.chunk_hist + row * a.n_chunks * kBins;
-
-    if (tid < kBins) {
-        uint32_t t = 0;
-        for (int64_t c = 0; c < a.n_chunks; ++c) t += ch[c * kBins + tid];
-        s_hist[tid] = t;
+    const int lane = threadIdx.x & 63;
+    const int64_t row = (int64_t)blockIdx.x * (kThrThreads / 64) + (threadIdx.x >> 6);
+    if (row >= (int64_t)a.batch * a.hq) return;
+    const uint32_t* sfx = a.chunk_sfx + row * a.n_chunks * kSfx;
+    // Whole-row suffix histogram; lane holds v = lane and v = 64 + lane.
+    uint32_t tl = 0, th = 0;
+    for (int64_t c = 0; c < a.n_chunks; ++c) {
+        tl += sfx[c * kSfx + lane];
+        if (lane < kSfx - 64) th += sfx[c * kSfx + 64 + lane];
     }
-    __syncthreads();
-    if (tid == 0) {
-        const uint32_t C = (uint32_t)a.c_eff;
-        uint32_t acc = 0;
-        int theta = 0;
-        for (int v = kMaxScore; v >= 0; --v) {
-            acc += s_hist[v];
-            if (acc >= C) { theta = v; break; }
-        }
-        const uint32_t gt = acc - s_hist[theta];
-        s_theta = theta;
-        int32_t* th = a.thresh + row * 4;
-        th[0] = theta;
-        th[1] = (int32_t)gt;
-        th[2] = (int32_t)(C - gt);
-        th[3] = (int32_t)C;
+    const uint32_t C = (uint32_t)a.c_eff;
+    // theta = largest v with #{S >= v} >= C (suffix counts fall with v; #{S >= 0} = n >= C).
+    const uint64_t ok_lo = __ballot(tl >= C);
+    const uint64_t ok_hi = __ballot(lane < kBins - 64 && th >= C);
+    const int theta = ok_hi ? 64 + (63 - __clzll(ok_hi)) : (63 - __clzll(ok_lo));
+    const uint32_t gt = theta + 1 < 64 ? __shfl(tl, theta + 1, 64) : __shfl(th, theta + 1 - 64, 64);
+    if (lane == 0) {
+        int32_t* t = a.thresh + row * 4;
+        t[0] = theta;
+        t[1] = (int32_t)gt;
+        t[2] = (int32_t)(C - gt);
+        t[3] = (int32_t)C;
     }
-    __syncthreads();
-    const int theta = s_theta;
-
-    // Exclusive prefix over chunks of (#S > theta, #S == theta).
+    // Keys with S > theta and S == theta in the chunks before each chunk.
     uint32_t carry_g = 0, carry_e = 0;
-    for (int64_t c0 = 0; c0 < a.n_chunks; c0 += kThrThreads) {
-        const int64_t c = c0 + tid;
+    for (int64_t cb = 0; cb < a.n_chunks; cb += 64) {
+        const int64_t c = cb + lane;
         uint32_t g = 0, e = 0;
         if (c < a.n_chunks) {
-            for (int v = theta + 1; v <= kMaxScore; ++v) g += ch[c * kBins + v];
-            e = ch[c * kBins + theta];
+            g = sfx[c * kSfx + theta + 1];
+            e = sfx[c * kSfx + theta] - g;
         }
         const uint32_t ig = wave_incl_scan_u32(g, lane);
         const uint32_t ie = wave_incl_scan_u32(e, lane);
-        if (lane == 63) { s_wsum[wave][0] = ig; s_wsum[wave][1] = ie; }
-        __syncthreads();
-        uint32_t pg = carry_g, pe = carry_e;
-        for (int w = 0; w < wave; ++w) { pg += s_wsum[w][0]; pe += s_wsum[w][1]; }
         if (c < a.n_chunks) {
-            int32_t* cb = a.chunk_base + (row * a.n_chunks + c) * 2;
-            cb[0] = (int32_t)(pg + ig - g);
-            cb[1] = (int32_t)(pe + ie - e);
+            int32_t* cbp = a.chunk_base + (row * a.n_chunks + c) * 2;
+            cbp[0] = (int32_t)(carry_g + ig - g);
+            cbp[1] = (int32_t)(carry_e + ie - e);
         }
-        for (int w = 0; w < kThrThreads / 64; ++w) { carry_g += s_wsum[w][0]; carry_e += s_wsum[w][1]; }
-        __syncthreads();
+        carry_g += __shfl(ig, 63, 64);
+        carry_e += __shfl(ie, 63, 64);
     }
 }
 
@@ -379,8 +443,9 @@ hipError_t launch_collide(const RetrieveArgs& a, hipStream_t s) {
 }
 
 hipError_t launch_threshold(const RetrieveArgs& a, hipStream_t s) {
+    const int64_t rows = (int64_t)a.batch * a.hq;
     prof_begin("threshold", s);
-    hipLaunchKernelGGL(threshold_kernel, dim3((unsigned)(a.batch * a.hq)), dim3(kThrThreads), 0, s, a);
+    hipLaunchKernelGGL(threshold_kernel, dim3((unsigned)((rows + 3) / 4)), dim3(kThrThreads), 0, s, a);
     prof_end(s);
     return hipGetLastError();
 }

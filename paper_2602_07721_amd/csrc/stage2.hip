@@ -15,10 +15,11 @@
 // subspaces in registers; the signed level table (16 floats) lives in LDS
 // and is read with at most 16 distinct addresses per instruction.
 //
-// topk_kernel: one block per query head.  Exact radix select (8-bit digits)
-// of the k-th largest estimate on order-preserving uint32 keys, ties at the
-// threshold taken in candidate order (= ascending key index), then a bitonic
-// sort of the k winners by (estimate desc, index asc).
+// topk_kernel: one block per query head.  Exact radix select (8-bit digits,
+// taken from the top of the occupied [min, max] key range so the histograms
+// spread) of the k-th largest estimate on order-preserving uint32 keys, ties
+// at the threshold taken in candidate order, then an ordered compaction: the
+// winners come out in ascending key index (candidate order), no sort.
 
 #include "internal.hpp"
 
@@ -93,7 +94,6 @@ __global__ __launch_bounds__(kRrThreads) void rerank_kernel(RetrieveArgs a) {
 // ---------------------------------------------------------------- top-k
 
 constexpr int kTkThreads = 1024;
-constexpr int kTopkLds = 2048;  // largest k served (power of two)
 constexpr int kTkWaves = kTkThreads / 64;
 
 __device__ __forceinline__ uint32_t order_key(float f) {
@@ -137,8 +137,8 @@ template <int EPT>
 __global__ __launch_bounds__(kTkThreads) void topk_kernel(RetrieveArgs a) {
     __shared__ uint32_t s_hist[256];
     __shared__ uint32_t s_w[kTkWaves];
+    __shared__ uint32_t s_mm[2][kTkWaves];
     __shared__ uint32_t s_digit, s_need;
-    __shared__ uint64_t s_sel[kTopkLds];
 
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int64_t row = blockIdx.x;
@@ -147,25 +147,49 @@ __global__ __launch_bounds__(kTkThreads) void topk_kernel(RetrieveArgs a) {
     const float* sc = a.cand_score + row * a.n_cand;
     const int32_t* cand = a.cand + row * a.n_cand;
 
+    // Order-preserving keys of this thread's contiguous run of candidates.
     uint32_t key[EPT];
+    uint32_t kmin = 0xffffffffu, kmax = 0u;
 #pragma unroll
     for (int e = 0; e < EPT; ++e) {
         const int p = tid * EPT + e;
         key[e] = p < C ? order_key(sc[p]) : 0u;  // valid keys are all > 0
+        if (p < C) {
+            kmin = min(kmin, key[e]);
+            kmax = max(kmax, key[e]);
+        }
+    }
+#pragma unroll
+    for (int d = 1; d < 64; d <<= 1) {
+        kmin = min(kmin, (uint32_t)__shfl_xor(kmin, d, 64));
+        kmax = max(kmax, (uint32_t)__shfl_xor(kmax, d, 64));
+    }
+    if (lane == 0) { s_mm[0][wave] = kmin; s_mm[1][wave] = kmax; }
+    __syncthreads();
+#pragma unroll
+    for (int w = 0; w < kTkWaves; ++w) {
+        kmin = min(kmin, s_mm[0][w]);
+        kmax = max(kmax, s_mm[1][w]);
     }
 
-    // Radix select of the kk-th largest key.
+    // Radix select of the kk-th largest u = key - kmin, 8-bit digits from the top
+    // of the occupied range (so the first histogram is spread over the data).
+    const uint32_t range = kmax - kmin;
+    const int nbits = range ? 32 - __clz(range) : 0;
     uint32_t prefix = 0, mask = 0, need = (uint32_t)kk;
+    int shift = nbits > 8 ? nbits - 8 : 0;
 #pragma unroll 1
-    for (int shift = 24; shift >= 0; shift -= 8) {
+    for (int pass = 0; pass < 4 && nbits > 0; ++pass) {
         if (tid < 256) s_hist[tid] = 0;
         __syncthreads();
 #pragma unroll
-        for (int e = 0; e < EPT; ++e)
-            if (key[e] != 0u && (key[e] & mask) == prefix) atomicAdd(&s_hist[(key[e] >> shift) & 255u], 1u);
+        for (int e = 0; e < EPT; ++e) {
+            const uint32_t u = key[e] - kmin;
+            if (key[e] != 0u && (u & mask) == prefix) atomicAdd(&s_hist[(u >> shift) & 255u], 1u);
+        }
         __syncthreads();
         if (wave == 0) {
-            // Suffix sums over digits 255..0: lane L owns digits 252-4L..255-4L.
+            // Suffix sums over digits 255..0: lane L owns digits 255-4L..252-4L.
             uint32_t h[4];
             uint32_t tot = 0;
 #pragma unroll
@@ -186,9 +210,11 @@ __global__ __launch_bounds__(kTkThreads) void topk_kernel(RetrieveArgs a) {
         mask |= 255u << shift;
         need = s_need;
         __syncthreads();
+        if (shift == 0) break;
+        shift = shift > 8 ? shift - 8 : 0;
     }
-    const uint32_t T = prefix;      // the kk-th largest key value
-    const uint32_t quota = need;    // how many keys equal to T are taken
+    const uint32_t T = kmin + prefix;  // the kk-th largest key value
+    const uint32_t quota = need;       // how many keys equal to T are taken
 
     uint32_t n_eq = 0;
 #pragma unroll
@@ -208,46 +234,23 @@ __global__ __launch_bounds__(kTkThreads) void topk_kernel(RetrieveArgs a) {
         n_sel += s ? 1u : 0u;
     }
     uint32_t pos = block_excl_scan(n_sel, s_w, &tot);
-
-    int kpad = 1;
-    while (kpad < kk) kpad <<= 1;
-    for (int i = tid; i < kpad; i += kTkThreads) s_sel[i] = 0ull;
-    __syncthreads();
+    // Winners in candidate order, i.e. ascending key index.
+    int32_t* oi = a.out_idx + row * a.top_k;
+    float* os = a.out_score ? a.out_score + row * a.top_k : nullptr;
 #pragma unroll
     for (int e = 0; e < EPT; ++e) {
         if ((selmask >> e) & 1ull) {
             const int p = tid * EPT + e;
-            const uint32_t idx = (uint32_t)cand[p];
-            if (pos < (uint32_t)kpad) s_sel[pos] = ((uint64_t)key[e] << 32) | (uint64_t)(0xffffffffu - idx);
+            if (pos < (uint32_t)kk) {
+                oi[pos] = cand[p];
+                if (os) os[pos] = key_float(key[e]);
+            }
             ++pos;
         }
     }
-    __syncthreads();
-    // Bitonic sort of kpad entries, descending.
-    for (int k = 2; k <= kpad; k <<= 1) {
-        for (int j = k >> 1; j > 0; j >>= 1) {
-            for (int i = tid; i < kpad; i += kTkThreads) {
-                const int l2 = i ^ j;
-                if (l2 > i) {
-                    const uint64_t x0 = s_sel[i], x1 = s_sel[l2];
-                    const bool desc = (i & k) == 0;
-                    if (desc ? (x0 < x1) : (x0 > x1)) { s_sel[i] = x1; s_sel[l2] = x0; }
-                }
-            }
-            __syncthreads();
-        }
-    }
-    int32_t* oi = a.out_idx + row * a.top_k;
-    float* os = a.out_score ? a.out_score + row * a.top_k : nullptr;
-    for (int r = tid; r < a.top_k; r += kTkThreads) {
-        if (r < kk) {
-            const uint64_t v = s_sel[r];
-            oi[r] = (int32_t)(0xffffffffu - (uint32_t)(v & 0xffffffffu));
-            if (os) os[r] = key_float((uint32_t)(v >> 32));
-        } else {
-            oi[r] = -1;
-            if (os) os[r] = -__builtin_huge_valf();
-        }
+    for (int r = kk + tid; r < a.top_k; r += kTkThreads) {
+        oi[r] = -1;
+        if (os) os[r] = -__builtin_huge_valf();
     }
 }
 

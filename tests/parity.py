@@ -171,10 +171,13 @@ def check_head(inter, seq, kvh, g, q_per_kv, q, oracle, signs, budget, n):
     for i in set(gi.tolist()) ^ set(int(x) for x in r["idx"][:kk]):
         p = pos[i]
         assert abs(o_sc[p] - kth) <= tol[p] + kth_tol, (i, o_sc[p], kth)
-    # the GPU's own ordering: estimates descending, ties by ascending index
-    assert np.all(np.diff(gsc) <= 0)
-    ties = np.flatnonzero(np.diff(gsc) == 0)
-    assert np.all(gi[ties] < gi[ties + 1])
+    # the winners are listed in ascending key index
+    assert np.all(np.diff(gi) > 0)
+    # and are exactly the top kk of the GPU's own float32 estimates (ties: lower index)
+    gcs = inter["cand_score"][seq, hq, :C]
+    own = np.sort(r["cand"][np.lexsort((r["cand"], -gcs.astype(np.float64)))[:kk]])
+    np.testing.assert_array_equal(gi, own)
+    np.testing.assert_array_equal(gsc.astype(np.float32), gcs[[pos[int(i)] for i in gi]])
     g_at = np.array([tol[pos[int(i)]] for i in gi])
     g_ref = np.array([o_sc[pos[int(i)]] for i in gi])
     assert np.all(np.abs(gsc - g_ref) <= g_at + 1e-30)

@@ -112,7 +112,7 @@ def test_workspace_layout_is_consistent():
     lay = pk.workspace_layout(cfg, 2, 4000, b)
     assert lay["total"] == pk.retrieve_workspace_size(cfg, 2, 4000, b)
     assert lay["n_pad"] == 4032 and lay["n_chunks"] == 1 and lay["c_eff"] == 512 and lay["quads"] == 1
-    offs = [lay[k] for k in ("zq", "lut", "score8", "chunk_hist", "chunk_base", "thresh", "cand",
+    offs = [lay[k] for k in ("zq", "lut", "score8", "chunk_sfx", "chunk_base", "thresh", "cand",
                              "cand_score")]
     assert offs == sorted(offs) and all(o % 256 == 0 for o in offs) and lay["total"] > offs[-1]
     assert lay["score8"] - lay["lut"] >= 2 * 8 * 1 * 16 * 256 * 4

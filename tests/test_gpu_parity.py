@@ -233,7 +233,7 @@ def test_batch8_128k_sampled_at_full_size():
             sel = S[s, hq, cand[s, hq]]
             assert sel.min() >= th[s, hq, 0]
             assert np.sum(S[s, hq] > th[s, hq, 0]) == th[s, hq, 1]
-    assert np.all(np.diff(inter["score"], axis=-1) <= 0)
+    assert np.all(np.diff(inter["idx"], axis=-1) > 0)
     # two whole groups through the oracle
     for s, h in ((0, 0), (5, 3)):
         orc = oracle_group(K[s, h], signs)

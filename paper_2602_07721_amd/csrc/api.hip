@@ -363,8 +363,7 @@ int pariskv_retrieve(const pariskv_config* cfg, const pariskv_index* index, cons
     if ((e = launch_query_lut(a, s)) != hipSuccess) return hip_fail(e, "query_lut launch");
     if ((e = launch_collide(a, s)) != hipSuccess) return hip_fail(e, "collide launch");
     if ((e = launch_threshold(a, s)) != hipSuccess) return hip_fail(e, "threshold launch");
-    if ((e = launch_compact(a, s)) != hipSuccess) return hip_fail(e, "compact launch");
-    if ((e = launch_rerank(a, s)) != hipSuccess) return hip_fail(e, "rerank launch");
+    if ((e = launch_compact_rerank(a, s)) != hipSuccess) return hip_fail(e, "compact_rerank launch");
     if ((e = launch_topk(a, s)) != hipSuccess) return hip_fail(e, "topk launch");
     return PARISKV_OK;
 }

@@ -5,11 +5,11 @@
 //
 //   o = sum_{i in idx} softmax_i(scale <k_i, q>) v_i,  fp16 in, fp32 math.
 //
-// One block per query head, 4 waves.  A wave works on 4 keys at a time, 16
+// One block per query head, 16 waves.  A wave works on 4 keys at a time, 16
 // lanes per key: lane l16 owns dims [8 l16, 8 l16 + 8), so each K or V row is
 // one 256-byte contiguous read by 16 lanes.  Indices outside
-// [0, kv_capacity) are skipped like -1.  Every (wave, key slot) keeps an
-// online-softmax state (running max, sum, 8 accumulators per lane); the 16
+// [0, kv_capacity) are skipped like -1.  Every one of the 64 key slots keeps
+// an online-softmax state (running max, sum, 8 accumulators per lane); the
 // states are merged in LDS at the end.  The row's indices are staged in LDS
 // first and every lane keeps 4 K and 4 V row segments in flight.
 
@@ -21,7 +21,7 @@ namespace pariskv {
 
 namespace {
 
-constexpr int kAtThreads = 256;
+constexpr int kAtThreads = 1024;
 constexpr int kAtGroups = kAtThreads / 16;  // concurrent key slots per block
 constexpr int kAtUnroll = 4;                // K/V rows in flight per lane
 constexpr int kAtMaxK = 4096;               // largest k a block stages in LDS
@@ -48,7 +48,7 @@ __global__ __launch_bounds__(kAtThreads) void attend_kernel(const __half* __rest
     __shared__ int32_t s_idx[kAtMaxK];
 
     const int tid = threadIdx.x;
-    const int grp16 = tid >> 4;      // key slot 0..15
+    const int grp16 = tid >> 4;      // key slot 0 .. kAtGroups-1
     const int l16 = tid & 15;
     const int64_t row = blockIdx.x;  // seq * hq + head
     const int seq = (int)(row / hq);
@@ -73,7 +73,7 @@ __global__ __launch_bounds__(kAtThreads) void attend_kernel(const __half* __rest
 #pragma unroll
     for (int d = 0; d < 8; ++d) acc[d] = 0.f;
 
-    // Slot grp16 takes keys grp16, grp16 + 16, ...; kAtUnroll rows in flight per lane.
+    // Slot grp16 takes keys grp16, grp16 + kAtGroups, ...; kAtUnroll rows in flight per lane.
     for (int base = 0; base < k; base += kAtGroups * kAtUnroll) {
         int32_t key[kAtUnroll];
         uint4 kc[kAtUnroll], vc[kAtUnroll];

@@ -73,8 +73,7 @@ struct RetrieveArgs {
 hipError_t launch_query_lut(const RetrieveArgs& a, hipStream_t s);
 hipError_t launch_collide(const RetrieveArgs& a, hipStream_t s);
 hipError_t launch_threshold(const RetrieveArgs& a, hipStream_t s);
-hipError_t launch_compact(const RetrieveArgs& a, hipStream_t s);
-hipError_t launch_rerank(const RetrieveArgs& a, hipStream_t s);
+hipError_t launch_compact_rerank(const RetrieveArgs& a, hipStream_t s);
 hipError_t launch_topk(const RetrieveArgs& a, hipStream_t s);
 hipError_t launch_pad_outputs(const RetrieveArgs& a, hipStream_t s);
 

@@ -16,15 +16,16 @@
 //   collide_kernel     streams the 16 id bytes of every key once per quad of
 //                      query heads, sums 16 packed LDS lookups (4 head scores in
 //                      the 4 bytes of one uint32; each is at most 96, so no
-//                      carries), writes S as bytes per head and a suffix
+//                      carries), writes S as bytes per head (64 consecutive
+//                      bytes per wave store) and a suffix
 //                      histogram #{S >= v} per head and 4096-key chunk (frequent
-//                      low scores counted by wave ballots, the rest by LDS atomics).
-//   threshold_kernel   one wave per query head: theta = largest v with
+//                      low scores counted in per-lane registers, the rest by LDS
+//                      atomics).
+//   threshold_kernel   one block per query head: theta = largest v with
 //                      #{S >= v} >= C_eff, the quota of S == theta keys, and per
 //                      chunk the number of S > theta / S == theta keys in
 //                      earlier chunks.
-//   compact_kernel     writes candidate indices in ascending key order: all
-//                      S > theta and the first `quota` S == theta keys.
+// The compaction of the candidates lives with the rerank (stage2.hip).
 
 #include <hip/hip_fp16.h>
 
@@ -177,7 +178,7 @@ __global__ __launch_bounds__(kLutThreads) void query_lut_kernel(RetrieveArgs a) 
 constexpr int kColThreads = 256;
 constexpr int kColWaves = kColThreads / 64;
 constexpr int kColKeysPerIter = 4 * kColThreads;  // 4 keys per thread per iteration
-constexpr int kLowCut = 4;  // scores below this are counted by ballot, not by LDS atomics
+constexpr int kLowCut = 4;  // scores below this are counted in registers, not by LDS atomics
 
 // Suffix sums of a 97-bin histogram held as (lo = bins 0..63 by lane, hi = bins
 // 64..96 by lane < 33): returns (sfx_lo, sfx_hi) with sfx[v] = sum_{u >= v} h[u].
@@ -200,8 +201,7 @@ __device__ __forceinline__ void wave_suffix97(uint32_t lo, uint32_t hi, int lane
 
 __global__ __launch_bounds__(kColThreads) void collide_kernel(RetrieveArgs a) {
     __shared__ uint32_t s_lut[kB * kCentroids];
-    __shared__ uint32_t s_hist[kColWaves][4][kBins + 3];
-    __shared__ uint32_t s_pack[kColKeysPerIter];
+    __shared__ uint32_t s_hist[4][kBins + 3];
     __shared__ uint32_t s_low[kColWaves][kLowCut - 1][4];
 
     const int tid = threadIdx.x;
@@ -219,17 +219,17 @@ __global__ __launch_bounds__(kColThreads) void collide_kernel(RetrieveArgs a) {
     const uint4* lsrc = reinterpret_cast<const uint4*>(a.lut + gq * (kB * kCentroids));
     for (int i = tid; i < kB * kCentroids / 4; i += kColThreads)
         reinterpret_cast<uint4*>(s_lut)[i] = lsrc[i];
-    for (int i = tid; i < kColWaves * 4 * (kBins + 3); i += kColThreads) (&s_hist[0][0][0])[i] = 0;
+    for (int i = tid; i < 4 * (kBins + 3); i += kColThreads) (&s_hist[0][0])[i] = 0;
     __syncthreads();
 
     const uint8_t* ids = a.ids + grp * a.capacity * kB;
     const int64_t c0 = chunk * kChunk;
     const int64_t c1 = min(c0 + (int64_t)kChunk, a.n);
-    uint32_t low[kLowCut - 1][4];  // wave-uniform: #{S >= v} for v = 1 .. kLowCut-1, per head
+    // Per-lane SWAR counters: byte h of cnt[v-1] = #{keys of this lane with S_h >= v}
+    // for v = 1 .. kLowCut-1 (a lane sees at most kChunk / kColThreads = 16 keys).
+    uint32_t cnt[kLowCut - 1];
 #pragma unroll
-    for (int v = 0; v < kLowCut - 1; ++v)
-#pragma unroll
-        for (int h = 0; h < 4; ++h) low[v][h] = 0;
+    for (int v = 0; v < kLowCut - 1; ++v) cnt[v] = 0;
 
     for (int64_t base = c0; base < c1; base += kColKeysPerIter) {
         // Key base + tid + 256 j: one 16-byte id row per lane, a wave reads 1 KiB contiguous.
@@ -248,64 +248,54 @@ __global__ __launch_bounds__(kColThreads) void collide_kernel(RetrieveArgs a) {
             for (int b = 0; b < kB; ++b)
                 acc += s_lut[b * kCentroids + ((ww[b >> 2] >> (8 * (b & 3))) & 0xffu)];
             const bool live = i < c1;
-            acc = live ? acc : 0u;
-            // Low scores are frequent: #{S >= v} for v < kLowCut is counted for all 4
-            // heads at once with a byte-wise compare ((x | 0x80) - v has its top bit set
-            // iff x >= v, for bytes below 128) and one wave ballot per head.
+            acc = live ? acc : 0u;  // a key past the end scores 0 for every head
+            // Low scores are frequent: count #{S >= v} for v < kLowCut for the 4 heads at
+            // once.  Bytes are at most 96, so (S | 0x80) - v keeps its top bit iff S >= v
+            // and no borrow crosses a byte.
+            const uint32_t x = acc | 0x80808080u;
 #pragma unroll
-            for (int v = 1; v < kLowCut; ++v) {
-                const uint32_t ge = ((acc | 0x80808080u) - (uint32_t)v * 0x01010101u) & 0x80808080u;
-#pragma unroll
-                for (int h = 0; h < 4; ++h)
-                    low[v - 1][h] += (uint32_t)__popcll(__ballot(live && ((ge >> (8 * h + 7)) & 1u)));
-            }
-            // Higher scores are rare and spread out: exact per-value LDS histogram.
+            for (int v = 1; v < kLowCut; ++v)
+                cnt[v - 1] += ((x - (uint32_t)v * 0x01010101u) & 0x80808080u) >> 7;
+            // Higher scores are rare and spread out: exact per-value LDS histogram.  Slots
+            // of the last quad without a head have an all-zero bonus table, so score 0.
 #pragma unroll
             for (int h = 0; h < 4; ++h) {
                 const uint32_t sh = (acc >> (8 * h)) & 0xffu;
-                if (h < nh && live && sh >= (uint32_t)kLowCut) atomicAdd(&s_hist[wave][h][sh], 1u);
+                if (sh >= (uint32_t)kLowCut) atomicAdd(&s_hist[h][sh], 1u);
             }
-            s_pack[tid + kColThreads * j] = acc;
-        }
-        __syncthreads();
-        // Thread t now writes keys base + 4t .. 4t+3 for every head: transpose 4 keys x 4
-        // heads of bytes into one word per head.
-        const int64_t k4 = base + 4 * tid;
-        if (k4 < c1) {
-            const uint4 sp = reinterpret_cast<const uint4*>(s_pack)[tid];
-            const uint32_t lo01 = __builtin_amdgcn_perm(sp.y, sp.x, 0x05010400u);
-            const uint32_t hi01 = __builtin_amdgcn_perm(sp.y, sp.x, 0x07030602u);
-            const uint32_t lo23 = __builtin_amdgcn_perm(sp.w, sp.z, 0x05010400u);
-            const uint32_t hi23 = __builtin_amdgcn_perm(sp.w, sp.z, 0x07030602u);
-            uint32_t o[4];
-            o[0] = __builtin_amdgcn_perm(lo23, lo01, 0x05040100u);
-            o[1] = __builtin_amdgcn_perm(lo23, lo01, 0x07060302u);
-            o[2] = __builtin_amdgcn_perm(hi23, hi01, 0x05040100u);
-            o[3] = __builtin_amdgcn_perm(hi23, hi01, 0x07060302u);
+            // A wave stores 64 consecutive score bytes of a head per instruction.
+            if (live) {
 #pragma unroll
-            for (int h = 0; h < 4; ++h)
-                if (h < nh) *reinterpret_cast<uint32_t*>(a.score8 + (row0 + h) * a.n_pad + k4) = o[h];
+                for (int h = 0; h < 4; ++h)
+                    if (h < nh) a.score8[(row0 + h) * a.n_pad + i] = (uint8_t)(acc >> (8 * h));
+            }
         }
-        __syncthreads();
     }
 
-    if (lane == 0) {
+    // Block totals of the low counts: widen the bytes to 16-bit fields (heads 0, 2 and
+    // heads 1, 3; a wave sums at most 64 * 16 per field) and reduce across the wave.
 #pragma unroll
-        for (int v = 0; v < kLowCut - 1; ++v)
+    for (int v = 0; v < kLowCut - 1; ++v) {
+        uint32_t e = cnt[v] & 0x00ff00ffu, o = (cnt[v] >> 8) & 0x00ff00ffu;
 #pragma unroll
-            for (int h = 0; h < 4; ++h) s_low[wave][v][h] = low[v][h];
+        for (int d = 1; d < 64; d <<= 1) {
+            e += __shfl_xor(e, d, 64);
+            o += __shfl_xor(o, d, 64);
+        }
+        if (lane == 0) {
+            s_low[wave][v][0] = e & 0xffffu;
+            s_low[wave][v][1] = o & 0xffffu;
+            s_low[wave][v][2] = e >> 16;
+            s_low[wave][v][3] = o >> 16;
+        }
     }
     __syncthreads();
 
     // Per-chunk suffix histogram of every head: sfx[v] = #{keys in chunk : S >= v}, v = 0..97.
     if (wave < nh) {
         const int h = wave;
-        uint32_t lo = 0, hi = 0;
-#pragma unroll
-        for (int w2 = 0; w2 < kColWaves; ++w2) {
-            lo += s_hist[w2][h][lane];
-            hi += lane < kBins - 64 ? s_hist[w2][h][64 + lane] : 0u;
-        }
+        const uint32_t lo = s_hist[h][lane];
+        const uint32_t hi = lane < kBins - 64 ? s_hist[h][64 + lane] : 0u;
         uint32_t sl, sh;
         wave_suffix97(lo, hi, lane, &sl, &sh);  // exact for v >= kLowCut
         if (lane == 0) sl = (uint32_t)(c1 - c0);
@@ -324,25 +314,44 @@ __global__ __launch_bounds__(kColThreads) void collide_kernel(RetrieveArgs a) {
 
 // ---------------------------------------------------------------- threshold
 
-constexpr int kThrThreads = 256;  // one wave per query head
+constexpr int kThrThreads = 256;  // one block per query head
 
 __global__ __launch_bounds__(kThrThreads) void threshold_kernel(RetrieveArgs a) {
-    const int lane = threadIdx.x & 63;
-    const int64_t row = (int64_t)blockIdx.x * (kThrThreads / 64) + (threadIdx.x >> 6);
-    if (row >= (int64_t)a.batch * a.hq) return;
+    __shared__ uint32_t s_part[kThrThreads / 64][2][64];
+    const int tid = threadIdx.x;
+    const int lane = tid & 63, wave = tid >> 6;
+    const int64_t row = blockIdx.x;
     const uint32_t* sfx = a.chunk_sfx + row * a.n_chunks * kSfx;
-    // Whole-row suffix histogram; lane holds v = lane and v = 64 + lane.
-    uint32_t tl = 0, th = 0;
-    for (int64_t c = 0; c < a.n_chunks; ++c) {
-        tl += sfx[c * kSfx + lane];
-        if (lane < kSfx - 64) th += sfx[c * kSfx + 64 + lane];
+    // Whole-row suffix histogram; lane holds v = lane and v = 64 + lane.  Each
+    // wave sums every 4th chunk with 8 independent loads in flight.
+    uint32_t tl[8], th[8];
+#pragma unroll
+    for (int u = 0; u < 8; ++u) tl[u] = th[u] = 0;
+    for (int64_t c0 = wave; c0 < a.n_chunks; c0 += 4 * 8) {
+#pragma unroll
+        for (int u = 0; u < 8; ++u) {
+            const int64_t c = c0 + 4 * u;
+            if (c < a.n_chunks) {
+                tl[u] += sfx[c * kSfx + lane];
+                if (lane < kSfx - 64) th[u] += sfx[c * kSfx + 64 + lane];
+            }
+        }
     }
+#pragma unroll
+    for (int u = 1; u < 8; ++u) { tl[0] += tl[u]; th[0] += th[u]; }
+    s_part[wave][0][lane] = tl[0];
+    s_part[wave][1][lane] = th[0];
+    __syncthreads();
+    if (wave != 0) return;
+    uint32_t ttl = 0, tth = 0;
+#pragma unroll
+    for (int w = 0; w < kThrThreads / 64; ++w) { ttl += s_part[w][0][lane]; tth += s_part[w][1][lane]; }
     const uint32_t C = (uint32_t)a.c_eff;
     // theta = largest v with #{S >= v} >= C (suffix counts fall with v; #{S >= 0} = n >= C).
-    const uint64_t ok_lo = __ballot(tl >= C);
-    const uint64_t ok_hi = __ballot(lane < kBins - 64 && th >= C);
+    const uint64_t ok_lo = __ballot(ttl >= C);
+    const uint64_t ok_hi = __ballot(lane < kBins - 64 && tth >= C);
     const int theta = ok_hi ? 64 + (63 - __clzll(ok_hi)) : (63 - __clzll(ok_lo));
-    const uint32_t gt = theta + 1 < 64 ? __shfl(tl, theta + 1, 64) : __shfl(th, theta + 1 - 64, 64);
+    const uint32_t gt = theta + 1 < 64 ? __shfl(ttl, theta + 1, 64) : __shfl(tth, theta + 1 - 64, 64);
     if (lane == 0) {
         int32_t* t = a.thresh + row * 4;
         t[0] = theta;
@@ -371,59 +380,6 @@ __global__ __launch_bounds__(kThrThreads) void threshold_kernel(RetrieveArgs a) 
     }
 }
 
-// ---------------------------------------------------------------- compaction
-
-constexpr int kCmpThreads = 256;  // 16 keys per thread, one chunk per block
-
-__global__ __launch_bounds__(kCmpThreads) void compact_kernel(RetrieveArgs a) {
-    __shared__ uint32_t s_wsum[kCmpThreads / 64];
-    const int tid = threadIdx.x;
-    const int lane = tid & 63, wave = tid >> 6;
-    const int64_t chunk = blockIdx.x;
-    const int64_t row = blockIdx.y;
-    const int32_t* th = a.thresh + row * 4;
-    const uint32_t theta = (uint32_t)th[0];
-    const uint32_t quota = (uint32_t)th[2];
-    const int32_t* cb = a.chunk_base + (row * a.n_chunks + chunk) * 2;
-    const uint32_t base_g = (uint32_t)cb[0], base_e = (uint32_t)cb[1];
-
-    const int64_t i0 = chunk * kChunk + 16 * tid;
-    uint32_t gmask = 0, emask = 0;
-    uint8_t sv[16];
-    if (i0 < a.n) {
-        const uint4 w = *reinterpret_cast<const uint4*>(a.score8 + row * a.n_pad + i0);
-        const uint32_t ww[4] = {w.x, w.y, w.z, w.w};
-#pragma unroll
-        for (int j = 0; j < 16; ++j) {
-            sv[j] = (uint8_t)((ww[j >> 2] >> (8 * (j & 3))) & 0xffu);
-            const bool in = i0 + j < a.n;
-            gmask |= (in && sv[j] > theta ? 1u : 0u) << j;
-            emask |= (in && sv[j] == theta ? 1u : 0u) << j;
-        }
-    }
-    // Packed (gt, eq) counts: each at most 4096 per chunk, 16 bits each.
-    const uint32_t mine = (uint32_t)__popc(gmask) | ((uint32_t)__popc(emask) << 16);
-    const uint32_t incl = wave_incl_scan_u32(mine, lane);
-    if (lane == 63) s_wsum[wave] = incl;
-    __syncthreads();
-    uint32_t pre = incl - mine;
-    for (int w = 0; w < wave; ++w) pre += s_wsum[w];
-    uint32_t gb = base_g + (pre & 0xffffu);
-    uint32_t eb = base_e + (pre >> 16);
-    int32_t* cand = a.cand + row * a.n_cand;
-#pragma unroll
-    for (int j = 0; j < 16; ++j) {
-        if ((gmask >> j) & 1u) {
-            const uint32_t p = gb + min(eb, quota);
-            if (p < (uint32_t)a.c_eff) cand[p] = (int32_t)(i0 + j);
-            ++gb;
-        } else if ((emask >> j) & 1u) {
-            if (eb < quota && gb + eb < (uint32_t)a.c_eff) cand[gb + eb] = (int32_t)(i0 + j);
-            ++eb;
-        }
-    }
-}
-
 }  // namespace
 
 hipError_t launch_query_lut(const RetrieveArgs& a, hipStream_t s) {
@@ -445,17 +401,10 @@ hipError_t launch_collide(const RetrieveArgs& a, hipStream_t s) {
 hipError_t launch_threshold(const RetrieveArgs& a, hipStream_t s) {
     const int64_t rows = (int64_t)a.batch * a.hq;
     prof_begin("threshold", s);
-    hipLaunchKernelGGL(threshold_kernel, dim3((unsigned)((rows + 3) / 4)), dim3(kThrThreads), 0, s, a);
+    hipLaunchKernelGGL(threshold_kernel, dim3((unsigned)rows), dim3(kThrThreads), 0, s, a);
     prof_end(s);
     return hipGetLastError();
 }
 
-hipError_t launch_compact(const RetrieveArgs& a, hipStream_t s) {
-    prof_begin("compact", s);
-    hipLaunchKernelGGL(compact_kernel, dim3((unsigned)a.n_chunks, (unsigned)(a.batch * a.hq)),
-                       dim3(kCmpThreads), 0, s, a);
-    prof_end(s);
-    return hipGetLastError();
-}
 
 }  // namespace pariskv

@@ -8,14 +8,17 @@
 // where v_b has coordinates sign * a[t] decoded from the 4-bit codes.  The
 // query side z/D arrives as float from the query kernel.
 //
-// rerank_kernel: 8 lanes per candidate; lane l reads the 16-byte chunk l of
-// the 128-byte record (codes of subspaces 2l, 2l+1 and their W), so one
-// candidate is one fully used 128-byte line and a wave reads 8 lines per
-// load instruction.  Lane l keeps the 16 query coordinates of its two
-// subspaces in registers; the signed level table (16 floats) lives in LDS
-// and is read with at most 16 distinct addresses per instruction.
+// compact_rerank_kernel: one block per (query head, 4096-key chunk).  It
+// selects the chunk's candidates (all S > theta, then S == theta in ascending
+// key order while the row's quota lasts), which occupy consecutive positions
+// of the row's candidate list, writes them, and scores them at once: 8 lanes
+// per candidate, lane l reads the 16-byte chunk l of the 128-byte record
+// (codes of subspaces 2l, 2l+1 and their W), so one candidate is one fully
+// used 128-byte line and a wave reads 8 lines per load instruction.  Lane l
+// keeps the 16 query coordinates of its two subspaces in registers; the
+// signed level table (16 floats) lives in LDS.
 //
-// topk_kernel: one block per query head.  Exact radix select (8-bit digits,
+// topk kernels: one block per query head.  Exact radix select (8-bit digits,
 // taken from the top of the occupied [min, max] key range so the histograms
 // spread) of the k-th largest estimate on order-preserving uint32 keys, ties
 // at the threshold taken in candidate order, then an ordered compaction: the
@@ -27,21 +30,46 @@ namespace pariskv {
 
 namespace {
 
-constexpr int kRrThreads = 256;
-constexpr int kRrSlots = kRrThreads / 8;    // candidates per block iteration
-constexpr int kRrTile = 8 * kRrSlots;       // candidates per block
+constexpr int kRrThreads = 256;           // one 4096-key chunk per block, 16 keys per thread
+constexpr int kRrSlots = kRrThreads / 8;  // candidates reranked per block iteration
+constexpr int kRrUnroll = 4;              // records in flight per lane
 
-__global__ __launch_bounds__(kRrThreads) void rerank_kernel(RetrieveArgs a) {
+__device__ __forceinline__ uint32_t wave_incl_scan32(uint32_t v, int lane) {
+#pragma unroll
+    for (int d = 1; d < 64; d <<= 1) {
+        uint32_t o = __shfl_up(v, d, 64);
+        if (lane >= d) v += o;
+    }
+    return v;
+}
+
+// Compaction of one chunk's candidates (Stage I selection) fused with their
+// RSQ-IP rerank (Stage II).  The selected keys of a chunk hold consecutive
+// positions [P0, P0 + m) of the row's ascending candidate list, so the block
+// writes them to `cand`, keeps them in LDS and scores them right away.
+__global__ __launch_bounds__(kRrThreads) void compact_rerank_kernel(RetrieveArgs a) {
     __shared__ float s_tab[16];
+    __shared__ uint32_t s_wsum[kRrThreads / 64];
+    __shared__ int32_t s_list[kChunk];
+
     const int tid = threadIdx.x;
-    const int l = tid & 7;
-    const int slot = tid >> 3;
-    const int64_t row = blockIdx.y;                 // seq * hq + hq
+    const int lane = tid & 63, wave = tid >> 6;
+    const int64_t chunk = blockIdx.x;
+    const int64_t row = blockIdx.y;  // seq * hq + head
     const int seq = (int)(row / a.hq);
     const int hq = (int)(row % a.hq);
     const int64_t grp = (int64_t)seq * a.hkv + hq / a.g;
 
-    if (tid < 16) s_tab[tid] = (tid & 8) ? -a.qc.a32[tid & 7] : a.qc.a32[tid & 7];
+    // Everything this block reads up front.
+    const int32_t* th = a.thresh + row * 4;
+    const uint32_t theta = (uint32_t)th[0];
+    const uint32_t quota = (uint32_t)th[2];
+    const int32_t* cb = a.chunk_base + (row * a.n_chunks + chunk) * 2;
+    const uint32_t base_g = (uint32_t)cb[0], base_e = (uint32_t)cb[1];
+    const int64_t i0 = chunk * kChunk + 16 * tid;
+    uint4 sw = make_uint4(0, 0, 0, 0);
+    if (i0 < a.n) sw = *reinterpret_cast<const uint4*>(a.score8 + row * a.n_pad + i0);
+    const int l = tid & 7;
     float z[16];
     {
         const float4* zp = reinterpret_cast<const float4*>(a.zq + row * kD + 16 * l);
@@ -51,50 +79,91 @@ __global__ __launch_bounds__(kRrThreads) void rerank_kernel(RetrieveArgs a) {
             z[4 * v] = t.x; z[4 * v + 1] = t.y; z[4 * v + 2] = t.z; z[4 * v + 3] = t.w;
         }
     }
+    if (tid < 16) s_tab[tid] = (tid & 8) ? -a.qc.a32[tid & 7] : a.qc.a32[tid & 7];
+
+    // ---- compaction: all S > theta, and S == theta while the row's quota lasts.
+    uint32_t gmask = 0, emask = 0;
+    {
+        const uint32_t ww[4] = {sw.x, sw.y, sw.z, sw.w};
+#pragma unroll
+        for (int j = 0; j < 16; ++j) {
+            const uint32_t sv = (ww[j >> 2] >> (8 * (j & 3))) & 0xffu;
+            const bool in = i0 + j < a.n;
+            gmask |= (in && sv > theta ? 1u : 0u) << j;
+            emask |= (in && sv == theta ? 1u : 0u) << j;
+        }
+    }
+    // Packed (gt, eq) counts: each at most 4096 per chunk, 16 bits each.
+    const uint32_t mine = (uint32_t)__popc(gmask) | ((uint32_t)__popc(emask) << 16);
+    const uint32_t incl = wave_incl_scan32(mine, lane);
+    if (lane == 63) s_wsum[wave] = incl;
+    __syncthreads();
+    uint32_t pre = incl - mine, tot = 0;
+#pragma unroll
+    for (int w = 0; w < kRrThreads / 64; ++w) {
+        const uint32_t x = s_wsum[w];
+        if (w < wave) pre += x;
+        tot += x;
+    }
+    const uint32_t P0 = base_g + min(base_e, quota);
+    const uint32_t m = (tot & 0xffffu) + (min(base_e + (tot >> 16), quota) - min(base_e, quota));
+    uint32_t gb = base_g + (pre & 0xffffu);
+    uint32_t eb = base_e + (pre >> 16);
+    int32_t* cand = a.cand + row * a.n_cand;
+#pragma unroll
+    for (int j = 0; j < 16; ++j) {
+        int64_t p = -1;
+        if ((gmask >> j) & 1u) {
+            p = gb + min(eb, quota);
+            ++gb;
+        } else if ((emask >> j) & 1u) {
+            if (eb < quota) p = gb + eb;
+            ++eb;
+        }
+        if (p >= 0 && p < a.c_eff) {
+            cand[p] = (int32_t)(i0 + j);
+            s_list[p - P0] = (int32_t)(i0 + j);
+        }
+    }
     __syncthreads();
 
-    const int32_t* cand = a.cand + row * a.n_cand;
-    float* out = a.cand_score + row * a.n_cand;
+    // ---- RSQ-IP: 8 lanes per candidate, lane l reads record chunk l (subspaces 2l, 2l+1).
+    const int slot = tid >> 3;
+    float* out = a.cand_score + row * a.n_cand + P0;
     const uint8_t* rec = a.rec + grp * a.capacity * kRec;
-    const int64_t t0 = (int64_t)blockIdx.x * kRrTile;
-
-    constexpr int kUnroll = 4;
 #pragma unroll 1
-    for (int it = 0; it < kRrTile / kRrSlots; it += kUnroll) {
-        uint4 chunk[kUnroll];
-        int64_t ci[kUnroll];
+    for (uint32_t it = 0; it < m; it += kRrSlots * kRrUnroll) {
+        uint4 rc[kRrUnroll];
+        uint32_t ci[kRrUnroll];
 #pragma unroll
-        for (int u = 0; u < kUnroll; ++u) {
-            ci[u] = t0 + (int64_t)(it + u) * kRrSlots + slot;
-            chunk[u] = make_uint4(0, 0, 0, 0);
-            if (ci[u] < a.c_eff) {
-                const int64_t key = cand[ci[u]];
-                if (key >= 0 && key < a.n) chunk[u] = reinterpret_cast<const uint4*>(rec + key * kRec)[l];
+        for (int u = 0; u < kRrUnroll; ++u) {
+            ci[u] = it + u * kRrSlots + slot;
+            rc[u] = make_uint4(0, 0, 0, 0);
+            if (ci[u] < m) {
+                const int64_t key = s_list[ci[u]];
+                rc[u] = reinterpret_cast<const uint4*>(rec + key * kRec)[l];
             }
         }
 #pragma unroll
-        for (int u = 0; u < kUnroll; ++u) {
-            const uint32_t c0 = chunk[u].x, c1 = chunk[u].y;
+        for (int u = 0; u < kRrUnroll; ++u) {
+            const uint32_t c0 = rc[u].x, c1 = rc[u].y;
             float d0 = 0.f, d1 = 0.f;
 #pragma unroll
             for (int j = 0; j < 8; ++j) {
                 d0 += s_tab[(c0 >> (4 * j)) & 15u] * z[j];
                 d1 += s_tab[(c1 >> (4 * j)) & 15u] * z[8 + j];
             }
-            float part = __uint_as_float(chunk[u].z) * d0 + __uint_as_float(chunk[u].w) * d1;
+            float part = __uint_as_float(rc[u].z) * d0 + __uint_as_float(rc[u].w) * d1;
             part += __shfl_xor(part, 1, 64);
             part += __shfl_xor(part, 2, 64);
             part += __shfl_xor(part, 4, 64);
             // + 0.0f turns -0 into +0, so equal estimates compare equal in the top-k keys.
-            if (l == 0 && ci[u] < a.c_eff) out[ci[u]] = part + 0.0f;
+            if (l == 0 && ci[u] < m) out[ci[u]] = part + 0.0f;
         }
     }
 }
 
 // ---------------------------------------------------------------- top-k
-
-constexpr int kTkThreads = 1024;
-constexpr int kTkWaves = kTkThreads / 64;
 
 __device__ __forceinline__ uint32_t order_key(float f) {
     const uint32_t u = __float_as_uint(f);
@@ -106,38 +175,47 @@ __device__ __forceinline__ float key_float(uint32_t k) {
     return __uint_as_float(u);
 }
 
-__device__ __forceinline__ uint32_t wave_incl_scan(uint32_t v, int lane) {
-#pragma unroll
-    for (int d = 1; d < 64; d <<= 1) {
-        uint32_t o = __shfl_up(v, d, 64);
-        if (lane >= d) v += o;
+// Shared by both top-k kernels: suffix scan of a histogram by wave 0 to find
+// the digit holding the need-th largest element.  Lane L owns digits
+// NB-1-L*PER .. NB-PER-L*PER (descending); writes s_digit / s_need.
+template <int NB>
+__device__ __forceinline__ void find_digit(const uint32_t* hist, uint32_t need, int lane, uint32_t* s_digit,
+                                           uint32_t* s_need) {
+    constexpr int PER = NB / 64;
+    const uint32_t* h = hist + NB - PER * (lane + 1);  // this lane's bins, ascending
+    uint32_t tot = 0;
+#pragma unroll 8
+    for (int r = 0; r < PER; ++r) tot += h[r];
+    const uint32_t incl = wave_incl_scan32(tot, lane);
+    uint32_t above = incl - tot;  // elements with a larger digit than this lane's bins
+    if (above < need && above + tot >= need) {
+        // Exactly one lane holds the crossing; walk its bins from the largest down.
+        for (int r = PER - 1; r >= 0; --r) {
+            const uint32_t c = h[r];
+            if (above + c >= need) {
+                *s_digit = (uint32_t)(NB - PER * (lane + 1) + r);
+                *s_need = need - above;
+                break;
+            }
+            above += c;
+        }
     }
-    return v;
 }
 
-// Exclusive block-wide prefix of v (all threads must call).
-__device__ __forceinline__ uint32_t block_excl_scan(uint32_t v, uint32_t* s_w, uint32_t* total) {
-    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-    const uint32_t incl = wave_incl_scan(v, lane);
-    if (lane == 63) s_w[wave] = incl;
-    __syncthreads();
-    uint32_t pre = 0, tot = 0;
-#pragma unroll
-    for (int w = 0; w < kTkWaves; ++w) {
-        const uint32_t x = s_w[w];
-        if (w < wave) pre += x;
-        tot += x;
-    }
-    __syncthreads();
-    *total = tot;
-    return pre + incl - v;
-}
-
-template <int EPT>
-__global__ __launch_bounds__(kTkThreads) void topk_kernel(RetrieveArgs a) {
-    __shared__ uint32_t s_hist[256];
-    __shared__ uint32_t s_w[kTkWaves];
-    __shared__ uint32_t s_mm[2][kTkWaves];
+// Top-k for C <= TH * EPT held in LDS.  Scores and candidate indices are staged
+// with coalesced 16-byte loads; each thread then owns EPT consecutive candidates.
+// Exact radix select with 11-bit digits taken from the top of the occupied
+// [min, max] key range, then an ordered compaction (ascending key index).
+template <int TH, int EPT>
+__global__ __launch_bounds__(TH) void topk_lds_kernel(RetrieveArgs a) {
+    constexpr int kWaves = TH / 64;
+    constexpr int kCap = TH * EPT;
+    constexpr int kNB = 2048;
+    __shared__ uint32_t s_key[kCap];
+    __shared__ int32_t s_idx[kCap];
+    __shared__ uint32_t s_hist[2][kNB];
+    __shared__ uint32_t s_w[kWaves];
+    __shared__ uint32_t s_mm[2][kWaves];
     __shared__ uint32_t s_digit, s_need;
 
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
@@ -147,7 +225,136 @@ __global__ __launch_bounds__(kTkThreads) void topk_kernel(RetrieveArgs a) {
     const float* sc = a.cand_score + row * a.n_cand;
     const int32_t* cand = a.cand + row * a.n_cand;
 
-    // Order-preserving keys of this thread's contiguous run of candidates.
+    // Coalesced staging (rows of cand / cand_score are 256-byte aligned).
+    for (int p4 = tid; p4 < kCap / 4; p4 += TH) {
+        const int p = 4 * p4;
+        uint4 kv = make_uint4(0, 0, 0, 0);
+        int4 iv = make_int4(-1, -1, -1, -1);
+        if (p + 3 < C) {
+            const float4 f = reinterpret_cast<const float4*>(sc)[p4];
+            kv = make_uint4(order_key(f.x), order_key(f.y), order_key(f.z), order_key(f.w));
+            iv = reinterpret_cast<const int4*>(cand)[p4];
+        } else {
+            uint32_t k4[4] = {0, 0, 0, 0};
+            int32_t i4[4] = {-1, -1, -1, -1};
+#pragma unroll
+            for (int q = 0; q < 4; ++q)
+                if (p + q < C) { k4[q] = order_key(sc[p + q]); i4[q] = cand[p + q]; }
+            kv = make_uint4(k4[0], k4[1], k4[2], k4[3]);
+            iv = make_int4(i4[0], i4[1], i4[2], i4[3]);
+        }
+        reinterpret_cast<uint4*>(s_key)[p4] = kv;
+        reinterpret_cast<int4*>(s_idx)[p4] = iv;
+    }
+    for (int i = tid; i < 2 * kNB; i += TH) (&s_hist[0][0])[i] = 0;
+    __syncthreads();
+
+    uint32_t key[EPT];
+    uint32_t kmin = 0xffffffffu, kmax = 0u;
+#pragma unroll
+    for (int e4 = 0; e4 < EPT / 4; ++e4) {
+        const uint4 kv = reinterpret_cast<const uint4*>(s_key)[tid * (EPT / 4) + e4];
+        key[4 * e4] = kv.x; key[4 * e4 + 1] = kv.y; key[4 * e4 + 2] = kv.z; key[4 * e4 + 3] = kv.w;
+    }
+#pragma unroll
+    for (int e = 0; e < EPT; ++e)
+        if (key[e] != 0u) { kmin = min(kmin, key[e]); kmax = max(kmax, key[e]); }
+#pragma unroll
+    for (int d = 1; d < 64; d <<= 1) {
+        kmin = min(kmin, (uint32_t)__shfl_xor(kmin, d, 64));
+        kmax = max(kmax, (uint32_t)__shfl_xor(kmax, d, 64));
+    }
+    if (lane == 0) { s_mm[0][wave] = kmin; s_mm[1][wave] = kmax; }
+    __syncthreads();
+#pragma unroll
+    for (int w = 0; w < kWaves; ++w) {
+        kmin = min(kmin, s_mm[0][w]);
+        kmax = max(kmax, s_mm[1][w]);
+    }
+
+    const uint32_t range = kmax - kmin;
+    const int nbits = range ? 32 - __clz(range) : 0;
+    uint32_t prefix = 0, mask = 0, need = (uint32_t)kk;
+    int shift = nbits > 11 ? nbits - 11 : 0;
+#pragma unroll 1
+    for (int pass = 0; pass < 3 && nbits > 0; ++pass) {
+        uint32_t* hist = s_hist[pass & 1];
+#pragma unroll
+        for (int e = 0; e < EPT; ++e) {
+            const uint32_t u = key[e] - kmin;
+            if (key[e] != 0u && (u & mask) == prefix) atomicAdd(&hist[(u >> shift) & (kNB - 1)], 1u);
+        }
+        __syncthreads();
+        if (wave == 0) find_digit<kNB>(hist, need, lane, &s_digit, &s_need);
+        // The other buffer was read in the previous pass; clear it for the next one.
+        for (int i = tid; i < kNB; i += TH) s_hist[(pass + 1) & 1][i] = 0;
+        __syncthreads();
+        prefix |= s_digit << shift;
+        mask |= (uint32_t)(kNB - 1) << shift;
+        need = s_need;
+        if (shift == 0) break;
+        shift = shift > 11 ? shift - 11 : 0;
+    }
+    const uint32_t T = kmin + prefix;  // the kk-th largest key value
+    const uint32_t quota = need;       // how many keys equal to T are taken (lowest indices)
+
+    // Ordered compaction: an element's output slot is (#keys > T before it) +
+    // min(#keys == T before it, quota), which lists the winners by ascending index.
+    uint32_t ng = 0, ne = 0;
+#pragma unroll
+    for (int e = 0; e < EPT; ++e) {
+        ng += (key[e] > T) ? 1u : 0u;
+        ne += (key[e] == T && key[e] != 0u) ? 1u : 0u;
+    }
+    const uint32_t mine = ng | (ne << 16);
+    const uint32_t incl = wave_incl_scan32(mine, lane);
+    if (lane == 63) s_w[wave] = incl;
+    __syncthreads();
+    uint32_t pre = incl - mine;
+#pragma unroll
+    for (int w = 0; w < kWaves; ++w)
+        if (w < wave) pre += s_w[w];
+    uint32_t gb = pre & 0xffffu, eb = pre >> 16;
+    int32_t* oi = a.out_idx + row * a.top_k;
+    float* os = a.out_score ? a.out_score + row * a.top_k : nullptr;
+#pragma unroll
+    for (int e = 0; e < EPT; ++e) {
+        uint32_t p = 0xffffffffu;
+        if (key[e] > T) {
+            p = gb + min(eb, quota);
+            ++gb;
+        } else if (key[e] == T && key[e] != 0u) {
+            if (eb < quota) p = gb + eb;
+            ++eb;
+        }
+        if (p < (uint32_t)kk) {
+            oi[p] = s_idx[tid * EPT + e];
+            if (os) os[p] = key_float(key[e]);
+        }
+    }
+    for (int r = kk + tid; r < a.top_k; r += TH) {
+        oi[r] = -1;
+        if (os) os[r] = -__builtin_huge_valf();
+    }
+}
+
+// Top-k for candidate lists too long for LDS: keys stay in registers, read
+// with a per-thread contiguous run.
+template <int TH, int EPT>
+__global__ __launch_bounds__(TH) void topk_reg_kernel(RetrieveArgs a) {
+    constexpr int kWaves = TH / 64;
+    __shared__ uint32_t s_hist[2][256];
+    __shared__ uint32_t s_w[kWaves];
+    __shared__ uint32_t s_mm[2][kWaves];
+    __shared__ uint32_t s_digit, s_need;
+
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int64_t row = blockIdx.x;
+    const int C = (int)a.c_eff;
+    const int kk = min(a.top_k, C);
+    const float* sc = a.cand_score + row * a.n_cand;
+    const int32_t* cand = a.cand + row * a.n_cand;
+
     uint32_t key[EPT];
     uint32_t kmin = 0xffffffffu, kmax = 0u;
 #pragma unroll
@@ -159,6 +366,7 @@ __global__ __launch_bounds__(kTkThreads) void topk_kernel(RetrieveArgs a) {
             kmax = max(kmax, key[e]);
         }
     }
+    for (int i = tid; i < 512; i += TH) (&s_hist[0][0])[i] = 0;
 #pragma unroll
     for (int d = 1; d < 64; d <<= 1) {
         kmin = min(kmin, (uint32_t)__shfl_xor(kmin, d, 64));
@@ -167,88 +375,72 @@ __global__ __launch_bounds__(kTkThreads) void topk_kernel(RetrieveArgs a) {
     if (lane == 0) { s_mm[0][wave] = kmin; s_mm[1][wave] = kmax; }
     __syncthreads();
 #pragma unroll
-    for (int w = 0; w < kTkWaves; ++w) {
+    for (int w = 0; w < kWaves; ++w) {
         kmin = min(kmin, s_mm[0][w]);
         kmax = max(kmax, s_mm[1][w]);
     }
 
-    // Radix select of the kk-th largest u = key - kmin, 8-bit digits from the top
-    // of the occupied range (so the first histogram is spread over the data).
     const uint32_t range = kmax - kmin;
     const int nbits = range ? 32 - __clz(range) : 0;
     uint32_t prefix = 0, mask = 0, need = (uint32_t)kk;
     int shift = nbits > 8 ? nbits - 8 : 0;
 #pragma unroll 1
     for (int pass = 0; pass < 4 && nbits > 0; ++pass) {
-        if (tid < 256) s_hist[tid] = 0;
-        __syncthreads();
+        uint32_t* hist = s_hist[pass & 1];
 #pragma unroll
         for (int e = 0; e < EPT; ++e) {
             const uint32_t u = key[e] - kmin;
-            if (key[e] != 0u && (u & mask) == prefix) atomicAdd(&s_hist[(u >> shift) & 255u], 1u);
+            if (key[e] != 0u && (u & mask) == prefix) atomicAdd(&hist[(u >> shift) & 255u], 1u);
         }
         __syncthreads();
         if (wave == 0) {
-            // Suffix sums over digits 255..0: lane L owns digits 255-4L..252-4L.
-            uint32_t h[4];
-            uint32_t tot = 0;
+            find_digit<256>(hist, need, lane, &s_digit, &s_need);
 #pragma unroll
-            for (int r = 0; r < 4; ++r) { h[r] = s_hist[255 - 4 * lane - r]; tot += h[r]; }
-            const uint32_t incl = wave_incl_scan(tot, lane);
-            uint32_t above = incl - tot;  // keys with a larger digit
-#pragma unroll
-            for (int r = 0; r < 4; ++r) {
-                if (above < need && above + h[r] >= need) {
-                    s_digit = 255u - 4u * lane - r;
-                    s_need = need - above;
-                }
-                above += h[r];
-            }
+            for (int r = 0; r < 4; ++r) s_hist[(pass + 1) & 1][4 * lane + r] = 0;
         }
         __syncthreads();
         prefix |= s_digit << shift;
         mask |= 255u << shift;
         need = s_need;
-        __syncthreads();
         if (shift == 0) break;
         shift = shift > 8 ? shift - 8 : 0;
     }
-    const uint32_t T = kmin + prefix;  // the kk-th largest key value
-    const uint32_t quota = need;       // how many keys equal to T are taken
+    const uint32_t T = kmin + prefix;
+    const uint32_t quota = need;
 
-    uint32_t n_eq = 0;
-#pragma unroll
-    for (int e = 0; e < EPT; ++e) n_eq += (key[e] == T && key[e] != 0u) ? 1u : 0u;
-    uint32_t tot;
-    uint32_t eq_before = block_excl_scan(n_eq, s_w, &tot);
-    uint32_t n_sel = 0;
-    uint64_t selmask = 0;
+    uint32_t ng = 0, ne = 0;
 #pragma unroll
     for (int e = 0; e < EPT; ++e) {
-        bool s = false;
-        if (key[e] != 0u) {
-            if (key[e] > T) s = true;
-            else if (key[e] == T) { s = eq_before < quota; ++eq_before; }
-        }
-        selmask |= (s ? 1ull : 0ull) << e;
-        n_sel += s ? 1u : 0u;
+        ng += (key[e] > T) ? 1u : 0u;
+        ne += (key[e] == T && key[e] != 0u) ? 1u : 0u;
     }
-    uint32_t pos = block_excl_scan(n_sel, s_w, &tot);
-    // Winners in candidate order, i.e. ascending key index.
+    const uint32_t mine = ng | (ne << 16);
+    const uint32_t incl = wave_incl_scan32(mine, lane);
+    if (lane == 63) s_w[wave] = incl;
+    __syncthreads();
+    uint32_t pre = incl - mine;
+#pragma unroll
+    for (int w = 0; w < kWaves; ++w)
+        if (w < wave) pre += s_w[w];
+    uint32_t gb = pre & 0xffffu, eb = pre >> 16;
     int32_t* oi = a.out_idx + row * a.top_k;
     float* os = a.out_score ? a.out_score + row * a.top_k : nullptr;
 #pragma unroll
     for (int e = 0; e < EPT; ++e) {
-        if ((selmask >> e) & 1ull) {
-            const int p = tid * EPT + e;
-            if (pos < (uint32_t)kk) {
-                oi[pos] = cand[p];
-                if (os) os[pos] = key_float(key[e]);
-            }
-            ++pos;
+        uint32_t p = 0xffffffffu;
+        if (key[e] > T) {
+            p = gb + min(eb, quota);
+            ++gb;
+        } else if (key[e] == T && key[e] != 0u) {
+            if (eb < quota) p = gb + eb;
+            ++eb;
+        }
+        if (p < (uint32_t)kk) {
+            oi[p] = cand[tid * EPT + e];
+            if (os) os[p] = key_float(key[e]);
         }
     }
-    for (int r = kk + tid; r < a.top_k; r += kTkThreads) {
+    for (int r = kk + tid; r < a.top_k; r += TH) {
         oi[r] = -1;
         if (os) os[r] = -__builtin_huge_valf();
     }
@@ -264,33 +456,28 @@ __global__ void pad_outputs_kernel(int32_t* out_idx, float* out_score, int64_t c
 
 }  // namespace
 
-hipError_t launch_rerank(const RetrieveArgs& a, hipStream_t s) {
-    const int64_t tiles = (a.c_eff + kRrTile - 1) / kRrTile;
-    prof_begin("rerank", s);
-    hipLaunchKernelGGL(rerank_kernel, dim3((unsigned)tiles, (unsigned)(a.batch * a.hq)), dim3(kRrThreads),
-                       0, s, a);
+hipError_t launch_compact_rerank(const RetrieveArgs& a, hipStream_t s) {
+    prof_begin("compact_rerank", s);
+    hipLaunchKernelGGL(compact_rerank_kernel, dim3((unsigned)a.n_chunks, (unsigned)(a.batch * a.hq)),
+                       dim3(kRrThreads), 0, s, a);
     prof_end(s);
     return hipGetLastError();
 }
 
 hipError_t launch_topk(const RetrieveArgs& a, hipStream_t s) {
-    const int64_t ept = (a.c_eff + kTkThreads - 1) / kTkThreads;
     const dim3 grid((unsigned)(a.batch * a.hq));
+    const int64_t C = a.c_eff;
     prof_begin("topk", s);
-    if (ept <= 1)
-        hipLaunchKernelGGL(topk_kernel<1>, grid, dim3(kTkThreads), 0, s, a);
-    else if (ept <= 2)
-        hipLaunchKernelGGL(topk_kernel<2>, grid, dim3(kTkThreads), 0, s, a);
-    else if (ept <= 4)
-        hipLaunchKernelGGL(topk_kernel<4>, grid, dim3(kTkThreads), 0, s, a);
-    else if (ept <= 8)
-        hipLaunchKernelGGL(topk_kernel<8>, grid, dim3(kTkThreads), 0, s, a);
-    else if (ept <= 16)
-        hipLaunchKernelGGL(topk_kernel<16>, grid, dim3(kTkThreads), 0, s, a);
-    else if (ept <= 32)
-        hipLaunchKernelGGL(topk_kernel<32>, grid, dim3(kTkThreads), 0, s, a);
+    if (C <= 1024 * 4)
+        hipLaunchKernelGGL((topk_lds_kernel<1024, 4>), grid, dim3(1024), 0, s, a);
+    else if (C <= 1024 * 8)
+        hipLaunchKernelGGL((topk_lds_kernel<1024, 8>), grid, dim3(1024), 0, s, a);
+    else if (C <= 1024 * 16)
+        hipLaunchKernelGGL((topk_lds_kernel<1024, 16>), grid, dim3(1024), 0, s, a);
+    else if (C <= 1024 * 32)
+        hipLaunchKernelGGL((topk_reg_kernel<1024, 32>), grid, dim3(1024), 0, s, a);
     else
-        hipLaunchKernelGGL(topk_kernel<64>, grid, dim3(kTkThreads), 0, s, a);
+        hipLaunchKernelGGL((topk_reg_kernel<1024, 64>), grid, dim3(1024), 0, s, a);
     prof_end(s);
     return hipGetLastError();
 }

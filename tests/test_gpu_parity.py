@@ -78,6 +78,8 @@ EDGE = [
     ("tiny_collide_budget", 1, 1, 4, 2000, (200, 1, 20)),
     ("collide_budget_above_n", 1, 1, 4, 2000, (200, 100000, 20)),
     ("k_odd_ragged", 1, 1, 2, 777, (333, 555, 77)),
+    ("big_C", 1, 1, 2, 40000, (10000, 20000, 300)),
+    ("huge_C", 1, 1, 1, 70000, (40000, 60000, 2048)),
 ]
 
 

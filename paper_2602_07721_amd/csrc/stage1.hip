@@ -48,6 +48,77 @@ __device__ __forceinline__ uint32_t wave_incl_scan_u32(uint32_t v, int lane) {
     return v;
 }
 
+// Bitonic sort of 256 int64 keys held 4 per lane (element e = 4 lane + r), descending.
+// Each compare-exchange is one 64-bit compare into a lane mask, a scalar XOR with
+// the stage's direction pattern, and two v_cndmask; partners 1 or 2 lanes away come
+// through DPP, 4..16 lanes away through ds_swizzle, 32 away through ds_bpermute.
+
+// Lanes whose bit t-2 is set (bit t of e = 4 lane + r for t >= 2); 0 past bit 7.
+__device__ constexpr uint64_t lane_bit_mask(int t) {
+    return t == 2 ? 0xAAAAAAAAAAAAAAAAull : t == 3 ? 0xCCCCCCCCCCCCCCCCull
+         : t == 4 ? 0xF0F0F0F0F0F0F0F0ull : t == 5 ? 0xFF00FF00FF00FF00ull
+         : t == 6 ? 0xFFFF0000FFFF0000ull : t == 7 ? 0xFFFFFFFF00000000ull : 0ull;
+}
+
+__device__ constexpr int log2i(int x) { return x <= 1 ? 0 : 1 + log2i(x >> 1); }
+
+// mask[lane] ? if1 : if0, with the mask in an SGPR pair.
+__device__ __forceinline__ uint32_t select_mask(uint64_t mask, uint32_t if1, uint32_t if0) {
+    uint32_t r;
+    asm("v_cndmask_b32 %0, %1, %2, %3" : "=v"(r) : "v"(if0), "v"(if1), "s"(mask));
+    return r;
+}
+
+// The value of lane ^ lm (lm a power of two below 64, known after unrolling).
+__device__ __forceinline__ uint32_t lane_xor(uint32_t v, int lm, int lane) {
+    switch (lm) {
+        case 1: return (uint32_t)__builtin_amdgcn_mov_dpp((int)v, 0xB1, 0xF, 0xF, false);
+        case 2: return (uint32_t)__builtin_amdgcn_mov_dpp((int)v, 0x4E, 0xF, 0xF, false);
+        case 4: return (uint32_t)__builtin_amdgcn_ds_swizzle((int)v, 0x1F | (4 << 10));
+        case 8: return (uint32_t)__builtin_amdgcn_ds_swizzle((int)v, 0x1F | (8 << 10));
+        case 16: return (uint32_t)__builtin_amdgcn_ds_swizzle((int)v, 0x1F | (16 << 10));
+        default: return (uint32_t)__builtin_amdgcn_ds_bpermute((lane ^ 32) << 2, (int)v);
+    }
+}
+
+__device__ __forceinline__ void sort256_desc(int64_t (&key)[4], int lane) {
+#pragma unroll
+    for (int k = 2; k <= 256; k <<= 1) {
+#pragma unroll
+        for (int j = k >> 1; j > 0; j >>= 1) {
+            if (j >= 4) {
+                // Element e keeps the larger key iff bits log2 j and log2 k of e agree.
+                const uint64_t keep_max = ~(lane_bit_mask(log2i(j)) ^ lane_bit_mask(log2i(k)));
+#pragma unroll
+                for (int r = 0; r < 4; ++r) {
+                    const uint32_t lo = (uint32_t)key[r], hi = (uint32_t)((uint64_t)key[r] >> 32);
+                    const uint32_t olo = lane_xor(lo, j >> 2, lane), ohi = lane_xor(hi, j >> 2, lane);
+                    const int64_t other = (int64_t)(((uint64_t)ohi << 32) | olo);
+                    // Keys are distinct: take the partner's key iff (other > key) == keep_max.
+                    const uint64_t take = ~(__ballot(other > key[r]) ^ keep_max);
+                    key[r] = (int64_t)(((uint64_t)select_mask(take, ohi, hi) << 32) |
+                                       select_mask(take, olo, lo));
+                }
+            } else {
+#pragma unroll
+                for (int r = 0; r < 4; ++r) {
+                    if (r & j) continue;
+                    const int r2 = r | j;
+                    // Descending where bit log2 k of e is clear (k = 2: bit 1 of r).
+                    const uint64_t desc = k == 2 ? ((r & 2) ? 0ull : ~0ull) : ~lane_bit_mask(log2i(k));
+                    const uint64_t swap = ~(__ballot(key[r] < key[r2]) ^ desc);
+                    const uint32_t lo0 = (uint32_t)key[r], hi0 = (uint32_t)((uint64_t)key[r] >> 32);
+                    const uint32_t lo1 = (uint32_t)key[r2], hi1 = (uint32_t)((uint64_t)key[r2] >> 32);
+                    key[r] = (int64_t)(((uint64_t)select_mask(swap, hi1, hi0) << 32) |
+                                       select_mask(swap, lo1, lo0));
+                    key[r2] = (int64_t)(((uint64_t)select_mask(swap, hi0, hi1) << 32) |
+                                        select_mask(swap, lo0, lo1));
+                }
+            }
+        }
+    }
+}
+
 // ---------------------------------------------------------------- query + LUT
 
 constexpr int kLutThreads = 1024;  // 16 waves: 4 head slots x 4 subspaces
@@ -114,39 +185,7 @@ __global__ __launch_bounds__(kLutThreads) void query_lut_kernel(RetrieveArgs a) 
             const int64_t pi = (int64_t)(p * 16777216.0);
             key[r] = pi * 256 + (255 - c);  // descending key: proxy desc, then id asc
         }
-        // Bitonic sort, descending, element e = 4*lane + r.
-#pragma unroll
-        for (int k = 2; k <= kCentroids; k <<= 1) {
-#pragma unroll
-            for (int j = k >> 1; j > 0; j >>= 1) {
-                if (j >= 4) {
-                    const int lm = j >> 2;
-#pragma unroll
-                    for (int r = 0; r < 4; ++r) {
-                        const int e = 4 * lane + r;
-                        const int64_t other = __shfl_xor(key[r], lm, 64);
-                        const bool lower = (e & j) == 0;
-                        const bool desc = (e & k) == 0;
-                        const int64_t mx = key[r] > other ? key[r] : other;
-                        const int64_t mn = key[r] > other ? other : key[r];
-                        key[r] = (lower == desc) ? mx : mn;
-                    }
-                } else {
-#pragma unroll
-                    for (int r = 0; r < 4; ++r) {
-                        const int r2 = r ^ j;
-                        if (r2 > r) {
-                            const int e = 4 * lane + r;
-                            const bool desc = (e & k) == 0;
-                            const int64_t x0 = key[r], x1 = key[r2];
-                            const bool swap = desc ? (x0 < x1) : (x0 > x1);
-                            key[r] = swap ? x1 : x0;
-                            key[r2] = swap ? x0 : x1;
-                        }
-                    }
-                }
-            }
-        }
+        sort256_desc(key, lane);
         // Exclusive prefix of cluster counts in rank order -> start rank P(c).
         uint32_t cc[4];
         int cid[4];

@@ -75,9 +75,18 @@ typedef struct pariskv_config {
  * ids, 4-bit codes and weights w).  All three arrays are device memory owned
  * by the caller, 16-byte aligned (128-byte alignment of rec is recommended).
  *
- *   ids    uint8 [batch][Hkv][capacity][B]: centroid id of subspace b (Eq.
- *          dir_assign).  Bit j is set when coordinate j of the rotated
- *          subspace is negative (a zero coordinate counts as positive).
+ *   ids    uint8 [batch][Hkv][capacity][B]: the centroid id c of subspace b
+ *          (Eq. dir_assign), stored relabelled as slot(c).  Bit j of c is set
+ *          when coordinate j of the rotated subspace is negative (a zero
+ *          coordinate counts as positive).  slot keeps bits 5..7 and XORs
+ *          bits 0..4 with M(c >> 5), M linear with M(1) = 0x07, M(2) = 0x19,
+ *          M(4) = 0x0E:
+ *            slot(c) = c ^ (c & 32 ? 0x07 : 0) ^ (c & 64 ? 0x19 : 0)
+ *                        ^ (c & 128 ? 0x0E : 0).
+ *          slot is its own inverse.  Ids within Hamming distance 3 get
+ *          different slot(c) mod 32, which spreads the popular clusters
+ *          around a dominant sign pattern over distinct LDS banks in the
+ *          collision scan.
  *   rec    [batch][Hkv][capacity][128] bytes, the rerank record of one key,
  *          eight 16-byte chunks; chunk c = 0..7 holds subspaces 2c and 2c+1:
  *            bytes 16c+0..3   uint32 code word of subspace 2c
@@ -109,7 +118,8 @@ typedef struct pariskv_budget {
 typedef struct pariskv_ws_layout {
     size_t total;       /* bytes needed                                         */
     size_t zq;          /* float [batch][Hq][D]: H(s*q)/D, rounded to float     */
-    size_t lut;         /* uint32 [batch][Hkv][quads][B][256]: tier bonus, byte
+    size_t lut;         /* uint32 [batch][Hkv][quads][B][256]: tier bonus of
+                           centroid c at entry slot(c) (the ids encoding); byte
                            h%4 of the word is query head 4*quad + h%4 of the group */
     size_t score8;      /* uint8 [batch][Hq][n_pad]: collision scores S_i        */
     size_t chunk_sfx;   /* uint32 [batch][Hq][n_chunks][98]: per chunk, #{S >= v}

@@ -8,7 +8,8 @@
 //   multiple of 2^-24 below 2^47 and is exact in float64 in any order.  y is
 //   sqrt(D) ||k|| times the rotated, normalised key, a positive factor that
 //   every decision below is invariant to.
-//   id bit j    = [y_j < 0]                      (argmax over {+-1/sqrt m}^m)
+//   id bit j    = [y_j < 0]                      (argmax over {+-1/sqrt m}^m),
+//                 stored as id_slot(id); counts are kept by the id itself
 //   Y_j         = fl(y_j * y_j)
 //   S_b         = ((Y0+Y1)+(Y2+Y3))+((Y4+Y5)+(Y6+Y7))
 //   t_j         = #{t : Y_j >= fl(tau_t^2 * S_b)}   (|u_j| >= tau_t), 0 if S_b = 0
@@ -121,7 +122,7 @@ __global__ __launch_bounds__(kThreads) void encode_kernel(
             }
         }
 
-        uint32_t id_word = 0;
+        uint32_t id_word = 0, slot_word = 0;  // true ids (for counts), stored slots
         uint32_t code[4];
         float wgt[4];
 #pragma unroll
@@ -152,11 +153,12 @@ __global__ __launch_bounds__(kThreads) void encode_kernel(
             wgt[sbi] = nz ? (float)(S / A) : 0.0f;
             code[sbi] = cw;
             id_word |= idb << (8 * sbi);
+            slot_word |= id_slot(idb) << (8 * sbi);
         }
 
         if (live) {
             const int64_t row = grp * capacity + row0 + i;
-            *reinterpret_cast<uint32_t*>(ids + row * kB + 4 * q) = id_word;
+            *reinterpret_cast<uint32_t*>(ids + row * kB + 4 * q) = slot_word;
             uint4* dst = reinterpret_cast<uint4*>(rec + row * kRec + 32 * q);
             dst[0] = make_uint4(code[0], code[1], __float_as_uint(wgt[0]), __float_as_uint(wgt[1]));
             dst[1] = make_uint4(code[2], code[3], __float_as_uint(wgt[2]), __float_as_uint(wgt[3]));

@@ -19,6 +19,14 @@ constexpr int kSfx = kBins + 1;     // suffix histogram entries v = 0..97 (entry
 constexpr int kChunk = 4096;      // keys per collision / selection chunk
 constexpr int kTierCount = 6;
 
+// Stored form of a centroid id (the ids array holds slot(c)): bits 5..7 kept,
+// bits 0..4 XORed with a linear function of bits 5..7 whose kernel code has
+// minimum distance 4, so ids within Hamming distance 3 differ modulo 32 (the
+// LDS bank of the collision scan's lookup).  An involution.
+__host__ __device__ __forceinline__ uint32_t id_slot(uint32_t c) {
+    return c ^ ((c >> 5) & 1u) * 0x07u ^ ((c >> 6) & 1u) * 0x19u ^ ((c >> 7) & 1u) * 0x0Eu;
+}
+
 // 128 rotation signs packed as bits: bit j of word j/32 set <=> s_j = -1.
 struct SignBits {
     uint32_t w[4];

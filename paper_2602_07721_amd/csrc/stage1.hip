@@ -203,7 +203,8 @@ __global__ __launch_bounds__(kLutThreads) void query_lut_kernel(RetrieveArgs a) 
 #pragma unroll
             for (int l = kTierCount - 1; l >= 0; --l)
                 if (start < a.cuts[l]) bonus = (uint32_t)(kTierCount - l);
-            if (bonus) atomicOr(&s_lut[sub][cid[r]], bonus << (8 * slot));
+            // The table is indexed like the stored ids, by slot.
+            if (bonus) atomicOr(&s_lut[sub][id_slot((uint32_t)cid[r])], bonus << (8 * slot));
             start += cc[r];
         }
     }
@@ -218,6 +219,13 @@ constexpr int kColThreads = 256;
 constexpr int kColWaves = kColThreads / 64;
 constexpr int kColKeysPerIter = 4 * kColThreads;  // 4 keys per thread per iteration
 constexpr int kLowCut = 4;  // scores below this are counted in registers, not by LDS atomics
+// Scores >= kLowCut go to one of 4 histogram copies picked by lane & 3 (fewer
+// same-address atomics per instruction), 16-bit counters (a copy sees at most
+// 1024 keys per chunk): value v sits in word (v - kLowCut) mod kHistWords, low
+// half below kLowCut + kHistWords, high half above.
+constexpr int kHistCopies = 4;
+constexpr int kHistWords = 50;
+static_assert(kMaxScore - kLowCut < 2 * kHistWords, "histogram halves");
 
 // Suffix sums of a 97-bin histogram held as (lo = bins 0..63 by lane, hi = bins
 // 64..96 by lane < 33): returns (sfx_lo, sfx_hi) with sfx[v] = sum_{u >= v} h[u].
@@ -240,7 +248,7 @@ __device__ __forceinline__ void wave_suffix97(uint32_t lo, uint32_t hi, int lane
 
 __global__ __launch_bounds__(kColThreads) void collide_kernel(RetrieveArgs a) {
     __shared__ uint32_t s_lut[kB * kCentroids];
-    __shared__ uint32_t s_hist[4][kBins + 3];
+    __shared__ uint32_t s_hist[kHistCopies][4][kHistWords];
     __shared__ uint32_t s_low[kColWaves][kLowCut - 1][4];
 
     const int tid = threadIdx.x;
@@ -258,7 +266,7 @@ __global__ __launch_bounds__(kColThreads) void collide_kernel(RetrieveArgs a) {
     const uint4* lsrc = reinterpret_cast<const uint4*>(a.lut + gq * (kB * kCentroids));
     for (int i = tid; i < kB * kCentroids / 4; i += kColThreads)
         reinterpret_cast<uint4*>(s_lut)[i] = lsrc[i];
-    for (int i = tid; i < 4 * (kBins + 3); i += kColThreads) (&s_hist[0][0])[i] = 0;
+    for (int i = tid; i < kHistCopies * 4 * kHistWords; i += kColThreads) (&s_hist[0][0][0])[i] = 0;
     __syncthreads();
 
     const uint8_t* ids = a.ids + grp * a.capacity * kB;
@@ -300,7 +308,12 @@ __global__ __launch_bounds__(kColThreads) void collide_kernel(RetrieveArgs a) {
 #pragma unroll
             for (int h = 0; h < 4; ++h) {
                 const uint32_t sh = (acc >> (8 * h)) & 0xffu;
-                if (sh >= (uint32_t)kLowCut) atomicAdd(&s_hist[h][sh], 1u);
+                if (sh >= (uint32_t)kLowCut) {
+                    const uint32_t idx = sh - kLowCut;
+                    const bool upper = idx >= (uint32_t)kHistWords;
+                    atomicAdd(&s_hist[lane & (kHistCopies - 1)][h][upper ? idx - kHistWords : idx],
+                              upper ? 0x10000u : 1u);
+                }
             }
             // A wave stores 64 consecutive score bytes of a head per instruction.
             if (live) {
@@ -333,8 +346,19 @@ __global__ __launch_bounds__(kColThreads) void collide_kernel(RetrieveArgs a) {
     // Per-chunk suffix histogram of every head: sfx[v] = #{keys in chunk : S >= v}, v = 0..97.
     if (wave < nh) {
         const int h = wave;
-        const uint32_t lo = s_hist[h][lane];
-        const uint32_t hi = lane < kBins - 64 ? s_hist[h][64 + lane] : 0u;
+        // Exact count of each value v >= kLowCut: lane holds v = lane and v = 64 + lane.
+        auto count_of = [&](int v) -> uint32_t {
+            if (v < kLowCut || v > kMaxScore) return 0u;
+            const int idx = v - kLowCut;
+            const int w = idx < kHistWords ? idx : idx - kHistWords;
+            const int sh = idx < kHistWords ? 0 : 16;
+            uint32_t t = 0;
+#pragma unroll
+            for (int c = 0; c < kHistCopies; ++c) t += (s_hist[c][h][w] >> sh) & 0xffffu;
+            return t;
+        };
+        const uint32_t lo = count_of(lane);
+        const uint32_t hi = count_of(64 + lane);
         uint32_t sl, sh;
         wave_suffix97(lo, hi, lane, &sl, &sh);  // exact for v >= kLowCut
         if (lane == 0) sl = (uint32_t)(c1 - c0);

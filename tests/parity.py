@@ -23,6 +23,15 @@ from oracle import quantizer as oq
 from oracle import retrieve as oret
 
 TAU, A, _ = oq.lloyd_max(8)
+
+
+def _slot(c):
+    """Stored form of centroid id c, as documented for pariskv_index.ids."""
+    return c ^ (0x07 if c & 32 else 0) ^ (0x19 if c & 64 else 0) ^ (0x0E if c & 128 else 0)
+
+
+# slot is an involution, so the same table maps stored bytes back to ids.
+SLOT = np.array([_slot(c) for c in range(256)], dtype=np.uint8)
 RTOL_SCORE = 1e-4
 RTOL_ATT = 2e-3
 
@@ -81,7 +90,7 @@ class GpuRun:
     def host_index(self, n=None):
         n = self.n if n is None else n
         torch.cuda.synchronize()
-        ids = self.index.ids[:, :, :n].cpu().numpy()
+        ids = SLOT[self.index.ids[:, :, :n].cpu().numpy()]
         rec = self.index.rec[:, :, :n].cpu().numpy()
         counts = self.index.counts.cpu().numpy().view(np.uint32)
         return ids, rec, counts
@@ -104,8 +113,9 @@ class GpuRun:
 
 
 def lut_for_head(lut, seq, kvh, g):
-    """Unpack the packed bonus table of query head g (within its KV group) -> [16][256]."""
-    words = lut[seq, kvh, g // 4]
+    """Unpack the packed bonus table of query head g (within its KV group) -> [16][256],
+    indexed by centroid id (the table itself is indexed by slot)."""
+    words = lut[seq, kvh, g // 4][:, SLOT]
     return ((words >> (8 * (g % 4))) & 0xFF).astype(np.int64)
 
 

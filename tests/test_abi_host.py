@@ -167,3 +167,17 @@ def test_sparse_attend_validation():
     assert call(scale=float("nan")) == pk.ERR_INVALID
     assert call(idx=FAKE + 2) == pk.ERR_INVALID
     assert call(out=0) == pk.ERR_INVALID
+
+
+def test_id_slot_encoding_spreads_near_ids_over_banks():
+    # The documented stored form of a centroid id: a bijection, its own inverse,
+    # and ids within Hamming distance 3 never share a value mod 32.
+    from parity import SLOT
+    s = SLOT.astype(np.int64)
+    assert sorted(s.tolist()) == list(range(256))
+    assert np.all(s[s] == np.arange(256))
+    assert np.all((s >> 5) == (np.arange(256) >> 5))
+    for c in range(256):
+        for d in range(1, 256):
+            if bin(d).count("1") <= 3:
+                assert s[c] % 32 != s[c ^ d] % 32, (c, d)

@@ -14,7 +14,8 @@ import workloads
 from oracle import attention as oatt
 from oracle import retrieve as oret
 
-from parity import (GpuRun, check_attention, check_head, check_index, decode_rec, oracle_group)
+from parity import (SLOT, GpuRun, check_attention, check_head, check_index, decode_rec,
+                    oracle_group)
 
 pytestmark = pytest.mark.gpu
 SCALE = 1.0 / np.sqrt(128.0)
@@ -213,7 +214,7 @@ def test_batch8_128k_sampled_at_full_size():
     for s in range(wc.batch):
         for h in range(wc.n_kv_heads):
             rows = np.sort(rng.choice(wc.n, size=512, replace=False))
-            gids = run.index.ids[s, h, rows].cpu().numpy()
+            gids = SLOT[run.index.ids[s, h, rows].cpu().numpy()]
             grec = run.index.rec[s, h, rows].cpu().numpy()
             from oracle import encode as oenc
             from parity import A, TAU
@@ -239,7 +240,7 @@ def test_batch8_128k_sampled_at_full_size():
     # two whole groups through the oracle
     for s, h in ((0, 0), (5, 3)):
         orc = oracle_group(K[s, h], signs)
-        check_index(run.index.ids[s, h].cpu().numpy(), run.index.rec[s, h].cpu().numpy(),
+        check_index(SLOT[run.index.ids[s, h].cpu().numpy()], run.index.rec[s, h].cpu().numpy(),
                     cnt[s, h].view(np.uint32), orc)
         for g in range(wc.q_per_kv):
             hq = h * wc.q_per_kv + g

@@ -216,7 +216,8 @@ __global__ __launch_bounds__(TH) void topk_lds_kernel(RetrieveArgs a) {
     __shared__ uint32_t s_hist[2][kNB];
     __shared__ uint32_t s_w[kWaves];
     __shared__ uint32_t s_mm[2][kWaves];
-    __shared__ uint32_t s_digit, s_need;
+    __shared__ uint32_t s_digit, s_need, s_nsmall;
+    __shared__ uint32_t s_small[64];
 
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int64_t row = blockIdx.x;
@@ -224,6 +225,7 @@ __global__ __launch_bounds__(TH) void topk_lds_kernel(RetrieveArgs a) {
     const int kk = min(a.top_k, C);
     const float* sc = a.cand_score + row * a.n_cand;
     const int32_t* cand = a.cand + row * a.n_cand;
+    if (tid == 0) s_nsmall = 0;
 
     // Coalesced staging (rows of cand / cand_score are 256-byte aligned).
     for (int p4 = tid; p4 < kCap / 4; p4 += TH) {
@@ -272,31 +274,76 @@ __global__ __launch_bounds__(TH) void topk_lds_kernel(RetrieveArgs a) {
         kmax = max(kmax, s_mm[1][w]);
     }
 
-    const uint32_t range = kmax - kmin;
-    const int nbits = range ? 32 - __clz(range) : 0;
-    uint32_t prefix = 0, mask = 0, need = (uint32_t)kk;
-    int shift = nbits > 11 ? nbits - 11 : 0;
-#pragma unroll 1
-    for (int pass = 0; pass < 3 && nbits > 0; ++pass) {
-        uint32_t* hist = s_hist[pass & 1];
+    // Pass 0: 2048 bins linear in the score over [min, max].  The float bit
+    // patterns of the scores are concentrated in few sign/exponent prefixes, so
+    // value-linear bins spread the counts (and the atomics) far better.  The bin
+    // index is a non-decreasing function of the score, so the keys of a higher
+    // bin are all larger.
+    const float fmin = key_float(kmin), fmax = key_float(kmax);
+    const float frange = fmax - fmin;
+    float inv = frange > 0.0f ? (float)kNB / frange : 0.0f;
+    if (!(inv < 1e30f)) inv = 0.0f;  // a range that under- or overflows: one bin
+    auto bin_of = [&](uint32_t k) -> uint32_t {
+        return (uint32_t)fminf((float)(kNB - 1), (key_float(k) - fmin) * inv);
+    };
 #pragma unroll
-        for (int e = 0; e < EPT; ++e) {
-            const uint32_t u = key[e] - kmin;
-            if (key[e] != 0u && (u & mask) == prefix) atomicAdd(&hist[(u >> shift) & (kNB - 1)], 1u);
+    for (int e = 0; e < EPT; ++e)
+        if (key[e] != 0u) atomicAdd(&s_hist[0][bin_of(key[e])], 1u);
+    __syncthreads();
+    if (wave == 0) find_digit<kNB>(s_hist[0], (uint32_t)kk, lane, &s_digit, &s_need);
+    __syncthreads();
+    const uint32_t bsel = s_digit;       // bin holding the kk-th largest key
+    uint32_t need = s_need;              // its rank (from the top) inside that bin
+    const uint32_t in_bin = s_hist[0][bsel];
+    uint32_t T, quota;
+    if (in_bin <= 64) {
+        // Few keys in the bin: gather them and rank them by brute force in one wave.
+#pragma unroll
+        for (int e = 0; e < EPT; ++e)
+            if (key[e] != 0u && bin_of(key[e]) == bsel) s_small[atomicAdd(&s_nsmall, 1u)] = key[e];
+        __syncthreads();
+        if (wave == 0) {
+            const uint32_t kl = lane < (int)in_bin ? s_small[lane] : 0u;
+            uint32_t gt = 0, eq = 0;
+            for (uint32_t j = 0; j < in_bin; ++j) {
+                const uint32_t kj = s_small[j];
+                gt += kj > kl ? 1u : 0u;
+                eq += kj == kl ? 1u : 0u;
+            }
+            const bool hit = lane < (int)in_bin && gt < need && need <= gt + eq;
+            const uint64_t hits = __ballot(hit);
+            if (hit && lane == __builtin_ctzll(hits)) {
+                s_digit = kl;
+                s_need = need - gt;
+            }
         }
         __syncthreads();
-        if (wave == 0) find_digit<kNB>(hist, need, lane, &s_digit, &s_need);
-        // The other buffer was read in the previous pass; clear it for the next one.
-        for (int i = tid; i < kNB; i += TH) s_hist[(pass + 1) & 1][i] = 0;
-        __syncthreads();
-        prefix |= s_digit << shift;
-        mask |= (uint32_t)(kNB - 1) << shift;
-        need = s_need;
-        if (shift == 0) break;
-        shift = shift > 11 ? shift - 11 : 0;
+        T = s_digit;
+        quota = s_need;
+    } else {
+        // Exact radix select on the full key restricted to the bin: 11, 11, 10 bits.
+        uint32_t prefix = 0, mask = 0;
+        int shift = 21;
+#pragma unroll 1
+        for (int pass = 1; pass <= 3; ++pass) {
+            uint32_t* hist = s_hist[pass & 1];
+#pragma unroll
+            for (int e = 0; e < EPT; ++e)
+                if (key[e] != 0u && (key[e] & mask) == prefix && bin_of(key[e]) == bsel)
+                    atomicAdd(&hist[(key[e] >> shift) & (kNB - 1)], 1u);
+            __syncthreads();
+            if (wave == 0) find_digit<kNB>(hist, need, lane, &s_digit, &s_need);
+            // The other buffer was read in the previous pass; clear it for the next one.
+            for (int i = tid; i < kNB; i += TH) s_hist[(pass + 1) & 1][i] = 0;
+            __syncthreads();
+            prefix |= s_digit << shift;
+            mask |= (uint32_t)(kNB - 1) << shift;
+            need = s_need;
+            shift = shift >= 11 ? shift - 11 : 0;
+        }
+        T = prefix;     // the kk-th largest key value
+        quota = need;   // how many keys equal to T are taken (lowest indices)
     }
-    const uint32_t T = kmin + prefix;  // the kk-th largest key value
-    const uint32_t quota = need;       // how many keys equal to T are taken (lowest indices)
 
     // Ordered compaction: an element's output slot is (#keys > T before it) +
     // min(#keys == T before it, quota), which lists the winners by ascending index.

@@ -11,7 +11,7 @@
 // [0, kv_capacity) are skipped like -1.  Every one of the 64 key slots keeps
 // an online-softmax state (running max, sum, 8 accumulators per lane); the
 // states are merged in LDS at the end.  The row's indices are staged in LDS
-// first and every lane keeps 4 K and 4 V row segments in flight.
+// first and every lane keeps 8 K and 8 V row segments in flight.
 
 #include <hip/hip_fp16.h>
 
@@ -23,7 +23,7 @@ namespace {
 
 constexpr int kAtThreads = 1024;
 constexpr int kAtGroups = kAtThreads / 16;  // concurrent key slots per block
-constexpr int kAtUnroll = 4;                // K/V rows in flight per lane
+constexpr int kAtUnroll = 8;                // K/V rows in flight per lane
 constexpr int kAtMaxK = 4096;               // largest k a block stages in LDS
 
 __device__ __forceinline__ void unpack8(const uint4 v, float* f) {

@@ -27,6 +27,54 @@ __host__ __device__ __forceinline__ uint32_t id_slot(uint32_t c) {
     return c ^ ((c >> 5) & 1u) * 0x07u ^ ((c >> 6) & 1u) * 0x19u ^ ((c >> 7) & 1u) * 0x0Eu;
 }
 
+// mask[lane] ? if1 : if0, with the mask in an SGPR pair.
+__device__ __forceinline__ uint32_t select_mask(uint64_t mask, uint32_t if1, uint32_t if0) {
+    uint32_t r;
+    asm("v_cndmask_b32 %0, %1, %2, %3" : "=v"(r) : "v"(if0), "v"(if1), "s"(mask));
+    return r;
+}
+
+// The value of lane ^ lm (lm a power of two below 64, known after unrolling).
+__device__ __forceinline__ uint32_t lane_xor(uint32_t v, int lm, int lane) {
+    switch (lm) {
+        case 1: return (uint32_t)__builtin_amdgcn_mov_dpp((int)v, 0xB1, 0xF, 0xF, false);
+        case 2: return (uint32_t)__builtin_amdgcn_mov_dpp((int)v, 0x4E, 0xF, 0xF, false);
+        case 4: return (uint32_t)__builtin_amdgcn_ds_swizzle((int)v, 0x1F | (4 << 10));
+        case 8: return (uint32_t)__builtin_amdgcn_ds_swizzle((int)v, 0x1F | (8 << 10));
+        case 16: return (uint32_t)__builtin_amdgcn_ds_swizzle((int)v, 0x1F | (16 << 10));
+        default: return (uint32_t)__builtin_amdgcn_ds_bpermute((lane ^ 32) << 2, (int)v);
+    }
+}
+
+// Byte k of x shifted left (right) by 2 in one SDWA instruction: the byte
+// offset of table entry byte_k(x) (byte_k(x) >> 4) for 4-byte entries.
+template <int K>
+__device__ __forceinline__ uint32_t byte_shl2(uint32_t x, uint32_t two) {
+    uint32_t r;
+    if constexpr (K == 0)
+        asm("v_lshlrev_b32_sdwa %0, %1, %2 dst_sel:DWORD dst_unused:UNUSED_PAD src0_sel:DWORD src1_sel:BYTE_0" : "=v"(r) : "v"(two), "v"(x));
+    else if constexpr (K == 1)
+        asm("v_lshlrev_b32_sdwa %0, %1, %2 dst_sel:DWORD dst_unused:UNUSED_PAD src0_sel:DWORD src1_sel:BYTE_1" : "=v"(r) : "v"(two), "v"(x));
+    else if constexpr (K == 2)
+        asm("v_lshlrev_b32_sdwa %0, %1, %2 dst_sel:DWORD dst_unused:UNUSED_PAD src0_sel:DWORD src1_sel:BYTE_2" : "=v"(r) : "v"(two), "v"(x));
+    else
+        asm("v_lshlrev_b32_sdwa %0, %1, %2 dst_sel:DWORD dst_unused:UNUSED_PAD src0_sel:DWORD src1_sel:BYTE_3" : "=v"(r) : "v"(two), "v"(x));
+    return r;
+}
+template <int K>
+__device__ __forceinline__ uint32_t byte_shr2(uint32_t x, uint32_t two) {
+    uint32_t r;
+    if constexpr (K == 0)
+        asm("v_lshrrev_b32_sdwa %0, %1, %2 dst_sel:DWORD dst_unused:UNUSED_PAD src0_sel:DWORD src1_sel:BYTE_0" : "=v"(r) : "v"(two), "v"(x));
+    else if constexpr (K == 1)
+        asm("v_lshrrev_b32_sdwa %0, %1, %2 dst_sel:DWORD dst_unused:UNUSED_PAD src0_sel:DWORD src1_sel:BYTE_1" : "=v"(r) : "v"(two), "v"(x));
+    else if constexpr (K == 2)
+        asm("v_lshrrev_b32_sdwa %0, %1, %2 dst_sel:DWORD dst_unused:UNUSED_PAD src0_sel:DWORD src1_sel:BYTE_2" : "=v"(r) : "v"(two), "v"(x));
+    else
+        asm("v_lshrrev_b32_sdwa %0, %1, %2 dst_sel:DWORD dst_unused:UNUSED_PAD src0_sel:DWORD src1_sel:BYTE_3" : "=v"(r) : "v"(two), "v"(x));
+    return r;
+}
+
 // 128 rotation signs packed as bits: bit j of word j/32 set <=> s_j = -1.
 struct SignBits {
     uint32_t w[4];

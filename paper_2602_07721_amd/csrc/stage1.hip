@@ -62,25 +62,6 @@ __device__ constexpr uint64_t lane_bit_mask(int t) {
 
 __device__ constexpr int log2i(int x) { return x <= 1 ? 0 : 1 + log2i(x >> 1); }
 
-// mask[lane] ? if1 : if0, with the mask in an SGPR pair.
-__device__ __forceinline__ uint32_t select_mask(uint64_t mask, uint32_t if1, uint32_t if0) {
-    uint32_t r;
-    asm("v_cndmask_b32 %0, %1, %2, %3" : "=v"(r) : "v"(if0), "v"(if1), "s"(mask));
-    return r;
-}
-
-// The value of lane ^ lm (lm a power of two below 64, known after unrolling).
-__device__ __forceinline__ uint32_t lane_xor(uint32_t v, int lm, int lane) {
-    switch (lm) {
-        case 1: return (uint32_t)__builtin_amdgcn_mov_dpp((int)v, 0xB1, 0xF, 0xF, false);
-        case 2: return (uint32_t)__builtin_amdgcn_mov_dpp((int)v, 0x4E, 0xF, 0xF, false);
-        case 4: return (uint32_t)__builtin_amdgcn_ds_swizzle((int)v, 0x1F | (4 << 10));
-        case 8: return (uint32_t)__builtin_amdgcn_ds_swizzle((int)v, 0x1F | (8 << 10));
-        case 16: return (uint32_t)__builtin_amdgcn_ds_swizzle((int)v, 0x1F | (16 << 10));
-        default: return (uint32_t)__builtin_amdgcn_ds_bpermute((lane ^ 32) << 2, (int)v);
-    }
-}
-
 __device__ __forceinline__ void sort256_desc(int64_t (&key)[4], int lane) {
 #pragma unroll
     for (int k = 2; k <= 256; k <<= 1) {

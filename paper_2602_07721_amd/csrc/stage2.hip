@@ -107,22 +107,26 @@ __global__ __launch_bounds__(kRrThreads) void compact_rerank_kernel(RetrieveArgs
     }
     const uint32_t P0 = base_g + min(base_e, quota);
     const uint32_t m = (tot & 0xffffu) + (min(base_e + (tot >> 16), quota) - min(base_e, quota));
-    uint32_t gb = base_g + (pre & 0xffffu);
-    uint32_t eb = base_e + (pre >> 16);
+    const uint32_t gb = base_g + (pre & 0xffffu);  // S > theta keys before this thread's 16
+    const uint32_t eb = base_e + (pre >> 16);      // S == theta keys before them
     int32_t* cand = a.cand + row * a.n_cand;
-#pragma unroll
-    for (int j = 0; j < 16; ++j) {
-        int64_t p = -1;
-        if ((gmask >> j) & 1u) {
-            p = gb + min(eb, quota);
-            ++gb;
-        } else if ((emask >> j) & 1u) {
-            if (eb < quota) p = gb + eb;
-            ++eb;
-        }
-        if (p >= 0 && p < a.c_eff) {
-            cand[p] = (int32_t)(i0 + j);
-            s_list[p - P0] = (int32_t)(i0 + j);
+    const uint32_t c_eff = (uint32_t)a.c_eff;
+    // Visit only the selected keys (about 1 in 16); a key's place in the row's
+    // ascending list is the number of taken keys before it.
+    for (uint32_t sel = gmask | emask; sel; sel &= sel - 1u) {
+        const int j = __builtin_ctz(sel);
+        const uint32_t below = (1u << j) - 1u;
+        const uint32_t g = gb + (uint32_t)__popc(gmask & below);
+        const uint32_t e = eb + (uint32_t)__popc(emask & below);
+        uint32_t p = 0xffffffffu;
+        if ((gmask >> j) & 1u)
+            p = g + min(e, quota);
+        else if (e < quota)
+            p = g + e;
+        if (p < c_eff) {
+            const int32_t key = (int32_t)i0 + j;
+            cand[p] = key;
+            s_list[p - P0] = key;
         }
     }
     __syncthreads();
@@ -130,35 +134,49 @@ __global__ __launch_bounds__(kRrThreads) void compact_rerank_kernel(RetrieveArgs
     // ---- RSQ-IP: 8 lanes per candidate, lane l reads record chunk l (subspaces 2l, 2l+1).
     const int slot = tid >> 3;
     float* out = a.cand_score + row * a.n_cand + P0;
-    const uint8_t* rec = a.rec + grp * a.capacity * kRec;
+    const uint4* rec = reinterpret_cast<const uint4*>(a.rec + grp * a.capacity * kRec);
+    const uint32_t two = 2u;
+    const char* tab = reinterpret_cast<const char*>(s_tab);
+    auto entry = [&](uint32_t byte_off) { return *reinterpret_cast<const float*>(tab + byte_off); };
 #pragma unroll 1
     for (uint32_t it = 0; it < m; it += kRrSlots * kRrUnroll) {
         uint4 rc[kRrUnroll];
-        uint32_t ci[kRrUnroll];
 #pragma unroll
         for (int u = 0; u < kRrUnroll; ++u) {
-            ci[u] = it + u * kRrSlots + slot;
-            rc[u] = make_uint4(0, 0, 0, 0);
-            if (ci[u] < m) {
-                const int64_t key = s_list[ci[u]];
-                rc[u] = reinterpret_cast<const uint4*>(rec + key * kRec)[l];
-            }
+            // Past the end, re-read the last candidate; its result is not stored.
+            const uint32_t ci = min(it + u * kRrSlots + slot, m - 1u);
+            rc[u] = rec[(uint64_t)(uint32_t)s_list[ci] * (kRec / 16) + l];
         }
 #pragma unroll
         for (int u = 0; u < kRrUnroll; ++u) {
-            const uint32_t c0 = rc[u].x, c1 = rc[u].y;
+            // Code of coordinate 2k in the low nibble of byte k, of 2k+1 in the high
+            // nibble: one mask per word, then one byte-select shift per lookup.
+            const uint32_t e0 = rc[u].x & 0x0f0f0f0fu, o0 = rc[u].x & 0xf0f0f0f0u;
+            const uint32_t e1 = rc[u].y & 0x0f0f0f0fu, o1 = rc[u].y & 0xf0f0f0f0u;
             float d0 = 0.f, d1 = 0.f;
-#pragma unroll
-            for (int j = 0; j < 8; ++j) {
-                d0 += s_tab[(c0 >> (4 * j)) & 15u] * z[j];
-                d1 += s_tab[(c1 >> (4 * j)) & 15u] * z[8 + j];
-            }
+            d0 += entry(byte_shl2<0>(e0, two)) * z[0];
+            d0 += entry(byte_shr2<0>(o0, two)) * z[1];
+            d0 += entry(byte_shl2<1>(e0, two)) * z[2];
+            d0 += entry(byte_shr2<1>(o0, two)) * z[3];
+            d0 += entry(byte_shl2<2>(e0, two)) * z[4];
+            d0 += entry(byte_shr2<2>(o0, two)) * z[5];
+            d0 += entry(byte_shl2<3>(e0, two)) * z[6];
+            d0 += entry(byte_shr2<3>(o0, two)) * z[7];
+            d1 += entry(byte_shl2<0>(e1, two)) * z[8];
+            d1 += entry(byte_shr2<0>(o1, two)) * z[9];
+            d1 += entry(byte_shl2<1>(e1, two)) * z[10];
+            d1 += entry(byte_shr2<1>(o1, two)) * z[11];
+            d1 += entry(byte_shl2<2>(e1, two)) * z[12];
+            d1 += entry(byte_shr2<2>(o1, two)) * z[13];
+            d1 += entry(byte_shl2<3>(e1, two)) * z[14];
+            d1 += entry(byte_shr2<3>(o1, two)) * z[15];
             float part = __uint_as_float(rc[u].z) * d0 + __uint_as_float(rc[u].w) * d1;
-            part += __shfl_xor(part, 1, 64);
-            part += __shfl_xor(part, 2, 64);
-            part += __shfl_xor(part, 4, 64);
+            part += __uint_as_float(lane_xor(__float_as_uint(part), 1, lane));
+            part += __uint_as_float(lane_xor(__float_as_uint(part), 2, lane));
+            part += __uint_as_float(lane_xor(__float_as_uint(part), 4, lane));
             // + 0.0f turns -0 into +0, so equal estimates compare equal in the top-k keys.
-            if (l == 0 && ci[u] < m) out[ci[u]] = part + 0.0f;
+            const uint32_t ci = it + u * kRrSlots + slot;
+            if (l == 0 && ci < m) out[ci] = part + 0.0f;
         }
     }
 }

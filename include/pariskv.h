@@ -214,7 +214,11 @@ int pariskv_sparse_attend(const pariskv_config* cfg, const void* q, const void* 
  * Errors: UNSUPPORTED for m != 8. */
 int pariskv_quantizer_table(int32_t m, double* tau, double* a);
 
-/* Per-kernel timing with HIP events recorded on the launch stream. */
+/* Per-kernel timing with HIP events attached to the kernel dispatches on the
+ * launch stream.  The first kernel of a call is timed from its dispatch to its
+ * completion; every following kernel of the same call, which the GPU starts as
+ * soon as its predecessor completes, from that predecessor's completion to its
+ * own.  Off by default; a launch while on adds no synchronisation. */
 int pariskv_profile_enable(int32_t on);
 int pariskv_profile_reset(void);
 /* Waits for the recorded events; fills at most max_entries rows. Returns the

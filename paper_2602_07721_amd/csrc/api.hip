@@ -158,6 +158,7 @@ int layout(const pariskv_config* cfg, int32_t batch, int64_t n, const pariskv_bu
 struct Pending {
     std::string name;
     hipEvent_t start, stop;
+    bool own_start;  // false: start is the previous launch's stop event
 };
 struct Acc {
     int64_t launches = 0;
@@ -169,8 +170,6 @@ bool g_prof_on = false;
 std::vector<Pending> g_pending;
 std::vector<hipEvent_t> g_pool;
 std::map<std::string, Acc> g_acc;
-thread_local Pending t_open;
-thread_local bool t_has_open = false;
 
 hipEvent_t pool_get() {
     if (!g_pool.empty()) {
@@ -178,8 +177,10 @@ hipEvent_t pool_get() {
         g_pool.pop_back();
         return e;
     }
+    // Timing-only events: without the system-scope fence the recording does not
+    // write back and invalidate the caches, which would delay and slow the next kernel.
     hipEvent_t e = nullptr;
-    if (hipEventCreate(&e) != hipSuccess) return nullptr;
+    if (hipEventCreateWithFlags(&e, hipEventDisableSystemFence) != hipSuccess) return nullptr;
     return e;
 }
 
@@ -192,7 +193,7 @@ int collect_locked() {
             a.launches += 1;
             a.ms += ms;
         }
-        g_pool.push_back(p.start);
+        if (p.own_start) g_pool.push_back(p.start);
         g_pool.push_back(p.stop);
     }
     g_pending.clear();
@@ -201,22 +202,31 @@ int collect_locked() {
 
 }  // namespace
 
-void prof_begin(const char* name, hipStream_t s) {
-    std::lock_guard<std::mutex> lk(g_prof_mu);
-    if (!g_prof_on) return;
-    hipEvent_t a = pool_get(), b = pool_get();
-    if (!a || !b) return;
-    t_open = Pending{name, a, b};
-    t_has_open = true;
-    hipEventRecord(a, s);
-}
+// Completion event of the previous profiled launch in the current API call.
+thread_local hipEvent_t t_chain = nullptr;
 
-void prof_end(hipStream_t s) {
+void prof_chain_start() { t_chain = nullptr; }
+
+ProfEvents prof_begin(const char* name) {
     std::lock_guard<std::mutex> lk(g_prof_mu);
-    if (!t_has_open) return;
-    t_has_open = false;
-    hipEventRecord(t_open.stop, s);
-    g_pending.push_back(t_open);
+    if (!g_prof_on) return {};
+    hipEvent_t stop = pool_get();
+    if (!stop) return {};
+    if (t_chain) {
+        // Launched right behind another kernel of the same call: timed from that
+        // kernel's completion to this one's.
+        g_pending.push_back(Pending{name, t_chain, stop, false});
+        t_chain = stop;
+        return {nullptr, stop};
+    }
+    hipEvent_t start = pool_get();
+    if (!start) {
+        g_pool.push_back(stop);
+        return {};
+    }
+    g_pending.push_back(Pending{name, start, stop, true});
+    t_chain = stop;
+    return {start, stop};
 }
 
 }  // namespace pariskv
@@ -250,6 +260,7 @@ int pariskv_quantizer_table(int32_t m, double* tau, double* a) {
 
 static int encode_common(const pariskv_config* cfg, const pariskv_index* index, const void* keys,
                          int64_t row0, int64_t t, int32_t batch, bool reset_counts, void* stream) {
+    prof_chain_start();
     int rc = check_config(cfg, batch);
     if (rc) return rc;
     rc = check_index(index);
@@ -300,6 +311,7 @@ int pariskv_workspace_layout(const pariskv_config* cfg, int32_t batch, int64_t n
 int pariskv_retrieve(const pariskv_config* cfg, const pariskv_index* index, const void* q,
                      int64_t n, int32_t batch, const pariskv_budget* budget, int32_t* out_idx,
                      float* out_score, void* workspace, size_t ws_bytes, void* stream) {
+    prof_chain_start();
     pariskv_ws_layout L;
     int rc = layout(cfg, batch, n, budget, &L);
     if (rc) return rc;
@@ -371,6 +383,7 @@ int pariskv_retrieve(const pariskv_config* cfg, const pariskv_index* index, cons
 int pariskv_sparse_attend(const pariskv_config* cfg, const void* q, const void* K, const void* V,
                           int32_t kv_host_mapped, int64_t kv_capacity, const int32_t* idx, int32_t k,
                           int32_t batch, float scale, float* out, void* stream) {
+    prof_chain_start();
     int rc = check_config(cfg, batch);
     if (rc) return rc;
     if (!q || !K || !V || !idx || !out)

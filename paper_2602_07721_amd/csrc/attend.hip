@@ -160,11 +160,10 @@ hipError_t launch_attend(const void* q, const void* K, const void* V, int64_t kv
                          const int32_t* idx, int32_t k, int32_t batch, int32_t hkv, int32_t g,
                          float scale, float* out, hipStream_t s) {
     const int32_t hq = hkv * g;
-    prof_begin("attend", s);
-    hipLaunchKernelGGL(attend_kernel, dim3((unsigned)(batch * hq)), dim3(kAtThreads), 0, s,
+    const ProfEvents pe = prof_begin("attend");
+    hipExtLaunchKernelGGL(attend_kernel, dim3((unsigned)(batch * hq)), dim3(kAtThreads), 0, s, pe.start, pe.stop, 0,
                        static_cast<const __half*>(q), static_cast<const __half*>(K),
                        static_cast<const __half*>(V), kv_capacity, idx, k, hkv, g, hq, scale, out);
-    prof_end(s);
     return hipGetLastError();
 }
 

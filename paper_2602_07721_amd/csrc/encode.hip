@@ -193,9 +193,8 @@ __global__ void zero_u32_kernel(uint32_t* p, int64_t count) {
 hipError_t launch_zero_u32(uint32_t* p, int64_t count, hipStream_t s) {
     if (count <= 0) return hipSuccess;
     const int64_t blocks = (count + 255) / 256;
-    prof_begin("zero_counts", s);
-    hipLaunchKernelGGL(zero_u32_kernel, dim3((unsigned)blocks), dim3(256), 0, s, p, count);
-    prof_end(s);
+    const ProfEvents pe = prof_begin("zero_counts");
+    hipExtLaunchKernelGGL(zero_u32_kernel, dim3((unsigned)blocks), dim3(256), 0, s, pe.start, pe.stop, 0, p, count);
     return hipGetLastError();
 }
 
@@ -208,18 +207,16 @@ hipError_t launch_encode(const void* keys, int64_t n_src, int64_t groups, int64_
         // Bulk: blocks of 2048 keys share one LDS histogram flush.
         const int64_t per = 2048;
         const int64_t bx = (n_src + per - 1) / per;
-        prof_begin("encode", s);
-        hipLaunchKernelGGL(encode_kernel<true>, dim3((unsigned)bx, (unsigned)groups), dim3(kThreads),
-                           0, s, k, n_src, per, row0, capacity, ids, rec, counts, sb, qc);
-        prof_end(s);
+        const ProfEvents pe = prof_begin("encode");
+        hipExtLaunchKernelGGL(encode_kernel<true>, dim3((unsigned)bx, (unsigned)groups), dim3(kThreads),
+                           0, s, pe.start, pe.stop, 0, k, n_src, per, row0, capacity, ids, rec, counts, sb, qc);
     } else {
         // Streaming append: few keys per group, count straight into global memory.
         const int64_t per = kKeysPerIter;
         const int64_t bx = (n_src + per - 1) / per;
-        prof_begin("append", s);
-        hipLaunchKernelGGL(encode_kernel<false>, dim3((unsigned)bx, (unsigned)groups), dim3(kThreads),
-                           0, s, k, n_src, per, row0, capacity, ids, rec, counts, sb, qc);
-        prof_end(s);
+        const ProfEvents pe = prof_begin("append");
+        hipExtLaunchKernelGGL(encode_kernel<false>, dim3((unsigned)bx, (unsigned)groups), dim3(kThreads),
+                           0, s, pe.start, pe.stop, 0, k, n_src, per, row0, capacity, ids, rec, counts, sb, qc);
     }
     return hipGetLastError();
 }

@@ -1,6 +1,7 @@
 // Library-internal declarations shared by the host API and the kernel files.
 #pragma once
 
+#include <hip/hip_ext.h>
 #include <hip/hip_runtime.h>
 
 #include <cstddef>
@@ -138,7 +139,14 @@ hipError_t launch_attend(const void* q, const void* K, const void* V, int64_t kv
                          float scale, float* out, hipStream_t s);
 
 // Kernel-level profiling hooks (no-ops unless enabled).
-void prof_begin(const char* name, hipStream_t s);
-void prof_end(hipStream_t s);
+// Event pair for one kernel launch when profiling is on (nulls otherwise), to be
+// passed to hipExtLaunchKernelGGL so the timestamps are the dispatch's own.
+struct ProfEvents {
+    hipEvent_t start = nullptr;
+    hipEvent_t stop = nullptr;
+};
+ProfEvents prof_begin(const char* name);
+// Starts a new chain of back-to-back launches (called at every API entry).
+void prof_chain_start();
 
 }  // namespace pariskv

@@ -428,25 +428,22 @@ __global__ __launch_bounds__(kThrThreads) void threshold_kernel(RetrieveArgs a) 
 
 hipError_t launch_query_lut(const RetrieveArgs& a, hipStream_t s) {
     const int64_t blocks = (int64_t)a.batch * a.hkv * a.quads * 4;
-    prof_begin("query_lut", s);
-    hipLaunchKernelGGL(query_lut_kernel, dim3((unsigned)blocks), dim3(kLutThreads), 0, s, a);
-    prof_end(s);
+    const ProfEvents pe = prof_begin("query_lut");
+    hipExtLaunchKernelGGL(query_lut_kernel, dim3((unsigned)blocks), dim3(kLutThreads), 0, s, pe.start, pe.stop, 0, a);
     return hipGetLastError();
 }
 
 hipError_t launch_collide(const RetrieveArgs& a, hipStream_t s) {
-    prof_begin("collide", s);
-    hipLaunchKernelGGL(collide_kernel, dim3((unsigned)a.n_chunks, (unsigned)(a.batch * a.hkv * a.quads)),
-                       dim3(kColThreads), 0, s, a);
-    prof_end(s);
+    const ProfEvents pe = prof_begin("collide");
+    hipExtLaunchKernelGGL(collide_kernel, dim3((unsigned)a.n_chunks, (unsigned)(a.batch * a.hkv * a.quads)),
+                       dim3(kColThreads), 0, s, pe.start, pe.stop, 0, a);
     return hipGetLastError();
 }
 
 hipError_t launch_threshold(const RetrieveArgs& a, hipStream_t s) {
     const int64_t rows = (int64_t)a.batch * a.hq;
-    prof_begin("threshold", s);
-    hipLaunchKernelGGL(threshold_kernel, dim3((unsigned)rows), dim3(kThrThreads), 0, s, a);
-    prof_end(s);
+    const ProfEvents pe = prof_begin("threshold");
+    hipExtLaunchKernelGGL(threshold_kernel, dim3((unsigned)rows), dim3(kThrThreads), 0, s, pe.start, pe.stop, 0, a);
     return hipGetLastError();
 }
 

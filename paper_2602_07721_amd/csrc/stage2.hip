@@ -522,37 +522,34 @@ __global__ void pad_outputs_kernel(int32_t* out_idx, float* out_score, int64_t c
 }  // namespace
 
 hipError_t launch_compact_rerank(const RetrieveArgs& a, hipStream_t s) {
-    prof_begin("compact_rerank", s);
-    hipLaunchKernelGGL(compact_rerank_kernel, dim3((unsigned)a.n_chunks, (unsigned)(a.batch * a.hq)),
-                       dim3(kRrThreads), 0, s, a);
-    prof_end(s);
+    const ProfEvents pe = prof_begin("compact_rerank");
+    hipExtLaunchKernelGGL(compact_rerank_kernel, dim3((unsigned)a.n_chunks, (unsigned)(a.batch * a.hq)),
+                       dim3(kRrThreads), 0, s, pe.start, pe.stop, 0, a);
     return hipGetLastError();
 }
 
 hipError_t launch_topk(const RetrieveArgs& a, hipStream_t s) {
     const dim3 grid((unsigned)(a.batch * a.hq));
     const int64_t C = a.c_eff;
-    prof_begin("topk", s);
+    const ProfEvents pe = prof_begin("topk");
     if (C <= 1024 * 4)
-        hipLaunchKernelGGL((topk_lds_kernel<1024, 4>), grid, dim3(1024), 0, s, a);
+        hipExtLaunchKernelGGL((topk_lds_kernel<1024, 4>), grid, dim3(1024), 0, s, pe.start, pe.stop, 0, a);
     else if (C <= 1024 * 8)
-        hipLaunchKernelGGL((topk_lds_kernel<1024, 8>), grid, dim3(1024), 0, s, a);
+        hipExtLaunchKernelGGL((topk_lds_kernel<1024, 8>), grid, dim3(1024), 0, s, pe.start, pe.stop, 0, a);
     else if (C <= 1024 * 16)
-        hipLaunchKernelGGL((topk_lds_kernel<1024, 16>), grid, dim3(1024), 0, s, a);
+        hipExtLaunchKernelGGL((topk_lds_kernel<1024, 16>), grid, dim3(1024), 0, s, pe.start, pe.stop, 0, a);
     else if (C <= 1024 * 32)
-        hipLaunchKernelGGL((topk_reg_kernel<1024, 32>), grid, dim3(1024), 0, s, a);
+        hipExtLaunchKernelGGL((topk_reg_kernel<1024, 32>), grid, dim3(1024), 0, s, pe.start, pe.stop, 0, a);
     else
-        hipLaunchKernelGGL((topk_reg_kernel<1024, 64>), grid, dim3(1024), 0, s, a);
-    prof_end(s);
+        hipExtLaunchKernelGGL((topk_reg_kernel<1024, 64>), grid, dim3(1024), 0, s, pe.start, pe.stop, 0, a);
     return hipGetLastError();
 }
 
 hipError_t launch_pad_outputs(const RetrieveArgs& a, hipStream_t s) {
     const int64_t count = (int64_t)a.batch * a.hq * a.top_k;
-    prof_begin("pad_outputs", s);
-    hipLaunchKernelGGL(pad_outputs_kernel, dim3((unsigned)((count + 255) / 256)), dim3(256), 0, s,
+    const ProfEvents pe = prof_begin("pad_outputs");
+    hipExtLaunchKernelGGL(pad_outputs_kernel, dim3((unsigned)((count + 255) / 256)), dim3(256), 0, s, pe.start, pe.stop, 0,
                        a.out_idx, a.out_score, count);
-    prof_end(s);
     return hipGetLastError();
 }
 

@@ -48,6 +48,13 @@ def parse():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-groups", type=int, default=8)
     ap.add_argument("--cpu-steps", type=int, default=8)
+    ap.add_argument("--kv-host", action="store_true",
+                    help="keep K/V in pinned host memory and attend through host-mapped pointers")
+    ap.add_argument("--extras", action="store_true",
+                    help="also measure the drift workload (append + retrieve + attend per step) and "
+                         "attention over K/V in pinned host memory")
+    ap.add_argument("--drift-steps", type=int, default=4096,
+                    help="decode steps of the drift measurement (the full workload runs 32768)")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="also run one plain 1 GiB device copy (for scaling HBM counters)")
     return ap.parse_args()
@@ -146,6 +153,115 @@ def cpu_baseline(wc, K, V, Qs, signs, budget, scale, groups, steps):
     }
 
 
+def drift_run(pk, torch, np, workloads, dev, steps):
+    """The drift workload: 32K-key prefill, then per step one appended key per
+    (sequence, KV head), retrieval with C = ceil(n/16), C_rho = 2C and attention.
+    Returns per-step time and recall@k against exact top-k every 256 steps."""
+    wc = workloads.CONFIGS["drift"]
+    signs = workloads.rotation_signs(wc.seed)
+    total = steps
+    cap = wc.n + total
+    K0, V0 = workloads.layer_kv(wc, threads=16)
+    Kall = np.zeros((wc.batch, wc.n_kv_heads, cap, wc.head_dim), np.float16)
+    Vall = np.zeros_like(Kall)
+    Kall[:, :, :wc.n] = K0
+    Vall[:, :, :wc.n] = V0
+    rng = np.random.default_rng(wc.seed)
+    for s in range(wc.batch):
+        for h in range(wc.n_kv_heads):
+            Kall[s, h, wc.n:] = workloads.drift_keys(wc.seed, s, h, 0, total, total)
+            Vall[s, h, wc.n:] = rng.standard_normal((total, wc.head_dim)).astype(np.float16)
+    Kd = torch.from_numpy(Kall).to(dev)
+    Vd = torch.from_numpy(Vall).to(dev)
+    cfg = pk.Config(wc.n_kv_heads, wc.q_per_kv, cap, signs)
+    index = pk.Index.empty(cfg, wc.batch, dev)
+    pk.encode(cfg, index, Kd[:, :, :wc.n].contiguous())
+    hq = cfg.n_q_heads
+    c_max = -(-cap // 16)
+    ws = torch.empty(pk.retrieve_workspace_size(cfg, wc.batch, cap, pk.Budget(c_max, 2 * c_max, wc.top_k)),
+                     dtype=torch.uint8, device=dev)
+    out_idx = torch.empty((wc.batch, hq, wc.top_k), dtype=torch.int32, device=dev)
+    out = torch.empty((wc.batch, hq, wc.head_dim), dtype=torch.float32, device=dev)
+    # Queries of step t: fresh draws from the current key law, one per query head.
+    evals = set(range(0, total, 256)) | {total - 1}
+    Qs = np.stack([np.stack([workloads.drift_queries(wc.seed, s, h, total, wc.q_per_kv)
+                             for h in range(wc.n_kv_heads)], axis=1)
+                   for s in range(wc.batch)], axis=1).reshape(total, wc.batch, hq, wc.head_dim)
+    Qd = torch.from_numpy(Qs).to(dev)
+    newk = Kd[:, :, wc.n:].permute(2, 0, 1, 3).contiguous()  # [t][b][Hkv][D]
+    scale = 1.0 / np.sqrt(wc.head_dim)
+    recalls = []
+    block_us = []  # per-step GPU time of each block of steps between evaluations
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    t_block = 0
+    for t in range(total):
+        n = wc.n + t + 1
+        C = -(-n // 16)
+        bud = pk.Budget(C, 2 * C, wc.top_k)
+        pk.append(cfg, index, newk[t].unsqueeze(2), wc.n + t)
+        pk.retrieve(cfg, index, Qd[t], n, bud, out_idx=out_idx, workspace=ws)
+        pk.sparse_attend(cfg, Qd[t], Kd, Vd, out_idx, scale, out=out)
+        t_block += 1
+        if t in evals:
+            e1.record()
+            torch.cuda.synchronize()
+            block_us.append((t, e0.elapsed_time(e1) * 1e3 / t_block))
+            # exact top-k by float32 inner products over the n cached keys (reference only)
+            kf = Kd[:, :, :n].float()
+            q = Qd[t].float().reshape(wc.batch, wc.n_kv_heads, wc.q_per_kv, wc.head_dim)
+            sc = torch.matmul(q, kf.transpose(2, 3).contiguous())
+            ex = torch.topk(sc, wc.top_k, dim=-1).indices.reshape(wc.batch, hq, wc.top_k)
+            got = out_idx.long()
+            hit = (got.unsqueeze(-1) == ex.unsqueeze(-2)).any(-1).float().mean().item()
+            recalls.append((t, hit))
+            del kf, sc
+            torch.cuda.synchronize()
+            t_block = 0
+            e0.record()
+    torch.cuda.synchronize()
+    steps_w = [b for b in block_us[1:]]  # the first block (step 0 alone) carries warm-up
+    us = float(np.mean([u for _, u in steps_w])) if steps_w else block_us[0][1]
+    r = np.array([h for _, h in recalls])
+    return {
+        "workload": (f"drift: {wc.batch} seqs x {wc.n_kv_heads} KV heads x {wc.q_per_kv} query heads, "
+                     f"{wc.n}-key prefill + {total} decode steps (1 appended key per KV head per step, "
+                     f"mean drifting 2 sigma), C = ceil(n/16), C_rho = 2C, k = {wc.top_k}"),
+        "us_per_step_append_retrieve_attend": round(us, 2),
+        "us_per_step_first_block": round(block_us[1][1], 2) if len(block_us) > 1 else None,
+        "us_per_step_last_block": round(block_us[-1][1], 2),
+        "timing": "HIP events around each block of 256 steps (host launch included), between recall checks",
+        "recall_at_k_vs_exact": {"first": round(float(r[0]), 4), "last": round(float(r[-1]), 4),
+                                 "min": round(float(r.min()), 4), "mean": round(float(r.mean()), 4),
+                                 "every": 256, "points": len(r)},
+        "note": "exact top-k by float32 inner products on the GPU (a quality figure, parity unpinned)",
+    }
+
+
+def host_link_run(pk, torch, np, cfg, K, V, Qd, idx_list, scale, dev, reps=8):
+    """Sparse attention with K/V in pinned host memory, read through host-mapped pointers."""
+    Kh = torch.from_numpy(K).pin_memory()
+    Vh = torch.from_numpy(V).pin_memory()
+    out = torch.empty((Qd.shape[1], cfg.n_q_heads, 128), dtype=torch.float32, device=dev)
+    pk.sparse_attend(cfg, Qd[0], Kh, Vh, idx_list[0], scale, out=out, kv_host_mapped=True)
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for r in range(reps):
+        i = r % len(idx_list)
+        pk.sparse_attend(cfg, Qd[i], Kh, Vh, idx_list[i], scale, out=out, kv_host_mapped=True)
+    e1.record()
+    torch.cuda.synchronize()
+    us = e0.elapsed_time(e1) * 1e3 / reps
+    k = idx_list[0].shape[-1]
+    rows = idx_list[0].numel()
+    row_bytes = rows * 2 * 128 * 2
+    return {"us_per_attend": round(us, 1), "kv_bytes": row_bytes,
+            "host_link_GBps": round(row_bytes / (us * 1e-6) / 1e9, 2),
+            "note": f"{rows} K and V rows of 256 B ({k} per query head) gathered over the host link per call"}
+
+
 def main():
     args = parse()
     world = int(os.environ.get("WORLD_SIZE", "1"))
@@ -178,8 +294,12 @@ def main():
           flush=True)
 
     dev = torch.device("cuda:0")
-    Kd = torch.from_numpy(K).to(dev)
-    Vd = torch.from_numpy(V).to(dev)
+    if args.kv_host:
+        Kd = torch.from_numpy(K).pin_memory()
+        Vd = torch.from_numpy(V).pin_memory()
+    else:
+        Kd = torch.from_numpy(K).to(dev)
+        Vd = torch.from_numpy(V).to(dev)
     Qd = torch.from_numpy(np.stack(Qs)).to(dev)
     cfg = pk.Config(wc.n_kv_heads, wc.q_per_kv, wc.n, signs)
     index = pk.Index.empty(cfg, wc.batch, dev)
@@ -194,11 +314,12 @@ def main():
 
     # Prefill encode, timed on its own.  The first call also loads the code objects,
     # so the timed call is the second (encode rewrites the index and its counts).
-    pk.encode(cfg, index, Kd)
+    Kenc = Kd.to(dev) if args.kv_host else Kd  # encode reads keys from device memory
+    pk.encode(cfg, index, Kenc)
     torch.cuda.synchronize()
     e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     e0.record()
-    pk.encode(cfg, index, Kd)
+    pk.encode(cfg, index, Kenc)
     e1.record()
     torch.cuda.synchronize()
     enc_ms = e0.elapsed_time(e1)
@@ -206,7 +327,7 @@ def main():
 
     def step(s):
         pk.retrieve(cfg, index, Qd[s], wc.n, budget, out_idx=out_idx, out_score=out_score, workspace=ws)
-        pk.sparse_attend(cfg, Qd[s], Kd, Vd, out_idx, scale, out=out)
+        pk.sparse_attend(cfg, Qd[s], Kd, Vd, out_idx, scale, out=out, kv_host_mapped=args.kv_host)
 
     for s in range(args.warmup):
         if not args.no_flush:
@@ -286,6 +407,23 @@ def main():
     else:
         copy_gbs = None
 
+    extras = {}
+    if args.extras:
+        if not args.kv_host:
+            # index sets of the last few timed steps, for host-mapped attention
+            idx_list = []
+            for i in range(4):
+                st = args.warmup + args.steps - 1 - i
+                oi = torch.empty_like(out_idx)
+                pk.retrieve(cfg, index, Qd[st], wc.n, budget, out_idx=oi, workspace=ws)
+                idx_list.append(oi)
+            torch.cuda.synchronize()
+            extras["host_link"] = host_link_run(pk, torch, np, cfg, K, V, Qd[-4:].flip(0), idx_list, scale, dev)
+            extras["host_link"]["workload"] = f"{wc.name}, K/V in pinned host memory"
+        del Kd, Vd
+        torch.cuda.empty_cache()
+        extras["drift"] = drift_run(pk, torch, np, workloads, dev, args.drift_steps)
+
     cpu = None
     if not args.no_cpu_baseline:
         cpu = cpu_baseline(wc, K, V, Qs, signs, budget, scale, args.cpu_groups,
@@ -308,7 +446,9 @@ def main():
         "config": {
             "workload": (f"{wc.name}: {wc.batch} seqs x {wc.n_kv_heads} KV heads x {wc.q_per_kv} query "
                          f"heads, N={wc.n}, D={wc.head_dim}, B=16, C={wc.n_cand}, C_rho={wc.n_collide}, "
-                         f"k={wc.top_k}, float16 K/V/Q in HBM"),
+                         f"k={wc.top_k}, float16 K/V/Q, "
+                         + ("K/V in pinned host memory read through host-mapped pointers, Q and index "
+                            "in HBM" if args.kv_host else "all in HBM")),
             "caches": "flushed between steps" if not args.no_flush else "warm",
         },
         "p10_us": round(float(np.percentile(step_ms, 10) * 1e3), 2),
@@ -328,6 +468,7 @@ def main():
         "copy_GBps": round(copy_gbs, 1) if copy_gbs else None,
         "cpu_baseline": cpu,
     }
+    result.update(extras)
     print(json.dumps(result), flush=True)
 
 

@@ -117,6 +117,18 @@ def drift_query(seed, seq, kvh, step, total_steps, n_queries, D=D_DEFAULT):
     return (mu[None, :] + law.scale[None, :] * eps).astype(np.float16)
 
 
+def drift_queries(seed, seq, kvh, total_steps, n_queries, D=D_DEFAULT):
+    """Queries of every step t in [0, total_steps) at once, [t][n_queries][D]: draws
+    from the key law of step t (as drift_query), one random stream per head."""
+    law = head_law(seed, seq, kvh, D)
+    delta = np.where(_rng(_TAG_DRIFT, seed, seq, kvh).integers(0, 2, size=D) == 1, -1.0, 1.0)
+    steps = np.arange(total_steps, dtype=np.float64)
+    mu = law.mu[None, :] + (steps / total_steps)[:, None] * 2.0 * (law.scale * delta)[None, :]
+    r = _rng(_TAG_QUERY, seed, seq, kvh, 2_000_000)
+    eps = r.standard_normal(size=(total_steps, n_queries, D))
+    return (mu[:, None, :] + law.scale[None, None, :] * eps).astype(np.float16)
+
+
 @dataclass
 class Config:
     """Shapes and budgets of one workload."""

@@ -436,7 +436,7 @@ hipError_t launch_query_lut(const RetrieveArgs& a, hipStream_t s) {
 hipError_t launch_collide(const RetrieveArgs& a, hipStream_t s) {
     const ProfEvents pe = prof_begin("collide");
     hipExtLaunchKernelGGL(collide_kernel, dim3((unsigned)a.n_chunks, (unsigned)(a.batch * a.hkv * a.quads)),
-                          dim3(kColThreads), 0, s, pe.start, pe.stop, 0, a);
+                       dim3(kColThreads), 0, s, pe.start, pe.stop, 0, a);
     return hipGetLastError();
 }
 

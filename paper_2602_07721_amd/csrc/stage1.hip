@@ -358,55 +358,61 @@ __global__ __launch_bounds__(kColThreads) void collide_kernel(RetrieveArgs a) {
 
 // ---------------------------------------------------------------- threshold
 
-constexpr int kThrThreads = 256;  // one block per query head
+constexpr int kThrThreads = 1024;  // one block per query head
+constexpr int kThrWaves = kThrThreads / 64;
 
 __global__ __launch_bounds__(kThrThreads) void threshold_kernel(RetrieveArgs a) {
-    __shared__ uint32_t s_part[kThrThreads / 64][2][64];
+    __shared__ uint32_t s_part[kThrWaves][2][64];
+    __shared__ uint32_t s_wtot[2][kThrWaves];
+    __shared__ int s_theta;
     const int tid = threadIdx.x;
     const int lane = tid & 63, wave = tid >> 6;
     const int64_t row = blockIdx.x;
     const uint32_t* sfx = a.chunk_sfx + row * a.n_chunks * kSfx;
-    // Whole-row suffix histogram; lane holds v = lane and v = 64 + lane.  Each
-    // wave sums every 4th chunk with 8 independent loads in flight.
-    uint32_t tl[8], th[8];
+    // Whole-row suffix histogram; lane holds v = lane and v = 64 + lane.  Wave w
+    // sums chunks w, w + 16, ... with 4 independent loads in flight.
+    uint32_t tl[4], th[4];
 #pragma unroll
-    for (int u = 0; u < 8; ++u) tl[u] = th[u] = 0;
-    for (int64_t c0 = wave; c0 < a.n_chunks; c0 += 4 * 8) {
+    for (int u = 0; u < 4; ++u) tl[u] = th[u] = 0;
+    for (int64_t c0 = wave; c0 < a.n_chunks; c0 += kThrWaves * 4) {
 #pragma unroll
-        for (int u = 0; u < 8; ++u) {
-            const int64_t c = c0 + 4 * u;
+        for (int u = 0; u < 4; ++u) {
+            const int64_t c = c0 + kThrWaves * u;
             if (c < a.n_chunks) {
                 tl[u] += sfx[c * kSfx + lane];
                 if (lane < kSfx - 64) th[u] += sfx[c * kSfx + 64 + lane];
             }
         }
     }
-#pragma unroll
-    for (int u = 1; u < 8; ++u) { tl[0] += tl[u]; th[0] += th[u]; }
-    s_part[wave][0][lane] = tl[0];
-    s_part[wave][1][lane] = th[0];
+    s_part[wave][0][lane] = (tl[0] + tl[1]) + (tl[2] + tl[3]);
+    s_part[wave][1][lane] = (th[0] + th[1]) + (th[2] + th[3]);
     __syncthreads();
-    if (wave != 0) return;
-    uint32_t ttl = 0, tth = 0;
-#pragma unroll
-    for (int w = 0; w < kThrThreads / 64; ++w) { ttl += s_part[w][0][lane]; tth += s_part[w][1][lane]; }
     const uint32_t C = (uint32_t)a.c_eff;
-    // theta = largest v with #{S >= v} >= C (suffix counts fall with v; #{S >= 0} = n >= C).
-    const uint64_t ok_lo = __ballot(ttl >= C);
-    const uint64_t ok_hi = __ballot(lane < kBins - 64 && tth >= C);
-    const int theta = ok_hi ? 64 + (63 - __clzll(ok_hi)) : (63 - __clzll(ok_lo));
-    const uint32_t gt = theta + 1 < 64 ? __shfl(ttl, theta + 1, 64) : __shfl(tth, theta + 1 - 64, 64);
-    if (lane == 0) {
-        int32_t* t = a.thresh + row * 4;
-        t[0] = theta;
-        t[1] = (int32_t)gt;
-        t[2] = (int32_t)(C - gt);
-        t[3] = (int32_t)C;
+    if (wave == 0) {
+        uint32_t ttl = 0, tth = 0;
+#pragma unroll
+        for (int w = 0; w < kThrWaves; ++w) { ttl += s_part[w][0][lane]; tth += s_part[w][1][lane]; }
+        // theta = largest v with #{S >= v} >= C (suffix counts fall with v; #{S >= 0} = n >= C).
+        const uint64_t ok_lo = __ballot(ttl >= C);
+        const uint64_t ok_hi = __ballot(lane < kBins - 64 && tth >= C);
+        const int theta = ok_hi ? 64 + (63 - __clzll(ok_hi)) : (63 - __clzll(ok_lo));
+        const uint32_t gt = theta + 1 < 64 ? __shfl(ttl, theta + 1, 64) : __shfl(tth, theta + 1 - 64, 64);
+        if (lane == 0) {
+            int32_t* t = a.thresh + row * 4;
+            t[0] = theta;
+            t[1] = (int32_t)gt;
+            t[2] = (int32_t)(C - gt);
+            t[3] = (int32_t)C;
+            s_theta = theta;
+        }
     }
-    // Keys with S > theta and S == theta in the chunks before each chunk.
+    __syncthreads();
+    const int theta = s_theta;
+    // Keys with S > theta and S == theta in the chunks before each chunk: thread t
+    // takes chunk cb + t; wave scans, then a scan of the wave totals.
     uint32_t carry_g = 0, carry_e = 0;
-    for (int64_t cb = 0; cb < a.n_chunks; cb += 64) {
-        const int64_t c = cb + lane;
+    for (int64_t cb = 0; cb < a.n_chunks; cb += kThrThreads) {
+        const int64_t c = cb + tid;
         uint32_t g = 0, e = 0;
         if (c < a.n_chunks) {
             g = sfx[c * kSfx + theta + 1];
@@ -414,13 +420,24 @@ __global__ __launch_bounds__(kThrThreads) void threshold_kernel(RetrieveArgs a) 
         }
         const uint32_t ig = wave_incl_scan_u32(g, lane);
         const uint32_t ie = wave_incl_scan_u32(e, lane);
+        if (lane == 63) { s_wtot[0][wave] = ig; s_wtot[1][wave] = ie; }
+        __syncthreads();
+        uint32_t pg = 0, pe = 0, tg = 0, te = 0;
+#pragma unroll
+        for (int w = 0; w < kThrWaves; ++w) {
+            const uint32_t xg = s_wtot[0][w], xe = s_wtot[1][w];
+            if (w < wave) { pg += xg; pe += xe; }
+            tg += xg;
+            te += xe;
+        }
         if (c < a.n_chunks) {
             int32_t* cbp = a.chunk_base + (row * a.n_chunks + c) * 2;
-            cbp[0] = (int32_t)(carry_g + ig - g);
-            cbp[1] = (int32_t)(carry_e + ie - e);
+            cbp[0] = (int32_t)(carry_g + pg + ig - g);
+            cbp[1] = (int32_t)(carry_e + pe + ie - e);
         }
-        carry_g += __shfl(ig, 63, 64);
-        carry_e += __shfl(ie, 63, 64);
+        carry_g += tg;
+        carry_e += te;
+        __syncthreads();  // s_wtot is rewritten by the next round
     }
 }
 

@@ -229,8 +229,12 @@ __global__ __launch_bounds__(TH) void topk_lds_kernel(RetrieveArgs a) {
     constexpr int kWaves = TH / 64;
     constexpr int kCap = TH * EPT;
     constexpr int kNB = 2048;
+    // Up to 16 keys per thread the candidate indices are staged in LDS too (the
+    // winners then read them without a global round trip); beyond that they are
+    // read back from global memory for the k winners only.
+    constexpr bool kStageIdx = EPT <= 16;
     __shared__ uint32_t s_key[kCap];
-    __shared__ int32_t s_idx[kCap];
+    __shared__ int32_t s_idx[kStageIdx ? kCap : 1];
     __shared__ uint32_t s_hist[2][kNB];
     __shared__ uint32_t s_w[kWaves];
     __shared__ uint32_t s_mm[2][kWaves];
@@ -245,7 +249,8 @@ __global__ __launch_bounds__(TH) void topk_lds_kernel(RetrieveArgs a) {
     const int32_t* cand = a.cand + row * a.n_cand;
     if (tid == 0) s_nsmall = 0;
 
-    // Coalesced staging (rows of cand / cand_score are 256-byte aligned).
+    // Coalesced staging of the estimates as order-preserving keys (rows of cand and
+    // cand_score are 256-byte aligned).
     for (int p4 = tid; p4 < kCap / 4; p4 += TH) {
         const int p = 4 * p4;
         uint4 kv = make_uint4(0, 0, 0, 0);
@@ -253,18 +258,21 @@ __global__ __launch_bounds__(TH) void topk_lds_kernel(RetrieveArgs a) {
         if (p + 3 < C) {
             const float4 f = reinterpret_cast<const float4*>(sc)[p4];
             kv = make_uint4(order_key(f.x), order_key(f.y), order_key(f.z), order_key(f.w));
-            iv = reinterpret_cast<const int4*>(cand)[p4];
+            if (kStageIdx) iv = reinterpret_cast<const int4*>(cand)[p4];
         } else {
             uint32_t k4[4] = {0, 0, 0, 0};
             int32_t i4[4] = {-1, -1, -1, -1};
 #pragma unroll
             for (int q = 0; q < 4; ++q)
-                if (p + q < C) { k4[q] = order_key(sc[p + q]); i4[q] = cand[p + q]; }
+                if (p + q < C) {
+                    k4[q] = order_key(sc[p + q]);
+                    if (kStageIdx) i4[q] = cand[p + q];
+                }
             kv = make_uint4(k4[0], k4[1], k4[2], k4[3]);
             iv = make_int4(i4[0], i4[1], i4[2], i4[3]);
         }
         reinterpret_cast<uint4*>(s_key)[p4] = kv;
-        reinterpret_cast<int4*>(s_idx)[p4] = iv;
+        if (kStageIdx) reinterpret_cast<int4*>(s_idx)[p4] = iv;
     }
     for (int i = tid; i < 2 * kNB; i += TH) (&s_hist[0][0])[i] = 0;
     __syncthreads();
@@ -393,7 +401,7 @@ __global__ __launch_bounds__(TH) void topk_lds_kernel(RetrieveArgs a) {
             ++eb;
         }
         if (p < (uint32_t)kk) {
-            oi[p] = s_idx[tid * EPT + e];
+            oi[p] = kStageIdx ? s_idx[tid * EPT + e] : cand[tid * EPT + e];
             if (os) os[p] = key_float(key[e]);
         }
     }
@@ -539,7 +547,7 @@ hipError_t launch_topk(const RetrieveArgs& a, hipStream_t s) {
     else if (C <= 1024 * 16)
         hipExtLaunchKernelGGL((topk_lds_kernel<1024, 16>), grid, dim3(1024), 0, s, pe.start, pe.stop, 0, a);
     else if (C <= 1024 * 32)
-        hipExtLaunchKernelGGL((topk_reg_kernel<1024, 32>), grid, dim3(1024), 0, s, pe.start, pe.stop, 0, a);
+        hipExtLaunchKernelGGL((topk_lds_kernel<1024, 32>), grid, dim3(1024), 0, s, pe.start, pe.stop, 0, a);
     else
         hipExtLaunchKernelGGL((topk_reg_kernel<1024, 64>), grid, dim3(1024), 0, s, pe.start, pe.stop, 0, a);
     return hipGetLastError();

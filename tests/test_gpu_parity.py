@@ -81,6 +81,8 @@ EDGE = [
     ("k_odd_ragged", 1, 1, 2, 777, (333, 555, 77)),
     ("big_C", 1, 1, 2, 40000, (10000, 20000, 300)),
     ("huge_C", 1, 1, 1, 70000, (40000, 60000, 2048)),
+    ("C_20000", 1, 1, 2, 40000, (20000, 30000, 1000)),      # top-k staging 32 keys per thread
+    ("many_chunks", 1, 1, 1, 300000, (4096, 8192, 256)),    # 74 chunks: multi-wave chunk prefix
 ]
 
 

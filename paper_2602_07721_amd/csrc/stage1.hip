@@ -199,7 +199,7 @@ __global__ __launch_bounds__(kLutThreads) void query_lut_kernel(RetrieveArgs a) 
 constexpr int kColThreads = 256;
 constexpr int kColWaves = kColThreads / 64;
 constexpr int kColKeysPerIter = 4 * kColThreads;  // 4 keys per thread per iteration
-constexpr int kLowCut = 4;  // scores below this are counted in registers, not by LDS atomics
+constexpr int kLowCut = 2;  // scores below this are counted in registers, not by LDS atomics
 // Scores >= kLowCut go to one of 4 histogram copies picked by lane & 3 (fewer
 // same-address atomics per instruction), 16-bit counters (a copy sees at most
 // 1024 keys per chunk): value v sits in word (v - kLowCut) mod kHistWords, low
@@ -259,23 +259,30 @@ __global__ __launch_bounds__(kColThreads) void collide_kernel(RetrieveArgs a) {
 #pragma unroll
     for (int v = 0; v < kLowCut - 1; ++v) cnt[v] = 0;
 
-    for (int64_t base = c0; base < c1; base += kColKeysPerIter) {
+    // 32-bit key offsets from block-uniform bases, so loads and stores use a scalar
+    // base address plus one vector offset.
+    const uint8_t* idc = ids + c0 * kB;
+    const uint32_t nkeys = (uint32_t)(c1 - c0);
+    uint8_t* sbase[4];
+#pragma unroll
+    for (int h = 0; h < 4; ++h) sbase[h] = a.score8 + (row0 + min(h, nh - 1)) * a.n_pad + c0;
+    for (uint32_t base = 0; base < nkeys; base += kColKeysPerIter) {
         // Key base + tid + 256 j: one 16-byte id row per lane, a wave reads 1 KiB contiguous.
         uint4 w[4];
 #pragma unroll
         for (int j = 0; j < 4; ++j) {
-            const int64_t i = base + tid + kColThreads * j;
-            w[j] = i < c1 ? *reinterpret_cast<const uint4*>(ids + i * kB) : make_uint4(0, 0, 0, 0);
+            const uint32_t i = base + tid + kColThreads * j;
+            w[j] = i < nkeys ? *reinterpret_cast<const uint4*>(idc + i * kB) : make_uint4(0, 0, 0, 0);
         }
 #pragma unroll
         for (int j = 0; j < 4; ++j) {
-            const int64_t i = base + tid + kColThreads * j;
+            const uint32_t i = base + tid + kColThreads * j;
             const uint32_t ww[4] = {w[j].x, w[j].y, w[j].z, w[j].w};
             uint32_t acc = 0;
 #pragma unroll
             for (int b = 0; b < kB; ++b)
                 acc += s_lut[b * kCentroids + ((ww[b >> 2] >> (8 * (b & 3))) & 0xffu)];
-            const bool live = i < c1;
+            const bool live = i < nkeys;
             acc = live ? acc : 0u;  // a key past the end scores 0 for every head
             // Low scores are frequent: count #{S >= v} for v < kLowCut for the 4 heads at
             // once.  Bytes are at most 96, so (S | 0x80) - v keeps its top bit iff S >= v
@@ -284,8 +291,8 @@ __global__ __launch_bounds__(kColThreads) void collide_kernel(RetrieveArgs a) {
 #pragma unroll
             for (int v = 1; v < kLowCut; ++v)
                 cnt[v - 1] += ((x - (uint32_t)v * 0x01010101u) & 0x80808080u) >> 7;
-            // Higher scores are rare and spread out: exact per-value LDS histogram.  Slots
-            // of the last quad without a head have an all-zero bonus table, so score 0.
+            // Higher scores: exact per-value LDS histogram.  Slots of the last quad
+            // without a head have an all-zero bonus table, so score 0.
 #pragma unroll
             for (int h = 0; h < 4; ++h) {
                 const uint32_t sh = (acc >> (8 * h)) & 0xffu;
@@ -300,7 +307,7 @@ __global__ __launch_bounds__(kColThreads) void collide_kernel(RetrieveArgs a) {
             if (live) {
 #pragma unroll
                 for (int h = 0; h < 4; ++h)
-                    if (h < nh) a.score8[(row0 + h) * a.n_pad + i] = (uint8_t)(acc >> (8 * h));
+                    if (h < nh) sbase[h][i] = (uint8_t)(acc >> (8 * h));
             }
         }
     }

@@ -214,6 +214,15 @@ int pariskv_sparse_attend(const pariskv_config* cfg, const void* q, const void* 
  * Errors: UNSUPPORTED for m != 8. */
 int pariskv_quantizer_table(int32_t m, double* tau, double* a);
 
+/* Rotation signs of R = H_D diag(s) / sqrt(D) (Sec. "Preprocessing" (1); the
+ * paper names an SRHT without a construction): s_j = -1 when bit 63 of
+ * splitmix64(seed + j) is set, else +1, where splitmix64(x) is the first output
+ * of a SplitMix64 generator whose state is x (state += 0x9E3779B97F4A7C15, then
+ * the two xor-shift-multiply rounds and a final xor-shift).  Writes D int8
+ * values to host memory `out`, ready for pariskv_config.rot_signs.  Host only.
+ * Errors: INVALID for D < 1 or a null `out`. */
+int pariskv_rotation_signs(uint64_t seed, int32_t D, int8_t* out);
+
 /* Per-kernel timing with HIP events attached to the kernel dispatches on the
  * launch stream.  The first kernel of a call is timed from its dispatch to its
  * completion; every following kernel of the same call, which the GPU starts as

@@ -8,9 +8,10 @@ randomized Hadamard transform
     R = H_D diag(s) / sqrt(D),
 
 with H_D the natural-order (Sylvester) Walsh-Hadamard matrix,
-H[i, j] = (-1)^{popcount(i & j)}, and s in {+1, -1}^D random signs drawn by
-the caller (they are an input, not generated here).  R is orthogonal
-because H H^T = D I.
+H[i, j] = (-1)^{popcount(i & j)}, and s in {+1, -1}^D random signs.  R is
+orthogonal because H H^T = D I.  The signs are an input everywhere; a seeded
+generator is provided (`seeded_signs`): s_j = -1 iff the top bit of the first
+SplitMix64 output from state seed + j is set.
 """
 
 import numpy as np
@@ -57,3 +58,22 @@ def fwht(x):
         y = y.reshape(y.shape[:-3] + (D,))
         h *= 2
     return y
+
+
+_MASK64 = (1 << 64) - 1
+
+
+def splitmix64(state):
+    """First output of the SplitMix64 generator (Steele, Lea, Flood, "Fast
+    splittable pseudorandom number generators", 2014) started at `state`:
+    advance the state by the golden-ratio increment, then mix it."""
+    z = (state + 0x9E3779B97F4A7C15) & _MASK64
+    z = ((z ^ (z >> 30)) * 0xBF58476D1CE4E5B9) & _MASK64
+    z = ((z ^ (z >> 27)) * 0x94D049BB133111EB) & _MASK64
+    return z ^ (z >> 31)
+
+
+def seeded_signs(seed, D):
+    """s_j = -1 if bit 63 of splitmix64(seed + j) is set, else +1 (int8)."""
+    return np.array([-1 if splitmix64((seed + j) & _MASK64) >> 63 else 1 for j in range(D)],
+                    dtype=np.int8)

@@ -19,7 +19,7 @@ import numpy as np
 
 __all__ = [
     "PariskvError", "Config", "Budget", "Index", "lib", "encode", "append", "retrieve",
-    "retrieve_workspace_size", "workspace_layout", "sparse_attend", "quantizer_table",
+    "retrieve_workspace_size", "workspace_layout", "sparse_attend", "quantizer_table", "rotation_signs",
     "profile_enable", "profile_reset", "profile_read",
 ]
 
@@ -78,6 +78,7 @@ def lib():
         L.pariskv_sparse_attend.argtypes = [P(_Config), VP, VP, VP, I32, I64, VP, I32, I32,
                                             ctypes.c_float, VP, VP]
         L.pariskv_quantizer_table.argtypes = [I32, P(ctypes.c_double), P(ctypes.c_double)]
+        L.pariskv_rotation_signs.argtypes = [ctypes.c_uint64, I32, P(ctypes.c_int8)]
         L.pariskv_profile_enable.argtypes = [I32]
         L.pariskv_profile_read.argtypes = [I32, P(ctypes.c_char_p), P(I64), P(ctypes.c_double)]
         L.pariskv_strerror.restype = ctypes.c_char_p
@@ -236,6 +237,13 @@ def quantizer_table(m=8):
     a = (ctypes.c_double * 8)()
     _check(lib().pariskv_quantizer_table(m, tau, a))
     return np.array(tau[:]), np.array(a[:])
+
+
+def rotation_signs(seed, D=HEAD_DIM):
+    """The library's seeded rotation signs s in {+1, -1}^D (int8), see pariskv_rotation_signs."""
+    out = (ctypes.c_int8 * D)()
+    _check(lib().pariskv_rotation_signs(ctypes.c_uint64(seed & (2**64 - 1)), D, out))
+    return np.array(out[:], dtype=np.int8)
 
 
 def profile_enable(on=True):

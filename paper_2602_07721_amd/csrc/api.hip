@@ -251,6 +251,19 @@ const char* pariskv_strerror(int code) {
 
 const char* pariskv_last_error(void) { return t_last_error.c_str(); }
 
+int pariskv_rotation_signs(uint64_t seed, int32_t D, int8_t* out) {
+    if (D < 1) return fail(PARISKV_ERR_INVALID, "D = %d < 1", D);
+    if (!out) return fail(PARISKV_ERR_INVALID, "out is null");
+    for (int32_t j = 0; j < D; ++j) {
+        uint64_t z = seed + (uint64_t)j + 0x9E3779B97F4A7C15ull;
+        z = (z ^ (z >> 30)) * 0xBF58476D1CE4E5B9ull;
+        z = (z ^ (z >> 27)) * 0x94D049BB133111EBull;
+        z ^= z >> 31;
+        out[j] = (z >> 63) ? int8_t(-1) : int8_t(1);
+    }
+    return PARISKV_OK;
+}
+
 int pariskv_quantizer_table(int32_t m, double* tau, double* a) {
     if (!tau || !a) return fail(PARISKV_ERR_INVALID, "NULL output");
     if (m != kM) return fail(PARISKV_ERR_UNSUPPORTED, "only m = 8 is built");

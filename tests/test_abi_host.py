@@ -181,3 +181,14 @@ def test_id_slot_encoding_spreads_near_ids_over_banks():
         for d in range(1, 256):
             if bin(d).count("1") <= 3:
                 assert s[c] % 32 != s[c ^ d] % 32, (c, d)
+
+
+def test_rotation_signs_match_the_oracle():
+    from oracle import rotation
+    for seed in (0, 1, 977, 2**63 + 11):
+        for D in (1, 7, 128, 256):
+            np.testing.assert_array_equal(pk.rotation_signs(seed, D), rotation.seeded_signs(seed, D))
+    L = pk.lib()
+    out = (ctypes.c_int8 * 4)()
+    assert L.pariskv_rotation_signs(ctypes.c_uint64(1), 0, out) == pk.ERR_INVALID
+    assert L.pariskv_rotation_signs(ctypes.c_uint64(1), 4, None) == pk.ERR_INVALID

@@ -129,3 +129,16 @@ def test_cluster_counts():
     for b in (0, 7, 15):
         for c in np.unique(ids[:, b])[:5]:
             assert cnt[b, c] == np.sum(ids[:, b] == c)
+
+
+def test_seeded_signs_follow_splitmix64():
+    # SplitMix64's first two outputs from state 0, as published with the generator.
+    assert rotation.splitmix64(0) == 0xE220A8397B1DCDAF
+    assert rotation.splitmix64(0x9E3779B97F4A7C15) == 0x6E789E6AA1B965F4
+    s = rotation.seeded_signs(41, 256)
+    assert s.dtype == np.int8 and set(np.unique(s)) <= {-1, 1}
+    # sign j depends on seed + j only
+    np.testing.assert_array_equal(rotation.seeded_signs(42, 255), s[1:])
+    # balanced: over 64 seeds x 128 signs the fraction of -1 is within 4 sigma of 1/2
+    frac = np.mean([rotation.seeded_signs(7000 + t, 128) == -1 for t in range(64)])
+    assert abs(frac - 0.5) < 4 * 0.5 / np.sqrt(64 * 128)

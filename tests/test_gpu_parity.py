@@ -183,6 +183,45 @@ def test_append_equals_bulk_encode():
         np.testing.assert_array_equal(a[k], b[k])
 
 
+def test_streaming_decode_steps_match_the_oracle():
+    # Prefill, then decode steps that append 1..55 keys per (sequence, KV head) and
+    # retrieve with budgets that grow with n: every step is checked in full against
+    # the oracle run on all keys cached so far.
+    wc = workloads.Config("stream", batch=1, n_kv_heads=2, q_per_kv=4, n=2600, n_cand=1,
+                          n_collide=1, top_k=32, seed=66)
+    K, V = workloads.layer_kv(wc)
+    signs = workloads.rotation_signs(wc.seed)
+    n0 = 2500
+    print("case streaming decode", flush=True)
+    run = GpuRun(K[:, :, :n0].copy(), V, K[:, :, 0, :].repeat(4, axis=1), signs, 4,
+                 pk.Budget(1, 1, 1), SCALE, capacity=wc.n)
+    run.K = torch.from_numpy(np.ascontiguousarray(K)).cuda()  # attention reads the full cache
+    n_cur = n0
+    for step, t in enumerate((1, 3, 1, 40, 55)):
+        chunk = torch.from_numpy(np.ascontiguousarray(K[:, :, n_cur:n_cur + t])).cuda()
+        pk.append(run.cfg, run.index, chunk, n_cur)
+        n_cur += t
+        C = -(-n_cur // 8)
+        budget = pk.Budget(C, 2 * C, 32)
+        Kc = np.ascontiguousarray(K[:, :, :n_cur])
+        Q, _ = workloads.layer_queries(wc, Kc, step=step)
+        run.Q = torch.from_numpy(np.ascontiguousarray(Q)).cuda()
+        run.budget, run.n = budget, n_cur
+        run.retrieve()
+        inter = run.intermediates()
+        o_gpu = run.attend()
+        gids, grec, gcnt = run.host_index()
+        for h in range(wc.n_kv_heads):
+            orc = oracle_group(Kc[0, h], signs)
+            check_index(gids[0, h], grec[0, h], gcnt[0, h], orc)
+            for g in range(wc.q_per_kv):
+                hq = h * wc.q_per_kv + g
+                check_head(inter, 0, h, g, wc.q_per_kv, Q[0, hq], orc, signs, budget, n_cur)
+                check_attention(o_gpu[0, hq], Q[0, hq], Kc[0, h], V[0, h, :n_cur], inter["idx"][0, hq],
+                                SCALE)
+    assert n_cur == wc.n
+
+
 def test_host_mapped_attention_matches_hbm():
     cfg = workloads.CONFIGS["layer32k"]
     wc, K, V, Q, _, signs = _inputs(cfg, n=8192)

@@ -9,22 +9,24 @@
 //                      wave per (head slot, subspace): z = H(s q) in exact
 //                      float64 (written as z/D float for the rerank), the 256
 //                      centroids ranked by the exact proxy sum_j +-z_j (ties:
-//                      lower id), cluster counts prefix-summed in that order, and
-//                      the tier bonus of each cluster placed in byte `slot` of a
-//                      packed word (4 query heads of a KV head share one uint32),
-//                      assembled in LDS and stored whole.
+//                      lower id) with a 64-bit bitonic sort held in registers,
+//                      cluster counts prefix-summed in that order, and the tier
+//                      bonus of each cluster placed in byte `slot` of a packed
+//                      word (4 query heads of a KV head share one uint32) at the
+//                      entry of the stored id form slot(c), assembled in LDS and
+//                      stored whole.
 //   collide_kernel     streams the 16 id bytes of every key once per quad of
 //                      query heads, sums 16 packed LDS lookups (4 head scores in
 //                      the 4 bytes of one uint32; each is at most 96, so no
 //                      carries), writes S as bytes per head (64 consecutive
-//                      bytes per wave store) and a suffix
-//                      histogram #{S >= v} per head and 4096-key chunk (frequent
-//                      low scores counted in per-lane registers, the rest by LDS
-//                      atomics).
-//   threshold_kernel   one block per query head: theta = largest v with
-//                      #{S >= v} >= C_eff, the quota of S == theta keys, and per
-//                      chunk the number of S > theta / S == theta keys in
-//                      earlier chunks.
+//                      bytes per wave store) and a suffix histogram
+//                      #{S >= v} per head and 4096-key chunk (score 1 counted
+//                      in per-lane registers, higher scores by LDS atomics into
+//                      four lane-partitioned copies).
+//   threshold_kernel   one block of 16 waves per query head: theta = largest v
+//                      with #{S >= v} >= C_eff, the quota of S == theta keys,
+//                      and per chunk the number of S > theta / S == theta keys
+//                      in earlier chunks.
 // The compaction of the candidates lives with the rerank (stage2.hip).
 
 #include <hip/hip_fp16.h>

@@ -18,11 +18,15 @@
 // keeps the 16 query coordinates of its two subspaces in registers; the
 // signed level table (16 floats) lives in LDS.
 //
-// topk kernels: one block per query head.  Exact radix select (8-bit digits,
-// taken from the top of the occupied [min, max] key range so the histograms
-// spread) of the k-th largest estimate on order-preserving uint32 keys, ties
-// at the threshold taken in candidate order, then an ordered compaction: the
-// winners come out in ascending key index (candidate order), no sort.
+// topk kernels: one block per query head; the k-th largest estimate is found
+// exactly on order-preserving uint32 keys, ties at it taken in candidate
+// order, then an ordered compaction lists the winners in ascending key index
+// (candidate order) without a sort.  topk_lds_kernel (C <= 32768) stages the
+// keys in LDS, bins them linearly in value over [min, max] (the float bit
+// patterns crowd into a few exponent prefixes), and ranks the boundary bin by
+// brute force when it holds at most 64 keys, else by 11/11/10-bit radix passes
+// restricted to it.  topk_reg_kernel (larger C) keeps the keys in registers and
+// runs 8-bit radix passes from the top of the occupied key range.
 
 #include "internal.hpp"
 

@@ -7,9 +7,10 @@ N = 131072 keys per sequence, D = 128, candidate budget C = 8192, collision
 budget C_rho = 16384, top-k = 512, synthetic keys (outlier-channel Gaussian,
 see workloads/) and fresh planted-needle queries at every step.
 
-One step = the whole hot path for the whole batch: pariskv_retrieve (query
-transform + bonus tables, collision scan, selection, RSQ-IP rerank, top-k)
-followed by pariskv_sparse_attend over the selected K/V rows.  Keys are
+One step = the whole hot path for the whole batch: pariskv_retrieve_attend
+(query transform + bonus tables, collision scan, selection, RSQ-IP rerank,
+top-k with the attention over the selected K/V rows fused into it), or with
+--separate pariskv_retrieve followed by pariskv_sparse_attend.  Keys are
 encoded once before timing (reported separately).  K, V, the index and all
 queries are resident in HBM before the timed region starts.
 
@@ -48,6 +49,9 @@ def parse():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-groups", type=int, default=8)
     ap.add_argument("--cpu-steps", type=int, default=8)
+    ap.add_argument("--separate", action="store_true",
+                    help="run the step as pariskv_retrieve + pariskv_sparse_attend instead of the fused "
+                         "pariskv_retrieve_attend")
     ap.add_argument("--kv-host", action="store_true",
                     help="keep K/V in pinned host memory and attend through host-mapped pointers")
     ap.add_argument("--extras", action="store_true",
@@ -83,6 +87,8 @@ def algorithmic_bytes(wc, c_eff):
         "topk": b * hq * (C * 8 + k * 8),
         # 256-byte K row + 256-byte V row + 4-byte index per selected key
         "attend": b * hq * k * (512 + 4),
+        # the fused top-k + attention: both, minus the index re-read
+        "topk_attend": b * hq * (C * 8 + k * 8) + b * hq * k * 512,
     }
 
 
@@ -326,8 +332,12 @@ def main():
     n_keys = wc.batch * wc.n_kv_heads * wc.n
 
     def step(s):
-        pk.retrieve(cfg, index, Qd[s], wc.n, budget, out_idx=out_idx, out_score=out_score, workspace=ws)
-        pk.sparse_attend(cfg, Qd[s], Kd, Vd, out_idx, scale, out=out, kv_host_mapped=args.kv_host)
+        if args.separate:
+            pk.retrieve(cfg, index, Qd[s], wc.n, budget, out_idx=out_idx, out_score=out_score, workspace=ws)
+            pk.sparse_attend(cfg, Qd[s], Kd, Vd, out_idx, scale, out=out, kv_host_mapped=args.kv_host)
+        else:
+            pk.retrieve_attend(cfg, index, Qd[s], wc.n, budget, Kd, Vd, scale, out_idx=out_idx,
+                               out_score=out_score, out=out, workspace=ws, kv_host_mapped=args.kv_host)
 
     for s in range(args.warmup):
         if not args.no_flush:
@@ -432,6 +442,7 @@ def main():
     mean_us = float(step_ms.mean() * 1e3)
     result = {
         "metric": "retrieve+attend us/step/layer at 128K ctx; code-scan HBM GB/s vs peak",
+        "path": "pariskv_retrieve + pariskv_sparse_attend" if args.separate else "pariskv_retrieve_attend",
         "value": round(mean_us, 2),
         "unit": "us/step/layer",
         "n_gpus": 1,

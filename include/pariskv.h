@@ -189,6 +189,21 @@ int pariskv_retrieve(const pariskv_config* cfg, const pariskv_index* index,
                      const pariskv_budget* budget, int32_t* out_idx, float* out_score,
                      void* workspace, size_t ws_bytes, void* stream);
 
+/* pariskv_retrieve followed by the attention of every query head over its k
+ * winners, in one call: the same out_idx / out_score as pariskv_retrieve and
+ * the same `out` as pariskv_sparse_attend(cfg, q, K, V, kv_host_mapped,
+ * kv_capacity, out_idx, k, batch, scale, out) would give, bit for bit.  For
+ * C <= 32768 the attention runs inside the top-k kernel over the winners it
+ * holds (no second pass over out_idx); otherwise the two kernels run in turn.
+ * Arguments as in those two functions.
+ * Errors: those of pariskv_retrieve and of pariskv_sparse_attend. */
+int pariskv_retrieve_attend(const pariskv_config* cfg, const pariskv_index* index,
+                            const void* q, int64_t n, int32_t batch,
+                            const pariskv_budget* budget, int32_t* out_idx, float* out_score,
+                            const void* K, const void* V, int32_t kv_host_mapped,
+                            int64_t kv_capacity, float scale, float* out, void* workspace,
+                            size_t ws_bytes, void* stream);
+
 /* Attention over the fetched keys only (Eqs. approx_weight, approx_output):
  *   o = sum_{i in idx} softmax_i(scale * <k_i, q>) v_i,
  * float16 inputs, float32 accumulation.

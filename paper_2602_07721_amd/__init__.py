@@ -19,7 +19,8 @@ import numpy as np
 
 __all__ = [
     "PariskvError", "Config", "Budget", "Index", "lib", "encode", "append", "retrieve",
-    "retrieve_workspace_size", "workspace_layout", "sparse_attend", "quantizer_table", "rotation_signs",
+    "retrieve_workspace_size", "workspace_layout", "sparse_attend", "retrieve_attend", "quantizer_table",
+    "rotation_signs",
     "profile_enable", "profile_reset", "profile_read",
 ]
 
@@ -77,6 +78,8 @@ def lib():
                                        SZ, VP]
         L.pariskv_sparse_attend.argtypes = [P(_Config), VP, VP, VP, I32, I64, VP, I32, I32,
                                             ctypes.c_float, VP, VP]
+        L.pariskv_retrieve_attend.argtypes = [P(_Config), P(_Index), VP, I64, I32, P(_Budget), VP, VP,
+                                              VP, VP, I32, I64, ctypes.c_float, VP, VP, SZ, VP]
         L.pariskv_quantizer_table.argtypes = [I32, P(ctypes.c_double), P(ctypes.c_double)]
         L.pariskv_rotation_signs.argtypes = [ctypes.c_uint64, I32, P(ctypes.c_int8)]
         L.pariskv_profile_enable.argtypes = [I32]
@@ -211,6 +214,34 @@ def retrieve(cfg, index, q, n, budget, out_idx=None, out_score=None, workspace=N
                                   _ptr(out_idx, "out_idx"), _ptr(out_score, "out_score"),
                                   _ptr(workspace, "workspace"), workspace.numel(), _stream(stream)))
     return out_idx, out_score, workspace
+
+
+def retrieve_attend(cfg, index, q, n, budget, K, V, scale, out_idx=None, out_score=None, out=None,
+                    workspace=None, kv_host_mapped=False, stream=None):
+    """retrieve + sparse_attend in one call (attention fused into the top-k when C <= 32768);
+    returns (idx, score, out, workspace)."""
+    import torch
+    batch = int(q.shape[0])
+    rows = batch * cfg.n_q_heads
+    if out_idx is None:
+        out_idx = torch.empty((batch, cfg.n_q_heads, budget.top_k), dtype=torch.int32, device=q.device)
+    if out is None:
+        out = torch.empty((batch, cfg.n_q_heads, HEAD_DIM), dtype=torch.float32, device=q.device)
+    if workspace is None:
+        workspace = torch.empty(max(256, retrieve_workspace_size(cfg, batch, n, budget)),
+                                dtype=torch.uint8, device=q.device)
+    if kv_host_mapped:
+        for t, nm in ((K, "K"), (V, "V")):
+            if t.is_cuda or not t.is_pinned():
+                raise ValueError(f"{nm} must be pinned host memory when kv_host_mapped")
+    assert out_idx.numel() == rows * budget.top_k
+    _check(lib().pariskv_retrieve_attend(cfg.c(), index.c(), _ptr(q, "q"), int(n), batch, budget.c(),
+                                         _ptr(out_idx, "out_idx"), _ptr(out_score, "out_score"),
+                                         _ptr(K, "K", not kv_host_mapped), _ptr(V, "V", not kv_host_mapped),
+                                         int(bool(kv_host_mapped)), int(K.shape[2]), float(scale),
+                                         _ptr(out, "out"), _ptr(workspace, "workspace"), workspace.numel(),
+                                         _stream(stream)))
+    return out_idx, out_score, out, workspace
 
 
 def sparse_attend(cfg, q, K, V, idx, scale, out=None, kv_host_mapped=False, stream=None):

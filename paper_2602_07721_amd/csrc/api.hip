@@ -321,9 +321,48 @@ int pariskv_workspace_layout(const pariskv_config* cfg, int32_t batch, int64_t n
     return layout(cfg, batch, n, budget, out);
 }
 
-int pariskv_retrieve(const pariskv_config* cfg, const pariskv_index* index, const void* q,
-                     int64_t n, int32_t batch, const pariskv_budget* budget, int32_t* out_idx,
-                     float* out_score, void* workspace, size_t ws_bytes, void* stream) {
+// Attention arguments of pariskv_retrieve_attend.
+struct AttendReq {
+    const void* K;
+    const void* V;
+    int32_t kv_host_mapped;
+    int64_t kv_capacity;
+    float scale;
+    float* out;
+};
+
+static int check_attend_args(const AttendReq& r) {
+    if (!r.K || !r.V || !r.out) return fail(PARISKV_ERR_INVALID, "K, V and out must be non-NULL");
+    if (!aligned16(r.K) || !aligned16(r.V) || !aligned16(r.out))
+        return fail(PARISKV_ERR_INVALID, "K, V and out must be 16-byte aligned");
+    if (r.kv_capacity < 1 || r.kv_capacity > INT32_MAX)
+        return fail(PARISKV_ERR_INVALID, "kv_capacity %lld outside 1..2^31-1", (long long)r.kv_capacity);
+    if (r.kv_host_mapped != 0 && r.kv_host_mapped != 1)
+        return fail(PARISKV_ERR_INVALID, "kv_host_mapped must be 0 or 1");
+    if (!std::isfinite(r.scale)) return fail(PARISKV_ERR_INVALID, "scale is not finite");
+    return PARISKV_OK;
+}
+
+// Device-usable K and V (host-mapped memory goes through its device pointer).
+static int device_kv(const AttendReq& r, const void** Kd, const void** Vd) {
+    *Kd = r.K;
+    *Vd = r.V;
+    if (r.kv_host_mapped) {
+        void* p = nullptr;
+        hipError_t e = hipHostGetDevicePointer(&p, const_cast<void*>(r.K), 0);
+        if (e != hipSuccess) return hip_fail(e, "hipHostGetDevicePointer(K)");
+        *Kd = p;
+        e = hipHostGetDevicePointer(&p, const_cast<void*>(r.V), 0);
+        if (e != hipSuccess) return hip_fail(e, "hipHostGetDevicePointer(V)");
+        *Vd = p;
+    }
+    return PARISKV_OK;
+}
+
+static int retrieve_impl(const pariskv_config* cfg, const pariskv_index* index, const void* q,
+                         int64_t n, int32_t batch, const pariskv_budget* budget, int32_t* out_idx,
+                         float* out_score, void* workspace, size_t ws_bytes, void* stream,
+                         const AttendReq* att) {
     prof_chain_start();
     pariskv_ws_layout L;
     int rc = layout(cfg, batch, n, budget, &L);
@@ -339,6 +378,12 @@ int pariskv_retrieve(const pariskv_config* cfg, const pariskv_index* index, cons
         return fail(PARISKV_ERR_WORKSPACE, "workspace must be non-NULL and 256-byte aligned");
     if (ws_bytes < L.total)
         return fail(PARISKV_ERR_WORKSPACE, "workspace has %zu bytes, needs %zu", ws_bytes, L.total);
+    const void* Kd = nullptr;
+    const void* Vd = nullptr;
+    if (att) {
+        if ((rc = check_attend_args(*att)) != PARISKV_OK) return rc;
+        if ((rc = device_kv(*att, &Kd, &Vd)) != PARISKV_OK) return rc;
+    }
 
     RetrieveArgs a{};
     a.batch = batch;
@@ -378,19 +423,52 @@ int pariskv_retrieve(const pariskv_config* cfg, const pariskv_index* index, cons
     a.out_score = out_score;
     a.sb = pack_signs(cfg->rot_signs);
     a.qc = quant_consts();
+    if (att) {
+        a.K = Kd;
+        a.V = Vd;
+        a.kv_capacity = att->kv_capacity;
+        a.scale = att->scale;
+        a.attn_out = att->out;
+    }
 
     hipStream_t s = static_cast<hipStream_t>(stream);
     hipError_t e;
+    // Attention by its own kernel over out_idx (when the top-k did not fuse it).
+    auto attend_separately = [&]() -> int {
+        const hipError_t ea = launch_attend(q, Kd, Vd, att->kv_capacity, out_idx, budget->top_k, batch,
+                                            a.hkv, a.g, att->scale, att->out, s);
+        return ea == hipSuccess ? PARISKV_OK : hip_fail(ea, "attend launch");
+    };
     if (n == 0) {
         e = launch_pad_outputs(a, s);
-        return e == hipSuccess ? PARISKV_OK : hip_fail(e, "pad outputs");
+        if (e != hipSuccess) return hip_fail(e, "pad outputs");
+        return att ? attend_separately() : PARISKV_OK;
     }
     if ((e = launch_query_lut(a, s)) != hipSuccess) return hip_fail(e, "query_lut launch");
     if ((e = launch_collide(a, s)) != hipSuccess) return hip_fail(e, "collide launch");
     if ((e = launch_threshold(a, s)) != hipSuccess) return hip_fail(e, "threshold launch");
     if ((e = launch_compact_rerank(a, s)) != hipSuccess) return hip_fail(e, "compact_rerank launch");
-    if ((e = launch_topk(a, s)) != hipSuccess) return hip_fail(e, "topk launch");
+    bool fused = false;
+    if ((e = launch_topk(a, s, att != nullptr, &fused)) != hipSuccess) return hip_fail(e, "topk launch");
+    if (att && !fused) return attend_separately();
     return PARISKV_OK;
+}
+
+int pariskv_retrieve(const pariskv_config* cfg, const pariskv_index* index, const void* q,
+                     int64_t n, int32_t batch, const pariskv_budget* budget, int32_t* out_idx,
+                     float* out_score, void* workspace, size_t ws_bytes, void* stream) {
+    return retrieve_impl(cfg, index, q, n, batch, budget, out_idx, out_score, workspace, ws_bytes,
+                         stream, nullptr);
+}
+
+int pariskv_retrieve_attend(const pariskv_config* cfg, const pariskv_index* index, const void* q,
+                            int64_t n, int32_t batch, const pariskv_budget* budget, int32_t* out_idx,
+                            float* out_score, const void* K, const void* V, int32_t kv_host_mapped,
+                            int64_t kv_capacity, float scale, float* out, void* workspace,
+                            size_t ws_bytes, void* stream) {
+    const AttendReq att{K, V, kv_host_mapped, kv_capacity, scale, out};
+    return retrieve_impl(cfg, index, q, n, batch, budget, out_idx, out_score, workspace, ws_bytes,
+                         stream, &att);
 }
 
 int pariskv_sparse_attend(const pariskv_config* cfg, const void* q, const void* K, const void* V,

@@ -1,0 +1,144 @@
+// Attention of one query head over a list of selected keys, for a block of
+// 1024 threads (Eqs. approx_weight, approx_output):
+//   o = sum_{i in list} softmax_i(scale <k_i, q>) v_i,  float16 in, float32 math.
+// Shared by the stand-alone attention kernel and the fused top-k + attention
+// kernel, so both produce the same bits.
+//
+// 64 key slots of 16 lanes: lane l16 owns dims [8 l16, 8 l16 + 8), so a K or
+// V row is one 256-byte contiguous read by 16 lanes.  Slot s takes list
+// entries s, s + 64, ...; every lane keeps 8 K and 8 V row segments in flight.
+// Each slot keeps an online-softmax state (running max, sum, 8 accumulators
+// per lane); the 64 states are merged in LDS at the end.  List entries outside
+// [0, kv_capacity) (for example -1) are skipped.
+#pragma once
+
+#include <hip/hip_fp16.h>
+
+#include "internal.hpp"
+
+namespace pariskv {
+
+constexpr int kAtThreads = 1024;
+constexpr int kAtGroups = kAtThreads / 16;  // concurrent key slots per block
+constexpr int kAtUnroll = 8;                // K/V rows in flight per lane
+
+// LDS the row needs beyond the key list: running max, sum and accumulators per slot.
+struct AttendScratch {
+    float m[kAtGroups];
+    float l[kAtGroups];
+    float acc[kAtGroups][kD];
+};
+
+__device__ __forceinline__ void unpack8_half(const uint4 v, float* f) {
+    const uint32_t w[4] = {v.x, v.y, v.z, v.w};
+#pragma unroll
+    for (int h = 0; h < 4; ++h) {
+        f[2 * h] = __half2float(__ushort_as_half((unsigned short)(w[h] & 0xffffu)));
+        f[2 * h + 1] = __half2float(__ushort_as_half((unsigned short)(w[h] >> 16)));
+    }
+}
+
+// q: the head's D float16 values; K, V: the KV head's rows [kv_capacity][D];
+// list: k entries in LDS (already synchronised); out: D floats.  Every thread
+// of the block must call it; it ends with the block synchronised.
+__device__ __forceinline__ void attend_row(const __half* __restrict__ q, const __half* __restrict__ K,
+                                           const __half* __restrict__ V, int64_t kv_capacity,
+                                           const int32_t* list, int32_t k, float scale,
+                                           float* __restrict__ out, AttendScratch& sm) {
+    const int tid = threadIdx.x;
+    const int grp16 = tid >> 4;  // key slot 0 .. kAtGroups-1
+    const int l16 = tid & 15;
+
+    float qf[8];
+    unpack8_half(reinterpret_cast<const uint4*>(q)[l16], qf);
+#pragma unroll
+    for (int d = 0; d < 8; ++d) qf[d] *= scale;
+
+    float m = -__builtin_huge_valf(), lsum = 0.f;
+    float acc[8];
+#pragma unroll
+    for (int d = 0; d < 8; ++d) acc[d] = 0.f;
+
+    for (int base = 0; base < k; base += kAtGroups * kAtUnroll) {
+        int32_t key[kAtUnroll];
+        uint4 kc[kAtUnroll], vc[kAtUnroll];
+#pragma unroll
+        for (int u = 0; u < kAtUnroll; ++u) {
+            const int r = base + grp16 + kAtGroups * u;
+            key[u] = r < k ? list[r] : -1;
+            if (key[u] >= kv_capacity) key[u] = -1;
+            kc[u] = make_uint4(0, 0, 0, 0);
+            vc[u] = make_uint4(0, 0, 0, 0);
+            if (key[u] >= 0) {
+                const int64_t off = (int64_t)key[u] * kD;
+                kc[u] = reinterpret_cast<const uint4*>(K + off)[l16];
+                vc[u] = reinterpret_cast<const uint4*>(V + off)[l16];
+            }
+        }
+        float dot[kAtUnroll];
+#pragma unroll
+        for (int u = 0; u < kAtUnroll; ++u) {
+            float kf[8];
+            unpack8_half(kc[u], kf);
+            float d0 = 0.f;
+#pragma unroll
+            for (int d = 0; d < 8; ++d) d0 += qf[d] * kf[d];
+            dot[u] = d0;
+        }
+#pragma unroll
+        for (int st = 1; st < 16; st <<= 1) {
+#pragma unroll
+            for (int u = 0; u < kAtUnroll; ++u) dot[u] += __shfl_xor(dot[u], st, 64);
+        }
+        float mn = m;
+#pragma unroll
+        for (int u = 0; u < kAtUnroll; ++u)
+            if (key[u] >= 0) mn = fmaxf(mn, dot[u]);
+        if (mn > -__builtin_huge_valf()) {
+            const float corr = __expf(m - mn);
+            lsum *= corr;
+#pragma unroll
+            for (int d = 0; d < 8; ++d) acc[d] *= corr;
+#pragma unroll
+            for (int u = 0; u < kAtUnroll; ++u) {
+                if (key[u] >= 0) {
+                    const float p = __expf(dot[u] - mn);
+                    float vf[8];
+                    unpack8_half(vc[u], vf);
+                    lsum += p;
+#pragma unroll
+                    for (int d = 0; d < 8; ++d) acc[d] += p * vf[d];
+                }
+            }
+            m = mn;
+        }
+    }
+
+    if (l16 == 0) {
+        sm.m[grp16] = m;
+        sm.l[grp16] = lsum;
+    }
+#pragma unroll
+    for (int d = 0; d < 8; ++d) sm.acc[grp16][8 * l16 + d] = acc[d];
+    __syncthreads();
+    if (tid < kD) {
+        float M = -__builtin_huge_valf();
+#pragma unroll
+        for (int j = 0; j < kAtGroups; ++j) M = fmaxf(M, sm.m[j]);
+        float L = 0.f, O = 0.f;
+        if (M > -__builtin_huge_valf()) {
+#pragma unroll
+            for (int j = 0; j < kAtGroups; ++j) {
+                if (sm.l[j] > 0.f) {
+                    const float c = __expf(sm.m[j] - M);
+                    L += sm.l[j] * c;
+                    O += sm.acc[j][tid] * c;
+                }
+            }
+        }
+        out[tid] = L > 0.f ? O / L : 0.f;
+    }
+    __syncthreads();
+}
+
+}  // namespace pariskv

@@ -7,6 +7,8 @@
 #include <cstddef>
 #include <cstdint>
 
+#include "pariskv.h"
+
 namespace pariskv {
 
 constexpr int kD = 128;           // head dimension
@@ -125,13 +127,22 @@ struct RetrieveArgs {
     float* out_score;
     SignBits sb;
     QuantConsts qc;
+    // attention over the winners, when fused with the top-k (device-usable K/V)
+    const void* K;
+    const void* V;
+    int64_t kv_capacity;
+    float scale;
+    float* attn_out;
 };
 
 hipError_t launch_query_lut(const RetrieveArgs& a, hipStream_t s);
 hipError_t launch_collide(const RetrieveArgs& a, hipStream_t s);
 hipError_t launch_threshold(const RetrieveArgs& a, hipStream_t s);
 hipError_t launch_compact_rerank(const RetrieveArgs& a, hipStream_t s);
-hipError_t launch_topk(const RetrieveArgs& a, hipStream_t s);
+// With `attend`, the top-k kernel also runs the attention over its winners
+// (a.K, a.V, a.kv_capacity, a.scale -> a.attn_out) when C fits the LDS variant;
+// returns false in `fused` when it did not (the caller then launches attention).
+hipError_t launch_topk(const RetrieveArgs& a, hipStream_t s, bool attend = false, bool* fused = nullptr);
 hipError_t launch_pad_outputs(const RetrieveArgs& a, hipStream_t s);
 
 hipError_t launch_attend(const void* q, const void* K, const void* V, int64_t kv_capacity,

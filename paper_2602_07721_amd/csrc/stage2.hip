@@ -28,6 +28,7 @@
 // restricted to it.  topk_reg_kernel (larger C) keeps the keys in registers and
 // runs 8-bit radix passes from the top of the occupied key range.
 
+#include "attend_row.hpp"
 #include "internal.hpp"
 
 namespace pariskv {
@@ -228,7 +229,7 @@ __device__ __forceinline__ void find_digit(const uint32_t* hist, uint32_t need, 
 // with coalesced 16-byte loads; each thread then owns EPT consecutive candidates.
 // Exact radix select with 11-bit digits taken from the top of the occupied
 // [min, max] key range, then an ordered compaction (ascending key index).
-template <int TH, int EPT>
+template <int TH, int EPT, bool kAttend>
 __global__ __launch_bounds__(TH) void topk_lds_kernel(RetrieveArgs a) {
     constexpr int kWaves = TH / 64;
     constexpr int kCap = TH * EPT;
@@ -237,9 +238,18 @@ __global__ __launch_bounds__(TH) void topk_lds_kernel(RetrieveArgs a) {
     // winners then read them without a global round trip); beyond that they are
     // read back from global memory for the k winners only.
     constexpr bool kStageIdx = EPT <= 16;
-    __shared__ uint32_t s_key[kCap];
-    __shared__ int32_t s_idx[kStageIdx ? kCap : 1];
-    __shared__ uint32_t s_hist[2][kNB];
+    // One LDS area: region A = staged keys (+ indices), region B = two histograms.
+    // With kAttend the winners list reuses B once the histograms are done, and
+    // the attention's per-slot state reuses A once the winners are out.
+    constexpr size_t kA0 = (size_t)kCap * 4 * (kStageIdx ? 2 : 1);
+    constexpr size_t kA = kAttend && kA0 < sizeof(AttendScratch) ? sizeof(AttendScratch) : kA0;
+    constexpr size_t kBytes = kA + 2 * kNB * 4;
+    static_assert(!kAttend || 2 * kNB * 4 >= PARISKV_MAX_TOPK * 4, "winners fit in region B");
+    __shared__ __align__(16) unsigned char s_raw[kBytes];
+    uint32_t* s_key = reinterpret_cast<uint32_t*>(s_raw);
+    int32_t* s_idx = reinterpret_cast<int32_t*>(s_raw + (size_t)kCap * 4);
+    uint32_t (*s_hist)[kNB] = reinterpret_cast<uint32_t (*)[kNB]>(s_raw + kA);
+    int32_t* s_win = reinterpret_cast<int32_t*>(s_raw + kA);
     __shared__ uint32_t s_w[kWaves];
     __shared__ uint32_t s_mm[2][kWaves];
     __shared__ uint32_t s_digit, s_need, s_nsmall;
@@ -405,13 +415,26 @@ __global__ __launch_bounds__(TH) void topk_lds_kernel(RetrieveArgs a) {
             ++eb;
         }
         if (p < (uint32_t)kk) {
-            oi[p] = kStageIdx ? s_idx[tid * EPT + e] : cand[tid * EPT + e];
+            const int32_t win = kStageIdx ? s_idx[tid * EPT + e] : cand[tid * EPT + e];
+            oi[p] = win;
             if (os) os[p] = key_float(key[e]);
+            if (kAttend) s_win[p] = win;
         }
     }
     for (int r = kk + tid; r < a.top_k; r += TH) {
         oi[r] = -1;
         if (os) os[r] = -__builtin_huge_valf();
+    }
+    if (kAttend) {
+        // Attention over the kk winners (Eqs. approx_weight, approx_output), from LDS.
+        __syncthreads();
+        const int seq = (int)(row / a.hq);
+        const int h = (int)(row % a.hq);
+        const int64_t kvrow0 = ((int64_t)seq * a.hkv + h / a.g) * a.kv_capacity;
+        attend_row(static_cast<const __half*>(a.q) + row * kD,
+                   static_cast<const __half*>(a.K) + kvrow0 * kD,
+                   static_cast<const __half*>(a.V) + kvrow0 * kD, a.kv_capacity, s_win, kk, a.scale,
+                   a.attn_out + row * kD, *reinterpret_cast<AttendScratch*>(s_raw));
     }
 }
 
@@ -540,20 +563,27 @@ hipError_t launch_compact_rerank(const RetrieveArgs& a, hipStream_t s) {
     return hipGetLastError();
 }
 
-hipError_t launch_topk(const RetrieveArgs& a, hipStream_t s) {
+hipError_t launch_topk(const RetrieveArgs& a, hipStream_t s, bool attend, bool* fused) {
     const dim3 grid((unsigned)(a.batch * a.hq));
     const int64_t C = a.c_eff;
-    const ProfEvents pe = prof_begin("topk");
+    if (fused) *fused = attend && C <= 1024 * 32;
+    const ProfEvents pe = prof_begin(attend && C <= 1024 * 32 ? "topk_attend" : "topk");
+#define PARISKV_TOPK_LDS(EPT)                                                                        \
+    (attend ? hipExtLaunchKernelGGL((topk_lds_kernel<1024, EPT, true>), grid, dim3(1024), 0, s,       \
+                                    pe.start, pe.stop, 0, a)                                          \
+            : hipExtLaunchKernelGGL((topk_lds_kernel<1024, EPT, false>), grid, dim3(1024), 0, s,      \
+                                    pe.start, pe.stop, 0, a))
     if (C <= 1024 * 4)
-        hipExtLaunchKernelGGL((topk_lds_kernel<1024, 4>), grid, dim3(1024), 0, s, pe.start, pe.stop, 0, a);
+        PARISKV_TOPK_LDS(4);
     else if (C <= 1024 * 8)
-        hipExtLaunchKernelGGL((topk_lds_kernel<1024, 8>), grid, dim3(1024), 0, s, pe.start, pe.stop, 0, a);
+        PARISKV_TOPK_LDS(8);
     else if (C <= 1024 * 16)
-        hipExtLaunchKernelGGL((topk_lds_kernel<1024, 16>), grid, dim3(1024), 0, s, pe.start, pe.stop, 0, a);
+        PARISKV_TOPK_LDS(16);
     else if (C <= 1024 * 32)
-        hipExtLaunchKernelGGL((topk_lds_kernel<1024, 32>), grid, dim3(1024), 0, s, pe.start, pe.stop, 0, a);
+        PARISKV_TOPK_LDS(32);
     else
         hipExtLaunchKernelGGL((topk_reg_kernel<1024, 64>), grid, dim3(1024), 0, s, pe.start, pe.stop, 0, a);
+#undef PARISKV_TOPK_LDS
     return hipGetLastError();
 }
 

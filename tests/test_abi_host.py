@@ -192,3 +192,24 @@ def test_rotation_signs_match_the_oracle():
     out = (ctypes.c_int8 * 4)()
     assert L.pariskv_rotation_signs(ctypes.c_uint64(1), 0, out) == pk.ERR_INVALID
     assert L.pariskv_rotation_signs(ctypes.c_uint64(1), 4, None) == pk.ERR_INVALID
+
+
+def test_retrieve_attend_validation():
+    cfg = _cfg()
+    b = pk.Budget(512, 1024, 64)
+    need = pk.retrieve_workspace_size(cfg, 1, 4000, b)
+    L = pk.lib()
+
+    def call(K=FAKE, V=FAKE, host=0, cap=4096, scale=0.1, out=FAKE, ws=FAKE, size=None):
+        return L.pariskv_retrieve_attend(cfg.c(), ctypes.byref(_index()), ctypes.c_void_p(FAKE), 4000, 1,
+                                         b.c(), ctypes.c_void_p(FAKE), None, ctypes.c_void_p(K),
+                                         ctypes.c_void_p(V), host, cap, ctypes.c_float(scale),
+                                         ctypes.c_void_p(out), ctypes.c_void_p(ws),
+                                         need if size is None else size, None)
+    assert call(K=0) == pk.ERR_INVALID
+    assert call(V=FAKE + 4) == pk.ERR_INVALID
+    assert call(out=0) == pk.ERR_INVALID
+    assert call(host=3) == pk.ERR_INVALID
+    assert call(cap=0) == pk.ERR_INVALID
+    assert call(scale=float("inf")) == pk.ERR_INVALID
+    assert call(size=need - 1) == pk.ERR_WORKSPACE

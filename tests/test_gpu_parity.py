@@ -291,3 +291,43 @@ def test_batch8_128k_sampled_at_full_size():
                     for s in range(wc.batch) for hq in range(wc.n_q_heads)])
     print(f"needle hit rate {hits:.3f}", flush=True)
     assert hits > 0.9
+
+
+@pytest.mark.parametrize("n,G,bud,host", [
+    (4096, 8, (512, 1024, 64), False),       # top-k staging 4 per thread, fused
+    (20000, 4, (8192, 16384, 512), False),   # 8 per thread, fused (the bench shape per head)
+    (40000, 2, (10000, 20000, 300), False),  # 16 per thread, fused
+    (40000, 2, (20000, 30000, 1000), False), # 32 per thread, fused
+    (70000, 1, (40000, 60000, 2048), False), # register top-k: attention as its own kernel
+    (0, 4, (64, 128, 16), False),            # empty cache: padding and zero outputs
+    (9000, 4, (700, 1500, 100), True),       # K/V in pinned host memory
+], ids=["C512", "C8192", "C10000", "C20000", "C40000", "n0", "host"])
+def test_retrieve_attend_equals_separate_calls(n, G, bud, host):
+    # The fused call must give the same bits as retrieve followed by sparse_attend.
+    wc = workloads.Config("fused", batch=2, n_kv_heads=2, q_per_kv=G, n=max(n, 1), n_cand=bud[0],
+                          n_collide=bud[1], top_k=bud[2], seed=88)
+    K, V = workloads.layer_kv(wc)
+    Q, _ = workloads.layer_queries(wc, K)
+    signs = workloads.rotation_signs(wc.seed)
+    print(f"case fused n={n} G={G} budget={bud} host={host}", flush=True)
+    cfg = pk.Config(2, G, max(n, 1), signs)
+    budget = pk.Budget(*bud)
+    Kd = torch.from_numpy(K).cuda()
+    Vd = torch.from_numpy(V).cuda()
+    Qd = torch.from_numpy(Q).cuda()
+    index = pk.Index.empty(cfg, 2)
+    pk.encode(cfg, index, Kd[:, :, :n].contiguous())
+    Ka, Va = (Kd.cpu().pin_memory(), Vd.cpu().pin_memory()) if host else (Kd, Vd)
+    hq = cfg.n_q_heads
+    s1 = torch.empty((2, hq, bud[2]), dtype=torch.float32, device="cuda")
+    i1, _, _ = pk.retrieve(cfg, index, Qd, n, budget, out_score=s1)
+    o1 = pk.sparse_attend(cfg, Qd, Ka, Va, i1, SCALE, kv_host_mapped=host)
+    s2 = torch.empty_like(s1)
+    i2, _, o2, _ = pk.retrieve_attend(cfg, index, Qd, n, budget, Ka, Va, SCALE, out_score=s2,
+                                      kv_host_mapped=host)
+    torch.cuda.synchronize()
+    np.testing.assert_array_equal(i1.cpu().numpy(), i2.cpu().numpy())
+    np.testing.assert_array_equal(s1.cpu().numpy().view(np.uint32), s2.cpu().numpy().view(np.uint32))
+    np.testing.assert_array_equal(o1.cpu().numpy().view(np.uint32), o2.cpu().numpy().view(np.uint32))
+    if n == 0:
+        assert np.all(i2.cpu().numpy() == -1) and np.all(o2.cpu().numpy() == 0)

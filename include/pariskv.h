@@ -112,6 +112,27 @@ typedef struct pariskv_budget {
     int32_t top_k;     /* k, 1..min(C, PARISKV_MAX_TOPK)                      */
 } pariskv_budget;
 
+/* Rows one query head attends at a decode step besides its retrieved keys
+ * (Sec. "Buffer Update": the KV cache is kept as Sink, Retrieval, Local and an
+ * Update Buffer; Sink, Local and the buffer stay on the GPU and are attended
+ * densely, Retrieval is indexed and only its top-k keys are attended).  Row
+ * numbers are K/V cache rows of the (sequence, KV head):
+ *   Sink            rows [0, sink_len)
+ *   retrieved keys  row retr_begin + i for retrieval index row i
+ *   Local + Buffer  rows [dense_begin, dense_end)
+ * A head attends sink_len + (dense_end - dense_begin) + k rows, at most
+ * PARISKV_MAX_ATTEND_ROWS.  The three sets must not share a row (a shared row
+ * would count twice).  All four fields 0 = the retrieved keys only, at their
+ * own row numbers (plain pariskv_sparse_attend). */
+typedef struct pariskv_window {
+    int64_t sink_len;
+    int64_t retr_begin;
+    int64_t dense_begin;
+    int64_t dense_end;
+} pariskv_window;
+
+#define PARISKV_MAX_ATTEND_ROWS 4096
+
 /* Byte offsets of the intermediate arrays inside a retrieve workspace.  They
  * are stable for given (config, batch, n, budget), so a caller may inspect
  * them after pariskv_retrieve (the parity tests do). */
@@ -155,6 +176,31 @@ int pariskv_encode(const pariskv_config* cfg, const pariskv_index* index,
 int pariskv_append(const pariskv_config* cfg, const pariskv_index* index,
                    const void* keys, int64_t n_cur, int64_t t, int32_t batch,
                    void* stream);
+
+/* Streaming update read straight from the layer's key cache (Sec. "Buffer
+ * Update" steps (i) and (iii): the oldest Local tokens move to Retrieval and
+ * their keys are encoded and indexed).  K: device float16
+ * [batch][Hkv][kv_capacity][D].  Encodes cache rows [row_begin, row_begin + t)
+ * of every (sequence, KV head) into index rows [n_cur, n_cur + t) and adds them
+ * to counts: the same bytes pariskv_append writes for those rows copied out.
+ * Errors: INVALID (row range outside the cache), CAPACITY (n_cur + t >
+ * capacity), HIP. */
+int pariskv_append_rows(const pariskv_config* cfg, const pariskv_index* index,
+                        const void* K, int64_t kv_capacity, int64_t row_begin,
+                        int64_t n_cur, int64_t t, int32_t batch, void* stream);
+
+/* The four regions after a prompt of P tokens and t decode steps (Sec.
+ * "Buffer Update"): the prompt's first min(sink, P) tokens are Sink, its last
+ * min(local, P - sink) tokens Local, the rest Retrieval; every decode token
+ * enters the Update Buffer, and when the buffer holds m tokens, Local becomes
+ * the most recent `local` tokens of Local + Buffer, the older ones joining
+ * Retrieval.  Fills `out` for pariskv_window_attend (Sink at rows [0,
+ * sink_len), Retrieval at rows [retr_begin, dense_begin), Local + Buffer at
+ * [dense_begin, P + t)) and *n_retrieval = dense_begin - retr_begin, the
+ * number of keys the retrieval index must hold.  Host only.
+ * Errors: INVALID (negative sizes, m < 1, overflow). */
+int pariskv_window_regions(int64_t P, int64_t t, int64_t sink, int64_t local, int64_t m,
+                           pariskv_window* out, int64_t* n_retrieval);
 
 /* ------------------------------------------------------------ retrieval */
 
@@ -220,6 +266,35 @@ int pariskv_sparse_attend(const pariskv_config* cfg, const void* q, const void* 
                           const void* V, int32_t kv_host_mapped, int64_t kv_capacity,
                           const int32_t* idx, int32_t k, int32_t batch, float scale,
                           float* out, void* stream);
+
+/* Attention of a decode step over Sink, the retrieved keys and Local + Update
+ * Buffer (Sec. "Buffer Update"; Eqs. approx_weight, approx_output with C(q)
+ * the union of the three row sets of `win`):
+ *   o = sum_{i in rows} softmax_i(scale * <k_i, q>) v_i.
+ * Arguments as in pariskv_sparse_attend; idx holds retrieval index rows
+ * (entry j attends cache row win->retr_begin + idx[j]; entries < 0 and rows
+ * outside [0, kv_capacity) are skipped).  win: host pointer.
+ * Errors: INVALID (window rows outside the cache or out of order: sink_len <=
+ * retr_begin <= dense_begin <= dense_end <= kv_capacity), UNSUPPORTED (more than
+ * PARISKV_MAX_ATTEND_ROWS rows per head), HIP. */
+int pariskv_window_attend(const pariskv_config* cfg, const void* q, const void* K,
+                          const void* V, int32_t kv_host_mapped, int64_t kv_capacity,
+                          const int32_t* idx, int32_t k, const pariskv_window* win,
+                          int32_t batch, float scale, float* out, void* stream);
+
+/* pariskv_retrieve over the Retrieval region (n index rows, the keys of cache
+ * rows [win->retr_begin, win->retr_begin + n)) followed by
+ * pariskv_window_attend over Sink + winners + Local/Buffer, in one call, with
+ * the same outputs bit for bit.  For C <= 32768 the attention runs inside the
+ * top-k kernel.  Also requires win->retr_begin + n <= win->dense_begin.
+ * Errors: those of pariskv_retrieve and pariskv_window_attend. */
+int pariskv_retrieve_window_attend(const pariskv_config* cfg, const pariskv_index* index,
+                                   const void* q, int64_t n, int32_t batch,
+                                   const pariskv_budget* budget, int32_t* out_idx,
+                                   float* out_score, const void* K, const void* V,
+                                   int32_t kv_host_mapped, int64_t kv_capacity,
+                                   const pariskv_window* win, float scale, float* out,
+                                   void* workspace, size_t ws_bytes, void* stream);
 
 /* ------------------------------------------------------------ utilities */
 

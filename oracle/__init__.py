@@ -24,10 +24,13 @@ retrieve    Query transform, tier-weighted collision scores (Eq.
             estimator (Eq. rsqip_raw_weighted) and the final top-k.
 attention   Exact and candidate-restricted softmax attention
             (Eqs. full_attention, approx_weight, approx_output).
+window      The four decode-time KV regions (Sink, Retrieval, Local, Update
+            Buffer) replayed token by token from Sec. "Buffer Update", and
+            attention over Sink + retrieved + Local + Buffer rows.
 
 Parity status: every function is pinned by a ``-m "not gpu"`` test against
 something other than itself (worked examples, closed forms, brute force,
 hand-computed fixtures or distributional facts).  None is "parity unpinned".
 """
 
-from . import quantizer, rotation, encode, retrieve, attention  # noqa: F401
+from . import quantizer, rotation, encode, retrieve, attention, window  # noqa: F401

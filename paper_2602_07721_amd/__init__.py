@@ -18,9 +18,9 @@ from dataclasses import dataclass
 import numpy as np
 
 __all__ = [
-    "PariskvError", "Config", "Budget", "Index", "lib", "encode", "append", "retrieve",
-    "retrieve_workspace_size", "workspace_layout", "sparse_attend", "retrieve_attend", "quantizer_table",
-    "rotation_signs",
+    "PariskvError", "Config", "Budget", "Index", "Window", "lib", "encode", "append", "append_rows",
+    "retrieve", "retrieve_workspace_size", "workspace_layout", "sparse_attend", "retrieve_attend",
+    "window_regions", "window_attend", "retrieve_window_attend", "quantizer_table", "rotation_signs",
     "profile_enable", "profile_reset", "profile_read",
 ]
 
@@ -28,6 +28,7 @@ LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libpariskv.
 
 OK, ERR_INVALID, ERR_CAPACITY, ERR_WORKSPACE, ERR_HIP, ERR_UNSUPPORTED = 0, -1, -2, -3, -4, -5
 HEAD_DIM, SUBSPACES, CENTROIDS, REC_BYTES = 128, 16, 256, 128
+MAX_ATTEND_ROWS = 4096
 
 
 class PariskvError(RuntimeError):
@@ -48,6 +49,11 @@ class _Index(ctypes.Structure):
 
 class _Budget(ctypes.Structure):
     _fields_ = [("n_cand", ctypes.c_int64), ("n_collide", ctypes.c_int64), ("top_k", ctypes.c_int32)]
+
+
+class _Window(ctypes.Structure):
+    _fields_ = [("sink_len", ctypes.c_int64), ("retr_begin", ctypes.c_int64),
+                ("dense_begin", ctypes.c_int64), ("dense_end", ctypes.c_int64)]
 
 
 class _Layout(ctypes.Structure):
@@ -71,6 +77,13 @@ def lib():
         P, VP, I32, I64, SZ = ctypes.POINTER, ctypes.c_void_p, ctypes.c_int32, ctypes.c_int64, ctypes.c_size_t
         L.pariskv_encode.argtypes = [P(_Config), P(_Index), VP, I64, I32, VP]
         L.pariskv_append.argtypes = [P(_Config), P(_Index), VP, I64, I64, I32, VP]
+        L.pariskv_append_rows.argtypes = [P(_Config), P(_Index), VP, I64, I64, I64, I64, I32, VP]
+        L.pariskv_window_regions.argtypes = [I64, I64, I64, I64, I64, P(_Window), P(I64)]
+        L.pariskv_window_attend.argtypes = [P(_Config), VP, VP, VP, I32, I64, VP, I32, P(_Window), I32,
+                                            ctypes.c_float, VP, VP]
+        L.pariskv_retrieve_window_attend.argtypes = [P(_Config), P(_Index), VP, I64, I32, P(_Budget), VP,
+                                                     VP, VP, VP, I32, I64, P(_Window), ctypes.c_float, VP,
+                                                     VP, SZ, VP]
         L.pariskv_retrieve_workspace.argtypes = [P(_Config), I32, I64, P(_Budget)]
         L.pariskv_retrieve_workspace.restype = SZ
         L.pariskv_workspace_layout.argtypes = [P(_Config), I32, I64, P(_Budget), P(_Layout)]
@@ -189,6 +202,42 @@ def append(cfg, index, keys, n_cur, stream=None):
                                 int(keys.shape[0]), _stream(stream)))
 
 
+def append_rows(cfg, index, K, row_begin, t, n_cur, stream=None):
+    """Streaming update from the key cache K [batch][Hkv][kv_capacity][D]: encode cache rows
+    [row_begin, row_begin + t) into index rows [n_cur, n_cur + t)."""
+    _check(lib().pariskv_append_rows(cfg.c(), index.c(), _ptr(K, "K"), int(K.shape[2]), int(row_begin),
+                                     int(n_cur), int(t), int(K.shape[0]), _stream(stream)))
+
+
+@dataclass
+class Window:
+    """Rows attended besides the retrieved keys (see ``pariskv_window``): Sink rows
+    [0, sink_len), retrieved index row i at cache row retr_begin + i, Local + Update Buffer
+    rows [dense_begin, dense_end)."""
+    sink_len: int = 0
+    retr_begin: int = 0
+    dense_begin: int = 0
+    dense_end: int = 0
+
+    @property
+    def dense_rows(self):
+        return self.sink_len + self.dense_end - self.dense_begin
+
+    def c(self):
+        self._c = _Window(self.sink_len, self.retr_begin, self.dense_begin, self.dense_end)
+        return ctypes.byref(self._c)
+
+
+def window_regions(P, t, sink=128, local=512, m=256):
+    """(Window, n_retrieval) after a prompt of P tokens and t decode steps, buffer updates
+    every m steps (Sec. "Buffer Update"); see ``pariskv_window_regions``."""
+    w = _Window()
+    n = ctypes.c_int64()
+    _check(lib().pariskv_window_regions(int(P), int(t), int(sink), int(local), int(m), ctypes.byref(w),
+                                        ctypes.byref(n)))
+    return Window(w.sink_len, w.retr_begin, w.dense_begin, w.dense_end), int(n.value)
+
+
 def retrieve_workspace_size(cfg, batch, n, budget):
     return int(lib().pariskv_retrieve_workspace(cfg.c(), batch, n, budget.c()))
 
@@ -260,6 +309,51 @@ def sparse_attend(cfg, q, K, V, idx, scale, out=None, kv_host_mapped=False, stre
                                        int(K.shape[2]), _ptr(idx, "idx"), k, batch, float(scale),
                                        _ptr(out, "out"), _stream(stream)))
     return out
+
+
+def window_attend(cfg, q, K, V, idx, win, scale, out=None, kv_host_mapped=False, stream=None):
+    """Attention over Sink + retrieved (retr_begin + idx) + Local/Buffer rows of ``win``."""
+    import torch
+    batch = int(q.shape[0])
+    if out is None:
+        out = torch.empty((batch, cfg.n_q_heads, HEAD_DIM), dtype=torch.float32, device=q.device)
+    if kv_host_mapped:
+        for t, nm in ((K, "K"), (V, "V")):
+            if t.is_cuda or not t.is_pinned():
+                raise ValueError(f"{nm} must be pinned host memory when kv_host_mapped")
+    k = int(idx.shape[-1])
+    _check(lib().pariskv_window_attend(cfg.c(), _ptr(q, "q"), _ptr(K, "K", not kv_host_mapped),
+                                       _ptr(V, "V", not kv_host_mapped), int(bool(kv_host_mapped)),
+                                       int(K.shape[2]), _ptr(idx, "idx"), k, win.c(), batch, float(scale),
+                                       _ptr(out, "out"), _stream(stream)))
+    return out
+
+
+def retrieve_window_attend(cfg, index, q, n, budget, K, V, win, scale, out_idx=None, out_score=None,
+                           out=None, workspace=None, kv_host_mapped=False, stream=None):
+    """retrieve over the Retrieval region + window_attend in one call; returns
+    (idx, score, out, workspace)."""
+    import torch
+    batch = int(q.shape[0])
+    rows = batch * cfg.n_q_heads
+    if out_idx is None:
+        out_idx = torch.empty((batch, cfg.n_q_heads, budget.top_k), dtype=torch.int32, device=q.device)
+    if out is None:
+        out = torch.empty((batch, cfg.n_q_heads, HEAD_DIM), dtype=torch.float32, device=q.device)
+    if workspace is None:
+        workspace = torch.empty(max(256, retrieve_workspace_size(cfg, batch, n, budget)),
+                                dtype=torch.uint8, device=q.device)
+    if kv_host_mapped:
+        for t, nm in ((K, "K"), (V, "V")):
+            if t.is_cuda or not t.is_pinned():
+                raise ValueError(f"{nm} must be pinned host memory when kv_host_mapped")
+    assert out_idx.numel() == rows * budget.top_k
+    _check(lib().pariskv_retrieve_window_attend(
+        cfg.c(), index.c(), _ptr(q, "q"), int(n), batch, budget.c(), _ptr(out_idx, "out_idx"),
+        _ptr(out_score, "out_score"), _ptr(K, "K", not kv_host_mapped), _ptr(V, "V", not kv_host_mapped),
+        int(bool(kv_host_mapped)), int(K.shape[2]), win.c(), float(scale), _ptr(out, "out"),
+        _ptr(workspace, "workspace"), workspace.numel(), _stream(stream)))
+    return out_idx, out_score, out, workspace
 
 
 def quantizer_table(m=8):

@@ -235,7 +235,7 @@ using namespace pariskv;
 
 extern "C" {
 
-int32_t pariskv_abi_version(void) { return 1; }
+int32_t pariskv_abi_version(void) { return 2; }
 
 const char* pariskv_strerror(int code) {
     switch (code) {
@@ -272,7 +272,8 @@ int pariskv_quantizer_table(int32_t m, double* tau, double* a) {
 }
 
 static int encode_common(const pariskv_config* cfg, const pariskv_index* index, const void* keys,
-                         int64_t row0, int64_t t, int32_t batch, bool reset_counts, void* stream) {
+                         int64_t src_stride, int64_t row0, int64_t t, int32_t batch, bool reset_counts,
+                         void* stream) {
     prof_chain_start();
     int rc = check_config(cfg, batch);
     if (rc) return rc;
@@ -291,8 +292,8 @@ static int encode_common(const pariskv_config* cfg, const pariskv_index* index, 
         e = launch_zero_u32(index->counts, groups * kB * kCentroids, s);
         if (e != hipSuccess) return hip_fail(e, "zero counts");
     }
-    e = launch_encode(keys, t, groups, row0, cfg->capacity, index->ids, index->rec, index->counts,
-                      pack_signs(cfg->rot_signs), quant_consts(), s);
+    e = launch_encode(keys, t, src_stride < 0 ? t : src_stride, groups, row0, cfg->capacity, index->ids,
+                      index->rec, index->counts, pack_signs(cfg->rot_signs), quant_consts(), s);
     if (e != hipSuccess) return hip_fail(e, "encode launch");
     return PARISKV_OK;
 }
@@ -300,12 +301,49 @@ static int encode_common(const pariskv_config* cfg, const pariskv_index* index, 
 int pariskv_encode(const pariskv_config* cfg, const pariskv_index* index, const void* keys,
                    int64_t n, int32_t batch, void* stream) {
     if (n < 0) return fail(PARISKV_ERR_INVALID, "n %lld < 0", (long long)n);
-    return encode_common(cfg, index, keys, 0, n, batch, true, stream);
+    return encode_common(cfg, index, keys, -1, 0, n, batch, true, stream);
 }
 
 int pariskv_append(const pariskv_config* cfg, const pariskv_index* index, const void* keys,
                    int64_t n_cur, int64_t t, int32_t batch, void* stream) {
-    return encode_common(cfg, index, keys, n_cur, t, batch, false, stream);
+    return encode_common(cfg, index, keys, -1, n_cur, t, batch, false, stream);
+}
+
+int pariskv_append_rows(const pariskv_config* cfg, const pariskv_index* index, const void* K,
+                        int64_t kv_capacity, int64_t row_begin, int64_t n_cur, int64_t t,
+                        int32_t batch, void* stream) {
+    if (kv_capacity < 1 || kv_capacity > INT32_MAX)
+        return fail(PARISKV_ERR_INVALID, "kv_capacity %lld outside 1..2^31-1", (long long)kv_capacity);
+    if (row_begin < 0 || t < 0 || row_begin > kv_capacity - t)
+        return fail(PARISKV_ERR_INVALID, "cache rows [%lld, %lld + %lld) outside [0, %lld)",
+                    (long long)row_begin, (long long)row_begin, (long long)t, (long long)kv_capacity);
+    const void* src = K ? static_cast<const void*>(static_cast<const char*>(K) + row_begin * kD * 2) : nullptr;
+    return encode_common(cfg, index, src, kv_capacity, n_cur, t, batch, false, stream);
+}
+
+int pariskv_window_regions(int64_t P, int64_t t, int64_t sink, int64_t local, int64_t m,
+                           pariskv_window* out, int64_t* n_retrieval) {
+    if (!out || !n_retrieval) return fail(PARISKV_ERR_INVALID, "NULL output");
+    if (P < 0 || t < 0 || sink < 0 || local < 0 || m < 1)
+        return fail(PARISKV_ERR_INVALID, "negative size or m < 1");
+    if (P > (int64_t(1) << 40) || t > (int64_t(1) << 40))
+        return fail(PARISKV_ERR_INVALID, "P or t above 2^40");
+    // After the prompt: Sink = first min(sink, P) tokens, Local = last min(local,
+    // rest) tokens, Retrieval in between.  After u = t / m buffer updates Local
+    // holds min(local, l0 + u m) tokens ending at P + u m; the buffer holds the
+    // t - u m newest tokens.
+    const int64_t s_len = sink < P ? sink : P;
+    const int64_t l0 = local < P - s_len ? local : P - s_len;
+    const int64_t u = t / m;
+    const int64_t grown = l0 + u * m;
+    const int64_t l_u = local < grown ? local : grown;
+    const int64_t local_end = P + u * m;
+    out->sink_len = s_len;
+    out->retr_begin = s_len;
+    out->dense_begin = local_end - l_u;
+    out->dense_end = P + t;
+    *n_retrieval = out->dense_begin - s_len;
+    return PARISKV_OK;
 }
 
 size_t pariskv_retrieve_workspace(const pariskv_config* cfg, int32_t batch, int64_t n,
@@ -329,7 +367,36 @@ struct AttendReq {
     int64_t kv_capacity;
     float scale;
     float* out;
+    AttendWindow win;
 };
+
+// Window rows in order and inside the cache; with k retrieved rows per head the
+// list fits one attention block.  n >= 0: the retrieval index holds n keys,
+// whose rows [retr_begin, retr_begin + n) must end before the dense rows.
+static int check_window(const pariskv_window* w, int64_t kv_capacity, int64_t k, int64_t n,
+                        AttendWindow* out) {
+    *out = AttendWindow{};
+    if (!w) return PARISKV_OK;
+    if (w->sink_len < 0 || w->retr_begin < w->sink_len || w->dense_begin < w->retr_begin ||
+        w->dense_end < w->dense_begin || w->dense_end > kv_capacity)
+        return fail(PARISKV_ERR_INVALID,
+                    "window needs 0 <= sink_len (%lld) <= retr_begin (%lld) <= dense_begin (%lld) <= "
+                    "dense_end (%lld) <= kv_capacity (%lld)",
+                    (long long)w->sink_len, (long long)w->retr_begin, (long long)w->dense_begin,
+                    (long long)w->dense_end, (long long)kv_capacity);
+    if (n >= 0 && w->retr_begin + n > w->dense_begin)
+        return fail(PARISKV_ERR_INVALID, "retrieval rows [%lld, %lld) overlap the dense rows from %lld",
+                    (long long)w->retr_begin, (long long)(w->retr_begin + n), (long long)w->dense_begin);
+    const int64_t rows = w->sink_len + (w->dense_end - w->dense_begin) + k;
+    if (rows > kMaxAttendRows)
+        return fail(PARISKV_ERR_UNSUPPORTED, "%lld attended rows per head, above %d", (long long)rows,
+                    kMaxAttendRows);
+    out->sink = w->sink_len;
+    out->retr_begin = w->retr_begin;
+    out->dense_begin = w->dense_begin;
+    out->dense_end = w->dense_end;
+    return PARISKV_OK;
+}
 
 static int check_attend_args(const AttendReq& r) {
     if (!r.K || !r.V || !r.out) return fail(PARISKV_ERR_INVALID, "K, V and out must be non-NULL");
@@ -429,6 +496,7 @@ static int retrieve_impl(const pariskv_config* cfg, const pariskv_index* index, 
         a.kv_capacity = att->kv_capacity;
         a.scale = att->scale;
         a.attn_out = att->out;
+        a.win = att->win;
     }
 
     hipStream_t s = static_cast<hipStream_t>(stream);
@@ -436,7 +504,7 @@ static int retrieve_impl(const pariskv_config* cfg, const pariskv_index* index, 
     // Attention by its own kernel over out_idx (when the top-k did not fuse it).
     auto attend_separately = [&]() -> int {
         const hipError_t ea = launch_attend(q, Kd, Vd, att->kv_capacity, out_idx, budget->top_k, batch,
-                                            a.hkv, a.g, att->scale, att->out, s);
+                                            a.hkv, a.g, att->scale, att->out, att->win, s);
         return ea == hipSuccess ? PARISKV_OK : hip_fail(ea, "attend launch");
     };
     if (n == 0) {
@@ -466,14 +534,31 @@ int pariskv_retrieve_attend(const pariskv_config* cfg, const pariskv_index* inde
                             float* out_score, const void* K, const void* V, int32_t kv_host_mapped,
                             int64_t kv_capacity, float scale, float* out, void* workspace,
                             size_t ws_bytes, void* stream) {
-    const AttendReq att{K, V, kv_host_mapped, kv_capacity, scale, out};
+    const AttendReq att{K, V, kv_host_mapped, kv_capacity, scale, out, AttendWindow{}};
     return retrieve_impl(cfg, index, q, n, batch, budget, out_idx, out_score, workspace, ws_bytes,
                          stream, &att);
 }
 
-int pariskv_sparse_attend(const pariskv_config* cfg, const void* q, const void* K, const void* V,
-                          int32_t kv_host_mapped, int64_t kv_capacity, const int32_t* idx, int32_t k,
-                          int32_t batch, float scale, float* out, void* stream) {
+int pariskv_retrieve_window_attend(const pariskv_config* cfg, const pariskv_index* index,
+                                   const void* q, int64_t n, int32_t batch,
+                                   const pariskv_budget* budget, int32_t* out_idx, float* out_score,
+                                   const void* K, const void* V, int32_t kv_host_mapped,
+                                   int64_t kv_capacity, const pariskv_window* win, float scale,
+                                   float* out, void* workspace, size_t ws_bytes, void* stream) {
+    prof_chain_start();
+    if (!win) return fail(PARISKV_ERR_INVALID, "win must be non-NULL");
+    if (!budget) return fail(PARISKV_ERR_INVALID, "budget must be non-NULL");
+    AttendReq att{K, V, kv_host_mapped, kv_capacity, scale, out, AttendWindow{}};
+    int rc = check_window(win, kv_capacity, budget->top_k, n < 0 ? 0 : n, &att.win);
+    if (rc) return rc;
+    return retrieve_impl(cfg, index, q, n, batch, budget, out_idx, out_score, workspace, ws_bytes,
+                         stream, &att);
+}
+
+static int attend_impl(const pariskv_config* cfg, const void* q, const void* K, const void* V,
+                       int32_t kv_host_mapped, int64_t kv_capacity, const int32_t* idx, int32_t k,
+                       const pariskv_window* win, int32_t batch, float scale, float* out,
+                       void* stream) {
     prof_chain_start();
     int rc = check_config(cfg, batch);
     if (rc) return rc;
@@ -483,12 +568,14 @@ int pariskv_sparse_attend(const pariskv_config* cfg, const void* q, const void* 
         (reinterpret_cast<uintptr_t>(idx) & 3u) != 0)
         return fail(PARISKV_ERR_INVALID, "q, K, V, out must be 16-byte aligned, idx 4-byte aligned");
     if (k < 1) return fail(PARISKV_ERR_INVALID, "k %d < 1", k);
-    if (k > 4096) return fail(PARISKV_ERR_UNSUPPORTED, "k %d above 4096", k);
+    if (k > kMaxAttendRows) return fail(PARISKV_ERR_UNSUPPORTED, "k %d above %d", k, kMaxAttendRows);
     if (kv_capacity < 1 || kv_capacity > INT32_MAX)
         return fail(PARISKV_ERR_INVALID, "kv_capacity %lld outside 1..2^31-1", (long long)kv_capacity);
     if (kv_host_mapped != 0 && kv_host_mapped != 1)
         return fail(PARISKV_ERR_INVALID, "kv_host_mapped must be 0 or 1");
     if (!std::isfinite(scale)) return fail(PARISKV_ERR_INVALID, "scale is not finite");
+    AttendWindow aw;
+    if ((rc = check_window(win, kv_capacity, k, -1, &aw)) != PARISKV_OK) return rc;
     const void* Kd = K;
     const void* Vd = V;
     if (kv_host_mapped) {
@@ -501,9 +588,25 @@ int pariskv_sparse_attend(const pariskv_config* cfg, const void* q, const void* 
         Vd = p;
     }
     hipError_t e = launch_attend(q, Kd, Vd, kv_capacity, idx, k, batch, cfg->n_kv_heads,
-                                 cfg->q_per_kv, scale, out, static_cast<hipStream_t>(stream));
+                                 cfg->q_per_kv, scale, out, aw, static_cast<hipStream_t>(stream));
     if (e != hipSuccess) return hip_fail(e, "attend launch");
     return PARISKV_OK;
+}
+
+int pariskv_sparse_attend(const pariskv_config* cfg, const void* q, const void* K, const void* V,
+                          int32_t kv_host_mapped, int64_t kv_capacity, const int32_t* idx, int32_t k,
+                          int32_t batch, float scale, float* out, void* stream) {
+    return attend_impl(cfg, q, K, V, kv_host_mapped, kv_capacity, idx, k, nullptr, batch, scale, out,
+                       stream);
+}
+
+int pariskv_window_attend(const pariskv_config* cfg, const void* q, const void* K, const void* V,
+                          int32_t kv_host_mapped, int64_t kv_capacity, const int32_t* idx, int32_t k,
+                          const pariskv_window* win, int32_t batch, float scale, float* out,
+                          void* stream) {
+    if (!win) return fail(PARISKV_ERR_INVALID, "win must be non-NULL");
+    return attend_impl(cfg, q, K, V, kv_host_mapped, kv_capacity, idx, k, win, batch, scale, out,
+                       stream);
 }
 
 int pariskv_profile_enable(int32_t on) {

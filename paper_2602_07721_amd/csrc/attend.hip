@@ -5,18 +5,19 @@
 //
 //   o = sum_{i in idx} softmax_i(scale <k_i, q>) v_i,  fp16 in, fp32 math.
 //
-// One block of 1024 threads per query head: the row's indices are staged in
-// LDS, then the shared attention body of attend_row.hpp (64 key slots of 16
-// lanes, 8 K and 8 V row segments in flight per lane, online softmax merged in
-// LDS) runs over them.  Indices outside [0, kv_capacity) are skipped like -1.
+// One block of 1024 threads per query head: the row's list is staged in LDS
+// -- Sink rows, then Local + Update Buffer rows, then the retrieved keys at
+// their cache rows (Sec. "Buffer Update"; with an all-zero window just the
+// retrieved keys) -- and the shared attention body of attend_row.hpp (64 key
+// slots of 16 lanes, 8 K and 8 V row segments in flight per lane, online
+// softmax merged in LDS) runs over it.  Retrieved entries that are negative or
+// land outside [0, kv_capacity) are empty slots.
 
 #include "attend_row.hpp"
 
 namespace pariskv {
 
 namespace {
-
-constexpr int kAtMaxK = 4096;  // largest k a block stages in LDS
 
 __global__ __launch_bounds__(kAtThreads) void attend_kernel(const __half* __restrict__ q,
                                                             const __half* __restrict__ K,
@@ -25,18 +26,32 @@ __global__ __launch_bounds__(kAtThreads) void attend_kernel(const __half* __rest
                                                             const int32_t* __restrict__ idx,
                                                             int32_t k, int32_t hkv, int32_t g,
                                                             int32_t hq, float scale,
-                                                            float* __restrict__ out) {
+                                                            float* __restrict__ out, AttendWindow win) {
     __shared__ AttendScratch s_sm;
-    __shared__ int32_t s_idx[kAtMaxK];
+    __shared__ int32_t s_idx[kMaxAttendRows];
     const int64_t row = blockIdx.x;  // seq * hq + head
     const int seq = (int)(row / hq);
     const int h = (int)(row % hq);
     const int64_t kvrow0 = ((int64_t)seq * hkv + h / g) * kv_capacity;
-    // Stage the row's indices so the row loads never wait on them.
+    // Stage the row's list so the row loads never wait on it (the host checked
+    // that dense rows + k fit kMaxAttendRows).
     const int32_t* ir = idx + row * k;
-    for (int r = threadIdx.x; r < k; r += kAtThreads) s_idx[r] = ir[r];
+    const int nd = (int)win.dense_rows();
+    for (int r = threadIdx.x; r < nd + k; r += kAtThreads) {
+        int32_t v;
+        if (r < win.sink) {
+            v = r;
+        } else if (r < nd) {
+            v = (int32_t)(win.dense_begin + (r - win.sink));
+        } else {
+            const int32_t j = ir[r - nd];
+            const int64_t cr = win.retr_begin + (int64_t)j;
+            v = (j >= 0 && cr < kv_capacity) ? (int32_t)cr : -1;
+        }
+        s_idx[r] = v;
+    }
     __syncthreads();
-    attend_row(q + row * kD, K + kvrow0 * kD, V + kvrow0 * kD, kv_capacity, s_idx, k, scale,
+    attend_row(q + row * kD, K + kvrow0 * kD, V + kvrow0 * kD, kv_capacity, s_idx, nd + k, scale,
                out + row * kD, s_sm);
 }
 
@@ -44,12 +59,12 @@ __global__ __launch_bounds__(kAtThreads) void attend_kernel(const __half* __rest
 
 hipError_t launch_attend(const void* q, const void* K, const void* V, int64_t kv_capacity,
                          const int32_t* idx, int32_t k, int32_t batch, int32_t hkv, int32_t g,
-                         float scale, float* out, hipStream_t s) {
+                         float scale, float* out, const AttendWindow& win, hipStream_t s) {
     const int32_t hq = hkv * g;
-    const ProfEvents pe = prof_begin("attend");
+    const ProfEvents pe = prof_begin(win.dense_rows() > 0 ? "window_attend" : "attend");
     hipExtLaunchKernelGGL(attend_kernel, dim3((unsigned)(batch * hq)), dim3(kAtThreads), 0, s, pe.start, pe.stop, 0,
                        static_cast<const __half*>(q), static_cast<const __half*>(K),
-                       static_cast<const __half*>(V), kv_capacity, idx, k, hkv, g, hq, scale, out);
+                       static_cast<const __half*>(V), kv_capacity, idx, k, hkv, g, hq, scale, out, win);
     return hipGetLastError();
 }
 

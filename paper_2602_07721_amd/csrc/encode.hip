@@ -48,7 +48,7 @@ __device__ __forceinline__ double tree8_sum(const double* v) {
 
 template <bool kLdsCounts>
 __global__ __launch_bounds__(kThreads) void encode_kernel(
-    const __half* __restrict__ keys, int64_t n_src, int64_t keys_per_block, int64_t row0,
+    const __half* __restrict__ keys, int64_t n_src, int64_t src_stride, int64_t keys_per_block, int64_t row0,
     int64_t capacity, uint8_t* __restrict__ ids, uint8_t* __restrict__ rec,
     uint32_t* __restrict__ counts, SignBits sb, QuantConsts qc) {
     __shared__ double s_a[8];
@@ -78,7 +78,7 @@ __global__ __launch_bounds__(kThreads) void encode_kernel(
         // Out-of-range lanes still join the shuffles (with zeros) and store nothing.
         double x[32];
         if (live) {
-            const uint4* src = reinterpret_cast<const uint4*>(keys + ((grp * n_src + i) * kD + 32 * q));
+            const uint4* src = reinterpret_cast<const uint4*>(keys + ((grp * src_stride + i) * kD + 32 * q));
 #pragma unroll
             for (int c = 0; c < 4; ++c) {
                 uint4 v = src[c];
@@ -198,9 +198,9 @@ hipError_t launch_zero_u32(uint32_t* p, int64_t count, hipStream_t s) {
     return hipGetLastError();
 }
 
-hipError_t launch_encode(const void* keys, int64_t n_src, int64_t groups, int64_t row0,
-                         int64_t capacity, uint8_t* ids, uint8_t* rec, uint32_t* counts,
-                         const SignBits& sb, const QuantConsts& qc, hipStream_t s) {
+hipError_t launch_encode(const void* keys, int64_t n_src, int64_t src_stride, int64_t groups,
+                         int64_t row0, int64_t capacity, uint8_t* ids, uint8_t* rec,
+                         uint32_t* counts, const SignBits& sb, const QuantConsts& qc, hipStream_t s) {
     if (n_src <= 0 || groups <= 0) return hipSuccess;
     const __half* k = static_cast<const __half*>(keys);
     if (n_src >= 1024) {
@@ -209,14 +209,14 @@ hipError_t launch_encode(const void* keys, int64_t n_src, int64_t groups, int64_
         const int64_t bx = (n_src + per - 1) / per;
         const ProfEvents pe = prof_begin("encode");
         hipExtLaunchKernelGGL(encode_kernel<true>, dim3((unsigned)bx, (unsigned)groups), dim3(kThreads),
-                           0, s, pe.start, pe.stop, 0, k, n_src, per, row0, capacity, ids, rec, counts, sb, qc);
+                           0, s, pe.start, pe.stop, 0, k, n_src, src_stride, per, row0, capacity, ids, rec, counts, sb, qc);
     } else {
         // Streaming append: few keys per group, count straight into global memory.
         const int64_t per = kKeysPerIter;
         const int64_t bx = (n_src + per - 1) / per;
         const ProfEvents pe = prof_begin("append");
         hipExtLaunchKernelGGL(encode_kernel<false>, dim3((unsigned)bx, (unsigned)groups), dim3(kThreads),
-                           0, s, pe.start, pe.stop, 0, k, n_src, per, row0, capacity, ids, rec, counts, sb, qc);
+                           0, s, pe.start, pe.stop, 0, k, n_src, src_stride, per, row0, capacity, ids, rec, counts, sb, qc);
     }
     return hipGetLastError();
 }

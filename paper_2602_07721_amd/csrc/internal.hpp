@@ -96,10 +96,25 @@ bool quantizer_table_m8(double* tau, double* a);
 
 hipError_t launch_zero_u32(uint32_t* p, int64_t count, hipStream_t s);
 
-// Encode keys [groups][n_src][D] into rows [row0, row0 + n_src) of each group.
-hipError_t launch_encode(const void* keys, int64_t n_src, int64_t groups, int64_t row0,
-                         int64_t capacity, uint8_t* ids, uint8_t* rec, uint32_t* counts,
-                         const SignBits& sb, const QuantConsts& qc, hipStream_t s);
+// Encode the first n_src rows of keys [groups][src_stride][D] into rows
+// [row0, row0 + n_src) of each group (src_stride = n_src for a packed batch of
+// keys, the cache capacity when the rows are read straight from a K cache).
+hipError_t launch_encode(const void* keys, int64_t n_src, int64_t src_stride, int64_t groups,
+                         int64_t row0, int64_t capacity, uint8_t* ids, uint8_t* rec,
+                         uint32_t* counts, const SignBits& sb, const QuantConsts& qc, hipStream_t s);
+
+// Rows one query head attends (Sec. "Buffer Update": Sink and Local + Update
+// Buffer densely, the retrieved keys sparsely).  The head's list is
+//   [0, sink) ++ [dense_begin, dense_end) ++ (retr_begin + idx_j for idx_j >= 0),
+// in that order (idx_j < 0 stays an empty slot).  All zero = the retrieved keys
+// only, at their own row numbers.
+struct AttendWindow {
+    int64_t sink = 0;
+    int64_t retr_begin = 0;
+    int64_t dense_begin = 0;
+    int64_t dense_end = 0;
+    __host__ __device__ int64_t dense_rows() const { return sink + (dense_end - dense_begin); }
+};
 
 struct RetrieveArgs {
     // shapes
@@ -133,6 +148,7 @@ struct RetrieveArgs {
     int64_t kv_capacity;
     float scale;
     float* attn_out;
+    AttendWindow win;  // dense rows attended next to the winners
 };
 
 hipError_t launch_query_lut(const RetrieveArgs& a, hipStream_t s);
@@ -147,7 +163,10 @@ hipError_t launch_pad_outputs(const RetrieveArgs& a, hipStream_t s);
 
 hipError_t launch_attend(const void* q, const void* K, const void* V, int64_t kv_capacity,
                          const int32_t* idx, int32_t k, int32_t batch, int32_t hkv, int32_t g,
-                         float scale, float* out, hipStream_t s);
+                         float scale, float* out, const AttendWindow& win, hipStream_t s);
+
+// Largest list (dense rows + retrieved rows) one attention block stages in LDS.
+constexpr int kMaxAttendRows = 4096;
 
 // Kernel-level profiling hooks (no-ops unless enabled).
 // Event pair for one kernel launch when profiling is on (nulls otherwise), to be

@@ -244,7 +244,7 @@ __global__ __launch_bounds__(TH) void topk_lds_kernel(RetrieveArgs a) {
     constexpr size_t kA0 = (size_t)kCap * 4 * (kStageIdx ? 2 : 1);
     constexpr size_t kA = kAttend && kA0 < sizeof(AttendScratch) ? sizeof(AttendScratch) : kA0;
     constexpr size_t kBytes = kA + 2 * kNB * 4;
-    static_assert(!kAttend || 2 * kNB * 4 >= PARISKV_MAX_TOPK * 4, "winners fit in region B");
+    static_assert(!kAttend || 2 * kNB * 4 >= kMaxAttendRows * 4, "the attention list fits in region B");
     __shared__ __align__(16) unsigned char s_raw[kBytes];
     uint32_t* s_key = reinterpret_cast<uint32_t*>(s_raw);
     int32_t* s_idx = reinterpret_cast<int32_t*>(s_raw + (size_t)kCap * 4);
@@ -404,6 +404,10 @@ __global__ __launch_bounds__(TH) void topk_lds_kernel(RetrieveArgs a) {
     uint32_t gb = pre & 0xffffu, eb = pre >> 16;
     int32_t* oi = a.out_idx + row * a.top_k;
     float* os = a.out_score ? a.out_score + row * a.top_k : nullptr;
+    // With kAttend the attention list in region B is Sink rows, then Local +
+    // Update Buffer rows (nd in all), then the winners at their cache rows
+    // (retr_begin + key; the host checked they stay below dense_begin).
+    const int nd = kAttend ? (int)a.win.dense_rows() : 0;
 #pragma unroll
     for (int e = 0; e < EPT; ++e) {
         uint32_t p = 0xffffffffu;
@@ -418,7 +422,7 @@ __global__ __launch_bounds__(TH) void topk_lds_kernel(RetrieveArgs a) {
             const int32_t win = kStageIdx ? s_idx[tid * EPT + e] : cand[tid * EPT + e];
             oi[p] = win;
             if (os) os[p] = key_float(key[e]);
-            if (kAttend) s_win[p] = win;
+            if (kAttend) s_win[nd + p] = (int32_t)(a.win.retr_begin + win);
         }
     }
     for (int r = kk + tid; r < a.top_k; r += TH) {
@@ -426,14 +430,17 @@ __global__ __launch_bounds__(TH) void topk_lds_kernel(RetrieveArgs a) {
         if (os) os[r] = -__builtin_huge_valf();
     }
     if (kAttend) {
-        // Attention over the kk winners (Eqs. approx_weight, approx_output), from LDS.
+        // Attention over the dense rows and the kk winners (Eqs. approx_weight,
+        // approx_output), from LDS.  Region B is free once the compaction runs.
+        for (int r = tid; r < nd; r += TH)
+            s_win[r] = r < a.win.sink ? r : (int32_t)(a.win.dense_begin + (r - a.win.sink));
         __syncthreads();
         const int seq = (int)(row / a.hq);
         const int h = (int)(row % a.hq);
         const int64_t kvrow0 = ((int64_t)seq * a.hkv + h / a.g) * a.kv_capacity;
         attend_row(static_cast<const __half*>(a.q) + row * kD,
                    static_cast<const __half*>(a.K) + kvrow0 * kD,
-                   static_cast<const __half*>(a.V) + kvrow0 * kD, a.kv_capacity, s_win, kk, a.scale,
+                   static_cast<const __half*>(a.V) + kvrow0 * kD, a.kv_capacity, s_win, nd + kk, a.scale,
                    a.attn_out + row * kD, *reinterpret_cast<AttendScratch*>(s_raw));
     }
 }

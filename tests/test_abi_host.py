@@ -31,7 +31,7 @@ def test_every_declared_symbol_is_exported():
     L = pk.lib()
     for n in names:
         assert hasattr(L, n), n
-    assert L.pariskv_abi_version() == 1
+    assert L.pariskv_abi_version() == 2
 
 
 def test_error_strings():
@@ -213,3 +213,83 @@ def test_retrieve_attend_validation():
     assert call(cap=0) == pk.ERR_INVALID
     assert call(scale=float("inf")) == pk.ERR_INVALID
     assert call(size=need - 1) == pk.ERR_WORKSPACE
+
+
+@pytest.mark.parametrize("P,sink,local,m", [(10, 2, 4, 3), (5, 4, 4, 2), (2000, 128, 512, 256), (2000, 128, 512, 512),
+                                            (700, 128, 512, 256), (100, 128, 512, 64), (3000, 0, 512, 1),
+                                            (1000, 16, 8, 32), (0, 128, 512, 256), (130, 128, 512, 7)])
+def test_window_regions_match_the_oracle_replay(P, sink, local, m):
+    # The library's closed form against the oracle's token-by-token replay of Sec. "Buffer Update".
+    from oracle import window
+    R = window.after_prefill(P, sink, local, m)
+    for t in range(0, 1200):
+        if t > 0:
+            window.decode_step(R)
+        w, n = pk.window_regions(P, t, sink, local, m)
+        assert (w.sink_len, w.retr_begin) == (len(R.sink), len(R.sink)), t
+        assert n == len(R.retrieval), t
+        assert list(range(w.retr_begin, w.retr_begin + n)) == R.retrieval, t
+        assert list(range(w.dense_begin, w.dense_end)) == R.local + R.buffer, t
+
+
+def test_window_regions_validation():
+    L = pk.lib()
+    w, n = pk._Window(), ctypes.c_int64()
+    for args in ((-1, 0, 1, 1, 1), (1, -1, 1, 1, 1), (1, 0, -1, 1, 1), (1, 0, 1, -1, 1), (1, 0, 1, 1, 0),
+                 (2**41, 0, 1, 1, 1)):
+        assert L.pariskv_window_regions(*args, ctypes.byref(w), ctypes.byref(n)) == pk.ERR_INVALID
+    assert L.pariskv_window_regions(1, 0, 1, 1, 1, None, ctypes.byref(n)) == pk.ERR_INVALID
+
+
+def test_window_attend_validation():
+    cfg = _cfg()
+    L = pk.lib()
+
+    def call(win, k=8, cap=4096):
+        return L.pariskv_window_attend(cfg.c(), ctypes.c_void_p(FAKE), ctypes.c_void_p(FAKE),
+                                       ctypes.c_void_p(FAKE), 0, cap, ctypes.c_void_p(FAKE), k,
+                                       None if win is None else win.c(), 1, ctypes.c_float(0.1),
+                                       ctypes.c_void_p(FAKE), None)
+    W = pk.Window
+    assert call(None) == pk.ERR_INVALID
+    assert call(W(-1, 0, 0, 0)) == pk.ERR_INVALID                 # negative sink
+    assert call(W(8, 4, 10, 12)) == pk.ERR_INVALID                # retrieval before the sink ends
+    assert call(W(4, 4, 3, 12)) == pk.ERR_INVALID                 # dense before retrieval
+    assert call(W(4, 4, 10, 9)) == pk.ERR_INVALID                 # empty range reversed
+    assert call(W(4, 4, 10, 5000)) == pk.ERR_INVALID              # past the cache
+    assert call(W(128, 128, 3000, 4000), k=2969) == pk.ERR_UNSUPPORTED  # 128 + 1000 + 2969 = 4097 rows
+    # (every case here fails validation: a valid window would launch a kernel on fake pointers)
+
+
+def test_retrieve_window_attend_validation():
+    cfg = _cfg()
+    b = pk.Budget(512, 1024, 64)
+    need = pk.retrieve_workspace_size(cfg, 1, 4000, b)
+    L = pk.lib()
+
+    def call(win, n=4000, cap=8192):
+        return L.pariskv_retrieve_window_attend(cfg.c(), ctypes.byref(_index()), ctypes.c_void_p(FAKE), n, 1,
+                                                b.c(), ctypes.c_void_p(FAKE), None, ctypes.c_void_p(FAKE),
+                                                ctypes.c_void_p(FAKE), 0, cap,
+                                                None if win is None else win.c(), ctypes.c_float(0.1),
+                                                ctypes.c_void_p(FAKE), ctypes.c_void_p(FAKE), need, None)
+    W = pk.Window
+    assert call(None) == pk.ERR_INVALID
+    assert call(W(128, 128, 4000, 4600)) == pk.ERR_INVALID        # retrieval rows run into the dense rows
+    assert call(W(128, 128, 4128, 9000)) == pk.ERR_INVALID        # past the cache
+    assert call(W(2048, 2048, 6048, 8192)) == pk.ERR_UNSUPPORTED  # 2048 + 2144 + 64 rows > 4096
+
+
+def test_append_rows_validation():
+    cfg = _cfg()
+    L = pk.lib()
+
+    def call(cap=4096, row_begin=0, n_cur=0, t=16, K=FAKE):
+        return L.pariskv_append_rows(cfg.c(), ctypes.byref(_index()), ctypes.c_void_p(K), cap, row_begin,
+                                     n_cur, t, 1, None)
+    assert call(cap=0) == pk.ERR_INVALID
+    assert call(row_begin=-1) == pk.ERR_INVALID
+    assert call(row_begin=4090, t=7) == pk.ERR_INVALID            # rows past the cache
+    assert call(t=-1) == pk.ERR_INVALID
+    assert call(K=0) == pk.ERR_INVALID
+    assert call(n_cur=4090, t=16) == pk.ERR_CAPACITY              # index rows past its capacity

@@ -55,8 +55,9 @@ def parse():
     ap.add_argument("--kv-host", action="store_true",
                     help="keep K/V in pinned host memory and attend through host-mapped pointers")
     ap.add_argument("--extras", action="store_true",
-                    help="also measure the drift workload (append + retrieve + attend per step) and "
-                         "attention over K/V in pinned host memory")
+                    help="also measure the drift workload (append + retrieve + attend per step), the "
+                         "same decode with Sink/Local/Update Buffer regions (buffer updates every 256 "
+                         "steps and every step), and attention over K/V in pinned host memory")
     ap.add_argument("--drift-steps", type=int, default=4096,
                     help="decode steps of the drift measurement (the full workload runs 32768)")
     ap.add_argument("--copy-calibration", action="store_true",
@@ -242,6 +243,101 @@ def drift_run(pk, torch, np, workloads, dev, steps):
                                  "min": round(float(r.min()), 4), "mean": round(float(r.mean()), 4),
                                  "every": 256, "points": len(r)},
         "note": "exact top-k by float32 inner products on the GPU (a quality figure, parity unpinned)",
+    }
+
+
+def window_run(pk, torch, np, workloads, dev, steps, sink=128, local=512, updates=(256, 1)):
+    """Decode with the four KV regions (Sec. "Buffer Update") on the drift workload's keys:
+    Sink 128 and Local 512 attended densely, the Retrieval region indexed; every m steps the
+    rows leaving Local are encoded straight from the key cache (pariskv_append_rows), and each
+    step runs pariskv_retrieve_window_attend (retrieval over Retrieval with C = ceil(n/16),
+    C_rho = 2C, then attention over Sink + winners + Local + Update Buffer).  Runs the same
+    decode once per update interval m; per-step GPU time from HIP events around every step."""
+    wc = workloads.CONFIGS["drift"]
+    signs = workloads.rotation_signs(wc.seed)
+    P = wc.n
+    cap = P + steps
+    K0, V0 = workloads.layer_kv(wc, threads=16)
+    Kall = np.zeros((wc.batch, wc.n_kv_heads, cap, wc.head_dim), np.float16)
+    Vall = np.zeros_like(Kall)
+    Kall[:, :, :P] = K0
+    Vall[:, :, :P] = V0
+    rng = np.random.default_rng(wc.seed)
+    for s in range(wc.batch):
+        for h in range(wc.n_kv_heads):
+            Kall[s, h, P:] = workloads.drift_keys(wc.seed, s, h, 0, steps, steps)
+            Vall[s, h, P:] = rng.standard_normal((steps, wc.head_dim)).astype(np.float16)
+    Kd = torch.from_numpy(Kall).to(dev)
+    Vd = torch.from_numpy(Vall).to(dev)
+    hq = wc.n_kv_heads * wc.q_per_kv
+    Qs = np.stack([np.stack([workloads.drift_queries(wc.seed, s, h, steps, wc.q_per_kv)
+                             for h in range(wc.n_kv_heads)], axis=1)
+                   for s in range(wc.batch)], axis=1).reshape(steps, wc.batch, hq, wc.head_dim)
+    Qd = torch.from_numpy(Qs).to(dev)
+    scale = 1.0 / np.sqrt(wc.head_dim)
+    cfg = pk.Config(wc.n_kv_heads, wc.q_per_kv, cap, signs)
+    c_max = -(-cap // 16)
+    ws = torch.empty(pk.retrieve_workspace_size(cfg, wc.batch, cap, pk.Budget(c_max, 2 * c_max, wc.top_k)),
+                     dtype=torch.uint8, device=dev)
+    out_idx = torch.empty((wc.batch, hq, wc.top_k), dtype=torch.int32, device=dev)
+    out = torch.empty((wc.batch, hq, wc.head_dim), dtype=torch.float32, device=dev)
+    evals = set(range(0, steps, 512)) | {steps - 1}
+    res = {}
+    for m in updates:
+        index = pk.Index.empty(cfg, wc.batch, dev)
+        win0, n_idx = pk.window_regions(P, 0, sink, local, m)
+        pk.append_rows(cfg, index, Kd, win0.retr_begin, n_idx, 0)  # the prompt's Retrieval region
+        starts = [torch.cuda.Event(enable_timing=True) for _ in range(steps)]
+        ends = [torch.cuda.Event(enable_timing=True) for _ in range(steps)]
+        upd = np.zeros(steps, bool)
+        recalls = []
+        torch.cuda.synchronize()
+        for t in range(steps):
+            win, n_retr = pk.window_regions(P, t, sink, local, m)
+            starts[t].record()
+            if n_retr > n_idx:
+                pk.append_rows(cfg, index, Kd, win.retr_begin + n_idx, n_retr - n_idx, n_idx)
+                n_idx = n_retr
+                upd[t] = True
+            C = -(-n_retr // 16)
+            pk.retrieve_window_attend(cfg, index, Qd[t], n_retr, pk.Budget(C, 2 * C, wc.top_k), Kd, Vd, win,
+                                      scale, out_idx=out_idx, out=out, workspace=ws)
+            ends[t].record()
+            if t in evals:
+                # recall of the exact top-k over all P + t tokens by the attended rows
+                # (Sink + Local/Buffer + the retrieved winners); a quality figure
+                T = P + t
+                kf = Kd[:, :, :T].float()
+                q = Qd[t].float().reshape(wc.batch, wc.n_kv_heads, wc.q_per_kv, wc.head_dim)
+                sc = torch.matmul(q, kf.transpose(2, 3).contiguous())
+                ex = torch.topk(sc, wc.top_k, dim=-1).indices.reshape(wc.batch, hq, wc.top_k)
+                dense = (ex < win.sink_len) | ((ex >= win.dense_begin) & (ex < win.dense_end))
+                got = out_idx.long() + win.retr_begin
+                got = torch.where(out_idx >= 0, got, torch.full_like(got, -1))
+                hit = dense | (ex.unsqueeze(-1) == got.unsqueeze(-2)).any(-1)
+                recalls.append(float(hit.float().mean().item()))
+                del kf, sc
+        torch.cuda.synchronize()
+        us = np.array([starts[t].elapsed_time(ends[t]) * 1e3 for t in range(steps)])
+        body = us[8:]
+        ub = upd[8:]
+        res[f"m{m}"] = {
+            "update_every": m,
+            "us_per_step": round(float(body.mean()), 2),
+            "us_per_update_step": round(float(body[ub].mean()), 2) if ub.any() else None,
+            "us_per_other_step": round(float(body[~ub].mean()), 2) if (~ub).any() else None,
+            "updates": int(upd.sum()),
+            "retrieval_keys_last": int(n_idx),
+            "recall_at_k_vs_exact_all_tokens": {"first": round(recalls[0], 4), "last": round(recalls[-1], 4),
+                                                "mean": round(float(np.mean(recalls)), 4)},
+        }
+    return {
+        "workload": (f"drift keys: {wc.batch} seqs x {wc.n_kv_heads} KV heads x {wc.q_per_kv} query heads, "
+                     f"{P}-token prompt + {steps} decode steps; Sink {sink}, Local {local}, Retrieval indexed "
+                     f"(C = ceil(n/16), C_rho = 2C, k = {wc.top_k}); buffer update every m steps"),
+        "timing": ("HIP events around each step's calls (GPU time incl. launch gaps); steps 0-7 left out; "
+                   "the prompt's Retrieval region is encoded before timing"),
+        **res,
     }
 
 
@@ -433,6 +529,8 @@ def main():
         del Kd, Vd
         torch.cuda.empty_cache()
         extras["drift"] = drift_run(pk, torch, np, workloads, dev, args.drift_steps)
+        torch.cuda.empty_cache()
+        extras["window"] = window_run(pk, torch, np, workloads, dev, args.drift_steps)
 
     cpu = None
     if not args.no_cpu_baseline:

@@ -32,6 +32,13 @@ are taken in a fixed order without fused multiply-adds:
     W_b = float32(fl(S_b / A_b)).
 This is the bit-exact definition the GPU encoder is compared against.
 
+Ablation variants (Sec. "Ablation Studies", Sec. "Low-Bit Rerank Metadata"):
+  * ``rotate=False`` drops the rotation (R = I): y = k, the ids are the sign
+    patterns of the raw subspaces and W_b = ||k_b|| / alpha_b = w_b (the
+    scale factor sqrt(D) belongs to the rotated form only);
+  * ``alpha_correction=False`` drops the correction of Eq. correct_term:
+    w_b = ||k|| r_b, i.e. W_b = float32(sqrt(S_b)) (IEEE square root).
+
 Conventions (readings where the paper is silent):
   * bit j of id_b is coordinate j of subspace b, set when that coordinate is
     negative; a zero coordinate counts as positive (it is the smallest id
@@ -69,7 +76,7 @@ def assign_centroid_bruteforce(u):
     return np.argmax(u @ omega.T, axis=-1)
 
 
-def encode_paper(K, signs, tau, a, n_subspaces):
+def encode_paper(K, signs, tau, a, n_subspaces, rotate=True, alpha_correction=True):
     """Literal float64 encode of keys K [n, D].
 
     Returns dict with ids [n,B] (int), sign [n,D] (+-1), bins [n,D] (0..7),
@@ -79,7 +86,7 @@ def encode_paper(K, signs, tau, a, n_subspaces):
     n, D = K.shape
     B = n_subspaces
     m = D // B
-    R = srht_matrix(signs)
+    R = srht_matrix(signs) if rotate else np.eye(D)
     norm = np.sqrt(np.sum(K * K, axis=1))
     safe = np.where(norm > 0, norm, 1.0)
     k_hat = K / safe[:, None]
@@ -95,12 +102,13 @@ def encode_paper(K, signs, tau, a, n_subspaces):
         bins += (np.abs(u) >= t)
     v = sgn * np.asarray(a)[bins]
     alpha = np.sum(v * u, axis=2)
-    w = np.where(r > 0, norm[:, None] * r / np.where(alpha != 0, alpha, 1.0), 0.0)
+    corr = np.where(alpha != 0, alpha, 1.0) if alpha_correction else 1.0
+    w = np.where(r > 0, norm[:, None] * r / corr, 0.0)
     return dict(ids=ids, sign=sgn.reshape(n, D), bins=bins.reshape(n, D), r=r,
                 u=u.reshape(n, D), alpha=alpha, w=w, norm=norm)
 
 
-def encode(K, signs, tau, a, n_subspaces):
+def encode(K, signs, tau, a, n_subspaces, rotate=True, alpha_correction=True):
     """Bit-exact float64 encode of float16 keys K [n, D] (scaled form, see module doc).
 
     Returns (ids uint8 [n,B], codes uint8 [n,D] with (sign<<3)|t, W float32 [n,B]).
@@ -110,7 +118,7 @@ def encode(K, signs, tau, a, n_subspaces):
     B = n_subspaces
     m = D // B
     s = np.asarray(signs, dtype=np.float64)
-    y = fwht(K.astype(np.float64) * s[None, :]).reshape(n, B, m)
+    y = (fwht(K.astype(np.float64) * s[None, :]) if rotate else K.astype(np.float64)).reshape(n, B, m)
     neg = y < 0
     ids = np.zeros((n, B), dtype=np.int64)
     for j in range(m):
@@ -125,7 +133,10 @@ def encode(K, signs, tau, a, n_subspaces):
     lev = np.asarray(a, dtype=np.float64)[bins]
     A = _tree_sum(lev * np.abs(y))
     with np.errstate(divide="ignore", invalid="ignore"):
-        W = np.where(S > 0, S / np.where(A > 0, A, 1.0), 0.0)
+        if alpha_correction:
+            W = np.where(S > 0, S / np.where(A > 0, A, 1.0), 0.0)
+        else:
+            W = np.sqrt(S)
     codes = (neg.astype(np.int64) << 3) | bins
     return (ids.astype(np.uint8), codes.reshape(n, D).astype(np.uint8),
             W.astype(np.float32))

@@ -31,6 +31,13 @@ list is returned in ascending key index.
 Stage II: s_hat_i = ||q|| sum_b w_{i,b} <v_{i,b}, q_tilde_b>, with the stored
 W (float32) giving w = W / sqrt(D).  Final top-k: (s_hat descending, key
 index ascending); short lists are padded with index -1.
+
+Ablation variants (Sec. "Ablation Studies"; App. "Coarse Candidate
+Generation", the binary 0/1 collision the tiers replace):
+  * ``binary=True``: every admitted cluster scores 1 (S_i in [0, B]);
+  * ``rotate=False``: R = I, so q_tilde = q/||q||; the transform returns
+    z = D q so that z / D = q keeps the scaled estimator's form, and the
+    stored W of an unrotated index is w itself (no sqrt(D) factor).
 """
 
 import numpy as np
@@ -42,10 +49,14 @@ TIER_WEIGHTS = (6, 5, 4, 3, 2, 1)
 TIER_PERCENTILES = (5, 15, 30, 50, 75, 100)
 
 
-def query_transform(q, signs):
-    """z = H (s (.) q) = sqrt(D) ||q|| q_tilde, exact in float64 for float16 q."""
+def query_transform(q, signs, rotate=True):
+    """z = H (s (.) q) = sqrt(D) ||q|| q_tilde, exact in float64 for float16 q.
+    Without the rotation: z = D q (exact: D is a power of two)."""
+    q = np.asarray(q).astype(np.float64)
+    if not rotate:
+        return q * q.shape[0]
     s = np.asarray(signs, dtype=np.float64)
-    return fwht(np.asarray(q).astype(np.float64) * s)
+    return fwht(q * s)
 
 
 def centroid_proxy(z_b):
@@ -65,15 +76,18 @@ def tier_cuts(n_collide):
     return tuple((p * int(n_collide) + 99) // 100 for p in TIER_PERCENTILES)
 
 
-def tier_bonus(start, cuts):
-    """Weight of the first tier whose cut exceeds the cluster start rank, else 0."""
+def tier_bonus(start, cuts, binary=False):
+    """Weight of the first tier whose cut exceeds the cluster start rank, else 0.
+    Binary collisions: 1 for every admitted cluster (start below C_rho)."""
+    if binary:
+        return 1 if start < cuts[-1] else 0
     for w, c in zip(TIER_WEIGHTS, cuts):
         if start < c:
             return w
     return 0
 
 
-def collision_scores_per_key(ids, z, n_collide, m):
+def collision_scores_per_key(ids, z, n_collide, m, binary=False):
     """Eq. collision_score evaluated from its definition, key by key.
 
     In each subspace the keys are ranked by their cluster's proxy (ties by
@@ -95,12 +109,12 @@ def collision_scores_per_key(ids, z, n_collide, m):
         for i in range(n):
             c = ids[i, b]
             start[c] = min(start.get(c, n), rank[i])
-        bonus = {c: tier_bonus(p, cuts) for c, p in start.items()}
+        bonus = {c: tier_bonus(p, cuts, binary) for c, p in start.items()}
         S += np.array([bonus[c] for c in ids[:, b]], dtype=np.int64)
     return S
 
 
-def collision_lut(counts, z, n_collide, m):
+def collision_lut(counts, z, n_collide, m, binary=False):
     """Per-subspace bonus table lut[b][c] from cluster counts (the form the GPU uses)."""
     counts = np.asarray(counts, dtype=np.int64)
     B = counts.shape[0]
@@ -111,7 +125,7 @@ def collision_lut(counts, z, n_collide, m):
         order = cluster_order(centroid_proxy(zb[b]))
         start = np.concatenate(([0], np.cumsum(counts[b][order])[:-1]))
         for c, p in zip(order, start):
-            lut[b, c] = tier_bonus(p, cuts)
+            lut[b, c] = tier_bonus(p, cuts, binary)
     return lut
 
 
@@ -142,7 +156,7 @@ def selection_threshold(S, n_cand):
     return theta, gt, C - gt
 
 
-def rsqip_scores(q, codes, W, signs, a, n_subspaces):
+def rsqip_scores(q, codes, W, signs, a, n_subspaces, rotate=True):
     """Eq. rsqip_raw_weighted for the keys whose (codes [c,D], W [c,B]) are given."""
     q = np.asarray(q).astype(np.float64)
     D = q.shape[0]
@@ -151,9 +165,9 @@ def rsqip_scores(q, codes, W, signs, a, n_subspaces):
     qn = np.sqrt(np.sum(q * q))
     if qn == 0:
         return np.zeros(np.asarray(codes).shape[0])
-    q_tilde = srht_matrix(signs) @ (q / qn)
+    q_tilde = (srht_matrix(signs) @ (q / qn)) if rotate else q / qn
     v = dequantize(codes, a).reshape(-1, B, m)
-    w = np.asarray(W, dtype=np.float64) / np.sqrt(D)
+    w = np.asarray(W, dtype=np.float64) / (np.sqrt(D) if rotate else 1.0)
     ip = np.einsum("cbj,bj->cb", v, q_tilde.reshape(B, m))
     return qn * np.sum(w * ip, axis=1)
 
@@ -171,19 +185,19 @@ def topk(cand, scores, k):
 
 
 def retrieve_head(q, ids, codes, W, counts, signs, a, n_subspaces,
-                  n_cand, n_collide, top_k):
+                  n_cand, n_collide, top_k, rotate=True, binary=False):
     """Alg. 1 decode for one query head over the n keys of its KV head.
 
     Returns dict(z, lut, S, cand, cand_scores, idx, scores).
     """
     D = np.asarray(q).shape[0]
     m = D // n_subspaces
-    z = query_transform(q, signs)
-    lut = collision_lut(counts, z, n_collide, m)
+    z = query_transform(q, signs, rotate)
+    lut = collision_lut(counts, z, n_collide, m, binary)
     S = collision_scores_from_lut(ids, lut)
     cand = select_candidates(S, n_cand)
     cs = rsqip_scores(q, np.asarray(codes)[cand], np.asarray(W)[cand], signs, a,
-                      n_subspaces)
+                      n_subspaces, rotate)
     idx, sc = topk(cand, cs, top_k)
     return dict(z=z, lut=lut, S=S, cand=cand, cand_scores=cs, idx=idx, scores=sc)
 

@@ -57,6 +57,19 @@ extern "C" {
 
 /* ---------------------------------------------------------------- types */
 
+/* Ablation variants of the index (Sec. "Ablation Studies"), for
+ * pariskv_config.flags; 0 = the method as published.  An index must be
+ * queried with the flags it was encoded with.
+ *   PARISKV_NO_ROTATION          R = I: keys and queries are split into
+ *                                subspaces as they are (ids = sign patterns
+ *                                of the raw subspaces, W_b = w_b, and the
+ *                                query transform is z = D q)
+ *   PARISKV_NO_ALPHA_CORRECTION  w_b = ||k|| r_b without the division by
+ *                                alpha_b of Eq. scaling_factor (stored
+ *                                W_b = sqrt(S_b), IEEE square root) */
+#define PARISKV_NO_ROTATION 1u
+#define PARISKV_NO_ALPHA_CORRECTION 2u
+
 /* Shape of one layer's KV cache and the shared rotation.
  *   rot_signs: HOST pointer to D int8 values, each +1 or -1: the diagonal s
  *   of the rotation R = H_D diag(s) / sqrt(D) (Sec. "Preprocessing" step (1),
@@ -69,6 +82,7 @@ typedef struct pariskv_config {
     int32_t q_per_kv;        /* G, 1..16                                        */
     int64_t capacity;        /* key slots per (sequence, KV head), 1..2^31-1    */
     const int8_t* rot_signs; /* host, [D], each +1 or -1                        */
+    uint32_t flags;          /* PARISKV_NO_ROTATION | PARISKV_NO_ALPHA_CORRECTION, or 0 */
 } pariskv_config;
 
 /* Per-key metadata kept on the GPU (Sec. "Low-Bit Rerank Metadata": centroid
@@ -105,11 +119,17 @@ typedef struct pariskv_index {
     uint32_t* counts;
 } pariskv_index;
 
+/* Binary (0/1) collisions for pariskv_budget.flags (the coarse score the
+ * tiers replace, App. "Coarse Candidate Generation"): every admitted cluster
+ * scores 1 instead of its tier weight, so S_i is in [0, B]. */
+#define PARISKV_BINARY_COLLISIONS 1
+
 /* Retrieval budgets of Alg. 1: C = ceil(beta n), C_rho = ceil(rho n), k. */
 typedef struct pariskv_budget {
     int64_t n_cand;    /* C, 1..PARISKV_MAX_CAND; clamped to n at run time    */
     int64_t n_collide; /* C_rho >= 1: keys covered by the admitted clusters   */
     int32_t top_k;     /* k, 1..min(C, PARISKV_MAX_TOPK)                      */
+    int32_t flags;     /* PARISKV_BINARY_COLLISIONS, or 0 (the paper's tiers) */
 } pariskv_budget;
 
 /* Rows one query head attends at a decode step besides its retrieved keys

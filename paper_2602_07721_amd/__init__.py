@@ -29,6 +29,9 @@ LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libpariskv.
 OK, ERR_INVALID, ERR_CAPACITY, ERR_WORKSPACE, ERR_HIP, ERR_UNSUPPORTED = 0, -1, -2, -3, -4, -5
 HEAD_DIM, SUBSPACES, CENTROIDS, REC_BYTES = 128, 16, 256, 128
 MAX_ATTEND_ROWS = 4096
+# Ablation variants (Sec. "Ablation Studies"): Config.flags, Budget.flags.
+NO_ROTATION, NO_ALPHA_CORRECTION = 1, 2
+BINARY_COLLISIONS = 1
 
 
 class PariskvError(RuntimeError):
@@ -40,7 +43,8 @@ class PariskvError(RuntimeError):
 class _Config(ctypes.Structure):
     _fields_ = [("head_dim", ctypes.c_int32), ("n_subspaces", ctypes.c_int32),
                 ("n_kv_heads", ctypes.c_int32), ("q_per_kv", ctypes.c_int32),
-                ("capacity", ctypes.c_int64), ("rot_signs", ctypes.POINTER(ctypes.c_int8))]
+                ("capacity", ctypes.c_int64), ("rot_signs", ctypes.POINTER(ctypes.c_int8)),
+                ("flags", ctypes.c_uint32)]
 
 
 class _Index(ctypes.Structure):
@@ -48,7 +52,8 @@ class _Index(ctypes.Structure):
 
 
 class _Budget(ctypes.Structure):
-    _fields_ = [("n_cand", ctypes.c_int64), ("n_collide", ctypes.c_int64), ("top_k", ctypes.c_int32)]
+    _fields_ = [("n_cand", ctypes.c_int64), ("n_collide", ctypes.c_int64), ("top_k", ctypes.c_int32),
+                ("flags", ctypes.c_int32)]
 
 
 class _Window(ctypes.Structure):
@@ -114,18 +119,20 @@ def _check(rc):
 
 @dataclass
 class Config:
-    """Layer shape and rotation signs (see ``pariskv_config``)."""
+    """Layer shape, rotation signs and index variant flags (see ``pariskv_config``)."""
     n_kv_heads: int
     q_per_kv: int
     capacity: int
     rot_signs: np.ndarray
     head_dim: int = HEAD_DIM
     n_subspaces: int = SUBSPACES
+    flags: int = 0
 
     def __post_init__(self):
         self._signs = np.ascontiguousarray(np.asarray(self.rot_signs, dtype=np.int8))
         self._c = _Config(self.head_dim, self.n_subspaces, self.n_kv_heads, self.q_per_kv,
-                          self.capacity, self._signs.ctypes.data_as(ctypes.POINTER(ctypes.c_int8)))
+                          self.capacity, self._signs.ctypes.data_as(ctypes.POINTER(ctypes.c_int8)),
+                          self.flags)
 
     @property
     def n_q_heads(self):
@@ -137,13 +144,14 @@ class Config:
 
 @dataclass
 class Budget:
-    """C = n_cand, C_rho = n_collide, k = top_k (see ``pariskv_budget``)."""
+    """C = n_cand, C_rho = n_collide, k = top_k, flags (see ``pariskv_budget``)."""
     n_cand: int
     n_collide: int
     top_k: int
+    flags: int = 0
 
     def c(self):
-        self._c = _Budget(self.n_cand, self.n_collide, self.top_k)
+        self._c = _Budget(self.n_cand, self.n_collide, self.top_k, self.flags)
         return ctypes.byref(self._c)
 
 

@@ -63,6 +63,8 @@ int check_config(const pariskv_config* cfg, int32_t batch) {
     if (cfg->capacity < 1 || cfg->capacity > INT32_MAX)
         return fail(PARISKV_ERR_INVALID, "capacity %lld outside 1..2^31-1", (long long)cfg->capacity);
     if (!cfg->rot_signs) return fail(PARISKV_ERR_INVALID, "rot_signs is NULL");
+    if (cfg->flags & ~(PARISKV_NO_ROTATION | PARISKV_NO_ALPHA_CORRECTION))
+        return fail(PARISKV_ERR_INVALID, "unknown config flags 0x%x", cfg->flags);
     for (int j = 0; j < D; ++j)
         if (cfg->rot_signs[j] != 1 && cfg->rot_signs[j] != -1)
             return fail(PARISKV_ERR_INVALID, "rot_signs[%d] = %d is not +1 or -1", j, cfg->rot_signs[j]);
@@ -125,6 +127,8 @@ int layout(const pariskv_config* cfg, int32_t batch, int64_t n, const pariskv_bu
         return fail(PARISKV_ERR_INVALID, "top_k %d outside 1..n_cand", bud->top_k);
     if (bud->top_k > PARISKV_MAX_TOPK)
         return fail(PARISKV_ERR_UNSUPPORTED, "top_k %d above %d", bud->top_k, PARISKV_MAX_TOPK);
+    if (bud->flags & ~PARISKV_BINARY_COLLISIONS)
+        return fail(PARISKV_ERR_INVALID, "unknown budget flags 0x%x", bud->flags);
 
     const int64_t hkv = cfg->n_kv_heads, g = cfg->q_per_kv, hq = hkv * g;
     const int64_t quads = (g + 3) / 4;
@@ -293,7 +297,10 @@ static int encode_common(const pariskv_config* cfg, const pariskv_index* index, 
         if (e != hipSuccess) return hip_fail(e, "zero counts");
     }
     e = launch_encode(keys, t, src_stride < 0 ? t : src_stride, groups, row0, cfg->capacity, index->ids,
-                      index->rec, index->counts, pack_signs(cfg->rot_signs), quant_consts(), s);
+                      index->rec, index->counts, pack_signs(cfg->rot_signs), quant_consts(),
+                      ((cfg->flags & PARISKV_NO_ROTATION) ? kFlagNoRotation : 0u) |
+                          ((cfg->flags & PARISKV_NO_ALPHA_CORRECTION) ? kFlagNoAlpha : 0u),
+                      s);
     if (e != hipSuccess) return hip_fail(e, "encode launch");
     return PARISKV_OK;
 }
@@ -465,6 +472,8 @@ static int retrieve_impl(const pariskv_config* cfg, const pariskv_index* index, 
     a.n_cand = budget->n_cand;
     a.c_eff = L.c_eff;
     a.top_k = budget->top_k;
+    a.flags = ((cfg->flags & PARISKV_NO_ROTATION) ? kFlagNoRotation : 0u) |
+              ((budget->flags & PARISKV_BINARY_COLLISIONS) ? kFlagBinary : 0u);
     for (int l = 0; l < kTierCount; ++l) {
         static const int64_t pct[kTierCount] = {5, 15, 30, 50, 75, 100};
         // ceil(pct * C_rho / 100) in integers; start ranks never exceed 2^31.

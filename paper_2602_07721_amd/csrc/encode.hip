@@ -50,7 +50,7 @@ template <bool kLdsCounts>
 __global__ __launch_bounds__(kThreads) void encode_kernel(
     const __half* __restrict__ keys, int64_t n_src, int64_t src_stride, int64_t keys_per_block, int64_t row0,
     int64_t capacity, uint8_t* __restrict__ ids, uint8_t* __restrict__ rec,
-    uint32_t* __restrict__ counts, SignBits sb, QuantConsts qc) {
+    uint32_t* __restrict__ counts, SignBits sb, QuantConsts qc, uint32_t flags) {
     __shared__ double s_a[8];
     __shared__ uint32_t s_cnt[kLdsCounts ? kB * kCentroids : 1];
 
@@ -95,30 +95,32 @@ __global__ __launch_bounds__(kThreads) void encode_kernel(
 #pragma unroll
             for (int j = 0; j < 32; ++j) x[j] = 0.0;
         }
+        if (!(flags & kFlagNoRotation)) {
 #pragma unroll
-        for (int j = 0; j < 32; ++j)
-            if ((smask >> j) & 1u) x[j] = -x[j];
+            for (int j = 0; j < 32; ++j)
+                if ((smask >> j) & 1u) x[j] = -x[j];
 
-        // In-register butterflies, strides 1..16 (exact).
+            // In-register butterflies, strides 1..16 (exact).
 #pragma unroll
-        for (int h = 1; h < 32; h <<= 1) {
+            for (int h = 1; h < 32; h <<= 1) {
 #pragma unroll
-            for (int j = 0; j < 32; ++j) {
-                if ((j & h) == 0) {
-                    double a0 = x[j], a1 = x[j + h];
-                    x[j] = __dadd_rn(a0, a1);
-                    x[j + h] = __dsub_rn(a0, a1);
+                for (int j = 0; j < 32; ++j) {
+                    if ((j & h) == 0) {
+                        double a0 = x[j], a1 = x[j + h];
+                        x[j] = __dadd_rn(a0, a1);
+                        x[j + h] = __dsub_rn(a0, a1);
+                    }
                 }
             }
-        }
-        // Cross-lane butterflies, strides 32 (lane q^1) and 64 (lane q^2).
+            // Cross-lane butterflies, strides 32 (lane q^1) and 64 (lane q^2).
 #pragma unroll
-        for (int m = 1; m <= 2; m <<= 1) {
-            const bool upper = (q & m) != 0;
+            for (int m = 1; m <= 2; m <<= 1) {
+                const bool upper = (q & m) != 0;
 #pragma unroll
-            for (int j = 0; j < 32; ++j) {
-                double p = __shfl_xor(x[j], m, 64);
-                x[j] = upper ? __dsub_rn(p, x[j]) : __dadd_rn(x[j], p);
+                for (int j = 0; j < 32; ++j) {
+                    double p = __shfl_xor(x[j], m, 64);
+                    x[j] = upper ? __dsub_rn(p, x[j]) : __dadd_rn(x[j], p);
+                }
             }
         }
 
@@ -150,7 +152,8 @@ __global__ __launch_bounds__(kThreads) void encode_kernel(
                 cw |= ((((idb >> j) & 1u) << 3) | t) << (4 * j);
             }
             const double A = tree8_sum(P);
-            wgt[sbi] = nz ? (float)(S / A) : 0.0f;
+            // Without the alpha-correction the weight is ||y_b|| = sqrt(S_b).
+            wgt[sbi] = !nz ? 0.0f : (flags & kFlagNoAlpha) ? (float)__dsqrt_rn(S) : (float)(S / A);
             code[sbi] = cw;
             id_word |= idb << (8 * sbi);
             slot_word |= id_slot(idb) << (8 * sbi);
@@ -200,7 +203,8 @@ hipError_t launch_zero_u32(uint32_t* p, int64_t count, hipStream_t s) {
 
 hipError_t launch_encode(const void* keys, int64_t n_src, int64_t src_stride, int64_t groups,
                          int64_t row0, int64_t capacity, uint8_t* ids, uint8_t* rec,
-                         uint32_t* counts, const SignBits& sb, const QuantConsts& qc, hipStream_t s) {
+                         uint32_t* counts, const SignBits& sb, const QuantConsts& qc, uint32_t flags,
+                         hipStream_t s) {
     if (n_src <= 0 || groups <= 0) return hipSuccess;
     const __half* k = static_cast<const __half*>(keys);
     if (n_src >= 1024) {
@@ -209,14 +213,14 @@ hipError_t launch_encode(const void* keys, int64_t n_src, int64_t src_stride, in
         const int64_t bx = (n_src + per - 1) / per;
         const ProfEvents pe = prof_begin("encode");
         hipExtLaunchKernelGGL(encode_kernel<true>, dim3((unsigned)bx, (unsigned)groups), dim3(kThreads),
-                           0, s, pe.start, pe.stop, 0, k, n_src, src_stride, per, row0, capacity, ids, rec, counts, sb, qc);
+                           0, s, pe.start, pe.stop, 0, k, n_src, src_stride, per, row0, capacity, ids, rec, counts, sb, qc, flags);
     } else {
         // Streaming append: few keys per group, count straight into global memory.
         const int64_t per = kKeysPerIter;
         const int64_t bx = (n_src + per - 1) / per;
         const ProfEvents pe = prof_begin("append");
         hipExtLaunchKernelGGL(encode_kernel<false>, dim3((unsigned)bx, (unsigned)groups), dim3(kThreads),
-                           0, s, pe.start, pe.stop, 0, k, n_src, src_stride, per, row0, capacity, ids, rec, counts, sb, qc);
+                           0, s, pe.start, pe.stop, 0, k, n_src, src_stride, per, row0, capacity, ids, rec, counts, sb, qc, flags);
     }
     return hipGetLastError();
 }

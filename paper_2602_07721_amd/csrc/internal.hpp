@@ -99,9 +99,16 @@ hipError_t launch_zero_u32(uint32_t* p, int64_t count, hipStream_t s);
 // Encode the first n_src rows of keys [groups][src_stride][D] into rows
 // [row0, row0 + n_src) of each group (src_stride = n_src for a packed batch of
 // keys, the cache capacity when the rows are read straight from a K cache).
+// flags: the index variant (kFlagNoRotation, kFlagNoAlpha).
 hipError_t launch_encode(const void* keys, int64_t n_src, int64_t src_stride, int64_t groups,
                          int64_t row0, int64_t capacity, uint8_t* ids, uint8_t* rec,
-                         uint32_t* counts, const SignBits& sb, const QuantConsts& qc, hipStream_t s);
+                         uint32_t* counts, const SignBits& sb, const QuantConsts& qc, uint32_t flags,
+                         hipStream_t s);
+
+// Variant bits carried to the kernels (the config's and the budget's flags).
+constexpr uint32_t kFlagNoRotation = 1u;     // R = I (encode and query transform)
+constexpr uint32_t kFlagNoAlpha = 2u;        // W_b = sqrt(S_b) (encode)
+constexpr uint32_t kFlagBinary = 1u << 8;    // admitted clusters score 1 (bonus tables)
 
 // Rows one query head attends (Sec. "Buffer Update": Sink and Local + Update
 // Buffer densely, the retrieved keys sparsely).  The head's list is
@@ -122,6 +129,7 @@ struct RetrieveArgs {
     int64_t n, n_pad, n_chunks, capacity;
     int64_t n_cand, c_eff;   // row stride of cand / cand_score, and min(C, n)
     int32_t top_k;
+    uint32_t flags;  // kFlagNoRotation, kFlagBinary
     uint32_t cuts[kTierCount];
     // inputs
     const void* q;

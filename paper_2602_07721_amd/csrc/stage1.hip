@@ -134,14 +134,16 @@ __global__ __launch_bounds__(kLutThreads) void query_lut_kernel(RetrieveArgs a) 
     (&s_lut[0][0])[tid] = 0u;
     const int zh = tid >> 7, zi = tid & (kD - 1);  // threads < 512: 4 heads x 128 coordinates
     const bool zlive = zh < 4 && quad * 4 + zh < a.g;
+    const bool rotate = !(a.flags & kFlagNoRotation);
     if (zlive) {
         const __half* qp = static_cast<const __half*>(a.q) + (row + (zh - slot)) * kD;
         double v = (double)__half2float(qp[zi]);
-        if ((a.sb.w[zi >> 5] >> (zi & 31)) & 1u) v = -v;
+        if (!rotate) v *= (double)kD;  // z = D q without the rotation (exact: D = 2^7)
+        else if ((a.sb.w[zi >> 5] >> (zi & 31)) & 1u) v = -v;
         s_z[zh][zi] = v;
     }
     __syncthreads();
-    for (int h = 1; h < kD; h <<= 1) {
+    for (int h = 1; rotate && h < kD; h <<= 1) {
         if (zi < kD / 2 && zlive) {
             const int i = ((zi / h) * 2 * h) + (zi % h);
             const double x0 = s_z[zh][i], x1 = s_z[zh][i + h];
@@ -186,6 +188,8 @@ __global__ __launch_bounds__(kLutThreads) void query_lut_kernel(RetrieveArgs a) 
 #pragma unroll
             for (int l = kTierCount - 1; l >= 0; --l)
                 if (start < a.cuts[l]) bonus = (uint32_t)(kTierCount - l);
+            // Binary collisions: every admitted cluster (start below C_rho) scores 1.
+            if (a.flags & kFlagBinary) bonus = bonus ? 1u : 0u;
             // The table is indexed like the stored ids, by slot.
             if (bonus) atomicOr(&s_lut[sub][id_slot((uint32_t)cid[r])], bonus << (8 * slot));
             start += cc[r];

@@ -119,19 +119,19 @@ def lut_for_head(lut, seq, kvh, g):
     return ((words >> (8 * (g % 4))) & 0xFF).astype(np.int64)
 
 
-def oracle_group(K_group, signs):
-    ids, codes, W = oenc.encode(K_group, signs, TAU, A, 16)
+def oracle_group(K_group, signs, rotate=True, alpha_correction=True):
+    ids, codes, W = oenc.encode(K_group, signs, TAU, A, 16, rotate, alpha_correction)
     return ids, codes, W, oenc.cluster_counts(ids, 8)
 
 
-def abs_terms(q, codes, W, signs):
+def abs_terms(q, codes, W, signs, rotate=True):
     """sum_b |W_b <v_b, z_b>| / D per key, via the oracle estimator one subspace at a time."""
     W = np.asarray(W, dtype=np.float64)
     tot = np.zeros(W.shape[0])
     for b in range(16):
         Wb = np.zeros_like(W)
         Wb[:, b] = W[:, b]
-        tot += np.abs(oret.rsqip_scores(q, codes, Wb, signs, A, 16))
+        tot += np.abs(oret.rsqip_scores(q, codes, Wb, signs, A, 16, rotate))
     return tot
 
 
@@ -144,12 +144,13 @@ def check_index(gpu_ids, gpu_rec, gpu_counts, oracle):
     np.testing.assert_array_equal(gpu_counts.astype(np.int64), cnt)
 
 
-def check_head(inter, seq, kvh, g, q_per_kv, q, oracle, signs, budget, n):
-    """Bit-exact Stage I, toleranced Stage II for one query head; returns oracle result dict."""
+def check_head(inter, seq, kvh, g, q_per_kv, q, oracle, signs, budget, n, rotate=True):
+    """Bit-exact Stage I, toleranced Stage II for one query head; returns oracle result dict.
+    rotate / budget.flags select the ablation variants the index and call used."""
     ids, codes, W, cnt = oracle
     hq = kvh * q_per_kv + g
     r = oret.retrieve_head(q, ids, codes, W, cnt, signs, A, 16, budget.n_cand, budget.n_collide,
-                           budget.top_k)
+                           budget.top_k, rotate=rotate, binary=bool(budget.flags & pk.BINARY_COLLISIONS))
     # query transform: z / D rounded to float
     np.testing.assert_array_equal(inter["zq"][seq, hq], (r["z"] / 128.0).astype(np.float32))
     np.testing.assert_array_equal(lut_for_head(inter["lut"], seq, kvh, g), r["lut"])
@@ -159,7 +160,7 @@ def check_head(inter, seq, kvh, g, q_per_kv, q, oracle, signs, budget, n):
     np.testing.assert_array_equal(inter["thresh"][seq, hq], [theta, gt, quota, C])
     np.testing.assert_array_equal(inter["cand"][seq, hq, :C], r["cand"])
     # RSQ-IP estimates
-    at = abs_terms(q, codes[r["cand"]], W[r["cand"]], signs)
+    at = abs_terms(q, codes[r["cand"]], W[r["cand"]], signs, rotate)
     gs = inter["cand_score"][seq, hq, :C].astype(np.float64)
     err = np.abs(gs - r["cand_scores"])
     bad = err > RTOL_SCORE * at + 1e-30

@@ -293,3 +293,14 @@ def test_append_rows_validation():
     assert call(t=-1) == pk.ERR_INVALID
     assert call(K=0) == pk.ERR_INVALID
     assert call(n_cur=4090, t=16) == pk.ERR_CAPACITY              # index rows past its capacity
+
+
+def test_variant_flag_validation():
+    L = pk.lib()
+    bad = _cfg(flags=4)
+    b = pk.Budget(512, 1024, 64)
+    assert L.pariskv_retrieve_workspace(bad.c(), 1, 4000, b.c()) == 0
+    assert _encode(bad, _index()) == pk.ERR_INVALID
+    assert pk.retrieve_workspace_size(_cfg(flags=pk.NO_ROTATION | pk.NO_ALPHA_CORRECTION), 1, 4000, b) > 0
+    assert L.pariskv_retrieve_workspace(_cfg().c(), 1, 4000, pk.Budget(512, 1024, 64, flags=2).c()) == 0
+    assert pk.retrieve_workspace_size(_cfg(), 1, 4000, pk.Budget(512, 1024, 64, flags=pk.BINARY_COLLISIONS)) > 0

@@ -57,7 +57,8 @@ def parse():
     ap.add_argument("--extras", action="store_true",
                     help="also measure the drift workload (append + retrieve + attend per step), the "
                          "same decode with Sink/Local/Update Buffer regions (buffer updates every 256 "
-                         "steps and every step), and attention over K/V in pinned host memory")
+                         "steps and every step), the recall of the ablation variants, and attention over "
+                         "K/V in pinned host memory")
     ap.add_argument("--drift-steps", type=int, default=4096,
                     help="decode steps of the drift measurement (the full workload runs 32768)")
     ap.add_argument("--copy-calibration", action="store_true",
@@ -341,6 +342,77 @@ def window_run(pk, torch, np, workloads, dev, steps, sink=128, local=512, update
     }
 
 
+def ablation_run(pk, torch, np, workloads, dev, drift_steps, n_queries=8):
+    """Recall of the ablation variants (Sec. "Ablation Studies") on the drift workload's keys
+    after `drift_steps` drifting decode keys: per variant, the coarse-stage recall (exact
+    top-k keys that reach the candidate set) and the final recall@k (exact top-k keys among
+    the k winners), averaged over all query heads and `n_queries` query draws from the last
+    step's key law; plus a candidate-ratio (beta) sweep of the published method."""
+    wc = workloads.CONFIGS["drift"]
+    signs = workloads.rotation_signs(wc.seed)
+    n = wc.n + drift_steps
+    K0, _ = workloads.layer_kv(wc, values=False, threads=16)
+    Kall = np.zeros((wc.batch, wc.n_kv_heads, n, wc.head_dim), np.float16)
+    Kall[:, :, :wc.n] = K0
+    for s in range(wc.batch):
+        for h in range(wc.n_kv_heads):
+            Kall[s, h, wc.n:] = workloads.drift_keys(wc.seed, s, h, 0, drift_steps, drift_steps)
+    Kd = torch.from_numpy(Kall).to(dev)
+    hq = wc.n_kv_heads * wc.q_per_kv
+    # queries from the key law of the last drift step
+    Qs = np.stack([np.stack([workloads.drift_queries(wc.seed, s, h, drift_steps, wc.q_per_kv)[-n_queries:]
+                             for h in range(wc.n_kv_heads)], axis=1)
+                   for s in range(wc.batch)], axis=1)  # [n_queries][b][Hkv][G][D]
+    Qd = torch.from_numpy(Qs.reshape(n_queries, wc.batch, hq, wc.head_dim)).to(dev)
+    k = wc.top_k
+    exact = []
+    for i in range(n_queries):
+        q = Qd[i].float().reshape(wc.batch, wc.n_kv_heads, wc.q_per_kv, wc.head_dim)
+        sc = torch.matmul(q, Kd.float().transpose(2, 3).contiguous())
+        exact.append(torch.topk(sc, k, dim=-1).indices.reshape(wc.batch, hq, k))
+        del sc
+    C16 = -(-n // 16)
+    runs = [("published (rotation + alpha-correction + 6 tiers)", 0, 0, C16),
+            ("binary 0/1 collisions", 0, pk.BINARY_COLLISIONS, C16),
+            ("no alpha-correction", pk.NO_ALPHA_CORRECTION, 0, C16),
+            ("no rotation", pk.NO_ROTATION, 0, C16),
+            ("no rotation, no alpha, binary", pk.NO_ROTATION | pk.NO_ALPHA_CORRECTION, pk.BINARY_COLLISIONS, C16),
+            ("published, beta = 1/32", 0, 0, -(-n // 32)),
+            ("published, beta = 1/8", 0, 0, -(-n // 8))]
+    out = []
+    indexes = {}
+    for name, cfl, bfl, C in runs:
+        cfg = pk.Config(wc.n_kv_heads, wc.q_per_kv, n, signs, flags=cfl)
+        if cfl not in indexes:
+            index = pk.Index.empty(cfg, wc.batch, dev)
+            pk.encode(cfg, index, Kd)
+            indexes[cfl] = index
+        index = indexes[cfl]
+        bud = pk.Budget(C, 2 * C, k, flags=bfl)
+        lay = pk.workspace_layout(cfg, wc.batch, n, bud)
+        ws = torch.empty(lay["total"], dtype=torch.uint8, device=dev)
+        coarse, final = [], []
+        for i in range(n_queries):
+            idx, _, _ = pk.retrieve(cfg, index, Qd[i], n, bud, workspace=ws)
+            cand = ws[lay["cand"]: lay["cand"] + wc.batch * hq * C * 4].view(torch.int32)
+            cand = cand.reshape(wc.batch, hq, C).long()
+            ex = exact[i]
+            # the candidate list is ascending: membership by binary search
+            pos = torch.searchsorted(cand, ex).clamp(max=C - 1)
+            coarse.append((cand.gather(-1, pos) == ex).float().mean().item())
+            final.append((ex.unsqueeze(-1) == idx.long().unsqueeze(-2)).any(-1).float().mean().item())
+        out.append({"variant": name, "C": int(C), "coarse_recall": round(float(np.mean(coarse)), 4),
+                    "recall_at_k": round(float(np.mean(final)), 4)})
+    return {
+        "workload": (f"drift keys: {wc.batch} seqs x {wc.n_kv_heads} KV heads x {wc.q_per_kv} query heads, "
+                     f"{wc.n}-key prefill + {drift_steps} drifted keys (n = {n}); {n_queries} query draws per "
+                     f"head from the last step's key law; C_rho = 2C, k = {k}; exact top-k by float32 "
+                     "inner products"),
+        "note": "quality figures on synthetic keys (the paper's recall is on real model keys): parity unpinned",
+        "variants": out,
+    }
+
+
 def host_link_run(pk, torch, np, cfg, K, V, Qd, idx_list, scale, dev, reps=8):
     """Sparse attention with K/V in pinned host memory, read through host-mapped pointers."""
     Kh = torch.from_numpy(K).pin_memory()
@@ -531,6 +603,8 @@ def main():
         extras["drift"] = drift_run(pk, torch, np, workloads, dev, args.drift_steps)
         torch.cuda.empty_cache()
         extras["window"] = window_run(pk, torch, np, workloads, dev, args.drift_steps)
+        torch.cuda.empty_cache()
+        extras["ablation"] = ablation_run(pk, torch, np, workloads, dev, args.drift_steps)
 
     cpu = None
     if not args.no_cpu_baseline:

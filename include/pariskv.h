@@ -316,6 +316,54 @@ int pariskv_retrieve_window_attend(const pariskv_config* cfg, const pariskv_inde
                                    const pariskv_window* win, float scale, float* out,
                                    void* workspace, size_t ws_bytes, void* stream);
 
+/* Tiered attention of the offload setting (Sec. "Buffer Update": Sink, Local
+ * and the Update Buffer stay on the GPU, the Retrieval region is offloaded to
+ * CPU memory; Sec. "On-Demand UVA Fetch": only the retrieved rows are read
+ * from there).  Same result as pariskv_window_attend, with the dense rows read
+ * from a window cache on the GPU:
+ *   K_win, V_win  device float16 [batch][Hkv][win_capacity][D]: Sink row r at
+ *                 slot r, Local / Buffer row r at slot
+ *                 sink_len + (r - sink_len) mod (win_capacity - sink_len)
+ *                 (a ring: the caller writes each new token at its slot)
+ *   K, V          the retrieval rows, float16 [batch][Hkv][kv_capacity][D],
+ *                 in pinned host memory (kv_host_mapped = 1) or device memory;
+ *                 retrieved index row i is row win->retr_begin + i
+ * Attention caches hold at most 2^30 - 1 rows.
+ * Errors: INVALID (also a window cache too small for sink_len + the dense
+ * rows), UNSUPPORTED (more than PARISKV_MAX_ATTEND_ROWS rows per head), HIP. */
+int pariskv_tiered_attend(const pariskv_config* cfg, const void* q, const void* K_win,
+                          const void* V_win, int64_t win_capacity, const void* K, const void* V,
+                          int32_t kv_host_mapped, int64_t kv_capacity, const int32_t* idx, int32_t k,
+                          const pariskv_window* win, int32_t batch, float scale, float* out,
+                          void* stream);
+
+/* pariskv_retrieve followed by pariskv_tiered_attend, in one call, with the
+ * same outputs bit for bit (attention inside the top-k kernel for C <= 32768).
+ * Also requires win->retr_begin + n <= min(win->dense_begin, kv_capacity).
+ * Errors: those of pariskv_retrieve and pariskv_tiered_attend. */
+int pariskv_retrieve_tiered_attend(const pariskv_config* cfg, const pariskv_index* index,
+                                   const void* q, int64_t n, int32_t batch,
+                                   const pariskv_budget* budget, int32_t* out_idx,
+                                   float* out_score, const void* K_win, const void* V_win,
+                                   int64_t win_capacity, const void* K, const void* V,
+                                   int32_t kv_host_mapped, int64_t kv_capacity,
+                                   const pariskv_window* win, float scale, float* out,
+                                   void* workspace, size_t ws_bytes, void* stream);
+
+/* Copy of t K and V rows of every (sequence, KV head): rows [src_row,
+ * src_row + t) of K_src / V_src ([batch][Hkv][src_capacity][D] float16) to rows
+ * [dst_row, dst_row + t) of K_dst / V_dst ([batch][Hkv][dst_capacity][D]).  The
+ * offload of the rows that leave Local (Sec. "Buffer Update" (i): evicted into
+ * Retrieval "via GPU->CPU transfer", asynchronously): from the GPU window cache
+ * to pinned host memory (or any direction the HIP runtime copies), as two
+ * pitched asynchronous copies on `stream` -- run it on a second stream to
+ * overlap the retrieval, and order the first attention that may read those
+ * rows after it.  A ring range that wraps takes two calls.
+ * Errors: INVALID (NULL pointers, rows outside either cache), HIP. */
+int pariskv_offload_rows(const void* K_src, const void* V_src, int64_t src_capacity, int64_t src_row,
+                         void* K_dst, void* V_dst, int64_t dst_capacity, int64_t dst_row, int64_t t,
+                         int32_t batch, int32_t n_kv_heads, void* stream);
+
 /* ------------------------------------------------------------ utilities */
 
 /* The offline magnitude quantizer (Appendix "Coordinate-Magnitude Quantizer"):

@@ -20,7 +20,8 @@ import numpy as np
 __all__ = [
     "PariskvError", "Config", "Budget", "Index", "Window", "lib", "encode", "append", "append_rows",
     "retrieve", "retrieve_workspace_size", "workspace_layout", "sparse_attend", "retrieve_attend",
-    "window_regions", "window_attend", "retrieve_window_attend", "quantizer_table", "rotation_signs",
+    "window_regions", "window_attend", "retrieve_window_attend", "tiered_attend", "retrieve_tiered_attend",
+    "offload_rows", "window_slot", "quantizer_table", "rotation_signs",
     "profile_enable", "profile_reset", "profile_read",
 ]
 
@@ -98,6 +99,12 @@ def lib():
                                             ctypes.c_float, VP, VP]
         L.pariskv_retrieve_attend.argtypes = [P(_Config), P(_Index), VP, I64, I32, P(_Budget), VP, VP,
                                               VP, VP, I32, I64, ctypes.c_float, VP, VP, SZ, VP]
+        L.pariskv_tiered_attend.argtypes = [P(_Config), VP, VP, VP, I64, VP, VP, I32, I64, VP, I32, P(_Window),
+                                            I32, ctypes.c_float, VP, VP]
+        L.pariskv_retrieve_tiered_attend.argtypes = [P(_Config), P(_Index), VP, I64, I32, P(_Budget), VP, VP,
+                                                     VP, VP, I64, VP, VP, I32, I64, P(_Window),
+                                                     ctypes.c_float, VP, VP, SZ, VP]
+        L.pariskv_offload_rows.argtypes = [VP, VP, I64, I64, VP, VP, I64, I64, I64, I32, I32, VP]
         L.pariskv_quantizer_table.argtypes = [I32, P(ctypes.c_double), P(ctypes.c_double)]
         L.pariskv_rotation_signs.argtypes = [ctypes.c_uint64, I32, P(ctypes.c_int8)]
         L.pariskv_profile_enable.argtypes = [I32]
@@ -362,6 +369,72 @@ def retrieve_window_attend(cfg, index, q, n, budget, K, V, win, scale, out_idx=N
         int(bool(kv_host_mapped)), int(K.shape[2]), win.c(), float(scale), _ptr(out, "out"),
         _ptr(workspace, "workspace"), workspace.numel(), _stream(stream)))
     return out_idx, out_score, out, workspace
+
+
+def window_slot(r, sink_len, win_capacity):
+    """Slot of cache row r in a window cache (see ``pariskv_tiered_attend``)."""
+    return r if r < sink_len else sink_len + (r - sink_len) % (win_capacity - sink_len)
+
+
+def tiered_attend(cfg, q, K_win, V_win, K, V, idx, win, scale, out=None, kv_host_mapped=False, stream=None):
+    """window_attend with Sink + Local/Buffer rows read from the GPU window cache K_win/V_win
+    [batch][Hkv][win_capacity][D] and the retrieved rows from K/V (pinned host memory when
+    kv_host_mapped)."""
+    import torch
+    batch = int(q.shape[0])
+    if out is None:
+        out = torch.empty((batch, cfg.n_q_heads, HEAD_DIM), dtype=torch.float32, device=q.device)
+    if kv_host_mapped:
+        for t, nm in ((K, "K"), (V, "V")):
+            if t.is_cuda or not t.is_pinned():
+                raise ValueError(f"{nm} must be pinned host memory when kv_host_mapped")
+    k = int(idx.shape[-1])
+    _check(lib().pariskv_tiered_attend(cfg.c(), _ptr(q, "q"), _ptr(K_win, "K_win"), _ptr(V_win, "V_win"),
+                                       int(K_win.shape[2]), _ptr(K, "K", not kv_host_mapped),
+                                       _ptr(V, "V", not kv_host_mapped), int(bool(kv_host_mapped)),
+                                       int(K.shape[2]), _ptr(idx, "idx"), k, win.c(), batch, float(scale),
+                                       _ptr(out, "out"), _stream(stream)))
+    return out
+
+
+def retrieve_tiered_attend(cfg, index, q, n, budget, K_win, V_win, K, V, win, scale, out_idx=None,
+                           out_score=None, out=None, workspace=None, kv_host_mapped=False, stream=None):
+    """retrieve over the Retrieval region + tiered_attend in one call; returns (idx, score, out, ws)."""
+    import torch
+    batch = int(q.shape[0])
+    rows = batch * cfg.n_q_heads
+    if out_idx is None:
+        out_idx = torch.empty((batch, cfg.n_q_heads, budget.top_k), dtype=torch.int32, device=q.device)
+    if out is None:
+        out = torch.empty((batch, cfg.n_q_heads, HEAD_DIM), dtype=torch.float32, device=q.device)
+    if workspace is None:
+        workspace = torch.empty(max(256, retrieve_workspace_size(cfg, batch, n, budget)),
+                                dtype=torch.uint8, device=q.device)
+    if kv_host_mapped:
+        for t, nm in ((K, "K"), (V, "V")):
+            if t.is_cuda or not t.is_pinned():
+                raise ValueError(f"{nm} must be pinned host memory when kv_host_mapped")
+    assert out_idx.numel() == rows * budget.top_k
+    _check(lib().pariskv_retrieve_tiered_attend(
+        cfg.c(), index.c(), _ptr(q, "q"), int(n), batch, budget.c(), _ptr(out_idx, "out_idx"),
+        _ptr(out_score, "out_score"), _ptr(K_win, "K_win"), _ptr(V_win, "V_win"), int(K_win.shape[2]),
+        _ptr(K, "K", not kv_host_mapped), _ptr(V, "V", not kv_host_mapped), int(bool(kv_host_mapped)),
+        int(K.shape[2]), win.c(), float(scale), _ptr(out, "out"), _ptr(workspace, "workspace"),
+        workspace.numel(), _stream(stream)))
+    return out_idx, out_score, out, workspace
+
+
+def offload_rows(K_src, V_src, src_row, K_dst, V_dst, dst_row, t, stream=None):
+    """Copy rows [src_row, src_row + t) of every (sequence, KV head) of K_src/V_src to rows
+    [dst_row, dst_row + t) of K_dst/V_dst (device or pinned host tensors [b][Hkv][cap][D])."""
+    for x, nm in ((K_src, "K_src"), (V_src, "V_src"), (K_dst, "K_dst"), (V_dst, "V_dst")):
+        if not x.is_cuda and not x.is_pinned():
+            raise ValueError(f"{nm} must be device or pinned host memory")
+    b, hkv = int(K_src.shape[0]), int(K_src.shape[1])
+    _check(lib().pariskv_offload_rows(_ptr(K_src, "K_src", False), _ptr(V_src, "V_src", False),
+                                      int(K_src.shape[2]), int(src_row), _ptr(K_dst, "K_dst", False),
+                                      _ptr(V_dst, "V_dst", False), int(K_dst.shape[2]), int(dst_row), int(t),
+                                      b, hkv, _stream(stream)))
 
 
 def quantizer_table(m=8):

@@ -366,7 +366,7 @@ int pariskv_workspace_layout(const pariskv_config* cfg, int32_t batch, int64_t n
     return layout(cfg, batch, n, budget, out);
 }
 
-// Attention arguments of pariskv_retrieve_attend.
+// Attention arguments of the retrieve + attend entry points.
 struct AttendReq {
     const void* K;
     const void* V;
@@ -375,17 +375,22 @@ struct AttendReq {
     float scale;
     float* out;
     AttendWindow win;
+    const void* Kw = nullptr;  // window cache (device), win.win_capacity > 0
+    const void* Vw = nullptr;
 };
 
-// Window rows in order and inside the cache; with k retrieved rows per head the
-// list fits one attention block.  n >= 0: the retrieval index holds n keys,
-// whose rows [retr_begin, retr_begin + n) must end before the dense rows.
+// Window rows in order; dense rows inside the main cache, or inside the window
+// cache's ring when win_capacity > 0; with k retrieved rows per head the list
+// fits one attention block.  n >= 0: the retrieval index holds n keys, whose
+// rows [retr_begin, retr_begin + n) must end before the dense rows (and, with a
+// window cache, inside the main cache).
 static int check_window(const pariskv_window* w, int64_t kv_capacity, int64_t k, int64_t n,
-                        AttendWindow* out) {
+                        int64_t win_capacity, AttendWindow* out) {
     *out = AttendWindow{};
     if (!w) return PARISKV_OK;
+    const int64_t dense_cap = win_capacity > 0 ? INT64_MAX : kv_capacity;
     if (w->sink_len < 0 || w->retr_begin < w->sink_len || w->dense_begin < w->retr_begin ||
-        w->dense_end < w->dense_begin || w->dense_end > kv_capacity)
+        w->dense_end < w->dense_begin || w->dense_end > dense_cap)
         return fail(PARISKV_ERR_INVALID,
                     "window needs 0 <= sink_len (%lld) <= retr_begin (%lld) <= dense_begin (%lld) <= "
                     "dense_end (%lld) <= kv_capacity (%lld)",
@@ -394,6 +399,19 @@ static int check_window(const pariskv_window* w, int64_t kv_capacity, int64_t k,
     if (n >= 0 && w->retr_begin + n > w->dense_begin)
         return fail(PARISKV_ERR_INVALID, "retrieval rows [%lld, %lld) overlap the dense rows from %lld",
                     (long long)w->retr_begin, (long long)(w->retr_begin + n), (long long)w->dense_begin);
+    if (win_capacity > 0) {
+        if (win_capacity > kMaxKvRows)
+            return fail(PARISKV_ERR_INVALID, "win_capacity %lld above 2^30-1", (long long)win_capacity);
+        if (w->sink_len > win_capacity ||
+            w->dense_end - w->dense_begin > win_capacity - w->sink_len)
+            return fail(PARISKV_ERR_INVALID,
+                        "window cache of %lld rows holds neither %lld Sink rows and a ring for %lld "
+                        "Local / Buffer rows", (long long)win_capacity, (long long)w->sink_len,
+                        (long long)(w->dense_end - w->dense_begin));
+        if (n >= 0 && w->retr_begin + n > kv_capacity)
+            return fail(PARISKV_ERR_INVALID, "retrieval rows end at %lld, past kv_capacity %lld",
+                        (long long)(w->retr_begin + n), (long long)kv_capacity);
+    }
     const int64_t rows = w->sink_len + (w->dense_end - w->dense_begin) + k;
     if (rows > kMaxAttendRows)
         return fail(PARISKV_ERR_UNSUPPORTED, "%lld attended rows per head, above %d", (long long)rows,
@@ -402,6 +420,14 @@ static int check_window(const pariskv_window* w, int64_t kv_capacity, int64_t k,
     out->retr_begin = w->retr_begin;
     out->dense_begin = w->dense_begin;
     out->dense_end = w->dense_end;
+    out->win_capacity = win_capacity > 0 ? win_capacity : 0;
+    return PARISKV_OK;
+}
+
+static int check_window_cache(const void* Kw, const void* Vw, int64_t win_capacity) {
+    if (win_capacity < 1) return fail(PARISKV_ERR_INVALID, "win_capacity %lld < 1", (long long)win_capacity);
+    if (!Kw || !Vw || !aligned16(Kw) || !aligned16(Vw))
+        return fail(PARISKV_ERR_INVALID, "K_win and V_win must be non-NULL and 16-byte aligned");
     return PARISKV_OK;
 }
 
@@ -409,8 +435,8 @@ static int check_attend_args(const AttendReq& r) {
     if (!r.K || !r.V || !r.out) return fail(PARISKV_ERR_INVALID, "K, V and out must be non-NULL");
     if (!aligned16(r.K) || !aligned16(r.V) || !aligned16(r.out))
         return fail(PARISKV_ERR_INVALID, "K, V and out must be 16-byte aligned");
-    if (r.kv_capacity < 1 || r.kv_capacity > INT32_MAX)
-        return fail(PARISKV_ERR_INVALID, "kv_capacity %lld outside 1..2^31-1", (long long)r.kv_capacity);
+    if (r.kv_capacity < 1 || r.kv_capacity > kMaxKvRows)
+        return fail(PARISKV_ERR_INVALID, "kv_capacity %lld outside 1..2^30-1", (long long)r.kv_capacity);
     if (r.kv_host_mapped != 0 && r.kv_host_mapped != 1)
         return fail(PARISKV_ERR_INVALID, "kv_host_mapped must be 0 or 1");
     if (!std::isfinite(r.scale)) return fail(PARISKV_ERR_INVALID, "scale is not finite");
@@ -503,6 +529,8 @@ static int retrieve_impl(const pariskv_config* cfg, const pariskv_index* index, 
         a.K = Kd;
         a.V = Vd;
         a.kv_capacity = att->kv_capacity;
+        a.Kw = att->Kw;
+        a.Vw = att->Vw;
         a.scale = att->scale;
         a.attn_out = att->out;
         a.win = att->win;
@@ -512,8 +540,9 @@ static int retrieve_impl(const pariskv_config* cfg, const pariskv_index* index, 
     hipError_t e;
     // Attention by its own kernel over out_idx (when the top-k did not fuse it).
     auto attend_separately = [&]() -> int {
-        const hipError_t ea = launch_attend(q, Kd, Vd, att->kv_capacity, out_idx, budget->top_k, batch,
-                                            a.hkv, a.g, att->scale, att->out, att->win, s);
+        const hipError_t ea = launch_attend(q, Kd, Vd, att->kv_capacity, att->Kw, att->Vw, out_idx,
+                                            budget->top_k, batch, a.hkv, a.g, att->scale, att->out,
+                                            att->win, s);
         return ea == hipSuccess ? PARISKV_OK : hip_fail(ea, "attend launch");
     };
     if (n == 0) {
@@ -558,8 +587,27 @@ int pariskv_retrieve_window_attend(const pariskv_config* cfg, const pariskv_inde
     if (!win) return fail(PARISKV_ERR_INVALID, "win must be non-NULL");
     if (!budget) return fail(PARISKV_ERR_INVALID, "budget must be non-NULL");
     AttendReq att{K, V, kv_host_mapped, kv_capacity, scale, out, AttendWindow{}};
-    int rc = check_window(win, kv_capacity, budget->top_k, n < 0 ? 0 : n, &att.win);
+    int rc = check_window(win, kv_capacity, budget->top_k, n < 0 ? 0 : n, 0, &att.win);
     if (rc) return rc;
+    return retrieve_impl(cfg, index, q, n, batch, budget, out_idx, out_score, workspace, ws_bytes,
+                         stream, &att);
+}
+
+int pariskv_retrieve_tiered_attend(const pariskv_config* cfg, const pariskv_index* index,
+                                   const void* q, int64_t n, int32_t batch,
+                                   const pariskv_budget* budget, int32_t* out_idx, float* out_score,
+                                   const void* K_win, const void* V_win, int64_t win_capacity,
+                                   const void* K, const void* V, int32_t kv_host_mapped,
+                                   int64_t kv_capacity, const pariskv_window* win, float scale,
+                                   float* out, void* workspace, size_t ws_bytes, void* stream) {
+    prof_chain_start();
+    if (!win) return fail(PARISKV_ERR_INVALID, "win must be non-NULL");
+    if (!budget) return fail(PARISKV_ERR_INVALID, "budget must be non-NULL");
+    int rc = check_window_cache(K_win, V_win, win_capacity);
+    if (rc) return rc;
+    AttendReq att{K, V, kv_host_mapped, kv_capacity, scale, out, AttendWindow{}, K_win, V_win};
+    if ((rc = check_window(win, kv_capacity, budget->top_k, n < 0 ? 0 : n, win_capacity, &att.win)))
+        return rc;
     return retrieve_impl(cfg, index, q, n, batch, budget, out_idx, out_score, workspace, ws_bytes,
                          stream, &att);
 }
@@ -567,7 +615,8 @@ int pariskv_retrieve_window_attend(const pariskv_config* cfg, const pariskv_inde
 static int attend_impl(const pariskv_config* cfg, const void* q, const void* K, const void* V,
                        int32_t kv_host_mapped, int64_t kv_capacity, const int32_t* idx, int32_t k,
                        const pariskv_window* win, int32_t batch, float scale, float* out,
-                       void* stream) {
+                       void* stream, const void* Kw = nullptr, const void* Vw = nullptr,
+                       int64_t win_capacity = 0) {
     prof_chain_start();
     int rc = check_config(cfg, batch);
     if (rc) return rc;
@@ -578,13 +627,13 @@ static int attend_impl(const pariskv_config* cfg, const void* q, const void* K, 
         return fail(PARISKV_ERR_INVALID, "q, K, V, out must be 16-byte aligned, idx 4-byte aligned");
     if (k < 1) return fail(PARISKV_ERR_INVALID, "k %d < 1", k);
     if (k > kMaxAttendRows) return fail(PARISKV_ERR_UNSUPPORTED, "k %d above %d", k, kMaxAttendRows);
-    if (kv_capacity < 1 || kv_capacity > INT32_MAX)
-        return fail(PARISKV_ERR_INVALID, "kv_capacity %lld outside 1..2^31-1", (long long)kv_capacity);
+    if (kv_capacity < 1 || kv_capacity > kMaxKvRows)
+        return fail(PARISKV_ERR_INVALID, "kv_capacity %lld outside 1..2^30-1", (long long)kv_capacity);
     if (kv_host_mapped != 0 && kv_host_mapped != 1)
         return fail(PARISKV_ERR_INVALID, "kv_host_mapped must be 0 or 1");
     if (!std::isfinite(scale)) return fail(PARISKV_ERR_INVALID, "scale is not finite");
     AttendWindow aw;
-    if ((rc = check_window(win, kv_capacity, k, -1, &aw)) != PARISKV_OK) return rc;
+    if ((rc = check_window(win, kv_capacity, k, -1, win_capacity, &aw)) != PARISKV_OK) return rc;
     const void* Kd = K;
     const void* Vd = V;
     if (kv_host_mapped) {
@@ -596,7 +645,7 @@ static int attend_impl(const pariskv_config* cfg, const void* q, const void* K, 
         if (e != hipSuccess) return hip_fail(e, "hipHostGetDevicePointer(V)");
         Vd = p;
     }
-    hipError_t e = launch_attend(q, Kd, Vd, kv_capacity, idx, k, batch, cfg->n_kv_heads,
+    hipError_t e = launch_attend(q, Kd, Vd, kv_capacity, Kw, Vw, idx, k, batch, cfg->n_kv_heads,
                                  cfg->q_per_kv, scale, out, aw, static_cast<hipStream_t>(stream));
     if (e != hipSuccess) return hip_fail(e, "attend launch");
     return PARISKV_OK;
@@ -616,6 +665,46 @@ int pariskv_window_attend(const pariskv_config* cfg, const void* q, const void* 
     if (!win) return fail(PARISKV_ERR_INVALID, "win must be non-NULL");
     return attend_impl(cfg, q, K, V, kv_host_mapped, kv_capacity, idx, k, win, batch, scale, out,
                        stream);
+}
+
+int pariskv_tiered_attend(const pariskv_config* cfg, const void* q, const void* K_win,
+                          const void* V_win, int64_t win_capacity, const void* K, const void* V,
+                          int32_t kv_host_mapped, int64_t kv_capacity, const int32_t* idx, int32_t k,
+                          const pariskv_window* win, int32_t batch, float scale, float* out,
+                          void* stream) {
+    if (!win) return fail(PARISKV_ERR_INVALID, "win must be non-NULL");
+    int rc = check_window_cache(K_win, V_win, win_capacity);
+    if (rc) return rc;
+    return attend_impl(cfg, q, K, V, kv_host_mapped, kv_capacity, idx, k, win, batch, scale, out,
+                       stream, K_win, V_win, win_capacity);
+}
+
+int pariskv_offload_rows(const void* K_src, const void* V_src, int64_t src_capacity, int64_t src_row,
+                         void* K_dst, void* V_dst, int64_t dst_capacity, int64_t dst_row, int64_t t,
+                         int32_t batch, int32_t n_kv_heads, void* stream) {
+    prof_chain_start();
+    if (!K_src || !V_src || !K_dst || !V_dst)
+        return fail(PARISKV_ERR_INVALID, "K/V source and destination must be non-NULL");
+    if (batch < 1 || n_kv_heads < 1) return fail(PARISKV_ERR_INVALID, "batch and n_kv_heads must be >= 1");
+    if (src_capacity < 1 || dst_capacity < 1) return fail(PARISKV_ERR_INVALID, "capacities must be >= 1");
+    if (t < 0 || src_row < 0 || dst_row < 0 || src_row > src_capacity - t || dst_row > dst_capacity - t)
+        return fail(PARISKV_ERR_INVALID, "rows [%lld, +%lld) -> [%lld, +%lld) outside the caches",
+                    (long long)src_row, (long long)t, (long long)dst_row, (long long)t);
+    if (t == 0) return PARISKV_OK;
+    // One pitched copy per tensor: height = the (sequence, KV head) groups, width = t rows.
+    const size_t row_bytes = (size_t)kD * 2;
+    const size_t groups = (size_t)batch * (size_t)n_kv_heads;
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    const void* src[2] = {K_src, V_src};
+    void* dst[2] = {K_dst, V_dst};
+    for (int i = 0; i < 2; ++i) {
+        const hipError_t e = hipMemcpy2DAsync(
+            static_cast<char*>(dst[i]) + (size_t)dst_row * row_bytes, (size_t)dst_capacity * row_bytes,
+            static_cast<const char*>(src[i]) + (size_t)src_row * row_bytes, (size_t)src_capacity * row_bytes,
+            (size_t)t * row_bytes, groups, hipMemcpyDefault, s);
+        if (e != hipSuccess) return hip_fail(e, "hipMemcpy2DAsync");
+    }
+    return PARISKV_OK;
 }
 
 int pariskv_profile_enable(int32_t on) {

@@ -26,7 +26,9 @@ __global__ __launch_bounds__(kAtThreads) void attend_kernel(const __half* __rest
                                                             const int32_t* __restrict__ idx,
                                                             int32_t k, int32_t hkv, int32_t g,
                                                             int32_t hq, float scale,
-                                                            float* __restrict__ out, AttendWindow win) {
+                                                            float* __restrict__ out, AttendWindow win,
+                                                            const __half* __restrict__ Kw,
+                                                            const __half* __restrict__ Vw) {
     __shared__ AttendScratch s_sm;
     __shared__ int32_t s_idx[kMaxAttendRows];
     const int64_t row = blockIdx.x;  // seq * hq + head
@@ -39,10 +41,8 @@ __global__ __launch_bounds__(kAtThreads) void attend_kernel(const __half* __rest
     const int nd = (int)win.dense_rows();
     for (int r = threadIdx.x; r < nd + k; r += kAtThreads) {
         int32_t v;
-        if (r < win.sink) {
-            v = r;
-        } else if (r < nd) {
-            v = (int32_t)(win.dense_begin + (r - win.sink));
+        if (r < nd) {
+            v = win.dense_entry(r);
         } else {
             const int32_t j = ir[r - nd];
             const int64_t cr = win.retr_begin + (int64_t)j;
@@ -51,20 +51,24 @@ __global__ __launch_bounds__(kAtThreads) void attend_kernel(const __half* __rest
         s_idx[r] = v;
     }
     __syncthreads();
-    attend_row(q + row * kD, K + kvrow0 * kD, V + kvrow0 * kD, kv_capacity, s_idx, nd + k, scale,
-               out + row * kD, s_sm);
+    const int64_t wrow0 = win.win_capacity > 0 ? ((int64_t)seq * hkv + h / g) * win.win_capacity : 0;
+    attend_row(q + row * kD, K + kvrow0 * kD, V + kvrow0 * kD, kv_capacity, Kw + wrow0 * kD,
+               Vw + wrow0 * kD, win.win_capacity, s_idx, nd + k, scale, out + row * kD, s_sm);
 }
 
 }  // namespace
 
 hipError_t launch_attend(const void* q, const void* K, const void* V, int64_t kv_capacity,
-                         const int32_t* idx, int32_t k, int32_t batch, int32_t hkv, int32_t g,
-                         float scale, float* out, const AttendWindow& win, hipStream_t s) {
+                         const void* Kw, const void* Vw, const int32_t* idx, int32_t k, int32_t batch,
+                         int32_t hkv, int32_t g, float scale, float* out, const AttendWindow& win,
+                         hipStream_t s) {
     const int32_t hq = hkv * g;
     const ProfEvents pe = prof_begin(win.dense_rows() > 0 ? "window_attend" : "attend");
     hipExtLaunchKernelGGL(attend_kernel, dim3((unsigned)(batch * hq)), dim3(kAtThreads), 0, s, pe.start, pe.stop, 0,
                        static_cast<const __half*>(q), static_cast<const __half*>(K),
-                       static_cast<const __half*>(V), kv_capacity, idx, k, hkv, g, hq, scale, out, win);
+                       static_cast<const __half*>(V), kv_capacity, idx, k, hkv, g, hq, scale, out, win,
+                       static_cast<const __half*>(win.win_capacity > 0 ? Kw : K),
+                       static_cast<const __half*>(win.win_capacity > 0 ? Vw : V));
     return hipGetLastError();
 }
 

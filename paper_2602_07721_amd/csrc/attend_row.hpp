@@ -8,8 +8,13 @@
 // V row is one 256-byte contiguous read by 16 lanes.  Slot s takes list
 // entries s, s + 64, ...; every lane keeps 8 K and 8 V row segments in flight.
 // Each slot keeps an online-softmax state (running max, sum, 8 accumulators
-// per lane); the 64 states are merged in LDS at the end.  List entries outside
-// [0, kv_capacity) (for example -1) are skipped.
+// per lane); the 64 states are merged in LDS at the end.
+//
+// Rows come from one of two caches: a list entry with kWinRow set names row
+// (entry - kWinRow) of the window cache (Kw, Vw, win_capacity: Sink and Local /
+// Update Buffer kept on the GPU), any other entry >= 0 a row of the main cache
+// (K, V, kv_capacity: the retrieval rows, in HBM or in host memory).  Entries
+// past their cache's capacity, and negative entries (-1 padding), are skipped.
 #pragma once
 
 #include <hip/hip_fp16.h>
@@ -39,12 +44,14 @@ __device__ __forceinline__ void unpack8_half(const uint4 v, float* f) {
 }
 
 // q: the head's D float16 values; K, V: the KV head's rows [kv_capacity][D];
+// Kw, Vw: its window-cache rows [win_capacity][D] (entries with kWinRow);
 // list: k entries in LDS (already synchronised); out: D floats.  Every thread
 // of the block must call it; it ends with the block synchronised.
 __device__ __forceinline__ void attend_row(const __half* __restrict__ q, const __half* __restrict__ K,
                                            const __half* __restrict__ V, int64_t kv_capacity,
-                                           const int32_t* list, int32_t k, float scale,
-                                           float* __restrict__ out, AttendScratch& sm) {
+                                           const __half* __restrict__ Kw, const __half* __restrict__ Vw,
+                                           int64_t win_capacity, const int32_t* list, int32_t k,
+                                           float scale, float* __restrict__ out, AttendScratch& sm) {
     const int tid = threadIdx.x;
     const int grp16 = tid >> 4;  // key slot 0 .. kAtGroups-1
     const int l16 = tid & 15;
@@ -66,13 +73,15 @@ __device__ __forceinline__ void attend_row(const __half* __restrict__ q, const _
         for (int u = 0; u < kAtUnroll; ++u) {
             const int r = base + grp16 + kAtGroups * u;
             key[u] = r < k ? list[r] : -1;
-            if (key[u] >= kv_capacity) key[u] = -1;
+            const bool win = key[u] >= kWinRow;
+            const int64_t rowi = win ? key[u] - kWinRow : key[u];
+            if (rowi >= (win ? win_capacity : kv_capacity)) key[u] = -1;
             kc[u] = make_uint4(0, 0, 0, 0);
             vc[u] = make_uint4(0, 0, 0, 0);
             if (key[u] >= 0) {
-                const int64_t off = (int64_t)key[u] * kD;
-                kc[u] = reinterpret_cast<const uint4*>(K + off)[l16];
-                vc[u] = reinterpret_cast<const uint4*>(V + off)[l16];
+                const int64_t off = rowi * kD;
+                kc[u] = reinterpret_cast<const uint4*>((win ? Kw : K) + off)[l16];
+                vc[u] = reinterpret_cast<const uint4*>((win ? Vw : V) + off)[l16];
             }
         }
         float dot[kAtUnroll];

@@ -110,17 +110,33 @@ constexpr uint32_t kFlagNoRotation = 1u;     // R = I (encode and query transfor
 constexpr uint32_t kFlagNoAlpha = 2u;        // W_b = sqrt(S_b) (encode)
 constexpr uint32_t kFlagBinary = 1u << 8;    // admitted clusters score 1 (bonus tables)
 
+// List-entry flag of the attention body: the entry names a row of the window
+// cache (Sink + Local / Update Buffer kept on the GPU), not of the main cache.
+constexpr int32_t kWinRow = 1 << 30;
+// Largest cache row an attention list can name (rows stay below the flag bit).
+constexpr int64_t kMaxKvRows = (int64_t)kWinRow - 1;
+
 // Rows one query head attends (Sec. "Buffer Update": Sink and Local + Update
 // Buffer densely, the retrieved keys sparsely).  The head's list is
 //   [0, sink) ++ [dense_begin, dense_end) ++ (retr_begin + idx_j for idx_j >= 0),
 // in that order (idx_j < 0 stays an empty slot).  All zero = the retrieved keys
-// only, at their own row numbers.
+// only, at their own row numbers.  With win_capacity > 0 the dense rows are read
+// from the window cache instead of the main cache: Sink row r at slot r, Local /
+// Buffer row r at slot sink + (r - sink) mod (win_capacity - sink).
 struct AttendWindow {
     int64_t sink = 0;
     int64_t retr_begin = 0;
     int64_t dense_begin = 0;
     int64_t dense_end = 0;
+    int64_t win_capacity = 0;
     __host__ __device__ int64_t dense_rows() const { return sink + (dense_end - dense_begin); }
+    // List entry of dense position r (0 <= r < dense_rows()).
+    __host__ __device__ int32_t dense_entry(int64_t r) const {
+        const int64_t row = r < sink ? r : dense_begin + (r - sink);
+        if (win_capacity <= 0) return (int32_t)row;
+        const int64_t slot = row < sink ? row : sink + (row - sink) % (win_capacity - sink);
+        return kWinRow | (int32_t)slot;
+    }
 };
 
 struct RetrieveArgs {
@@ -154,6 +170,8 @@ struct RetrieveArgs {
     const void* K;
     const void* V;
     int64_t kv_capacity;
+    const void* Kw;    // window cache (win.win_capacity > 0)
+    const void* Vw;
     float scale;
     float* attn_out;
     AttendWindow win;  // dense rows attended next to the winners
@@ -169,9 +187,12 @@ hipError_t launch_compact_rerank(const RetrieveArgs& a, hipStream_t s);
 hipError_t launch_topk(const RetrieveArgs& a, hipStream_t s, bool attend = false, bool* fused = nullptr);
 hipError_t launch_pad_outputs(const RetrieveArgs& a, hipStream_t s);
 
+// Kw, Vw: the window cache [batch][Hkv][win.win_capacity][D] when
+// win.win_capacity > 0 (ignored otherwise).
 hipError_t launch_attend(const void* q, const void* K, const void* V, int64_t kv_capacity,
-                         const int32_t* idx, int32_t k, int32_t batch, int32_t hkv, int32_t g,
-                         float scale, float* out, const AttendWindow& win, hipStream_t s);
+                         const void* Kw, const void* Vw, const int32_t* idx, int32_t k, int32_t batch,
+                         int32_t hkv, int32_t g, float scale, float* out, const AttendWindow& win,
+                         hipStream_t s);
 
 // Largest list (dense rows + retrieved rows) one attention block stages in LDS.
 constexpr int kMaxAttendRows = 4096;

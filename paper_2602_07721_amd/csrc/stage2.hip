@@ -432,15 +432,19 @@ __global__ __launch_bounds__(TH) void topk_lds_kernel(RetrieveArgs a) {
     if (kAttend) {
         // Attention over the dense rows and the kk winners (Eqs. approx_weight,
         // approx_output), from LDS.  Region B is free once the compaction runs.
-        for (int r = tid; r < nd; r += TH)
-            s_win[r] = r < a.win.sink ? r : (int32_t)(a.win.dense_begin + (r - a.win.sink));
+        for (int r = tid; r < nd; r += TH) s_win[r] = a.win.dense_entry(r);
         __syncthreads();
         const int seq = (int)(row / a.hq);
         const int h = (int)(row % a.hq);
         const int64_t kvrow0 = ((int64_t)seq * a.hkv + h / a.g) * a.kv_capacity;
+        const bool wc = a.win.win_capacity > 0;
+        const int64_t wrow0 = wc ? ((int64_t)seq * a.hkv + h / a.g) * a.win.win_capacity : kvrow0;
         attend_row(static_cast<const __half*>(a.q) + row * kD,
                    static_cast<const __half*>(a.K) + kvrow0 * kD,
-                   static_cast<const __half*>(a.V) + kvrow0 * kD, a.kv_capacity, s_win, nd + kk, a.scale,
+                   static_cast<const __half*>(a.V) + kvrow0 * kD, a.kv_capacity,
+                   static_cast<const __half*>(wc ? a.Kw : a.K) + wrow0 * kD,
+                   static_cast<const __half*>(wc ? a.Vw : a.V) + wrow0 * kD, a.win.win_capacity,
+                   s_win, nd + kk, a.scale,
                    a.attn_out + row * kD, *reinterpret_cast<AttendScratch*>(s_raw));
     }
 }

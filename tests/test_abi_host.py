@@ -304,3 +304,33 @@ def test_variant_flag_validation():
     assert pk.retrieve_workspace_size(_cfg(flags=pk.NO_ROTATION | pk.NO_ALPHA_CORRECTION), 1, 4000, b) > 0
     assert L.pariskv_retrieve_workspace(_cfg().c(), 1, 4000, pk.Budget(512, 1024, 64, flags=2).c()) == 0
     assert pk.retrieve_workspace_size(_cfg(), 1, 4000, pk.Budget(512, 1024, 64, flags=pk.BINARY_COLLISIONS)) > 0
+
+
+def test_tiered_attend_and_offload_validation():
+    cfg = _cfg()
+    L = pk.lib()
+    W = pk.Window
+
+    def call(win, wcap=1000, kw=FAKE, k=8, cap=4096):
+        return L.pariskv_tiered_attend(cfg.c(), ctypes.c_void_p(FAKE), ctypes.c_void_p(kw), ctypes.c_void_p(FAKE),
+                                       wcap, ctypes.c_void_p(FAKE), ctypes.c_void_p(FAKE), 0, cap,
+                                       ctypes.c_void_p(FAKE), k, None if win is None else win.c(), 1,
+                                       ctypes.c_float(0.1), ctypes.c_void_p(FAKE), None)
+    assert call(None) == pk.ERR_INVALID
+    assert call(W(128, 128, 3000, 3600), kw=0) == pk.ERR_INVALID           # no window cache
+    assert call(W(128, 128, 3000, 3600), wcap=0) == pk.ERR_INVALID
+    assert call(W(128, 128, 3000, 3600), wcap=700) == pk.ERR_INVALID       # 128 + ring 572 < 600 rows
+    assert call(W(128, 128, 3000, 3600), wcap=2 ** 30) == pk.ERR_INVALID  # past the row limit
+    assert call(W(128, 128, 3000, 3600), cap=2 ** 30) == pk.ERR_INVALID    # main cache past the limit
+    assert call(W(128, 128, 3000, 3600), k=3400) == pk.ERR_UNSUPPORTED     # 128 + 600 + 3400 rows
+    # dense rows may lie past the main cache: they live in the window cache (would launch: not run here)
+
+    def off(src_row=0, dst_row=0, t=16, scap=100, dcap=100, kd=FAKE):
+        return L.pariskv_offload_rows(ctypes.c_void_p(FAKE), ctypes.c_void_p(FAKE), scap, src_row,
+                                      ctypes.c_void_p(kd), ctypes.c_void_p(FAKE), dcap, dst_row, t, 1, 8, None)
+    assert off(kd=0) == pk.ERR_INVALID
+    assert off(src_row=90) == pk.ERR_INVALID
+    assert off(dst_row=-1) == pk.ERR_INVALID
+    assert off(t=-1) == pk.ERR_INVALID
+    assert off(dcap=0) == pk.ERR_INVALID
+    assert off(t=0) == pk.OK                                               # nothing to copy

@@ -223,3 +223,98 @@ def test_decode_loop_with_buffer_updates_matches_the_oracle():
                 retrieved = [win.retr_begin + int(j) for j in inter["idx"][0, hq] if j >= 0]
                 ref = owin.window_attention(Q[0, hq], K[0, h], V[0, h], owin.dense_rows(R), retrieved, SCALE)
                 _close(o[0, hq], ref, (t, hq))
+
+
+def _window_cache(K, V, win, wcap):
+    """The dense rows of `win` placed at their slots of a window cache of wcap rows."""
+    b, hkv, _, D = K.shape
+    Kw = np.zeros((b, hkv, wcap, D), np.float16)
+    Vw = np.zeros_like(Kw)
+    for r in _dense(win):
+        s = pk.window_slot(r, win.sink_len, wcap)
+        Kw[:, :, s] = K[:, :, r]
+        Vw[:, :, s] = V[:, :, r]
+    return Kw, Vw
+
+
+@pytest.mark.parametrize("host", [False, True], ids=["retrieval_in_hbm", "retrieval_in_host_memory"])
+def test_tiered_attend_equals_window_attend_bit_for_bit(host):
+    b, hkv, g, cap, k = 1, 2, 4, 6000, 256
+    win = pk.Window(128, 128, 5000, 5700)      # 700 Local/Buffer rows
+    wcap = 128 + 720                           # a ring of 720 slots: rows 5000..5699 wrap around it
+    K, V = _cache(b, hkv, cap, seed=27)
+    Q = _queries(K, g, seed=27)
+    cfg = pk.Config(hkv, g, cap, workloads.rotation_signs(27))
+    idx = np.random.default_rng(2).integers(-1, 4872, size=(b, hkv * g, k)).astype(np.int32)
+    Qd, Id = torch.from_numpy(Q).cuda(), torch.from_numpy(idx).cuda()
+    ref = pk.window_attend(cfg, Qd, torch.from_numpy(K).cuda(), torch.from_numpy(V).cuda(), Id, win, SCALE)
+    Kw, Vw = _window_cache(K, V, win, wcap)
+    # the main cache's copies of the dense rows are wrong on purpose: they must be read from the window cache
+    Kr, Vr = K.copy(), V.copy()
+    Kr[:, :, :128] = 7.0
+    Vr[:, :, 5000:5700] = -3.0
+    Kr_t, Vr_t = torch.from_numpy(Kr), torch.from_numpy(Vr)
+    if host:
+        Kr_t, Vr_t = Kr_t.pin_memory(), Vr_t.pin_memory()
+    else:
+        Kr_t, Vr_t = Kr_t.cuda(), Vr_t.cuda()
+    out = pk.tiered_attend(cfg, Qd, torch.from_numpy(Kw).cuda(), torch.from_numpy(Vw).cuda(), Kr_t, Vr_t, Id,
+                           win, SCALE, kv_host_mapped=host)
+    torch.cuda.synchronize()
+    np.testing.assert_array_equal(out.cpu().numpy().view(np.uint32), ref.cpu().numpy().view(np.uint32))
+
+
+@pytest.mark.parametrize("n_cand,host", [(512, True), (4096, False), (34000, True)],
+                         ids=["C512_host", "C4096_hbm", "C34000_split_host"])
+def test_fused_tiered_equals_separate_and_window_paths(n_cand, host):
+    b, hkv, g, k = 1, 2, 4, 128
+    sink, local, buf = 128, 512, 60
+    n = max(6000, n_cand + 100)
+    cap = sink + n + local + buf
+    win = pk.Window(sink, sink, sink + n, cap)
+    wcap = sink + local + 2 * 256
+    print(f"[tiered] C {n_cand} n {n} host {host}", flush=True)
+    K, V = _cache(b, hkv, cap, seed=28)
+    Q = _queries(K, g, seed=28)
+    cfg = pk.Config(hkv, g, n, workloads.rotation_signs(28))
+    budget = pk.Budget(n_cand, 2 * n_cand, k)
+    Kd, Vd, Qd = (torch.from_numpy(x).cuda() for x in (K, V, Q))
+    index = _index_over(cfg, Kd, sink, n)
+    Kw, Vw = (torch.from_numpy(x).cuda() for x in _window_cache(K, V, win, wcap))
+    Kr, Vr = (torch.from_numpy(x) for x in (K, V))
+    Kr, Vr = (Kr.pin_memory(), Vr.pin_memory()) if host else (Kd, Vd)
+    sc1 = torch.empty((b, hkv * g, k), dtype=torch.float32, device="cuda")
+    i1, _, o1, _ = pk.retrieve_tiered_attend(cfg, index, Qd, n, budget, Kw, Vw, Kr, Vr, win, SCALE,
+                                             out_score=sc1, kv_host_mapped=host)
+    i2, _, _ = pk.retrieve(cfg, index, Qd, n, budget)
+    o2 = pk.tiered_attend(cfg, Qd, Kw, Vw, Kr, Vr, i2, win, SCALE, kv_host_mapped=host)
+    _, _, o3, _ = pk.retrieve_window_attend(cfg, index, Qd, n, budget, Kd, Vd, win, SCALE)
+    torch.cuda.synchronize()
+    np.testing.assert_array_equal(i1.cpu().numpy(), i2.cpu().numpy())
+    for o in (o2, o3):
+        np.testing.assert_array_equal(o1.cpu().numpy().view(np.uint32), o.cpu().numpy().view(np.uint32))
+
+
+@pytest.mark.parametrize("to_host", [True, False], ids=["to_pinned_host", "device_to_device"])
+def test_offload_rows_copies_exactly(to_host):
+    b, hkv, D = 2, 3, 128
+    r = np.random.default_rng(3)
+    Ks = torch.from_numpy(r.standard_normal((b, hkv, 300, D)).astype(np.float16)).cuda()
+    Vs = torch.from_numpy(r.standard_normal((b, hkv, 300, D)).astype(np.float16)).cuda()
+    Kd = torch.zeros((b, hkv, 1000, D), dtype=torch.float16)
+    Vd = torch.zeros_like(Kd)
+    Kd, Vd = (Kd.pin_memory(), Vd.pin_memory()) if to_host else (Kd.cuda(), Vd.cuda())
+    side = torch.cuda.Stream()   # default priority
+    with torch.cuda.stream(side):
+        pk.offload_rows(Ks, Vs, 40, Kd, Vd, 700, 100)
+        pk.offload_rows(Ks, Vs, 250, Kd, Vd, 0, 50)   # a second segment, as a wrapped ring range needs
+    side.synchronize()
+    Kh, Vh, Ksh, Vsh = (x.cpu().numpy() for x in (Kd, Vd, Ks, Vs))
+    np.testing.assert_array_equal(Kh[:, :, 700:800], Ksh[:, :, 40:140])
+    np.testing.assert_array_equal(Vh[:, :, 700:800], Vsh[:, :, 40:140])
+    np.testing.assert_array_equal(Kh[:, :, 0:50], Ksh[:, :, 250:300])
+    np.testing.assert_array_equal(Vh[:, :, 0:50], Vsh[:, :, 250:300])
+    untouched = np.ones(1000, bool)
+    untouched[700:800] = False
+    untouched[0:50] = False
+    assert not Kh[:, :, untouched].any() and not Vh[:, :, untouched].any()

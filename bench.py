@@ -61,6 +61,9 @@ def parse():
                          "K/V in pinned host memory")
     ap.add_argument("--drift-steps", type=int, default=4096,
                     help="decode steps of the drift measurement (the full workload runs 32768)")
+    ap.add_argument("--offload-steps", type=int, default=0,
+                    help="also run the 1M-token offload setting (GPU window ring, Retrieval K/V in pinned "
+                         "host memory, buffer updates offloaded on a second stream) for this many steps")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="also run one plain 1 GiB device copy (for scaling HBM counters)")
     return ap.parse_args()
@@ -413,6 +416,126 @@ def ablation_run(pk, torch, np, workloads, dev, drift_steps, n_queries=8):
     }
 
 
+def offload_run(pk, torch, np, workloads, dev, steps, sink=128, local=512, m=256):
+    """The offload setting at 1M tokens (Sec. "Buffer Update" with GPU->CPU offload; Sec.
+    "On-Demand UVA Fetch"): Sink and Local + Update Buffer K/V in a GPU window ring, the
+    Retrieval region's K/V in pinned host memory.  Each decode step writes the new token into
+    the ring and runs pariskv_retrieve_tiered_attend (retrieved rows read over the host link);
+    every m steps the rows leaving Local are encoded from the ring (pariskv_append_rows) and
+    copied to host memory by pariskv_offload_rows on a second stream, which the step's
+    retrieval waits for only before it starts."""
+    wc = workloads.CONFIGS["host1m"]
+    signs = workloads.rotation_signs(wc.seed)
+    P = wc.n
+    total = P + steps
+    K, V = workloads.layer_kv(wc, n=total, threads=16)
+    Q = np.stack([workloads.layer_queries(wc, K[:, :, :P], step=t)[0] for t in range(steps)])
+    Kh = torch.from_numpy(K).pin_memory()   # the offloaded cache (rows of Retrieval)
+    Vh = torch.from_numpy(V).pin_memory()
+    hq = wc.n_kv_heads * wc.q_per_kv
+    wcap = sink + local + 2 * m
+    # decode tokens' K/V staged on the GPU (the model would produce them step by step)
+    Knew = torch.from_numpy(K[:, :, P:]).to(dev)
+    Vnew = torch.from_numpy(V[:, :, P:]).to(dev)
+    Kw = torch.zeros((wc.batch, wc.n_kv_heads, wcap, wc.head_dim), dtype=torch.float16, device=dev)
+    Vw = torch.zeros_like(Kw)
+    win0, n_idx = pk.window_regions(P, 0, sink, local, m)
+    for r in list(range(win0.sink_len)) + list(range(win0.dense_begin, win0.dense_end)):
+        slot = pk.window_slot(r, sink, wcap)
+        Kw[:, :, slot] = torch.from_numpy(K[:, :, r]).to(dev)
+        Vw[:, :, slot] = torch.from_numpy(V[:, :, r]).to(dev)
+    cfg = pk.Config(wc.n_kv_heads, wc.q_per_kv, total, signs)
+    index = pk.Index.empty(cfg, wc.batch, dev)
+    Kd = torch.from_numpy(K[:, :, :P]).to(dev)   # prefill: encode the prompt's Retrieval region
+    pk.append_rows(cfg, index, Kd, win0.retr_begin, n_idx, 0)
+    torch.cuda.synchronize()
+    del Kd
+    torch.cuda.empty_cache()
+    Qd = torch.from_numpy(Q).to(dev)
+    budget = pk.Budget(wc.n_cand, wc.n_collide, wc.top_k)
+    scale = 1.0 / np.sqrt(wc.head_dim)
+    ws = torch.empty(pk.retrieve_workspace_size(cfg, wc.batch, total, budget), dtype=torch.uint8, device=dev)
+    out_idx = torch.empty((wc.batch, hq, wc.top_k), dtype=torch.int32, device=dev)
+    out = torch.empty((wc.batch, hq, wc.head_dim), dtype=torch.float32, device=dev)
+    main = torch.cuda.current_stream()
+    side = torch.cuda.Stream()  # default priority
+    starts = [torch.cuda.Event(enable_timing=True) for _ in range(steps)]
+    ends = [torch.cuda.Event(enable_timing=True) for _ in range(steps)]
+    copies = []
+    upd = np.zeros(steps, bool)
+
+    def ring_ranges(r0, cnt):
+        """[(slot, row, count)] contiguous slot runs of Local/Buffer rows [r0, r0 + cnt)."""
+        runs, r = [], r0
+        while r < r0 + cnt:
+            slot = pk.window_slot(r, sink, wcap)
+            c = min(r0 + cnt - r, wcap - slot)
+            runs.append((slot, r, c))
+            r += c
+        return runs
+
+    pk.profile_reset()
+    pk.profile_enable(True)
+    torch.cuda.synchronize()
+    for t in range(1, steps + 1):
+        i = t - 1
+        starts[i].record()
+        slot = pk.window_slot(P + t - 1, sink, wcap)   # the new token enters the Update Buffer
+        Kw[:, :, slot].copy_(Knew[:, :, t - 1])
+        Vw[:, :, slot].copy_(Vnew[:, :, t - 1])
+        win, n_retr = pk.window_regions(P, t, sink, local, m)
+        if n_retr > n_idx:
+            upd[i] = True
+            r0, cnt = win.retr_begin + n_idx, n_retr - n_idx
+            side.wait_stream(main)
+            c0, c1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            with torch.cuda.stream(side):
+                c0.record()
+                for sl, row, c in ring_ranges(r0, cnt):
+                    pk.offload_rows(Kw, Vw, sl, Kh, Vh, row, c)
+                c1.record()
+            copies.append((c0, c1, cnt))
+            done = n_idx
+            for sl, row, c in ring_ranges(r0, cnt):
+                pk.append_rows(cfg, index, Kw, sl, c, done)
+                done += c
+            n_idx = n_retr
+            main.wait_event(c1)   # the retrieval may now pick the evicted rows from host memory
+        pk.retrieve_tiered_attend(cfg, index, Qd[i], n_idx, budget, Kw, Vw, Kh, Vh, win, scale,
+                                  out_idx=out_idx, out=out, workspace=ws, kv_host_mapped=True)
+        ends[i].record()
+    torch.cuda.synchronize()
+    pk.profile_enable(False)
+    prof = pk.profile_read()
+    us = np.array([starts[i].elapsed_time(ends[i]) * 1e3 for i in range(steps)])
+    body, ub = us[8:], upd[8:]
+    copy_bytes = [2 * wc.batch * wc.n_kv_heads * c * wc.head_dim * 2 for _, _, c in copies]
+    copy_us = [a.elapsed_time(b) * 1e3 for a, b, _ in copies]
+    fetch_bytes = wc.batch * hq * wc.top_k * 2 * wc.head_dim * 2
+    ta = prof.get("topk_attend")
+    ta_us = ta[1] * 1e3 / ta[0] if ta else None
+    return {
+        "workload": (f"host1m: {wc.batch} seq x {wc.n_kv_heads} KV heads x {wc.q_per_kv} query heads, "
+                     f"{P}-token prompt + {steps} decode steps; Sink {sink} + Local {local} + Update Buffer "
+                     f"in a GPU window ring of {wcap} rows, Retrieval K/V in pinned host memory; "
+                     f"C = {wc.n_cand}, C_rho = {wc.n_collide}, k = {wc.top_k}; buffer update every {m} steps"),
+        "us_per_step": round(float(body.mean()), 1),
+        "us_per_update_step": round(float(body[ub].mean()), 1) if ub.any() else None,
+        "us_per_other_step": round(float(body[~ub].mean()), 1),
+        "updates": int(upd.sum()),
+        "offload_d2h": {"bytes_per_update": int(copy_bytes[0]) if copy_bytes else 0,
+                        "us_per_update": round(float(np.mean(copy_us)), 1) if copy_us else None,
+                        "GBps": (round(float(np.sum(copy_bytes) / (np.sum(copy_us) * 1e-6) / 1e9), 2)
+                                 if copy_us else None)},
+        "fetch_h2d": {"bytes_per_step": int(fetch_bytes),
+                      "topk_attend_us": round(ta_us, 1) if ta_us else None,
+                      "GBps_of_topk_attend": round(fetch_bytes / (ta_us * 1e-6) / 1e9, 2) if ta_us else None},
+        "kernels_avg_us": {k: round(v[1] * 1e3 / max(1, v[0]), 1) for k, v in prof.items()},
+        "timing": ("HIP events on the main stream around each step (steps 1-8 left out); the offload "
+                   "copies timed on their own stream"),
+    }
+
+
 def host_link_run(pk, torch, np, cfg, K, V, Qd, idx_list, scale, dev, reps=8):
     """Sparse attention with K/V in pinned host memory, read through host-mapped pointers."""
     Kh = torch.from_numpy(K).pin_memory()
@@ -605,6 +728,9 @@ def main():
         extras["window"] = window_run(pk, torch, np, workloads, dev, args.drift_steps)
         torch.cuda.empty_cache()
         extras["ablation"] = ablation_run(pk, torch, np, workloads, dev, args.drift_steps)
+    if args.offload_steps > 0:
+        torch.cuda.empty_cache()
+        extras["offload"] = offload_run(pk, torch, np, workloads, dev, args.offload_steps)
 
     cpu = None
     if not args.no_cpu_baseline:

@@ -316,6 +316,20 @@ int pariskv_retrieve_window_attend(const pariskv_config* cfg, const pariskv_inde
                                    const pariskv_window* win, float scale, float* out,
                                    void* workspace, size_t ws_bytes, void* stream);
 
+/* pariskv_sparse_attend with every distinct K/V row fetched once per KV head:
+ * the query heads of a KV head (in quads of 4) attend over the union of their
+ * lists, each union row is read once and feeds every head that selected it
+ * (GQA-group de-duplication of the fetch; the saving is the heads' overlap,
+ * on the host link when kv_host_mapped).  Same arguments and, up to float32
+ * rounding order, the same result as pariskv_sparse_attend; each head's list
+ * must be ascending with any -1 padding at its end, as pariskv_retrieve writes
+ * it (other orders give unspecified values, never an access outside K/V).
+ *   union_rows  device int32 [batch][Hkv][ceil(G/4)] or NULL: rows fetched
+ * Errors: INVALID, UNSUPPORTED (min(G, 4) * k > PARISKV_MAX_ATTEND_ROWS), HIP. */
+int pariskv_group_attend(const pariskv_config* cfg, const void* q, const void* K, const void* V,
+                         int32_t kv_host_mapped, int64_t kv_capacity, const int32_t* idx, int32_t k,
+                         int32_t batch, float scale, float* out, int32_t* union_rows, void* stream);
+
 /* Tiered attention of the offload setting (Sec. "Buffer Update": Sink, Local
  * and the Update Buffer stay on the GPU, the Retrieval region is offloaded to
  * CPU memory; Sec. "On-Demand UVA Fetch": only the retrieved rows are read

@@ -21,7 +21,7 @@ __all__ = [
     "PariskvError", "Config", "Budget", "Index", "Window", "lib", "encode", "append", "append_rows",
     "retrieve", "retrieve_workspace_size", "workspace_layout", "sparse_attend", "retrieve_attend",
     "window_regions", "window_attend", "retrieve_window_attend", "tiered_attend", "retrieve_tiered_attend",
-    "offload_rows", "window_slot", "quantizer_table", "rotation_signs",
+    "offload_rows", "window_slot", "group_attend", "quantizer_table", "rotation_signs",
     "profile_enable", "profile_reset", "profile_read",
 ]
 
@@ -104,6 +104,8 @@ def lib():
         L.pariskv_retrieve_tiered_attend.argtypes = [P(_Config), P(_Index), VP, I64, I32, P(_Budget), VP, VP,
                                                      VP, VP, I64, VP, VP, I32, I64, P(_Window),
                                                      ctypes.c_float, VP, VP, SZ, VP]
+        L.pariskv_group_attend.argtypes = [P(_Config), VP, VP, VP, I32, I64, VP, I32, I32, ctypes.c_float, VP,
+                                           VP, VP]
         L.pariskv_offload_rows.argtypes = [VP, VP, I64, I64, VP, VP, I64, I64, I64, I32, I32, VP]
         L.pariskv_quantizer_table.argtypes = [I32, P(ctypes.c_double), P(ctypes.c_double)]
         L.pariskv_rotation_signs.argtypes = [ctypes.c_uint64, I32, P(ctypes.c_int8)]
@@ -369,6 +371,26 @@ def retrieve_window_attend(cfg, index, q, n, budget, K, V, win, scale, out_idx=N
         int(bool(kv_host_mapped)), int(K.shape[2]), win.c(), float(scale), _ptr(out, "out"),
         _ptr(workspace, "workspace"), workspace.numel(), _stream(stream)))
     return out_idx, out_score, out, workspace
+
+
+def group_attend(cfg, q, K, V, idx, scale, out=None, union_rows=None, kv_host_mapped=False, stream=None):
+    """sparse_attend with each distinct K/V row fetched once per KV head (quads of query heads
+    attend over the union of their ascending lists); union_rows: optional int32 tensor
+    [batch][Hkv][ceil(G/4)] that receives the number of rows fetched."""
+    import torch
+    batch = int(q.shape[0])
+    if out is None:
+        out = torch.empty((batch, cfg.n_q_heads, HEAD_DIM), dtype=torch.float32, device=q.device)
+    if kv_host_mapped:
+        for t, nm in ((K, "K"), (V, "V")):
+            if t.is_cuda or not t.is_pinned():
+                raise ValueError(f"{nm} must be pinned host memory when kv_host_mapped")
+    k = int(idx.shape[-1])
+    _check(lib().pariskv_group_attend(cfg.c(), _ptr(q, "q"), _ptr(K, "K", not kv_host_mapped),
+                                      _ptr(V, "V", not kv_host_mapped), int(bool(kv_host_mapped)),
+                                      int(K.shape[2]), _ptr(idx, "idx"), k, batch, float(scale),
+                                      _ptr(out, "out"), _ptr(union_rows, "union_rows"), _stream(stream)))
+    return out
 
 
 def window_slot(r, sink_len, win_capacity):

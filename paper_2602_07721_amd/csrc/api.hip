@@ -667,6 +667,43 @@ int pariskv_window_attend(const pariskv_config* cfg, const void* q, const void* 
                        stream);
 }
 
+int pariskv_group_attend(const pariskv_config* cfg, const void* q, const void* K, const void* V,
+                         int32_t kv_host_mapped, int64_t kv_capacity, const int32_t* idx, int32_t k,
+                         int32_t batch, float scale, float* out, int32_t* union_rows, void* stream) {
+    prof_chain_start();
+    int rc = check_config(cfg, batch);
+    if (rc) return rc;
+    if (!q || !K || !V || !idx || !out)
+        return fail(PARISKV_ERR_INVALID, "q, K, V, idx and out must be non-NULL");
+    if (!aligned16(q) || !aligned16(K) || !aligned16(V) || !aligned16(out) ||
+        (reinterpret_cast<uintptr_t>(idx) & 3u) != 0 || (reinterpret_cast<uintptr_t>(union_rows) & 3u) != 0)
+        return fail(PARISKV_ERR_INVALID, "q, K, V, out must be 16-byte aligned, idx and union_rows 4-byte");
+    if (k < 1) return fail(PARISKV_ERR_INVALID, "k %d < 1", k);
+    const int64_t per = (int64_t)(cfg->q_per_kv < 4 ? cfg->q_per_kv : 4) * k;
+    if (per > kMaxAttendRows)
+        return fail(PARISKV_ERR_UNSUPPORTED, "min(G, 4) * k = %lld above %d", (long long)per, kMaxAttendRows);
+    if (kv_capacity < 1 || kv_capacity > kMaxKvRows)
+        return fail(PARISKV_ERR_INVALID, "kv_capacity %lld outside 1..2^30-1", (long long)kv_capacity);
+    if (kv_host_mapped != 0 && kv_host_mapped != 1)
+        return fail(PARISKV_ERR_INVALID, "kv_host_mapped must be 0 or 1");
+    if (!std::isfinite(scale)) return fail(PARISKV_ERR_INVALID, "scale is not finite");
+    const void* Kd = K;
+    const void* Vd = V;
+    if (kv_host_mapped) {
+        void* p = nullptr;
+        hipError_t e = hipHostGetDevicePointer(&p, const_cast<void*>(K), 0);
+        if (e != hipSuccess) return hip_fail(e, "hipHostGetDevicePointer(K)");
+        Kd = p;
+        e = hipHostGetDevicePointer(&p, const_cast<void*>(V), 0);
+        if (e != hipSuccess) return hip_fail(e, "hipHostGetDevicePointer(V)");
+        Vd = p;
+    }
+    hipError_t e = launch_group_attend(q, Kd, Vd, kv_capacity, idx, k, batch, cfg->n_kv_heads,
+                                       cfg->q_per_kv, scale, out, union_rows, static_cast<hipStream_t>(stream));
+    if (e != hipSuccess) return hip_fail(e, "group_attend launch");
+    return PARISKV_OK;
+}
+
 int pariskv_tiered_attend(const pariskv_config* cfg, const void* q, const void* K_win,
                           const void* V_win, int64_t win_capacity, const void* K, const void* V,
                           int32_t kv_host_mapped, int64_t kv_capacity, const int32_t* idx, int32_t k,

@@ -197,6 +197,13 @@ hipError_t launch_attend(const void* q, const void* K, const void* V, int64_t kv
 // Largest list (dense rows + retrieved rows) one attention block stages in LDS.
 constexpr int kMaxAttendRows = 4096;
 
+// Attention of each quad of query heads sharing a KV head over the union of
+// their (ascending) lists, every distinct row fetched once; min(G, 4) * k must
+// not exceed kMaxAttendRows.  union_rows (nullable): [batch][Hkv][quads] sizes.
+hipError_t launch_group_attend(const void* q, const void* K, const void* V, int64_t kv_capacity,
+                               const int32_t* idx, int32_t k, int32_t batch, int32_t hkv, int32_t g,
+                               float scale, float* out, int32_t* union_rows, hipStream_t s);
+
 // Kernel-level profiling hooks (no-ops unless enabled).
 // Event pair for one kernel launch when profiling is on (nulls otherwise), to be
 // passed to hipExtLaunchKernelGGL so the timestamps are the dispatch's own.

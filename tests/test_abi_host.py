@@ -334,3 +334,17 @@ def test_tiered_attend_and_offload_validation():
     assert off(t=-1) == pk.ERR_INVALID
     assert off(dcap=0) == pk.ERR_INVALID
     assert off(t=0) == pk.OK                                               # nothing to copy
+
+
+def test_group_attend_validation():
+    L = pk.lib()
+
+    def call(cfg, k=256, union=FAKE, cap=4096):
+        return L.pariskv_group_attend(cfg.c(), ctypes.c_void_p(FAKE), ctypes.c_void_p(FAKE), ctypes.c_void_p(FAKE), 0,
+                                      cap, ctypes.c_void_p(FAKE), k, 1, ctypes.c_float(0.1), ctypes.c_void_p(FAKE),
+                                      ctypes.c_void_p(union), None)
+    assert call(_cfg(), k=1025) == pk.ERR_UNSUPPORTED        # 4 heads x 1025 entries per quad
+    assert call(_cfg(q_per_kv=2), k=2049) == pk.ERR_UNSUPPORTED
+    assert call(_cfg(), k=0) == pk.ERR_INVALID
+    assert call(_cfg(), union=FAKE + 2) == pk.ERR_INVALID
+    assert call(_cfg(), cap=2 ** 30) == pk.ERR_INVALID

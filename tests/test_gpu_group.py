@@ -1,0 +1,85 @@
+"""GPU parity of the GQA-group attention (each distinct K/V row fetched once per KV head):
+every head's output against the float64 oracle over that head's own list, and the number
+of rows fetched against the union computed on the host."""
+
+import numpy as np
+import pytest
+import torch
+
+import paper_2602_07721_amd as pk
+import workloads
+from parity import check_attention
+
+pytestmark = pytest.mark.gpu
+
+SCALE = 1.0 / np.sqrt(128.0)
+
+
+def _lists(b, hkv, g, k, cap, overlap, seed):
+    """Ascending per-head lists with -1 padding at the end; heads of a KV head share a pool
+    of rows (overlap = share of each list drawn from the pool)."""
+    r = np.random.default_rng(seed)
+    idx = np.full((b, hkv * g, k), -1, dtype=np.int32)
+    for s in range(b):
+        for h in range(hkv):
+            pool = r.choice(cap, size=k, replace=False)
+            for j in range(g):
+                valid = int(r.integers(k // 2, k + 1))
+                shared = r.choice(pool, size=int(overlap * valid), replace=False)
+                rest = np.setdiff1d(np.arange(cap), shared)
+                own = r.choice(rest, size=valid - shared.size, replace=False)
+                idx[s, h * g + j, :valid] = np.sort(np.concatenate([shared, own]))
+    return idx
+
+
+@pytest.mark.parametrize("g,k,overlap,host", [(4, 256, 0.6, False), (4, 1024, 0.3, False), (1, 512, 0.0, False),
+                                              (3, 300, 0.9, False), (6, 128, 0.5, False), (4, 256, 0.6, True)],
+                         ids=["g4", "g4_k1024", "g1", "g3_odd_k", "g6_two_quads", "g4_host"])
+def test_group_attend_matches_the_oracle_per_head(g, k, overlap, host):
+    b, hkv, cap = 2, 2, 5000
+    print(f"[group_attend] g {g} k {k} overlap {overlap} host {host}", flush=True)
+    K = np.stack([np.stack([workloads.head_keys(51, s, h, cap) for h in range(hkv)]) for s in range(b)])
+    V = np.stack([np.stack([workloads.head_values(51, s, h, cap) for h in range(hkv)]) for s in range(b)])
+    Q = np.stack([np.concatenate([workloads.needle_queries(K[s, h], 51, s, h, g)[0] for h in range(hkv)])
+                  for s in range(b)])
+    idx = _lists(b, hkv, g, k, cap, overlap, seed=g * 1000 + k)
+    cfg = pk.Config(hkv, g, cap, workloads.rotation_signs(51))
+    Kt, Vt = torch.from_numpy(K), torch.from_numpy(V)
+    Kt, Vt = (Kt.pin_memory(), Vt.pin_memory()) if host else (Kt.cuda(), Vt.cuda())
+    quads = (g + 3) // 4
+    un = torch.zeros((b, hkv, quads), dtype=torch.int32, device="cuda")
+    out = pk.group_attend(cfg, torch.from_numpy(Q).cuda(), Kt, Vt, torch.from_numpy(idx).cuda(), SCALE,
+                          union_rows=un, kv_host_mapped=host)
+    out, un = out.cpu().numpy(), un.cpu().numpy()
+    for s in range(b):
+        for h in range(hkv):
+            for qd in range(quads):
+                heads = range(h * g + 4 * qd, h * g + min(g, 4 * qd + 4))
+                rows = set()
+                for hq in heads:
+                    rows |= set(int(x) for x in idx[s, hq] if x >= 0)
+                assert un[s, h, qd] == len(rows), (s, h, qd)
+            for j in range(g):
+                hq = h * g + j
+                check_attention(out[s, hq], Q[s, hq], K[s, h], V[s, h], idx[s, hq], SCALE)
+
+
+def test_group_attend_on_retrieval_output_and_empty_lists():
+    wc = workloads.Config("grp", batch=1, n_kv_heads=2, q_per_kv=4, n=6000, n_cand=512, n_collide=1024,
+                          top_k=128, seed=52)
+    K, V = workloads.layer_kv(wc)
+    Q, _ = workloads.layer_queries(wc, K)
+    cfg = pk.Config(2, 4, wc.n, workloads.rotation_signs(52))
+    Kd, Vd, Qd = (torch.from_numpy(x).cuda() for x in (K, V, Q))
+    index = pk.Index.empty(cfg, 1)
+    pk.encode(cfg, index, Kd)
+    idx, _, _ = pk.retrieve(cfg, index, Qd, wc.n, pk.Budget(512, 1024, 128))
+    # head 5's list emptied: it must come out as zeros
+    idx[0, 5] = -1
+    out = pk.group_attend(cfg, Qd, Kd, Vd, idx, SCALE).cpu().numpy()
+    ref = pk.sparse_attend(cfg, Qd, Kd, Vd, idx, SCALE).cpu().numpy()
+    ih = idx.cpu().numpy()
+    for hq in range(8):
+        check_attention(out[0, hq], Q[0, hq], K[0, hq // 4], V[0, hq // 4], ih[0, hq], SCALE)
+    assert not out[0, 5].any() and not ref[0, 5].any()
+    np.testing.assert_allclose(out, ref, rtol=0, atol=1e-5 * np.abs(ref).max())

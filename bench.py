@@ -57,8 +57,8 @@ def parse():
     ap.add_argument("--extras", action="store_true",
                     help="also measure the drift workload (append + retrieve + attend per step), the "
                          "same decode with Sink/Local/Update Buffer regions (buffer updates every 256 "
-                         "steps and every step), the recall of the ablation variants, and attention over "
-                         "K/V in pinned host memory")
+                         "steps and every step), the recall of the ablation variants, GQA-group "
+                         "de-duplication of the host-link fetch, and attention over K/V in pinned host memory")
     ap.add_argument("--drift-steps", type=int, default=4096,
                     help="decode steps of the drift measurement (the full workload runs 32768)")
     ap.add_argument("--offload-steps", type=int, default=0,
@@ -536,6 +536,74 @@ def offload_run(pk, torch, np, workloads, dev, steps, sink=128, local=512, m=256
     }
 
 
+def group_run(pk, torch, np, workloads, dev, drift_steps, reps=8):
+    """GQA-group de-duplication of the fetch over the host link: the drift workload's keys
+    (K/V in pinned host memory), top-256 retrieved per query head, then attention per head
+    (pariskv_sparse_attend) and per KV head over the union of its heads' lists
+    (pariskv_group_attend), for planted-needle queries (a different needle per head) and for
+    queries drawn from the key law (the heads of a group ask similar questions)."""
+    wc = workloads.CONFIGS["drift"]
+    signs = workloads.rotation_signs(wc.seed)
+    n = wc.n + drift_steps
+    K0, V0 = workloads.layer_kv(wc, threads=16)
+    K = np.zeros((wc.batch, wc.n_kv_heads, n, wc.head_dim), np.float16)
+    V = np.zeros_like(K)
+    K[:, :, :wc.n], V[:, :, :wc.n] = K0, V0
+    rng = np.random.default_rng(wc.seed)
+    for s in range(wc.batch):
+        for h in range(wc.n_kv_heads):
+            K[s, h, wc.n:] = workloads.drift_keys(wc.seed, s, h, 0, drift_steps, drift_steps)
+            V[s, h, wc.n:] = rng.standard_normal((drift_steps, wc.head_dim)).astype(np.float16)
+    Kd = torch.from_numpy(K).to(dev)
+    Kh, Vh = torch.from_numpy(K).pin_memory(), torch.from_numpy(V).pin_memory()
+    hq = wc.n_kv_heads * wc.q_per_kv
+    cfg = pk.Config(wc.n_kv_heads, wc.q_per_kv, n, signs)
+    index = pk.Index.empty(cfg, wc.batch, dev)
+    pk.encode(cfg, index, Kd)
+    C = -(-n // 16)
+    bud = pk.Budget(C, 2 * C, wc.top_k)
+    scale = 1.0 / np.sqrt(wc.head_dim)
+    queries = {
+        "needle queries (one needle per head)": workloads.layer_queries(wc, K)[0],
+        "queries from the key law": np.stack([np.stack([workloads.drift_queries(wc.seed, s, h, drift_steps,
+                                                                                wc.q_per_kv)[-1]
+                                                        for h in range(wc.n_kv_heads)])
+                                              for s in range(wc.batch)]).reshape(wc.batch, hq, wc.head_dim),
+    }
+    out = torch.empty((wc.batch, hq, wc.head_dim), dtype=torch.float32, device=dev)
+    un = torch.zeros((wc.batch, wc.n_kv_heads, 1), dtype=torch.int32, device=dev)
+    res = {}
+    for name, Q in queries.items():
+        Qd = torch.from_numpy(Q).to(dev)
+        idx, _, _ = pk.retrieve(cfg, index, Qd, n, bud)
+        rows = int((idx >= 0).sum().item())
+        times = {}
+        for label, fn in (("per_head", lambda: pk.sparse_attend(cfg, Qd, Kh, Vh, idx, scale, out=out,
+                                                               kv_host_mapped=True)),
+                          ("group", lambda: pk.group_attend(cfg, Qd, Kh, Vh, idx, scale, out=out, union_rows=un,
+                                                            kv_host_mapped=True))):
+            fn()
+            torch.cuda.synchronize()
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record()
+            for _ in range(reps):
+                fn()
+            e1.record()
+            torch.cuda.synchronize()
+            times[label] = e0.elapsed_time(e1) * 1e3 / reps
+        urows = int(un.sum().item())
+        row_b = 2 * wc.head_dim * 2
+        res[name] = {"rows_per_head_lists": rows, "rows_fetched_by_group": urows,
+                     "fetch_ratio": round(urows / rows, 4),
+                     "us_per_head_attend": round(times["per_head"], 1),
+                     "us_group_attend": round(times["group"], 1),
+                     "host_link_GBps_per_head": round(rows * row_b / (times["per_head"] * 1e-6) / 1e9, 2),
+                     "host_link_GBps_group": round(urows * row_b / (times["group"] * 1e-6) / 1e9, 2)}
+    return {"workload": (f"drift keys ({wc.batch} seqs x {wc.n_kv_heads} KV heads x {wc.q_per_kv} query heads, "
+                         f"n = {n}), K/V in pinned host memory, top-{wc.top_k} per head from C = {C}"),
+            **res}
+
+
 def host_link_run(pk, torch, np, cfg, K, V, Qd, idx_list, scale, dev, reps=8):
     """Sparse attention with K/V in pinned host memory, read through host-mapped pointers."""
     Kh = torch.from_numpy(K).pin_memory()
@@ -728,6 +796,8 @@ def main():
         extras["window"] = window_run(pk, torch, np, workloads, dev, args.drift_steps)
         torch.cuda.empty_cache()
         extras["ablation"] = ablation_run(pk, torch, np, workloads, dev, args.drift_steps)
+        torch.cuda.empty_cache()
+        extras["group_dedup"] = group_run(pk, torch, np, workloads, dev, args.drift_steps)
     if args.offload_steps > 0:
         torch.cuda.empty_cache()
         extras["offload"] = offload_run(pk, torch, np, workloads, dev, args.offload_steps)

@@ -22,7 +22,10 @@
 //                      bytes per wave store) and a suffix histogram
 //                      #{S >= v} per head and 4096-key chunk (score 1 counted
 //                      in per-lane registers, higher scores by LDS atomics into
-//                      four lane-partitioned copies).
+//                      two lane-partitioned copies).  Loads and stores go
+//                      through range-checked buffer descriptors, so the ragged
+//                      last chunk needs no branches, and each XCD scans whole
+//                      score rows.
 //   threshold_kernel   one block of 16 waves per query head: theta = largest v
 //                      with #{S >= v} >= C_eff, the quota of S == theta keys,
 //                      and per chunk the number of S > theta / S == theta keys
@@ -206,13 +209,15 @@ constexpr int kColThreads = 256;
 constexpr int kColWaves = kColThreads / 64;
 constexpr int kColKeysPerIter = 4 * kColThreads;  // 4 keys per thread per iteration
 constexpr int kLowCut = 2;  // scores below this are counted in registers, not by LDS atomics
-// Scores >= kLowCut go to one of 4 histogram copies picked by lane & 3 (fewer
-// same-address atomics per instruction), 16-bit counters (a copy sees at most
-// 1024 keys per chunk): value v sits in word (v - kLowCut) mod kHistWords, low
-// half below kLowCut + kHistWords, high half above.
-constexpr int kHistCopies = 4;
-constexpr int kHistWords = 50;
-static_assert(kMaxScore - kLowCut < 2 * kHistWords, "histogram halves");
+// Scores >= kLowCut go to one of two histogram copies picked by lane & 1 (fewer
+// same-address atomics per instruction), one 32-bit counter per (copy, head, value).
+constexpr int kHistCopies = 2;
+constexpr int kHistStride = 100;  // counters per (copy, head): values 0 .. kMaxScore
+static_assert(kMaxScore < kHistStride, "histogram row");
+// Word 3 of a gfx9 buffer descriptor for raw (untyped, unswizzled) access.
+constexpr int kRawBufferWord3 = 0x00020000;
+// A buffer offset past every range: the access is dropped (stores) or reads 0 (loads).
+constexpr uint32_t kOffsetOutOfRange = 0x80000000u;
 
 // Suffix sums of a 97-bin histogram held as (lo = bins 0..63 by lane, hi = bins
 // 64..96 by lane < 33): returns (sfx_lo, sfx_hi) with sfx[v] = sum_{u >= v} h[u].
@@ -235,14 +240,25 @@ __device__ __forceinline__ void wave_suffix97(uint32_t lo, uint32_t hi, int lane
 
 __global__ __launch_bounds__(kColThreads) void collide_kernel(RetrieveArgs a) {
     __shared__ uint32_t s_lut[kB * kCentroids];
-    __shared__ uint32_t s_hist[kHistCopies][4][kHistWords];
+    __shared__ uint32_t s_hist[kHistCopies * 4 * kHistStride];
     __shared__ uint32_t s_low[kColWaves][kLowCut - 1][4];
 
     const int tid = threadIdx.x;
     const int lane = tid & 63;
     const int wave = tid >> 6;
-    const int64_t chunk = blockIdx.x;
-    const int64_t gq = blockIdx.y;             // (seq * hkv + kvh) * quads + quad
+    // Workgroups go to the 8 XCDs round-robin in dispatch order L.  When the rows split
+    // evenly, XCD x scans every chunk of the rows gq = x (mod 8): a row's chunks and its
+    // bonus table stay in one L2, and each XCD's id rows are spread over the whole array
+    // (measured faster than giving each XCD a contiguous eighth of it).
+    const uint32_t nx = gridDim.x;
+    const uint32_t L = blockIdx.y * nx + blockIdx.x;
+    int64_t chunk = blockIdx.x;
+    int64_t gq = blockIdx.y;                   // (seq * hkv + kvh) * quads + quad
+    if ((gridDim.y & 7u) == 0) {
+        const uint32_t slot = L >> 3;
+        chunk = slot % nx;
+        gq = (L & 7u) + 8u * (slot / nx);
+    }
     const int quad = (int)(gq % a.quads);
     const int64_t grp = gq / a.quads;          // seq * hkv + kvh
     const int seq = (int)(grp / a.hkv);
@@ -253,32 +269,39 @@ __global__ __launch_bounds__(kColThreads) void collide_kernel(RetrieveArgs a) {
     const uint4* lsrc = reinterpret_cast<const uint4*>(a.lut + gq * (kB * kCentroids));
     for (int i = tid; i < kB * kCentroids / 4; i += kColThreads)
         reinterpret_cast<uint4*>(s_lut)[i] = lsrc[i];
-    for (int i = tid; i < kHistCopies * 4 * kHistWords; i += kColThreads) (&s_hist[0][0][0])[i] = 0;
+    for (int i = tid; i < kHistCopies * 4 * kHistStride; i += kColThreads) s_hist[i] = 0;
     __syncthreads();
 
-    const uint8_t* ids = a.ids + grp * a.capacity * kB;
     const int64_t c0 = chunk * kChunk;
     const int64_t c1 = min(c0 + (int64_t)kChunk, a.n);
+    const uint32_t nkeys = (uint32_t)(c1 - c0);
     // Per-lane SWAR counters: byte h of cnt[v-1] = #{keys of this lane with S_h >= v}
     // for v = 1 .. kLowCut-1 (a lane sees at most kChunk / kColThreads = 16 keys).
     uint32_t cnt[kLowCut - 1];
 #pragma unroll
     for (int v = 0; v < kLowCut - 1; ++v) cnt[v] = 0;
 
-    // 32-bit key offsets from block-uniform bases, so loads and stores use a scalar
-    // base address plus one vector offset.
-    const uint8_t* idc = ids + c0 * kB;
-    const uint32_t nkeys = (uint32_t)(c1 - c0);
-    uint8_t* sbase[4];
+    // Buffer descriptors over the chunk: the id rows (nkeys x 16 bytes) and each head's
+    // score bytes (nkeys, or none for a slot past the quad's last head).  The whole
+    // offset goes in the VGPR operand, which the range check covers, so keys past the
+    // chunk read 0 and store nothing without a branch.
+    const __amdgpu_buffer_rsrc_t rid = __builtin_amdgcn_make_buffer_rsrc(
+        const_cast<uint8_t*>(a.ids + (grp * a.capacity + c0) * kB), 0, (int)(nkeys * kB), kRawBufferWord3);
+    __amdgpu_buffer_rsrc_t rsc[4];
 #pragma unroll
-    for (int h = 0; h < 4; ++h) sbase[h] = a.score8 + (row0 + min(h, nh - 1)) * a.n_pad + c0;
+    for (int h = 0; h < 4; ++h)
+        rsc[h] = __builtin_amdgcn_make_buffer_rsrc(a.score8 + (row0 + min(h, nh - 1)) * a.n_pad + c0, 0,
+                                                   h < nh ? (int)nkeys : 0, kRawBufferWord3);
+    uint32_t* hcopy = s_hist + (lane & (kHistCopies - 1)) * (4 * kHistStride);
+
     for (uint32_t base = 0; base < nkeys; base += kColKeysPerIter) {
         // Key base + tid + 256 j: one 16-byte id row per lane, a wave reads 1 KiB contiguous.
         uint4 w[4];
 #pragma unroll
         for (int j = 0; j < 4; ++j) {
-            const uint32_t i = base + tid + kColThreads * j;
-            w[j] = i < nkeys ? *reinterpret_cast<const uint4*>(idc + i * kB) : make_uint4(0, 0, 0, 0);
+            typedef unsigned int v4u __attribute__((ext_vector_type(4)));
+            const v4u t = __builtin_amdgcn_raw_buffer_load_b128(rid, (int)((base + tid + kColThreads * j) * kB), 0, 0);
+            w[j] = make_uint4(t.x, t.y, t.z, t.w);
         }
 #pragma unroll
         for (int j = 0; j < 4; ++j) {
@@ -302,19 +325,13 @@ __global__ __launch_bounds__(kColThreads) void collide_kernel(RetrieveArgs a) {
 #pragma unroll
             for (int h = 0; h < 4; ++h) {
                 const uint32_t sh = (acc >> (8 * h)) & 0xffu;
-                if (sh >= (uint32_t)kLowCut) {
-                    const uint32_t idx = sh - kLowCut;
-                    const bool upper = idx >= (uint32_t)kHistWords;
-                    atomicAdd(&s_hist[lane & (kHistCopies - 1)][h][upper ? idx - kHistWords : idx],
-                              upper ? 0x10000u : 1u);
-                }
+                if (sh >= (uint32_t)kLowCut) atomicAdd(hcopy + h * kHistStride + sh, 1u);
             }
             // A wave stores 64 consecutive score bytes of a head per instruction.
-            if (live) {
+            const uint32_t off = live ? i : kOffsetOutOfRange;
 #pragma unroll
-                for (int h = 0; h < 4; ++h)
-                    if (h < nh) sbase[h][i] = (uint8_t)(acc >> (8 * h));
-            }
+            for (int h = 0; h < 4; ++h)
+                __builtin_amdgcn_raw_buffer_store_b8((uint8_t)(acc >> (8 * h)), rsc[h], (int)off, 0, 0);
         }
     }
 
@@ -343,12 +360,9 @@ __global__ __launch_bounds__(kColThreads) void collide_kernel(RetrieveArgs a) {
         // Exact count of each value v >= kLowCut: lane holds v = lane and v = 64 + lane.
         auto count_of = [&](int v) -> uint32_t {
             if (v < kLowCut || v > kMaxScore) return 0u;
-            const int idx = v - kLowCut;
-            const int w = idx < kHistWords ? idx : idx - kHistWords;
-            const int sh = idx < kHistWords ? 0 : 16;
             uint32_t t = 0;
 #pragma unroll
-            for (int c = 0; c < kHistCopies; ++c) t += (s_hist[c][h][w] >> sh) & 0xffffu;
+            for (int c = 0; c < kHistCopies; ++c) t += s_hist[(c * 4 + h) * kHistStride + v];
             return t;
         };
         const uint32_t lo = count_of(lane);

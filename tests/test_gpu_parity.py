@@ -83,6 +83,10 @@ EDGE = [
     ("huge_C", 1, 1, 1, 70000, (40000, 60000, 2048)),
     ("C_20000", 1, 1, 2, 40000, (20000, 30000, 1000)),      # top-k staging 32 keys per thread
     ("many_chunks", 1, 1, 1, 300000, (4096, 8192, 256)),    # 74 chunks: multi-wave chunk prefix
+    # score rows a multiple of 8 (the scan spreads rows over XCDs) with a ragged last chunk
+    ("rows8_ragged", 1, 8, 4, 5000, (512, 1024, 64)),
+    ("rows8_two_quads_ragged", 1, 4, 8, 4099, (300, 700, 40)),
+    ("rows16_one_chunk", 2, 8, 3, 100, (64, 80, 16)),
 ]
 
 

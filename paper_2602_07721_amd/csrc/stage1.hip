@@ -9,7 +9,8 @@
 //                      wave per (head slot, subspace): z = H(s q) in exact
 //                      float64 (written as z/D float for the rerank), the 256
 //                      centroids ranked by the exact proxy sum_j +-z_j (ties:
-//                      lower id) with a 64-bit bitonic sort held in registers,
+//                      lower id) by a 64-bit bitonic sort of the 128 with bit 7
+//                      clear and a merge with their complements, in registers,
 //                      cluster counts prefix-summed in that order, and the tier
 //                      bonus of each cluster placed in byte `slot` of a packed
 //                      word (4 query heads of a KV head share one uint32) at the
@@ -53,56 +54,92 @@ __device__ __forceinline__ uint32_t wave_incl_scan_u32(uint32_t v, int lane) {
     return v;
 }
 
-// Bitonic sort of 256 int64 keys held 4 per lane (element e = 4 lane + r), descending.
+// Ranking the 256 centroids of a subspace.  Flipping every sign of a centroid
+// negates its proxy, so once the 128 centroids with bit 7 clear are sorted, the
+// other 128 (their complements c ^ 255, keys from the same values) come in the
+// reverse order, and the two halves form one bitonic sequence: a 128-key sort
+// and one bitonic merge replace a 256-key sort (22 stages' worth of
+// compare-exchanges on 2 or 4 keys per lane instead of 36 on 4).
+//
 // Each compare-exchange is one 64-bit compare into a lane mask, a scalar XOR with
 // the stage's direction pattern, and two v_cndmask; partners 1 or 2 lanes away come
 // through DPP, 4..16 lanes away through ds_swizzle, 32 away through ds_bpermute.
 
-// Lanes whose bit t-2 is set (bit t of e = 4 lane + r for t >= 2); 0 past bit 7.
-__device__ constexpr uint64_t lane_bit_mask(int t) {
-    return t == 2 ? 0xAAAAAAAAAAAAAAAAull : t == 3 ? 0xCCCCCCCCCCCCCCCCull
-         : t == 4 ? 0xF0F0F0F0F0F0F0F0ull : t == 5 ? 0xFF00FF00FF00FF00ull
-         : t == 6 ? 0xFFFF0000FFFF0000ull : t == 7 ? 0xFFFFFFFF00000000ull : 0ull;
+// Lanes whose bit t is set (t = 0 .. 5); 0 past bit 5.
+__device__ constexpr uint64_t lane_bit(int t) {
+    return t == 0 ? 0xAAAAAAAAAAAAAAAAull : t == 1 ? 0xCCCCCCCCCCCCCCCCull
+         : t == 2 ? 0xF0F0F0F0F0F0F0F0ull : t == 3 ? 0xFF00FF00FF00FF00ull
+         : t == 4 ? 0xFFFF0000FFFF0000ull : t == 5 ? 0xFFFFFFFF00000000ull : 0ull;
 }
 
 __device__ constexpr int log2i(int x) { return x <= 1 ? 0 : 1 + log2i(x >> 1); }
 
-__device__ __forceinline__ void sort256_desc(int64_t (&key)[4], int lane) {
+// Key a takes its partner's key b iff (b > a) == keep_max, lane by lane.
+__device__ __forceinline__ int64_t exchange(int64_t a, uint32_t blo, uint32_t bhi, uint64_t keep_max) {
+    const int64_t b = (int64_t)(((uint64_t)bhi << 32) | blo);
+    const uint64_t take = ~(__ballot(b > a) ^ keep_max);  // keys are distinct
+    const uint32_t alo = (uint32_t)a, ahi = (uint32_t)((uint64_t)a >> 32);
+    return (int64_t)(((uint64_t)select_mask(take, bhi, ahi) << 32) | select_mask(take, blo, alo));
+}
+
+// In-lane pair (x, y): afterwards x >= y on lanes in desc, x <= y elsewhere.
+__device__ __forceinline__ void order_pair(int64_t& x, int64_t& y, uint64_t desc) {
+    const uint64_t swap = ~(__ballot(x < y) ^ desc);
+    const uint32_t xl = (uint32_t)x, xh = (uint32_t)((uint64_t)x >> 32);
+    const uint32_t yl = (uint32_t)y, yh = (uint32_t)((uint64_t)y >> 32);
+    x = (int64_t)(((uint64_t)select_mask(swap, yh, xh) << 32) | select_mask(swap, yl, xl));
+    y = (int64_t)(((uint64_t)select_mask(swap, xh, yh) << 32) | select_mask(swap, xl, yl));
+}
+
+// Bitonic sort of the 128 keys key[0..1] of every lane (element e = 2 lane + r),
+// descending.  Bit b >= 1 of e is bit b - 1 of the lane.
+__device__ __forceinline__ void sort128_desc(int64_t (&key)[4], int lane) {
 #pragma unroll
-    for (int k = 2; k <= 256; k <<= 1) {
+    for (int k = 2; k <= 128; k <<= 1) {
 #pragma unroll
         for (int j = k >> 1; j > 0; j >>= 1) {
-            if (j >= 4) {
+            if (j >= 2) {
                 // Element e keeps the larger key iff bits log2 j and log2 k of e agree.
-                const uint64_t keep_max = ~(lane_bit_mask(log2i(j)) ^ lane_bit_mask(log2i(k)));
+                const uint64_t keep_max = ~(lane_bit(log2i(j) - 1) ^ lane_bit(log2i(k) - 1));
 #pragma unroll
-                for (int r = 0; r < 4; ++r) {
+                for (int r = 0; r < 2; ++r) {
                     const uint32_t lo = (uint32_t)key[r], hi = (uint32_t)((uint64_t)key[r] >> 32);
-                    const uint32_t olo = lane_xor(lo, j >> 2, lane), ohi = lane_xor(hi, j >> 2, lane);
-                    const int64_t other = (int64_t)(((uint64_t)ohi << 32) | olo);
-                    // Keys are distinct: take the partner's key iff (other > key) == keep_max.
-                    const uint64_t take = ~(__ballot(other > key[r]) ^ keep_max);
-                    key[r] = (int64_t)(((uint64_t)select_mask(take, ohi, hi) << 32) |
-                                       select_mask(take, olo, lo));
+                    key[r] = exchange(key[r], lane_xor(lo, j >> 1, lane), lane_xor(hi, j >> 1, lane), keep_max);
                 }
             } else {
-#pragma unroll
-                for (int r = 0; r < 4; ++r) {
-                    if (r & j) continue;
-                    const int r2 = r | j;
-                    // Descending where bit log2 k of e is clear (k = 2: bit 1 of r).
-                    const uint64_t desc = k == 2 ? ((r & 2) ? 0ull : ~0ull) : ~lane_bit_mask(log2i(k));
-                    const uint64_t swap = ~(__ballot(key[r] < key[r2]) ^ desc);
-                    const uint32_t lo0 = (uint32_t)key[r], hi0 = (uint32_t)((uint64_t)key[r] >> 32);
-                    const uint32_t lo1 = (uint32_t)key[r2], hi1 = (uint32_t)((uint64_t)key[r2] >> 32);
-                    key[r] = (int64_t)(((uint64_t)select_mask(swap, hi1, hi0) << 32) |
-                                       select_mask(swap, lo1, lo0));
-                    key[r2] = (int64_t)(((uint64_t)select_mask(swap, hi0, hi1) << 32) |
-                                        select_mask(swap, lo0, lo1));
-                }
+                // Descending where bit log2 k of e is clear.
+                order_pair(key[0], key[1], ~lane_bit(log2i(k) - 1));
             }
         }
     }
+}
+
+// The key of centroid c ^ 255 from the key of c: proxy negated, id complemented
+// (keys are proxy * 256 + (255 - id)).
+__device__ __forceinline__ int64_t complement_key(int64_t k) {
+    const int64_t low = k & 255;
+    return -(k >> 8) * 256 + (255 - low);
+}
+
+// key[0..1] hold the sorted first half (positions 2 lane + r), key[2..3] get the
+// complements (positions 128 + 2 lane + r - 2, ascending); the bitonic merge leaves
+// all 256 keys descending in those positions.
+__device__ __forceinline__ void merge_complements_desc(int64_t (&key)[4], int lane) {
+    key[2] = complement_key(key[0]);
+    key[3] = complement_key(key[1]);
+    order_pair(key[0], key[2], ~0ull);  // j = 128: the half below keeps the larger key
+    order_pair(key[1], key[3], ~0ull);
+#pragma unroll
+    for (int j = 64; j >= 2; j >>= 1) {
+        const uint64_t keep_max = ~lane_bit(log2i(j) - 1);  // position bit log2 j clear
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+            const uint32_t lo = (uint32_t)key[r], hi = (uint32_t)((uint64_t)key[r] >> 32);
+            key[r] = exchange(key[r], lane_xor(lo, j >> 1, lane), lane_xor(hi, j >> 1, lane), keep_max);
+        }
+    }
+    order_pair(key[0], key[1], ~0ull);  // j = 1
+    order_pair(key[2], key[3], ~0ull);
 }
 
 // ---------------------------------------------------------------- query + LUT
@@ -164,8 +201,8 @@ __global__ __launch_bounds__(kLutThreads) void query_lut_kernel(RetrieveArgs a) 
         for (int j = 0; j < 8; ++j) zb[j] = s_z[slot][8 * b + j];
         int64_t key[4];
 #pragma unroll
-        for (int r = 0; r < 4; ++r) {
-            const int c = 4 * lane + r;
+        for (int r = 0; r < 2; ++r) {
+            const int c = 2 * lane + r;  // the centroids with bit 7 clear
             double p = 0.0;
 #pragma unroll
             for (int j = 0; j < 8; ++j) p = ((c >> j) & 1) ? __dsub_rn(p, zb[j]) : __dadd_rn(p, zb[j]);
@@ -173,8 +210,10 @@ __global__ __launch_bounds__(kLutThreads) void query_lut_kernel(RetrieveArgs a) 
             const int64_t pi = (int64_t)(p * 16777216.0);
             key[r] = pi * 256 + (255 - c);  // descending key: proxy desc, then id asc
         }
-        sort256_desc(key, lane);
-        // Exclusive prefix of cluster counts in rank order -> start rank P(c).
+        sort128_desc(key, lane);
+        merge_complements_desc(key, lane);
+        // Exclusive prefix of cluster counts in rank order -> start rank P(c).  Ranks
+        // 2 lane + r (r = 0, 1) and 128 + 2 lane + r - 2 (r = 2, 3).
         uint32_t cc[4];
         int cid[4];
 #pragma unroll
@@ -182,11 +221,18 @@ __global__ __launch_bounds__(kLutThreads) void query_lut_kernel(RetrieveArgs a) 
             cid[r] = 255 - (int)(key[r] & 255);
             cc[r] = s_cnt[sub][cid[r]];
         }
-        const uint32_t tot = cc[0] + cc[1] + cc[2] + cc[3];
-        const uint32_t incl = wave_incl_scan_u32(tot, lane);
-        uint32_t start = incl - tot;
+        const uint32_t t0 = cc[0] + cc[1], t1 = cc[2] + cc[3];
+        const uint32_t incl0 = wave_incl_scan_u32(t0, lane);
+        const uint32_t incl1 = wave_incl_scan_u32(t1, lane);
+        const uint32_t half = __shfl(incl0, 63, 64);  // counts of the first 128 ranks
+        uint32_t starts[4];
+        starts[0] = incl0 - t0;
+        starts[1] = starts[0] + cc[0];
+        starts[2] = half + incl1 - t1;
+        starts[3] = starts[2] + cc[2];
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
+            const uint32_t start = starts[r];
             uint32_t bonus = 0;
 #pragma unroll
             for (int l = kTierCount - 1; l >= 0; --l)
@@ -195,7 +241,6 @@ __global__ __launch_bounds__(kLutThreads) void query_lut_kernel(RetrieveArgs a) 
             if (a.flags & kFlagBinary) bonus = bonus ? 1u : 0u;
             // The table is indexed like the stored ids, by slot.
             if (bonus) atomicOr(&s_lut[sub][id_slot((uint32_t)cid[r])], bonus << (8 * slot));
-            start += cc[r];
         }
     }
     __syncthreads();

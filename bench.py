@@ -57,7 +57,8 @@ def parse():
     ap.add_argument("--extras", action="store_true",
                     help="also measure the drift workload (append + retrieve + attend per step), the "
                          "same decode with Sink/Local/Update Buffer regions (buffer updates every 256 "
-                         "steps and every step), the recall of the ablation variants, GQA-group "
+                         "steps and every step), the recall of the ablation variants, the candidate ratio "
+                         "needed at each KV length, GQA-group "
                          "de-duplication of the host-link fetch, and attention over K/V in pinned host memory")
     ap.add_argument("--drift-steps", type=int, default=4096,
                     help="decode steps of the drift measurement (the full workload runs 32768)")
@@ -413,6 +414,63 @@ def ablation_run(pk, torch, np, workloads, dev, drift_steps, n_queries=8):
                      "inner products"),
         "note": "quality figures on synthetic keys (the paper's recall is on real model keys): parity unpinned",
         "variants": out,
+    }
+
+
+def beta_length_run(pk, torch, np, workloads, dev, lengths=(4096, 16384, 65536, 131072),
+                    betas=(1 / 64, 1 / 32, 3 / 64, 1 / 16, 3 / 32, 1 / 8, 3 / 16, 1 / 4), k=100, n_queries=8,
+                    target=0.9):
+    """Candidate ratio needed at each KV length (Sec. "Top-beta selection"; the paper reads that
+    with k fixed, short caches need a larger beta and long ones allow a smaller one): the keys
+    of 2 sequences x 8 KV heads (the prefill law of the drift workload, no drift), prefixes of
+    each length, `n_queries` draws per query head from the key law; recall@k of the published
+    method against exact top-k, for each beta (C = max(ceil(beta n), k), C_rho = 2C)."""
+    wc = workloads.CONFIGS["drift"]
+    batch = 2
+    signs = workloads.rotation_signs(wc.seed)
+    nmax = max(lengths)
+    K = np.stack([np.stack([workloads.head_keys(wc.seed, s, h, nmax) for h in range(wc.n_kv_heads)])
+                  for s in range(batch)])
+    Kfull = torch.from_numpy(K).to(dev)
+    hq = wc.n_kv_heads * wc.q_per_kv
+    Q = np.stack([np.stack([workloads.drift_query(wc.seed, s, h, 0, 1, n_queries * wc.q_per_kv)
+                            .reshape(n_queries, wc.q_per_kv, wc.head_dim) for h in range(wc.n_kv_heads)], axis=1)
+                  for s in range(batch)], axis=1)  # [n_queries][b][Hkv][G][D]
+    Qd = torch.from_numpy(Q.reshape(n_queries, batch, hq, wc.head_dim)).to(dev)
+    rows = []
+    for n in lengths:
+        Kd = Kfull[:, :, :n].contiguous()
+        exact = []
+        for i in range(n_queries):
+            q = Qd[i].float().reshape(batch, wc.n_kv_heads, wc.q_per_kv, wc.head_dim)
+            sc = torch.matmul(q, Kd.float().transpose(2, 3).contiguous())
+            exact.append(torch.topk(sc, k, dim=-1).indices.reshape(batch, hq, k))
+            del sc
+        cfg = pk.Config(wc.n_kv_heads, wc.q_per_kv, n, signs)
+        index = pk.Index.empty(cfg, batch, dev)
+        pk.encode(cfg, index, Kd)
+        rec = {}
+        for beta in betas:
+            C = min(max(-(-n * beta // 1), k), n)
+            C = int(C)
+            bud = pk.Budget(C, min(2 * C, n), k)
+            ws = torch.empty(pk.retrieve_workspace_size(cfg, batch, n, bud), dtype=torch.uint8, device=dev)
+            hits = []
+            for i in range(n_queries):
+                idx, _, _ = pk.retrieve(cfg, index, Qd[i], n, bud, workspace=ws)
+                hits.append((exact[i].unsqueeze(-1) == idx.long().unsqueeze(-2)).any(-1).float().mean().item())
+            rec[f"{beta:.4f}"] = {"C": C, "recall_at_k": round(float(np.mean(hits)), 4)}
+        ok = [b for b in betas if rec[f"{b:.4f}"]["recall_at_k"] >= target]
+        rows.append({"n": n, "recall_by_beta": rec,
+                     f"smallest_beta_for_recall_{target}": round(min(ok), 4) if ok else None})
+        del Kd, index
+        torch.cuda.empty_cache()
+    return {
+        "workload": (f"{batch} seqs x {wc.n_kv_heads} KV heads x {wc.q_per_kv} query heads, prefill-law keys "
+                     f"(prefixes of {nmax}), {n_queries} query draws per head from the key law; k = {k}, "
+                     "C = max(ceil(beta n), k), C_rho = 2C; exact top-k by float32 inner products"),
+        "note": "quality figures on synthetic keys (the paper's figure is on real model keys): parity unpinned",
+        "lengths": rows,
     }
 
 
@@ -796,6 +854,8 @@ def main():
         extras["window"] = window_run(pk, torch, np, workloads, dev, args.drift_steps)
         torch.cuda.empty_cache()
         extras["ablation"] = ablation_run(pk, torch, np, workloads, dev, args.drift_steps)
+        torch.cuda.empty_cache()
+        extras["beta_vs_length"] = beta_length_run(pk, torch, np, workloads, dev)
         torch.cuda.empty_cache()
         extras["group_dedup"] = group_run(pk, torch, np, workloads, dev, args.drift_steps)
     if args.offload_steps > 0:

@@ -119,6 +119,23 @@ def test_degenerate_keys_and_queries():
     _full_check(wc, K, V, Q, signs, pk.Budget(300, 600, 40))
 
 
+def test_keys_spanning_the_float16_range():
+    # Key coordinates from the subnormals to 65504 in one key: the float64 transform,
+    # codes, weights and collision scores must still match the oracle bit for bit.
+    wc = workloads.Config("wide_range", batch=1, n_kv_heads=2, q_per_kv=4, n=2500, n_cand=250,
+                          n_collide=500, top_k=32, seed=91)
+    rng = np.random.default_rng(91)
+    K = rng.standard_normal((1, 2, wc.n, 128)) * np.exp2(rng.integers(-26, 16, size=(1, 2, wc.n, 128)))
+    K = np.clip(K, -65504.0, 65504.0).astype(np.float16)
+    K[0, 0, :50] = np.float16(65504.0)      # the largest finite value in every coordinate
+    K[0, 1, :50] = np.float16(2.0 ** -24)   # the smallest subnormal
+    V = rng.standard_normal((1, 2, wc.n, 128)).astype(np.float16)
+    Q = rng.standard_normal((1, 8, 128)).astype(np.float16)
+    signs = workloads.rotation_signs(wc.seed)
+    print("case wide_range", flush=True)
+    _full_check(wc, K, V, Q, signs, pk.Budget(250, 500, 32), attention=False)
+
+
 def test_full_budget_reproduces_full_attention():
     # C = n and k = n: every key is selected, so the sparse output is full attention.
     wc = workloads.Config("full", batch=1, n_kv_heads=2, q_per_kv=4, n=512, n_cand=512,

@@ -291,15 +291,17 @@ __global__ __launch_bounds__(kColThreads) void collide_kernel(RetrieveArgs a) {
     const int tid = threadIdx.x;
     const int lane = tid & 63;
     const int wave = tid >> 6;
-    // Workgroups go to the 8 XCDs round-robin in dispatch order L.  When the rows split
-    // evenly, XCD x scans every chunk of the rows gq = x (mod 8): a row's chunks and its
-    // bonus table stay in one L2, and each XCD's id rows are spread over the whole array
-    // (measured faster than giving each XCD a contiguous eighth of it).
+    // Workgroups go to the 8 XCDs round-robin in dispatch order L.  With at least 4 rows
+    // per XCD, XCD x scans every chunk of the rows gq = x (mod 8): a row's chunks and its
+    // bonus table stay in one L2, and each XCD's id rows are still spread over the whole
+    // array.  With fewer rows the plain order (XCD = chunk mod 8) keeps that spread; one
+    // row per XCD, a contiguous stretch of ids, measured slower, as did giving each XCD a
+    // contiguous eighth of a larger array.
     const uint32_t nx = gridDim.x;
     const uint32_t L = blockIdx.y * nx + blockIdx.x;
     int64_t chunk = blockIdx.x;
     int64_t gq = blockIdx.y;                   // (seq * hkv + kvh) * quads + quad
-    if ((gridDim.y & 7u) == 0) {
+    if ((gridDim.y & 7u) == 0 && gridDim.y >= 32) {
         const uint32_t slot = L >> 3;
         chunk = slot % nx;
         gq = (L & 7u) + 8u * (slot / nx);

@@ -21,9 +21,8 @@
 //                      the 4 bytes of one uint32; each is at most 96, so no
 //                      carries), writes S as bytes per head (64 consecutive
 //                      bytes per wave store) and a suffix histogram
-//                      #{S >= v} per head and 4096-key chunk (score 1 counted
-//                      in per-lane registers, higher scores by LDS atomics into
-//                      two lane-partitioned copies).  Loads and stores go
+//                      #{S >= v} per head and 4096-key chunk (nonzero scores
+//                      by LDS atomics into two lane-partitioned copies).  Loads and stores go
 //                      through range-checked buffer descriptors, so the ragged
 //                      last chunk needs no branches, and each XCD scans whole
 //                      score rows.
@@ -251,11 +250,10 @@ __global__ __launch_bounds__(kLutThreads) void query_lut_kernel(RetrieveArgs a) 
 // ---------------------------------------------------------------- collision scan
 
 constexpr int kColThreads = 256;
-constexpr int kColWaves = kColThreads / 64;
 constexpr int kColKeysPerIter = 4 * kColThreads;  // 4 keys per thread per iteration
-constexpr int kLowCut = 2;  // scores below this are counted in registers, not by LDS atomics
-// Scores >= kLowCut go to one of two histogram copies picked by lane & 1 (fewer
-// same-address atomics per instruction), one 32-bit counter per (copy, head, value).
+// Scores >= 1 go to one of two histogram copies picked by lane & 1 (fewer
+// same-address atomics per instruction), one 32-bit counter per (copy, head, value);
+// #{S >= 0} is the chunk's key count.
 constexpr int kHistCopies = 2;
 constexpr int kHistStride = 100;  // counters per (copy, head): values 0 .. kMaxScore
 static_assert(kMaxScore < kHistStride, "histogram row");
@@ -286,7 +284,6 @@ __device__ __forceinline__ void wave_suffix97(uint32_t lo, uint32_t hi, int lane
 __global__ __launch_bounds__(kColThreads) void collide_kernel(RetrieveArgs a) {
     __shared__ uint32_t s_lut[kB * kCentroids];
     __shared__ uint32_t s_hist[kHistCopies * 4 * kHistStride];
-    __shared__ uint32_t s_low[kColWaves][kLowCut - 1][4];
 
     const int tid = threadIdx.x;
     const int lane = tid & 63;
@@ -322,11 +319,6 @@ __global__ __launch_bounds__(kColThreads) void collide_kernel(RetrieveArgs a) {
     const int64_t c0 = chunk * kChunk;
     const int64_t c1 = min(c0 + (int64_t)kChunk, a.n);
     const uint32_t nkeys = (uint32_t)(c1 - c0);
-    // Per-lane SWAR counters: byte h of cnt[v-1] = #{keys of this lane with S_h >= v}
-    // for v = 1 .. kLowCut-1 (a lane sees at most kChunk / kColThreads = 16 keys).
-    uint32_t cnt[kLowCut - 1];
-#pragma unroll
-    for (int v = 0; v < kLowCut - 1; ++v) cnt[v] = 0;
 
     // Buffer descriptors over the chunk: the id rows (nkeys x 16 bytes) and each head's
     // score bytes (nkeys, or none for a slot past the quad's last head).  The whole
@@ -360,19 +352,12 @@ __global__ __launch_bounds__(kColThreads) void collide_kernel(RetrieveArgs a) {
                 acc += s_lut[b * kCentroids + ((ww[b >> 2] >> (8 * (b & 3))) & 0xffu)];
             const bool live = i < nkeys;
             acc = live ? acc : 0u;  // a key past the end scores 0 for every head
-            // Low scores are frequent: count #{S >= v} for v < kLowCut for the 4 heads at
-            // once.  Bytes are at most 96, so (S | 0x80) - v keeps its top bit iff S >= v
-            // and no borrow crosses a byte.
-            const uint32_t x = acc | 0x80808080u;
-#pragma unroll
-            for (int v = 1; v < kLowCut; ++v)
-                cnt[v - 1] += ((x - (uint32_t)v * 0x01010101u) & 0x80808080u) >> 7;
-            // Higher scores: exact per-value LDS histogram.  Slots of the last quad
-            // without a head have an all-zero bonus table, so score 0.
+            // Exact per-value LDS histogram of the nonzero scores.  Slots of the last
+            // quad without a head have an all-zero bonus table, so score 0.
 #pragma unroll
             for (int h = 0; h < 4; ++h) {
                 const uint32_t sh = (acc >> (8 * h)) & 0xffu;
-                if (sh >= (uint32_t)kLowCut) atomicAdd(hcopy + h * kHistStride + sh, 1u);
+                if (sh != 0u) atomicAdd(hcopy + h * kHistStride + sh, 1u);
             }
             // A wave stores 64 consecutive score bytes of a head per instruction.
             const uint32_t off = live ? i : kOffsetOutOfRange;
@@ -382,31 +367,14 @@ __global__ __launch_bounds__(kColThreads) void collide_kernel(RetrieveArgs a) {
         }
     }
 
-    // Block totals of the low counts: widen the bytes to 16-bit fields (heads 0, 2 and
-    // heads 1, 3; a wave sums at most 64 * 16 per field) and reduce across the wave.
-#pragma unroll
-    for (int v = 0; v < kLowCut - 1; ++v) {
-        uint32_t e = cnt[v] & 0x00ff00ffu, o = (cnt[v] >> 8) & 0x00ff00ffu;
-#pragma unroll
-        for (int d = 1; d < 64; d <<= 1) {
-            e += __shfl_xor(e, d, 64);
-            o += __shfl_xor(o, d, 64);
-        }
-        if (lane == 0) {
-            s_low[wave][v][0] = e & 0xffffu;
-            s_low[wave][v][1] = o & 0xffffu;
-            s_low[wave][v][2] = e >> 16;
-            s_low[wave][v][3] = o >> 16;
-        }
-    }
     __syncthreads();
 
     // Per-chunk suffix histogram of every head: sfx[v] = #{keys in chunk : S >= v}, v = 0..97.
     if (wave < nh) {
         const int h = wave;
-        // Exact count of each value v >= kLowCut: lane holds v = lane and v = 64 + lane.
+        // Exact count of each value v >= 1: lane holds v = lane and v = 64 + lane.
         auto count_of = [&](int v) -> uint32_t {
-            if (v < kLowCut || v > kMaxScore) return 0u;
+            if (v < 1 || v > kMaxScore) return 0u;
             uint32_t t = 0;
 #pragma unroll
             for (int c = 0; c < kHistCopies; ++c) t += s_hist[(c * 4 + h) * kHistStride + v];
@@ -415,14 +383,8 @@ __global__ __launch_bounds__(kColThreads) void collide_kernel(RetrieveArgs a) {
         const uint32_t lo = count_of(lane);
         const uint32_t hi = count_of(64 + lane);
         uint32_t sl, sh;
-        wave_suffix97(lo, hi, lane, &sl, &sh);  // exact for v >= kLowCut
+        wave_suffix97(lo, hi, lane, &sl, &sh);  // exact for v >= 1
         if (lane == 0) sl = (uint32_t)(c1 - c0);
-        if (lane >= 1 && lane < kLowCut) {
-            uint32_t t = 0;
-#pragma unroll
-            for (int w2 = 0; w2 < kColWaves; ++w2) t += s_low[w2][lane - 1][h];
-            sl = t;
-        }
         uint32_t* dst = a.chunk_sfx + ((row0 + h) * a.n_chunks + chunk) * kSfx;
         dst[lane] = sl;
         if (lane < kSfx - 64) dst[64 + lane] = lane < kBins - 64 ? sh : 0u;

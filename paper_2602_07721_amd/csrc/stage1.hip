@@ -7,7 +7,8 @@
 // Kernels, in launch order:
 //   query_lut_kernel   one block per (sequence, KV head, quad, 4 subspaces), one
 //                      wave per (head slot, subspace): z = H(s q) in exact
-//                      float64 (written as z/D float for the rerank), the 256
+//                      float64 by a register FWHT in one wave per head
+//                      (written as z/D float for the rerank), the 256
 //                      centroids ranked by the exact proxy sum_j +-z_j (ties:
 //                      lower id) by a 64-bit bitonic sort of the 128 with bit 7
 //                      clear and a merge with their complements, in registers,
@@ -167,32 +168,52 @@ __global__ __launch_bounds__(kLutThreads) void query_lut_kernel(RetrieveArgs a) 
     const bool live = hg < a.g;
     const int64_t row = (int64_t)seq * a.hq + kvh * a.g + hg;
 
-    // Cluster counts of the 4 subspaces; z = H (s (.) q) of the 4 heads, exactly in float64.
+    // Cluster counts of the 4 subspaces.
     const uint32_t* cnt = a.counts + grp * (kB * kCentroids) + (4 * sg) * kCentroids;
     (&s_cnt[0][0])[tid] = cnt[tid];
     (&s_lut[0][0])[tid] = 0u;
-    const int zh = tid >> 7, zi = tid & (kD - 1);  // threads < 512: 4 heads x 128 coordinates
-    const bool zlive = zh < 4 && quad * 4 + zh < a.g;
+    // z = H (s (.) q) of the 4 heads exactly in float64: wave `slot` of subspace 0 takes
+    // head `slot` in registers (coordinates 2 lane + r; stride-1 butterflies inside a
+    // lane, the others across lanes) and leaves it in LDS for the other three waves.
     const bool rotate = !(a.flags & kFlagNoRotation);
-    if (zlive) {
-        const __half* qp = static_cast<const __half*>(a.q) + (row + (zh - slot)) * kD;
-        double v = (double)__half2float(qp[zi]);
-        if (!rotate) v *= (double)kD;  // z = D q without the rotation (exact: D = 2^7)
-        else if ((a.sb.w[zi >> 5] >> (zi & 31)) & 1u) v = -v;
-        s_z[zh][zi] = v;
+    if (sub == 0 && live) {
+        const uint32_t qw = reinterpret_cast<const uint32_t*>(static_cast<const __half*>(a.q) + row * kD)[lane];
+        double z[2];
+#pragma unroll
+        for (int r = 0; r < 2; ++r) {
+            const int zi = 2 * lane + r;
+            double v = (double)__half2float(__ushort_as_half((unsigned short)(r ? qw >> 16 : qw & 0xffffu)));
+            if (!rotate) v *= (double)kD;  // z = D q without the rotation (exact: D = 2^7)
+            else if ((a.sb.w[zi >> 5] >> (zi & 31)) & 1u) v = -v;
+            z[r] = v;
+        }
+        if (rotate) {
+            {
+                const double x0 = z[0], x1 = z[1];
+                z[0] = __dadd_rn(x0, x1);
+                z[1] = __dsub_rn(x0, x1);
+            }
+#pragma unroll
+            for (int h = 2; h < kD; h <<= 1) {
+                // Partner index e ^ h is lane ^ (h / 2); the element with bit log2 h of
+                // its index clear takes the sum, the other the difference.
+                const bool upper = (lane & (h >> 1)) != 0;
+#pragma unroll
+                for (int r = 0; r < 2; ++r) {
+                    const uint64_t u = (uint64_t)__double_as_longlong(z[r]);
+                    const uint32_t lo = lane_xor((uint32_t)u, h >> 1, lane), hi = lane_xor((uint32_t)(u >> 32), h >> 1, lane);
+                    const double o = __longlong_as_double((long long)(((uint64_t)hi << 32) | lo));
+                    z[r] = upper ? __dsub_rn(o, z[r]) : __dadd_rn(z[r], o);
+                }
+            }
+        }
+#pragma unroll
+        for (int r = 0; r < 2; ++r) {
+            s_z[slot][2 * lane + r] = z[r];
+            if (sg == 0) a.zq[row * kD + 2 * lane + r] = (float)(z[r] * (1.0 / kD));
+        }
     }
     __syncthreads();
-    for (int h = 1; rotate && h < kD; h <<= 1) {
-        if (zi < kD / 2 && zlive) {
-            const int i = ((zi / h) * 2 * h) + (zi % h);
-            const double x0 = s_z[zh][i], x1 = s_z[zh][i + h];
-            s_z[zh][i] = __dadd_rn(x0, x1);
-            s_z[zh][i + h] = __dsub_rn(x0, x1);
-        }
-        __syncthreads();
-    }
-    if (sg == 0 && zlive)
-        a.zq[(row + (zh - slot)) * kD + zi] = (float)(s_z[zh][zi] * (1.0 / kD));
 
     if (live) {
         double zb[8];

@@ -183,6 +183,88 @@ def _stream(stream):
     return ctypes.c_void_p(s.cuda_stream)
 
 
+def _arg(t, name, dtype, shape, dev=None, optional=False):
+    """Pointer of a tensor argument after checking its dtype and its shape (None entries are
+    free; the sizes the library derives from shapes must be consistent).  The kernels trust
+    these, so a mismatch is refused here rather than read past the end of an allocation.
+    A tensor that must live on the GPU is appended to the list `dev`, checked by
+    _require_device once every argument of the call has passed these checks."""
+    import torch
+    if t is None:
+        if optional:
+            return None
+        raise ValueError(f"{name} is required")
+    if not isinstance(t, torch.Tensor):
+        raise TypeError(f"{name} must be a torch tensor")
+    if t.dtype != dtype:
+        raise TypeError(f"{name} must be {dtype}, got {t.dtype}")
+    if t.dim() != len(shape) or any(w is not None and int(d) != int(w) for d, w in zip(t.shape, shape)):
+        want = "[" + ", ".join("*" if w is None else str(w) for w in shape) + "]"
+        raise ValueError(f"{name} must have shape {want}, got {list(t.shape)}")
+    if dev is not None:
+        dev.append((t, name))
+    return _ptr(t, name, False)
+
+
+def _require_device(dev):
+    for t, name in dev:
+        if not t.is_cuda:
+            raise ValueError(f"{name} must be a GPU tensor")
+
+
+def _kv_args(cfg, batch, K, V, kv_host_mapped, dev, names=("K", "V")):
+    """Pointers of a K/V cache pair [batch][Hkv][capacity][D] float16 (pinned host memory when
+    kv_host_mapped) and its capacity."""
+    import torch
+    shape = (batch, cfg.n_kv_heads, None, HEAD_DIM)
+    kp = _arg(K, names[0], torch.float16, shape, None if kv_host_mapped else dev)
+    cap = int(K.shape[2])
+    vp = _arg(V, names[1], torch.float16, (batch, cfg.n_kv_heads, cap, HEAD_DIM), None if kv_host_mapped else dev)
+    if kv_host_mapped:
+        for t, nm in ((K, names[0]), (V, names[1])):
+            if t.is_cuda or not t.is_pinned():
+                raise ValueError(f"{nm} must be pinned host memory when kv_host_mapped")
+    return kp, vp, cap
+
+
+def _q_arg(cfg, q, dev):
+    import torch
+    if not isinstance(q, torch.Tensor) or q.dim() != 3:
+        raise ValueError("q must be a [batch][Hq][D] tensor")
+    batch = int(q.shape[0])
+    return _arg(q, "q", torch.float16, (batch, cfg.n_q_heads, HEAD_DIM), dev), batch
+
+
+def _out_arg(cfg, out, batch, device, dev):
+    import torch
+    if out is None:
+        out = torch.empty((batch, cfg.n_q_heads, HEAD_DIM), dtype=torch.float32, device=device)
+    return out, _arg(out, "out", torch.float32, (batch, cfg.n_q_heads, HEAD_DIM), dev)
+
+
+def _idx_arg(cfg, idx, batch, dev, name="idx"):
+    import torch
+    if not isinstance(idx, torch.Tensor) or idx.dim() != 3:
+        raise ValueError(f"{name} must be a [batch][Hq][k] int32 tensor")
+    k = int(idx.shape[-1])
+    return _arg(idx, name, torch.int32, (batch, cfg.n_q_heads, k), dev), k
+
+
+def _retrieve_outs(cfg, budget, batch, out_idx, out_score, workspace, n, device, dev):
+    """Allocate what the caller left out and check the rest: (out_idx, out_score, workspace, ptrs)."""
+    import torch
+    if out_idx is None:
+        out_idx = torch.empty((batch, cfg.n_q_heads, budget.top_k), dtype=torch.int32, device=device)
+    if workspace is None:
+        workspace = torch.empty(max(256, retrieve_workspace_size(cfg, batch, n, budget)),
+                                dtype=torch.uint8, device=device)
+    rows = (batch, cfg.n_q_heads, budget.top_k)
+    ptrs = (_arg(out_idx, "out_idx", torch.int32, rows, dev),
+            _arg(out_score, "out_score", torch.float32, rows, dev, optional=True),
+            _arg(workspace, "workspace", torch.uint8, (None,), dev))
+    return out_idx, out_score, workspace, ptrs
+
+
 class Index:
     """Device arrays of the per-key metadata (see ``pariskv_index``)."""
 
@@ -201,29 +283,59 @@ class Index:
     def batch(self):
         return int(self.ids.shape[0])
 
-    def c(self):
-        self._c = _Index(_ptr(self.ids, "ids"), _ptr(self.rec, "rec"), _ptr(self.counts, "counts"))
+    def c(self, cfg=None, batch=None, dev=None):
+        if cfg is not None:
+            import torch
+            b = self.batch if batch is None else batch
+            cap = cfg.capacity
+            own = dev is None
+            dev = [] if own else dev
+            ptrs = (_arg(self.ids, "index.ids", torch.uint8, (b, cfg.n_kv_heads, cap, SUBSPACES), dev),
+                    _arg(self.rec, "index.rec", torch.uint8, (b, cfg.n_kv_heads, cap, REC_BYTES), dev),
+                    _arg(self.counts, "index.counts", torch.int32, (b, cfg.n_kv_heads, SUBSPACES, CENTROIDS), dev))
+            if own:
+                _require_device(dev)
+        else:
+            ptrs = (_ptr(self.ids, "ids"), _ptr(self.rec, "rec"), _ptr(self.counts, "counts"))
+        self._c = _Index(*ptrs)
         return ctypes.byref(self._c)
+
+
+def _keys_arg(cfg, keys, dev, name="keys"):
+    import torch
+    if not isinstance(keys, torch.Tensor) or keys.dim() != 4:
+        raise ValueError(f"{name} must be a [batch][Hkv][n][D] float16 tensor")
+    b = int(keys.shape[0])
+    return _arg(keys, name, torch.float16, (b, cfg.n_kv_heads, None, HEAD_DIM), dev), b
 
 
 def encode(cfg, index, keys, stream=None):
     """Prefill: encode keys [batch][Hkv][n][D] float16 into rows [0, n); resets counts."""
-    n = int(keys.shape[2])
-    _check(lib().pariskv_encode(cfg.c(), index.c(), _ptr(keys, "keys"), n, int(keys.shape[0]),
-                                _stream(stream)))
+    dev = []
+    kp, b = _keys_arg(cfg, keys, dev)
+    ic = index.c(cfg, b, dev)
+    _require_device(dev)
+    _check(lib().pariskv_encode(cfg.c(), ic, kp, int(keys.shape[2]), b, _stream(stream)))
 
 
 def append(cfg, index, keys, n_cur, stream=None):
     """Streaming update: encode keys [batch][Hkv][t][D] into rows [n_cur, n_cur + t)."""
-    _check(lib().pariskv_append(cfg.c(), index.c(), _ptr(keys, "keys"), int(n_cur), int(keys.shape[2]),
-                                int(keys.shape[0]), _stream(stream)))
+    dev = []
+    kp, b = _keys_arg(cfg, keys, dev)
+    ic = index.c(cfg, b, dev)
+    _require_device(dev)
+    _check(lib().pariskv_append(cfg.c(), ic, kp, int(n_cur), int(keys.shape[2]), b, _stream(stream)))
 
 
 def append_rows(cfg, index, K, row_begin, t, n_cur, stream=None):
     """Streaming update from the key cache K [batch][Hkv][kv_capacity][D]: encode cache rows
     [row_begin, row_begin + t) into index rows [n_cur, n_cur + t)."""
-    _check(lib().pariskv_append_rows(cfg.c(), index.c(), _ptr(K, "K"), int(K.shape[2]), int(row_begin),
-                                     int(n_cur), int(t), int(K.shape[0]), _stream(stream)))
+    dev = []
+    kp, b = _keys_arg(cfg, K, dev, "K")
+    ic = index.c(cfg, b, dev)
+    _require_device(dev)
+    _check(lib().pariskv_append_rows(cfg.c(), ic, kp, int(K.shape[2]), int(row_begin), int(n_cur), int(t), b,
+                                     _stream(stream)))
 
 
 @dataclass
@@ -267,18 +379,14 @@ def workspace_layout(cfg, batch, n, budget):
 
 def retrieve(cfg, index, q, n, budget, out_idx=None, out_score=None, workspace=None, stream=None):
     """Alg. 1 decode for all query heads; returns (idx, score, workspace) tensors."""
-    import torch
-    batch = int(q.shape[0])
-    rows = batch * cfg.n_q_heads
-    if out_idx is None:
-        out_idx = torch.empty((batch, cfg.n_q_heads, budget.top_k), dtype=torch.int32, device=q.device)
-    if workspace is None:
-        workspace = torch.empty(max(256, retrieve_workspace_size(cfg, batch, n, budget)),
-                                dtype=torch.uint8, device=q.device)
-    assert out_idx.numel() == rows * budget.top_k
-    _check(lib().pariskv_retrieve(cfg.c(), index.c(), _ptr(q, "q"), int(n), batch, budget.c(),
-                                  _ptr(out_idx, "out_idx"), _ptr(out_score, "out_score"),
-                                  _ptr(workspace, "workspace"), workspace.numel(), _stream(stream)))
+    dev = []
+    qp, batch = _q_arg(cfg, q, dev)
+    out_idx, out_score, workspace, (ip, sp, wp) = _retrieve_outs(cfg, budget, batch, out_idx, out_score,
+                                                                 workspace, n, q.device, dev)
+    ic = index.c(cfg, batch, dev)
+    _require_device(dev)
+    _check(lib().pariskv_retrieve(cfg.c(), ic, qp, int(n), batch, budget.c(), ip, sp, wp,
+                                  workspace.numel(), _stream(stream)))
     return out_idx, out_score, workspace
 
 
@@ -286,63 +394,43 @@ def retrieve_attend(cfg, index, q, n, budget, K, V, scale, out_idx=None, out_sco
                     workspace=None, kv_host_mapped=False, stream=None):
     """retrieve + sparse_attend in one call (attention fused into the top-k when C <= 32768);
     returns (idx, score, out, workspace)."""
-    import torch
-    batch = int(q.shape[0])
-    rows = batch * cfg.n_q_heads
-    if out_idx is None:
-        out_idx = torch.empty((batch, cfg.n_q_heads, budget.top_k), dtype=torch.int32, device=q.device)
-    if out is None:
-        out = torch.empty((batch, cfg.n_q_heads, HEAD_DIM), dtype=torch.float32, device=q.device)
-    if workspace is None:
-        workspace = torch.empty(max(256, retrieve_workspace_size(cfg, batch, n, budget)),
-                                dtype=torch.uint8, device=q.device)
-    if kv_host_mapped:
-        for t, nm in ((K, "K"), (V, "V")):
-            if t.is_cuda or not t.is_pinned():
-                raise ValueError(f"{nm} must be pinned host memory when kv_host_mapped")
-    assert out_idx.numel() == rows * budget.top_k
-    _check(lib().pariskv_retrieve_attend(cfg.c(), index.c(), _ptr(q, "q"), int(n), batch, budget.c(),
-                                         _ptr(out_idx, "out_idx"), _ptr(out_score, "out_score"),
-                                         _ptr(K, "K", not kv_host_mapped), _ptr(V, "V", not kv_host_mapped),
-                                         int(bool(kv_host_mapped)), int(K.shape[2]), float(scale),
-                                         _ptr(out, "out"), _ptr(workspace, "workspace"), workspace.numel(),
-                                         _stream(stream)))
+    dev = []
+    qp, batch = _q_arg(cfg, q, dev)
+    kp, vp, cap = _kv_args(cfg, batch, K, V, kv_host_mapped, dev)
+    out, op = _out_arg(cfg, out, batch, q.device, dev)
+    out_idx, out_score, workspace, (ip, sp, wp) = _retrieve_outs(cfg, budget, batch, out_idx, out_score,
+                                                                 workspace, n, q.device, dev)
+    ic = index.c(cfg, batch, dev)
+    _require_device(dev)
+    _check(lib().pariskv_retrieve_attend(cfg.c(), ic, qp, int(n), batch, budget.c(), ip, sp,
+                                         kp, vp, int(bool(kv_host_mapped)), cap, float(scale), op, wp,
+                                         workspace.numel(), _stream(stream)))
     return out_idx, out_score, out, workspace
 
 
 def sparse_attend(cfg, q, K, V, idx, scale, out=None, kv_host_mapped=False, stream=None):
     """Attention over idx only; K, V [batch][Hkv][kv_capacity][D] float16 (device or pinned host)."""
-    import torch
-    batch = int(q.shape[0])
-    if out is None:
-        out = torch.empty((batch, cfg.n_q_heads, HEAD_DIM), dtype=torch.float32, device=q.device)
-    if kv_host_mapped:
-        for t, nm in ((K, "K"), (V, "V")):
-            if t.is_cuda or not t.is_pinned():
-                raise ValueError(f"{nm} must be pinned host memory when kv_host_mapped")
-    k = int(idx.shape[-1])
-    _check(lib().pariskv_sparse_attend(cfg.c(), _ptr(q, "q"), _ptr(K, "K", not kv_host_mapped),
-                                       _ptr(V, "V", not kv_host_mapped), int(bool(kv_host_mapped)),
-                                       int(K.shape[2]), _ptr(idx, "idx"), k, batch, float(scale),
-                                       _ptr(out, "out"), _stream(stream)))
+    dev = []
+    qp, batch = _q_arg(cfg, q, dev)
+    kp, vp, cap = _kv_args(cfg, batch, K, V, kv_host_mapped, dev)
+    xp, k = _idx_arg(cfg, idx, batch, dev)
+    out, op = _out_arg(cfg, out, batch, q.device, dev)
+    _require_device(dev)
+    _check(lib().pariskv_sparse_attend(cfg.c(), qp, kp, vp, int(bool(kv_host_mapped)), cap, xp, k, batch,
+                                       float(scale), op, _stream(stream)))
     return out
 
 
 def window_attend(cfg, q, K, V, idx, win, scale, out=None, kv_host_mapped=False, stream=None):
     """Attention over Sink + retrieved (retr_begin + idx) + Local/Buffer rows of ``win``."""
-    import torch
-    batch = int(q.shape[0])
-    if out is None:
-        out = torch.empty((batch, cfg.n_q_heads, HEAD_DIM), dtype=torch.float32, device=q.device)
-    if kv_host_mapped:
-        for t, nm in ((K, "K"), (V, "V")):
-            if t.is_cuda or not t.is_pinned():
-                raise ValueError(f"{nm} must be pinned host memory when kv_host_mapped")
-    k = int(idx.shape[-1])
-    _check(lib().pariskv_window_attend(cfg.c(), _ptr(q, "q"), _ptr(K, "K", not kv_host_mapped),
-                                       _ptr(V, "V", not kv_host_mapped), int(bool(kv_host_mapped)),
-                                       int(K.shape[2]), _ptr(idx, "idx"), k, win.c(), batch, float(scale),
-                                       _ptr(out, "out"), _stream(stream)))
+    dev = []
+    qp, batch = _q_arg(cfg, q, dev)
+    kp, vp, cap = _kv_args(cfg, batch, K, V, kv_host_mapped, dev)
+    xp, k = _idx_arg(cfg, idx, batch, dev)
+    out, op = _out_arg(cfg, out, batch, q.device, dev)
+    _require_device(dev)
+    _check(lib().pariskv_window_attend(cfg.c(), qp, kp, vp, int(bool(kv_host_mapped)), cap, xp, k, win.c(),
+                                       batch, float(scale), op, _stream(stream)))
     return out
 
 
@@ -350,26 +438,17 @@ def retrieve_window_attend(cfg, index, q, n, budget, K, V, win, scale, out_idx=N
                            out=None, workspace=None, kv_host_mapped=False, stream=None):
     """retrieve over the Retrieval region + window_attend in one call; returns
     (idx, score, out, workspace)."""
-    import torch
-    batch = int(q.shape[0])
-    rows = batch * cfg.n_q_heads
-    if out_idx is None:
-        out_idx = torch.empty((batch, cfg.n_q_heads, budget.top_k), dtype=torch.int32, device=q.device)
-    if out is None:
-        out = torch.empty((batch, cfg.n_q_heads, HEAD_DIM), dtype=torch.float32, device=q.device)
-    if workspace is None:
-        workspace = torch.empty(max(256, retrieve_workspace_size(cfg, batch, n, budget)),
-                                dtype=torch.uint8, device=q.device)
-    if kv_host_mapped:
-        for t, nm in ((K, "K"), (V, "V")):
-            if t.is_cuda or not t.is_pinned():
-                raise ValueError(f"{nm} must be pinned host memory when kv_host_mapped")
-    assert out_idx.numel() == rows * budget.top_k
+    dev = []
+    qp, batch = _q_arg(cfg, q, dev)
+    kp, vp, cap = _kv_args(cfg, batch, K, V, kv_host_mapped, dev)
+    out, op = _out_arg(cfg, out, batch, q.device, dev)
+    out_idx, out_score, workspace, (ip, sp, wp) = _retrieve_outs(cfg, budget, batch, out_idx, out_score,
+                                                                 workspace, n, q.device, dev)
+    ic = index.c(cfg, batch, dev)
+    _require_device(dev)
     _check(lib().pariskv_retrieve_window_attend(
-        cfg.c(), index.c(), _ptr(q, "q"), int(n), batch, budget.c(), _ptr(out_idx, "out_idx"),
-        _ptr(out_score, "out_score"), _ptr(K, "K", not kv_host_mapped), _ptr(V, "V", not kv_host_mapped),
-        int(bool(kv_host_mapped)), int(K.shape[2]), win.c(), float(scale), _ptr(out, "out"),
-        _ptr(workspace, "workspace"), workspace.numel(), _stream(stream)))
+        cfg.c(), ic, qp, int(n), batch, budget.c(), ip, sp, kp, vp, int(bool(kv_host_mapped)),
+        cap, win.c(), float(scale), op, wp, workspace.numel(), _stream(stream)))
     return out_idx, out_score, out, workspace
 
 
@@ -378,18 +457,16 @@ def group_attend(cfg, q, K, V, idx, scale, out=None, union_rows=None, kv_host_ma
     attend over the union of their ascending lists); union_rows: optional int32 tensor
     [batch][Hkv][ceil(G/4)] that receives the number of rows fetched."""
     import torch
-    batch = int(q.shape[0])
-    if out is None:
-        out = torch.empty((batch, cfg.n_q_heads, HEAD_DIM), dtype=torch.float32, device=q.device)
-    if kv_host_mapped:
-        for t, nm in ((K, "K"), (V, "V")):
-            if t.is_cuda or not t.is_pinned():
-                raise ValueError(f"{nm} must be pinned host memory when kv_host_mapped")
-    k = int(idx.shape[-1])
-    _check(lib().pariskv_group_attend(cfg.c(), _ptr(q, "q"), _ptr(K, "K", not kv_host_mapped),
-                                      _ptr(V, "V", not kv_host_mapped), int(bool(kv_host_mapped)),
-                                      int(K.shape[2]), _ptr(idx, "idx"), k, batch, float(scale),
-                                      _ptr(out, "out"), _ptr(union_rows, "union_rows"), _stream(stream)))
+    dev = []
+    qp, batch = _q_arg(cfg, q, dev)
+    kp, vp, cap = _kv_args(cfg, batch, K, V, kv_host_mapped, dev)
+    xp, k = _idx_arg(cfg, idx, batch, dev)
+    out, op = _out_arg(cfg, out, batch, q.device, dev)
+    up = _arg(union_rows, "union_rows", torch.int32, (batch, cfg.n_kv_heads, (cfg.q_per_kv + 3) // 4), dev,
+              optional=True)
+    _require_device(dev)
+    _check(lib().pariskv_group_attend(cfg.c(), qp, kp, vp, int(bool(kv_host_mapped)), cap, xp, k, batch,
+                                      float(scale), op, up, _stream(stream)))
     return out
 
 
@@ -402,61 +479,54 @@ def tiered_attend(cfg, q, K_win, V_win, K, V, idx, win, scale, out=None, kv_host
     """window_attend with Sink + Local/Buffer rows read from the GPU window cache K_win/V_win
     [batch][Hkv][win_capacity][D] and the retrieved rows from K/V (pinned host memory when
     kv_host_mapped)."""
-    import torch
-    batch = int(q.shape[0])
-    if out is None:
-        out = torch.empty((batch, cfg.n_q_heads, HEAD_DIM), dtype=torch.float32, device=q.device)
-    if kv_host_mapped:
-        for t, nm in ((K, "K"), (V, "V")):
-            if t.is_cuda or not t.is_pinned():
-                raise ValueError(f"{nm} must be pinned host memory when kv_host_mapped")
-    k = int(idx.shape[-1])
-    _check(lib().pariskv_tiered_attend(cfg.c(), _ptr(q, "q"), _ptr(K_win, "K_win"), _ptr(V_win, "V_win"),
-                                       int(K_win.shape[2]), _ptr(K, "K", not kv_host_mapped),
-                                       _ptr(V, "V", not kv_host_mapped), int(bool(kv_host_mapped)),
-                                       int(K.shape[2]), _ptr(idx, "idx"), k, win.c(), batch, float(scale),
-                                       _ptr(out, "out"), _stream(stream)))
+    dev = []
+    qp, batch = _q_arg(cfg, q, dev)
+    kwp, vwp, wcap = _kv_args(cfg, batch, K_win, V_win, False, dev, ("K_win", "V_win"))
+    kp, vp, cap = _kv_args(cfg, batch, K, V, kv_host_mapped, dev)
+    xp, k = _idx_arg(cfg, idx, batch, dev)
+    out, op = _out_arg(cfg, out, batch, q.device, dev)
+    _require_device(dev)
+    _check(lib().pariskv_tiered_attend(cfg.c(), qp, kwp, vwp, wcap, kp, vp, int(bool(kv_host_mapped)), cap,
+                                       xp, k, win.c(), batch, float(scale), op, _stream(stream)))
     return out
 
 
 def retrieve_tiered_attend(cfg, index, q, n, budget, K_win, V_win, K, V, win, scale, out_idx=None,
                            out_score=None, out=None, workspace=None, kv_host_mapped=False, stream=None):
     """retrieve over the Retrieval region + tiered_attend in one call; returns (idx, score, out, ws)."""
-    import torch
-    batch = int(q.shape[0])
-    rows = batch * cfg.n_q_heads
-    if out_idx is None:
-        out_idx = torch.empty((batch, cfg.n_q_heads, budget.top_k), dtype=torch.int32, device=q.device)
-    if out is None:
-        out = torch.empty((batch, cfg.n_q_heads, HEAD_DIM), dtype=torch.float32, device=q.device)
-    if workspace is None:
-        workspace = torch.empty(max(256, retrieve_workspace_size(cfg, batch, n, budget)),
-                                dtype=torch.uint8, device=q.device)
-    if kv_host_mapped:
-        for t, nm in ((K, "K"), (V, "V")):
-            if t.is_cuda or not t.is_pinned():
-                raise ValueError(f"{nm} must be pinned host memory when kv_host_mapped")
-    assert out_idx.numel() == rows * budget.top_k
+    dev = []
+    qp, batch = _q_arg(cfg, q, dev)
+    kwp, vwp, wcap = _kv_args(cfg, batch, K_win, V_win, False, dev, ("K_win", "V_win"))
+    kp, vp, cap = _kv_args(cfg, batch, K, V, kv_host_mapped, dev)
+    out, op = _out_arg(cfg, out, batch, q.device, dev)
+    out_idx, out_score, workspace, (ip, sp, wp) = _retrieve_outs(cfg, budget, batch, out_idx, out_score,
+                                                                 workspace, n, q.device, dev)
+    ic = index.c(cfg, batch, dev)
+    _require_device(dev)
     _check(lib().pariskv_retrieve_tiered_attend(
-        cfg.c(), index.c(), _ptr(q, "q"), int(n), batch, budget.c(), _ptr(out_idx, "out_idx"),
-        _ptr(out_score, "out_score"), _ptr(K_win, "K_win"), _ptr(V_win, "V_win"), int(K_win.shape[2]),
-        _ptr(K, "K", not kv_host_mapped), _ptr(V, "V", not kv_host_mapped), int(bool(kv_host_mapped)),
-        int(K.shape[2]), win.c(), float(scale), _ptr(out, "out"), _ptr(workspace, "workspace"),
-        workspace.numel(), _stream(stream)))
+        cfg.c(), ic, qp, int(n), batch, budget.c(), ip, sp, kwp, vwp, wcap, kp, vp,
+        int(bool(kv_host_mapped)), cap, win.c(), float(scale), op, wp, workspace.numel(), _stream(stream)))
     return out_idx, out_score, out, workspace
 
 
 def offload_rows(K_src, V_src, src_row, K_dst, V_dst, dst_row, t, stream=None):
     """Copy rows [src_row, src_row + t) of every (sequence, KV head) of K_src/V_src to rows
     [dst_row, dst_row + t) of K_dst/V_dst (device or pinned host tensors [b][Hkv][cap][D])."""
-    for x, nm in ((K_src, "K_src"), (V_src, "V_src"), (K_dst, "K_dst"), (V_dst, "V_dst")):
+    import torch
+    named = ((K_src, "K_src"), (V_src, "V_src"), (K_dst, "K_dst"), (V_dst, "V_dst"))
+    for x, nm in named:
+        if not isinstance(x, torch.Tensor) or x.dim() != 4:
+            raise ValueError(f"{nm} must be a [batch][Hkv][capacity][D] float16 tensor")
+    b, hkv = int(K_src.shape[0]), int(K_src.shape[1])
+    src_cap, dst_cap = int(K_src.shape[2]), int(K_dst.shape[2])
+    ps = [_arg(x, nm, torch.float16, (b, hkv, c, HEAD_DIM))
+          for x, nm, c in ((K_src, "K_src", src_cap), (V_src, "V_src", src_cap),
+                           (K_dst, "K_dst", dst_cap), (V_dst, "V_dst", dst_cap))]
+    for x, nm in named:
         if not x.is_cuda and not x.is_pinned():
             raise ValueError(f"{nm} must be device or pinned host memory")
-    b, hkv = int(K_src.shape[0]), int(K_src.shape[1])
-    _check(lib().pariskv_offload_rows(_ptr(K_src, "K_src", False), _ptr(V_src, "V_src", False),
-                                      int(K_src.shape[2]), int(src_row), _ptr(K_dst, "K_dst", False),
-                                      _ptr(V_dst, "V_dst", False), int(K_dst.shape[2]), int(dst_row), int(t),
-                                      b, hkv, _stream(stream)))
+    _check(lib().pariskv_offload_rows(ps[0], ps[1], src_cap, int(src_row), ps[2], ps[3], dst_cap, int(dst_row),
+                                      int(t), b, hkv, _stream(stream)))
 
 
 def quantizer_table(m=8):

@@ -348,3 +348,58 @@ def test_group_attend_validation():
     assert call(_cfg(), k=0) == pk.ERR_INVALID
     assert call(_cfg(), union=FAKE + 2) == pk.ERR_INVALID
     assert call(_cfg(), cap=2 ** 30) == pk.ERR_INVALID
+
+
+def test_binding_refuses_mismatched_tensors_before_any_launch():
+    # The Python binding derives sizes from tensor shapes; a wrong dtype or shape is refused
+    # on the host (CPU tensors here: the checks run before the device check and the call).
+    import torch
+    signs = workloads.rotation_signs(3)
+    cfg = pk.Config(2, 4, 64, signs)
+    f16 = torch.float16
+    keys = torch.zeros((1, 2, 64, 128), dtype=f16)
+    index = pk.Index(torch.zeros((1, 2, 64, 16), dtype=torch.uint8), torch.zeros((1, 2, 64, 128), dtype=torch.uint8),
+                     torch.zeros((1, 2, 16, 256), dtype=torch.int32))
+    with pytest.raises(TypeError, match="keys must be torch.float16"):
+        pk.encode(cfg, index, keys.to(torch.int8))
+    with pytest.raises(ValueError, match="keys must have shape"):
+        pk.encode(cfg, index, torch.zeros((1, 3, 64, 128), dtype=f16))     # 3 KV heads, config has 2
+    with pytest.raises(ValueError, match="keys must have shape"):
+        pk.encode(cfg, index, torch.zeros((1, 2, 64, 64), dtype=f16))      # D = 64
+    with pytest.raises(ValueError, match="must be a GPU tensor"):
+        pk.encode(cfg, index, keys)                                        # right shapes, host memory
+    short = pk.Index(index.ids[:, :, :32].contiguous(), index.rec, index.counts)
+    with pytest.raises(ValueError, match="index.ids must have shape"):
+        short.c(cfg, 1)                                                    # rows below the capacity
+    with pytest.raises(TypeError, match="index.counts must be torch.int32"):
+        pk.Index(index.ids, index.rec, index.counts.long()).c(cfg, 1)
+
+    bud = pk.Budget(16, 32, 8)
+    q = torch.zeros((1, 8, 128), dtype=f16)
+    ws = torch.zeros(1024, dtype=torch.uint8)
+    with pytest.raises(TypeError, match="q must be torch.float16"):
+        pk.retrieve(cfg, index, q.float(), 64, bud, workspace=ws)
+    with pytest.raises(ValueError, match="q must have shape"):
+        pk.retrieve(cfg, index, torch.zeros((1, 4, 128), dtype=f16), 64, bud, workspace=ws)
+    with pytest.raises(ValueError, match="out_idx must have shape"):
+        pk.retrieve(cfg, index, q, 64, bud, out_idx=torch.zeros((1, 8, 4), dtype=torch.int32), workspace=ws)
+    with pytest.raises(TypeError, match="out_score must be torch.float32"):
+        pk.retrieve(cfg, index, q, 64, bud, out_idx=torch.zeros((1, 8, 8), dtype=torch.int32),
+                    out_score=torch.zeros((1, 8, 8), dtype=torch.float64), workspace=ws)
+
+    K = torch.zeros((1, 2, 64, 128), dtype=f16)
+    idx = torch.zeros((1, 8, 8), dtype=torch.int32)
+    with pytest.raises(TypeError, match="idx must be torch.int32"):
+        pk.sparse_attend(cfg, q, K, K, idx.long(), 0.1)
+    with pytest.raises(ValueError, match="V must have shape"):
+        pk.sparse_attend(cfg, q, K, K[:, :, :32].contiguous(), idx, 0.1)  # V rows != K rows
+    with pytest.raises(ValueError, match="must be pinned host memory"):
+        pk.sparse_attend(cfg, q, K, K, idx, 0.1, kv_host_mapped=True)      # pageable host memory
+    with pytest.raises(ValueError, match="out must have shape"):
+        pk.sparse_attend(cfg, q, K, K, idx, 0.1, out=torch.zeros((1, 8, 64), dtype=torch.float32))
+    with pytest.raises(ValueError, match="union_rows must have shape"):
+        pk.group_attend(cfg, q, K, K, idx, 0.1, union_rows=torch.zeros((1, 2, 2), dtype=torch.int32))
+    with pytest.raises(ValueError, match="K_win must have shape"):
+        pk.tiered_attend(cfg, q, torch.zeros((1, 1, 16, 128), dtype=f16), K, K, K, idx, pk.Window(), 0.1)
+    with pytest.raises(ValueError, match="V_dst must have shape"):
+        pk.offload_rows(K, K, 0, K, K[:1, :1].contiguous(), 0, 4)

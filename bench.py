@@ -689,9 +689,9 @@ def main():
     args = parse()
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
-        print(f"bench.py: this build runs on exactly one GPU (asked for --gpus {args.gpus}, "
-              f"WORLD_SIZE {world}); the retrieval path shards by (sequence, KV head) with no "
-              f"exchange, so a multi-GPU figure would add no information here.", file=sys.stderr)
+        print(f"bench.py measures one GPU only (asked for --gpus {args.gpus}, WORLD_SIZE {world}): "
+              f"the retrieval path shards by (sequence, KV head) with no exchange, so each GPU "
+              f"of a larger run would repeat the one-GPU figure.", file=sys.stderr)
         sys.exit(2)
 
     import numpy as np

@@ -44,7 +44,7 @@ extern "C" {
 #define PARISKV_ERR_CAPACITY (-2)    /* keys would not fit in the index arrays  */
 #define PARISKV_ERR_WORKSPACE (-3)   /* workspace missing or too small           */
 #define PARISKV_ERR_HIP (-4)         /* a HIP runtime call or launch failed      */
-#define PARISKV_ERR_UNSUPPORTED (-5) /* valid but outside what this build serves */
+#define PARISKV_ERR_UNSUPPORTED (-5) /* valid but outside what the library serves */
 
 #define PARISKV_HEAD_DIM 128
 #define PARISKV_SUBSPACES 16

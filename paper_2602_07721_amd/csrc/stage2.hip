@@ -263,13 +263,15 @@ __global__ __launch_bounds__(TH) void topk_lds_kernel(RetrieveArgs a) {
     const int32_t* cand = a.cand + row * a.n_cand;
     if (tid == 0) s_nsmall = 0;
 
-    // Coalesced staging of the estimates as order-preserving keys (rows of cand and
-    // cand_score are 256-byte aligned).
+    // Coalesced staging of the estimates as order-preserving keys.  The arrays start
+    // 256-byte aligned and a row is n_cand entries long, so the 16-byte loads are taken
+    // only when n_cand is a multiple of 4 (every row start then 16-byte aligned).
+    const bool vec16 = (a.n_cand & 3) == 0;
     for (int p4 = tid; p4 < kCap / 4; p4 += TH) {
         const int p = 4 * p4;
         uint4 kv = make_uint4(0, 0, 0, 0);
         int4 iv = make_int4(-1, -1, -1, -1);
-        if (p + 3 < C) {
+        if (vec16 && p + 3 < C) {
             const float4 f = reinterpret_cast<const float4*>(sc)[p4];
             kv = make_uint4(order_key(f.x), order_key(f.y), order_key(f.z), order_key(f.w));
             if (kStageIdx) iv = reinterpret_cast<const int4*>(cand)[p4];

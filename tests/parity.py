@@ -76,6 +76,21 @@ class GpuRun:
         self.layout = pk.workspace_layout(self.cfg, b, n, self.budget)
         return self
 
+    def retrieve_attend(self, K=None, V=None, host_mapped=False):
+        """pariskv_retrieve_attend (retrieval with the attention fused into its top-k), the
+        call the benchmark times; returns the attention output on the host."""
+        b = self.Q.shape[0]
+        K = self.K if K is None else K
+        V = self.V if V is None else V
+        self.out_score = torch.empty((b, self.cfg.n_q_heads, self.budget.top_k), dtype=torch.float32,
+                                     device="cuda")
+        self.out_idx, _, self.out, self.ws = pk.retrieve_attend(
+            self.cfg, self.index, self.Q, self.n, self.budget, K, V, self.scale, out_score=self.out_score,
+            kv_host_mapped=host_mapped)
+        self.layout = pk.workspace_layout(self.cfg, b, self.n, self.budget)
+        torch.cuda.synchronize()
+        return self.out.cpu().numpy()
+
     def attend(self, idx=None, host_mapped=False):
         idx = self.out_idx if idx is None else idx
         K, V = self.K, self.V

@@ -83,10 +83,15 @@ EDGE = [
     ("huge_C", 1, 1, 1, 70000, (40000, 60000, 2048)),
     ("C_20000", 1, 1, 2, 40000, (20000, 30000, 1000)),      # top-k staging 32 keys per thread
     ("many_chunks", 1, 1, 1, 300000, (4096, 8192, 256)),    # 74 chunks: multi-wave chunk prefix
-    # score rows a multiple of 8 (the scan spreads rows over XCDs) with a ragged last chunk
+    # fewer than 32 score rows (quads of query heads): the scan keeps its plain block order
     ("rows8_ragged", 1, 8, 4, 5000, (512, 1024, 64)),
     ("rows8_two_quads_ragged", 1, 4, 8, 4099, (300, 700, 40)),
     ("rows16_one_chunk", 2, 8, 3, 100, (64, 80, 16)),
+    # 32 or more score rows, a multiple of 8: the scan hands each XCD whole rows
+    # (rows = x mod 8), here with a ragged last chunk
+    ("rows32_xcd_ragged", 4, 8, 4, 5000, (512, 1024, 64)),
+    ("rows32_two_quads_3key_tail", 4, 4, 8, 4099, (300, 700, 40)),
+    ("rows48_partial_quads_ragged", 3, 8, 6, 9000, (700, 1500, 100)),
 ]
 
 
@@ -263,14 +268,24 @@ def test_batch8_128k_sampled_at_full_size():
     # oracle can recompute in seconds is checked (two whole (sequence, KV head)
     # groups with their 8 query heads, plus encode of 4096 sampled keys from
     # every group), the rest through properties that hold at any size.
+    # The call is pariskv_retrieve_attend, the one the benchmark times (top-k with the
+    # attention fused into it, 8 estimates per thread); retrieve + sparse_attend must give
+    # the same bits for every head.
     cfg = workloads.CONFIGS["batch8_128k"]
     wc, K, V, Q, needles, signs = _inputs(cfg)
     print("case batch8_128k", flush=True)
     budget = pk.Budget(cfg.n_cand, cfg.n_collide, cfg.top_k)
-    run = GpuRun(K, V, Q, signs, wc.q_per_kv, budget, SCALE).retrieve()
+    run = GpuRun(K, V, Q, signs, wc.q_per_kv, budget, SCALE)
+    o_gpu = run.retrieve_attend()
     inter = run.intermediates()
-    o_gpu = run.attend()
+    sep_idx, sep_score, _ = pk.retrieve(run.cfg, run.index, run.Q, wc.n, budget,
+                                        out_score=torch.empty_like(run.out_score))
+    sep_o = pk.sparse_attend(run.cfg, run.Q, run.K, run.V, sep_idx, SCALE)
     torch.cuda.synchronize()
+    np.testing.assert_array_equal(sep_idx.cpu().numpy(), inter["idx"])
+    np.testing.assert_array_equal(sep_score.cpu().numpy().view(np.uint32), inter["score"].view(np.uint32))
+    np.testing.assert_array_equal(sep_o.cpu().numpy().view(np.uint32), o_gpu.view(np.uint32))
+    del sep_idx, sep_score, sep_o
     rng = np.random.default_rng(0)
     # encode, sampled keys of every group
     for s in range(wc.batch):
@@ -299,8 +314,8 @@ def test_batch8_128k_sampled_at_full_size():
             assert sel.min() >= th[s, hq, 0]
             assert np.sum(S[s, hq] > th[s, hq, 0]) == th[s, hq, 1]
     assert np.all(np.diff(inter["idx"], axis=-1) > 0)
-    # two whole groups through the oracle
-    for s, h in ((0, 0), (5, 3)):
+    # three whole groups through the oracle
+    for s, h in ((0, 0), (5, 3), (7, 7)):
         orc = oracle_group(K[s, h], signs)
         check_index(SLOT[run.index.ids[s, h].cpu().numpy()], run.index.rec[s, h].cpu().numpy(),
                     cnt[s, h].view(np.uint32), orc)
@@ -318,13 +333,16 @@ def test_host1m_sampled_at_full_size():
     # The 1M-key workload in its launch configuration, K/V in pinned host memory read
     # over the host link: one whole (KV head, 4 query heads) group through the oracle,
     # properties of every head, sampled encode of every group.
+    # The call is pariskv_retrieve_attend with host-mapped K/V, as the benchmark runs it.
     cfg = workloads.CONFIGS["host1m"]
     wc, K, V, Q, needles, signs = _inputs(cfg)
     print("case host1m", flush=True)
     budget = pk.Budget(cfg.n_cand, cfg.n_collide, cfg.top_k)
-    run = GpuRun(K, V, Q, signs, wc.q_per_kv, budget, SCALE).retrieve()
+    run = GpuRun(K, None, Q, signs, wc.q_per_kv, budget, SCALE)
+    Kh = torch.from_numpy(K).pin_memory()
+    Vh = torch.from_numpy(V).pin_memory()
+    o_gpu = run.retrieve_attend(Kh, Vh, host_mapped=True)
     inter = run.intermediates()
-    o_gpu = run.attend(host_mapped=True)
     rng = np.random.default_rng(1)
     from oracle import encode as oenc
     from parity import A, TAU

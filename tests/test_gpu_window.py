@@ -261,7 +261,13 @@ def test_tiered_attend_equals_window_attend_bit_for_bit(host):
     out = pk.tiered_attend(cfg, Qd, torch.from_numpy(Kw).cuda(), torch.from_numpy(Vw).cuda(), Kr_t, Vr_t, Id,
                            win, SCALE, kv_host_mapped=host)
     torch.cuda.synchronize()
-    np.testing.assert_array_equal(out.cpu().numpy().view(np.uint32), ref.cpu().numpy().view(np.uint32))
+    o = out.cpu().numpy()
+    np.testing.assert_array_equal(o.view(np.uint32), ref.cpu().numpy().view(np.uint32))
+    # and against the oracle over the true rows: Sink + Local/Buffer + retrieved
+    for hq in range(hkv * g):
+        retrieved = [win.retr_begin + int(j) for j in idx[0, hq] if j >= 0]
+        want = owin.window_attention(Q[0, hq], K[0, hq // g], V[0, hq // g], _dense(win), retrieved, SCALE)
+        _close(o[0, hq], want, hq)
 
 
 @pytest.mark.parametrize("n_cand,host", [(512, True), (4096, False), (34000, True)],
@@ -284,15 +290,38 @@ def test_fused_tiered_equals_separate_and_window_paths(n_cand, host):
     Kr, Vr = (torch.from_numpy(x) for x in (K, V))
     Kr, Vr = (Kr.pin_memory(), Vr.pin_memory()) if host else (Kd, Vd)
     sc1 = torch.empty((b, hkv * g, k), dtype=torch.float32, device="cuda")
-    i1, _, o1, _ = pk.retrieve_tiered_attend(cfg, index, Qd, n, budget, Kw, Vw, Kr, Vr, win, SCALE,
-                                             out_score=sc1, kv_host_mapped=host)
+    i1, _, o1, ws = pk.retrieve_tiered_attend(cfg, index, Qd, n, budget, Kw, Vw, Kr, Vr, win, SCALE,
+                                              out_score=sc1, kv_host_mapped=host)
+    torch.cuda.synchronize()
+    # the fused call against the oracle: retrieval over the Retrieval rows, then attention
+    # over Sink + winners + Local/Buffer
+    from parity import SLOT, ws_array
+    lay = pk.workspace_layout(cfg, b, n, budget)
+    inter = dict(
+        zq=ws_array(ws, lay["zq"], np.float32, (b, hkv * g, 128)),
+        lut=ws_array(ws, lay["lut"], np.uint32, (b, hkv, lay["quads"], 16, 256)),
+        S=ws_array(ws, lay["score8"], np.uint8, (b, hkv * g, lay["n_pad"])),
+        thresh=ws_array(ws, lay["thresh"], np.int32, (b, hkv * g, 4)),
+        cand=ws_array(ws, lay["cand"], np.int32, (b, hkv * g, budget.n_cand)),
+        cand_score=ws_array(ws, lay["cand_score"], np.float32, (b, hkv * g, budget.n_cand)),
+        idx=i1.cpu().numpy(), score=sc1.cpu().numpy())
+    o1h = o1.cpu().numpy()
+    signs = workloads.rotation_signs(28)
+    for h in range(hkv):
+        orc = oracle_group(K[0, h, sink:sink + n], signs)
+        for gg in range(g):
+            hq = h * g + gg
+            check_head(inter, 0, h, gg, g, Q[0, hq], orc, signs, budget, n)
+            retrieved = [sink + int(j) for j in inter["idx"][0, hq] if j >= 0]
+            _close(o1h[0, hq], owin.window_attention(Q[0, hq], K[0, h], V[0, h], _dense(win), retrieved, SCALE),
+                   (h, gg))
     i2, _, _ = pk.retrieve(cfg, index, Qd, n, budget)
     o2 = pk.tiered_attend(cfg, Qd, Kw, Vw, Kr, Vr, i2, win, SCALE, kv_host_mapped=host)
     _, _, o3, _ = pk.retrieve_window_attend(cfg, index, Qd, n, budget, Kd, Vd, win, SCALE)
     torch.cuda.synchronize()
     np.testing.assert_array_equal(i1.cpu().numpy(), i2.cpu().numpy())
     for o in (o2, o3):
-        np.testing.assert_array_equal(o1.cpu().numpy().view(np.uint32), o.cpu().numpy().view(np.uint32))
+        np.testing.assert_array_equal(o1h.view(np.uint32), o.cpu().numpy().view(np.uint32))
 
 
 @pytest.mark.parametrize("to_host", [True, False], ids=["to_pinned_host", "device_to_device"])

@@ -12,8 +12,10 @@
  *
  * General rules for every entry point
  *   - Device pointers are caller-owned memory on the current HIP device
- *     (for example torch tensors).  The library allocates no device memory,
- *     keeps no per-index state, and never synchronises a stream: every call
+ *     (for example torch tensors).  The library allocates no device memory
+ *     (its one device array is the static scratch of
+ *     pariskv_retrieve_attend_noalloc, part of its code object), keeps no
+ *     per-index state, and never synchronises a stream: every call
  *     validates its arguments on the host, enqueues kernels on `stream`
  *     (a hipStream_t; NULL = the default stream) and returns.
  *   - Validation happens before any launch.  On error nothing is enqueued
@@ -377,6 +379,39 @@ int pariskv_retrieve_tiered_attend(const pariskv_config* cfg, const pariskv_inde
 int pariskv_offload_rows(const void* K_src, const void* V_src, int64_t src_capacity, int64_t src_row,
                          void* K_dst, void* V_dst, int64_t dst_capacity, int64_t dst_row, int64_t t,
                          int32_t batch, int32_t n_kv_heads, void* stream);
+
+/* ------------------------------------------------- without a caller workspace */
+
+/* Bytes of the static scratch array pariskv_retrieve_attend_noalloc keeps its
+ * intermediates in, on every device the library runs on. */
+#define PARISKV_NOALLOC_SCRATCH_BYTES ((size_t)64 << 20)
+
+/* For callers that cannot allocate device memory: code under HIP graph capture,
+ * tight serving loops, harnesses that forbid hipMalloc.  pariskv_retrieve_attend
+ * without a workspace argument: the same out_idx, out_score and out, bit for bit,
+ * with the retrieve intermediates kept in a library-owned device array of
+ * PARISKV_NOALLOC_SCRATCH_BYTES (64 MiB) instead.  The array belongs to the
+ * library's code object: each device holds its own copy from the first call on
+ * it until the process ends, and its device address is looked up once per
+ * device, at that first call, with the device current.  The call itself
+ * allocates nothing (no hipMalloc, hipFree or allocating library routine; with
+ * the event profiler off), validates on the host, enqueues on `stream` (which
+ * must belong to the current device) and returns.
+ * Sharing: every call on one device uses the same array and leaves its
+ * intermediates there.  Calls that overlap on one device (unordered streams or
+ * host threads) race on it and give undefined outputs; order them.  Nothing in
+ * the array has to start at zero: a call writes every intermediate before it
+ * reads it.  pariskv_workspace_layout describes where they lie.
+ * Errors: those of pariskv_retrieve_attend; WORKSPACE when these shapes need
+ * more than PARISKV_NOALLOC_SCRATCH_BYTES of intermediates
+ * (pariskv_retrieve_workspace gives the need), checked before any HIP call;
+ * HIP also when the array's device address cannot be obtained. */
+int pariskv_retrieve_attend_noalloc(const pariskv_config* cfg, const pariskv_index* index,
+                                    const void* q, int64_t n, int32_t batch,
+                                    const pariskv_budget* budget, int32_t* out_idx,
+                                    float* out_score, const void* K, const void* V,
+                                    int32_t kv_host_mapped, int64_t kv_capacity, float scale,
+                                    float* out, void* stream);
 
 /* ------------------------------------------------------------ utilities */
 

@@ -20,6 +20,7 @@ import numpy as np
 __all__ = [
     "PariskvError", "Config", "Budget", "Index", "Window", "lib", "encode", "append", "append_rows",
     "retrieve", "retrieve_workspace_size", "workspace_layout", "sparse_attend", "retrieve_attend",
+    "retrieve_attend_noalloc", "NOALLOC_SCRATCH_BYTES",
     "window_regions", "window_attend", "retrieve_window_attend", "tiered_attend", "retrieve_tiered_attend",
     "offload_rows", "window_slot", "group_attend", "quantizer_table", "rotation_signs",
     "profile_enable", "profile_reset", "profile_read",
@@ -95,6 +96,8 @@ def lib():
         L.pariskv_workspace_layout.argtypes = [P(_Config), I32, I64, P(_Budget), P(_Layout)]
         L.pariskv_retrieve.argtypes = [P(_Config), P(_Index), VP, I64, I32, P(_Budget), VP, VP, VP,
                                        SZ, VP]
+        L.pariskv_retrieve_attend_noalloc.argtypes = [P(_Config), P(_Index), VP, I64, I32, P(_Budget), VP, VP,
+                                                      VP, VP, I32, I64, ctypes.c_float, VP, VP]
         L.pariskv_sparse_attend.argtypes = [P(_Config), VP, VP, VP, I32, I64, VP, I32, I32,
                                             ctypes.c_float, VP, VP]
         L.pariskv_retrieve_attend.argtypes = [P(_Config), P(_Index), VP, I64, I32, P(_Budget), VP, VP,
@@ -406,6 +409,31 @@ def retrieve_attend(cfg, index, q, n, budget, K, V, scale, out_idx=None, out_sco
                                          kp, vp, int(bool(kv_host_mapped)), cap, float(scale), op, wp,
                                          workspace.numel(), _stream(stream)))
     return out_idx, out_score, out, workspace
+
+
+NOALLOC_SCRATCH_BYTES = 64 << 20
+
+
+def retrieve_attend_noalloc(cfg, index, q, n, budget, K, V, scale, out_idx, out, out_score=None,
+                            kv_host_mapped=False, stream=None):
+    """pariskv_retrieve_attend_noalloc: retrieve_attend with the intermediates in the library's
+    static per-device scratch array (NOALLOC_SCRATCH_BYTES), for callers that cannot allocate.
+    Allocates nothing, so out_idx [batch][Hq][k] int32 and out [batch][Hq][D] float32 must be
+    given.  Calls that overlap on one device race on the shared array."""
+    import torch
+    dev = []
+    qp, batch = _q_arg(cfg, q, dev)
+    kp, vp, cap = _kv_args(cfg, batch, K, V, kv_host_mapped, dev)
+    rows = (batch, cfg.n_q_heads, budget.top_k)
+    ip = _arg(out_idx, "out_idx", torch.int32, rows, dev)
+    sp = _arg(out_score, "out_score", torch.float32, rows, dev, optional=True)
+    op = _arg(out, "out", torch.float32, (batch, cfg.n_q_heads, HEAD_DIM), dev)
+    ic = index.c(cfg, batch, dev)
+    _require_device(dev)
+    _check(lib().pariskv_retrieve_attend_noalloc(cfg.c(), ic, qp, int(n), batch, budget.c(), ip, sp,
+                                                 kp, vp, int(bool(kv_host_mapped)), cap, float(scale), op,
+                                                 _stream(stream)))
+    return out_idx, out_score, out
 
 
 def sparse_attend(cfg, q, K, V, idx, scale, out=None, kv_host_mapped=False, stream=None):

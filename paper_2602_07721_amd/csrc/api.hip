@@ -233,6 +233,37 @@ ProfEvents prof_begin(const char* name) {
     return {start, stop};
 }
 
+// ---- pariskv_retrieve_attend_noalloc: intermediates in a static device array
+
+// One copy per device, loaded with the code object and kept until the process ends.
+// In host code `scratch` names a host-side stand-in, never the device array: only the
+// address hipGetSymbolAddress returns for the current device is passed to kernels.
+static __device__ __align__(256) unsigned char scratch[PARISKV_NOALLOC_SCRATCH_BYTES];
+
+constexpr int kMaxScratchDevices = 64;
+std::mutex g_scratch_mu;
+void* g_scratch_ptr[kMaxScratchDevices] = {};
+
+// Device address of the current device's scratch array, looked up on its first use.
+int scratch_ptr(void** out) {
+    int dev = -1;
+    hipError_t e = hipGetDevice(&dev);
+    if (e != hipSuccess) return hip_fail(e, "hipGetDevice");
+    if (dev < 0 || dev >= kMaxScratchDevices)
+        return fail(PARISKV_ERR_UNSUPPORTED, "device %d above the %d devices served", dev, kMaxScratchDevices);
+    std::lock_guard<std::mutex> lk(g_scratch_mu);
+    if (!g_scratch_ptr[dev]) {
+        void* p = nullptr;
+        e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+        if (e != hipSuccess) return hip_fail(e, "hipGetSymbolAddress(scratch)");
+        if (!p || (reinterpret_cast<uintptr_t>(p) & 255u) != 0)
+            return fail(PARISKV_ERR_HIP, "scratch array at %p is not 256-byte aligned", p);
+        g_scratch_ptr[dev] = p;
+    }
+    *out = g_scratch_ptr[dev];
+    return PARISKV_OK;
+}
+
 }  // namespace pariskv
 
 using namespace pariskv;
@@ -575,6 +606,27 @@ int pariskv_retrieve_attend(const pariskv_config* cfg, const pariskv_index* inde
     const AttendReq att{K, V, kv_host_mapped, kv_capacity, scale, out, AttendWindow{}};
     return retrieve_impl(cfg, index, q, n, batch, budget, out_idx, out_score, workspace, ws_bytes,
                          stream, &att);
+}
+
+int pariskv_retrieve_attend_noalloc(const pariskv_config* cfg, const pariskv_index* index,
+                                    const void* q, int64_t n, int32_t batch,
+                                    const pariskv_budget* budget, int32_t* out_idx, float* out_score,
+                                    const void* K, const void* V, int32_t kv_host_mapped,
+                                    int64_t kv_capacity, float scale, float* out, void* stream) {
+    prof_chain_start();
+    pariskv_ws_layout L;
+    int rc = layout(cfg, batch, n, budget, &L);
+    if (rc) return rc;
+    if (L.total > PARISKV_NOALLOC_SCRATCH_BYTES)
+        return fail(PARISKV_ERR_WORKSPACE,
+                    "these shapes need %zu bytes of intermediates, above the %zu-byte static scratch; "
+                    "call pariskv_retrieve_attend with a workspace",
+                    L.total, (size_t)PARISKV_NOALLOC_SCRATCH_BYTES);
+    void* ws = nullptr;
+    if ((rc = scratch_ptr(&ws)) != PARISKV_OK) return rc;
+    const AttendReq att{K, V, kv_host_mapped, kv_capacity, scale, out, AttendWindow{}};
+    return retrieve_impl(cfg, index, q, n, batch, budget, out_idx, out_score, ws,
+                         PARISKV_NOALLOC_SCRATCH_BYTES, stream, &att);
 }
 
 int pariskv_retrieve_window_attend(const pariskv_config* cfg, const pariskv_index* index,

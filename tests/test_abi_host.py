@@ -215,6 +215,29 @@ def test_retrieve_attend_validation():
     assert call(size=need - 1) == pk.ERR_WORKSPACE
 
 
+def test_noalloc_validation_before_any_hip_call():
+    # The shapes are checked against the 64 MiB static scratch before the library
+    # touches HIP (no device here): 8 x 32 query heads over 300000 keys need more.
+    L = pk.lib()
+    b = pk.Budget(8192, 16384, 512)
+
+    def call(cfg, n, batch, K=FAKE, out=FAKE, bud=b):
+        return L.pariskv_retrieve_attend_noalloc(cfg.c(), ctypes.byref(_index()), ctypes.c_void_p(FAKE), n,
+                                                 batch, bud.c(), ctypes.c_void_p(FAKE), None,
+                                                 ctypes.c_void_p(K), ctypes.c_void_p(FAKE), 0, 4096,
+                                                 ctypes.c_float(0.1), ctypes.c_void_p(out), None)
+    big = _cfg(capacity=300000)
+    assert pk.retrieve_workspace_size(big, 8, 300000, b) > pk.NOALLOC_SCRATCH_BYTES
+    assert call(big, 300000, 8) == pk.ERR_WORKSPACE
+    assert b"static scratch" in L.pariskv_last_error()
+    # the bench workload's intermediates fit
+    assert pk.retrieve_workspace_size(_cfg(capacity=131072), 8, 131072, b) <= pk.NOALLOC_SCRATCH_BYTES
+    small = _cfg()
+    assert call(small, 5000, 1) == pk.ERR_INVALID                       # n above capacity
+    assert call(small, 4000, 1, bud=pk.Budget(512, 1024, 600)) == pk.ERR_INVALID  # k > C
+    assert pk.NOALLOC_SCRATCH_BYTES == 64 << 20
+
+
 @pytest.mark.parametrize("P,sink,local,m", [(10, 2, 4, 3), (5, 4, 4, 2), (2000, 128, 512, 256), (2000, 128, 512, 512),
                                             (700, 128, 512, 256), (100, 128, 512, 64), (3000, 0, 512, 1),
                                             (1000, 16, 8, 32), (0, 128, 512, 256), (130, 128, 512, 7)])

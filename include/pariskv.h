@@ -125,13 +125,19 @@ typedef struct pariskv_index {
  * tiers replace, App. "Coarse Candidate Generation"): every admitted cluster
  * scores 1 instead of its tier weight, so S_i is in [0, B]. */
 #define PARISKV_BINARY_COLLISIONS 1
+/* Diagnostic for pariskv_budget.flags: the collision scan histograms no score,
+ * so every selection threshold comes from the exact recount over the stored
+ * scores (see pariskv_ws_layout.thresh).  Same outputs, slower; it exercises
+ * the recount that otherwise runs only when the histogram floor is too high. */
+#define PARISKV_EXACT_RECOUNT 2
 
 /* Retrieval budgets of Alg. 1: C = ceil(beta n), C_rho = ceil(rho n), k. */
 typedef struct pariskv_budget {
     int64_t n_cand;    /* C, 1..PARISKV_MAX_CAND; clamped to n at run time    */
     int64_t n_collide; /* C_rho >= 1: keys covered by the admitted clusters   */
     int32_t top_k;     /* k, 1..min(C, PARISKV_MAX_TOPK)                      */
-    int32_t flags;     /* PARISKV_BINARY_COLLISIONS, or 0 (the paper's tiers) */
+    int32_t flags;     /* PARISKV_BINARY_COLLISIONS (else the paper's tiers),
+                          PARISKV_EXACT_RECOUNT, or 0                          */
 } pariskv_budget;
 
 /* Rows one query head attends at a decode step besides its retrieved keys
@@ -166,12 +172,19 @@ typedef struct pariskv_ws_layout {
                            h%4 of the word is query head 4*quad + h%4 of the group */
     size_t score8;      /* uint8 [batch][Hq][n_pad]: collision scores S_i        */
     size_t chunk_sfx;   /* uint32 [batch][Hq][n_chunks][98]: per chunk, #{S >= v}
-                           for v = 0..97                                        */
+                           for v = 0 and v_lo <= v <= 97; entries 1 <= v < v_lo
+                           hold #{S >= v_lo} (scores below the floor v_lo are
+                           not histogrammed, see thresh)                         */
     size_t chunk_base;  /* int32 [batch][Hq][n_chunks][2]: selected keys (S>theta,
                            S==theta) in earlier chunks                          */
-    size_t thresh;      /* int32 [batch][Hq][4]: theta, #(S>theta), quota, C_eff */
+    size_t thresh;      /* int32 [batch][Hq][8]: theta, #(S>theta), quota, C_eff,
+                           the histogram floor v_lo, 1 if the threshold came from
+                           the recount over the stored scores (else 0), 0, 0     */
     size_t cand;        /* int32 [batch][Hq][n_cand]: candidates, ascending      */
     size_t cand_score;  /* float [batch][Hq][n_cand]: RSQ-IP estimates           */
+    size_t stats;       /* float [batch][Hq][B][2]: per subspace, sum over the
+                           clusters of count * bonus and of count * bonus^2 (the
+                           moments that set the histogram floor v_lo)           */
     int64_t n_pad;      /* row length of score8 (n rounded up to 64)             */
     int64_t n_chunks;   /* ceil(n / chunk_keys)                                  */
     int64_t chunk_keys; /* keys per selection chunk                              */
@@ -250,7 +263,12 @@ int pariskv_workspace_layout(const pariskv_config* cfg, int32_t batch, int64_t n
  * them, gives tier weights 6..1 at cuts ceil({5,15,30,50,75,100}% * C_rho)
  * by the number of keys preceding the cluster, and sums over subspaces.
  * Selection keeps the min(C, n) best scores, ties at the threshold in
- * ascending key index.  Stage II estimates <k_i, q> for those candidates.
+ * ascending key index: theta is the largest v with #{S >= v} >= min(C, n).
+ * The scan histograms only scores at or above a per-head floor v_lo, one
+ * below a normal-law estimate of theta from the bonus moments (stats); when
+ * #{S >= v_lo} < min(C, n) the threshold is found by an exact recount over
+ * the stored scores instead, so the result never depends on the floor.
+ * Stage II estimates <k_i, q> for those candidates.
  * Errors: INVALID, UNSUPPORTED (C or k above the served maximum), WORKSPACE, HIP. */
 int pariskv_retrieve(const pariskv_config* cfg, const pariskv_index* index,
                      const void* q, int64_t n, int32_t batch,

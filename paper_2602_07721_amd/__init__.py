@@ -34,6 +34,8 @@ MAX_ATTEND_ROWS = 4096
 # Ablation variants (Sec. "Ablation Studies"): Config.flags, Budget.flags.
 NO_ROTATION, NO_ALPHA_CORRECTION = 1, 2
 BINARY_COLLISIONS = 1
+# Diagnostic Budget.flags bit: every selection threshold from the exact recount.
+EXACT_RECOUNT = 2
 
 
 class PariskvError(RuntimeError):
@@ -66,7 +68,7 @@ class _Window(ctypes.Structure):
 class _Layout(ctypes.Structure):
     _fields_ = [(name, ctypes.c_size_t) for name in
                 ("total", "zq", "lut", "score8", "chunk_sfx", "chunk_base", "thresh", "cand",
-                 "cand_score")] + \
+                 "cand_score", "stats")] + \
                [(name, ctypes.c_int64) for name in ("n_pad", "n_chunks", "chunk_keys", "c_eff")] + \
                [("quads", ctypes.c_int32), ("reserved", ctypes.c_int32)]
 

@@ -127,7 +127,7 @@ int layout(const pariskv_config* cfg, int32_t batch, int64_t n, const pariskv_bu
         return fail(PARISKV_ERR_INVALID, "top_k %d outside 1..n_cand", bud->top_k);
     if (bud->top_k > PARISKV_MAX_TOPK)
         return fail(PARISKV_ERR_UNSUPPORTED, "top_k %d above %d", bud->top_k, PARISKV_MAX_TOPK);
-    if (bud->flags & ~PARISKV_BINARY_COLLISIONS)
+    if (bud->flags & ~(PARISKV_BINARY_COLLISIONS | PARISKV_EXACT_RECOUNT))
         return fail(PARISKV_ERR_INVALID, "unknown budget flags 0x%x", bud->flags);
 
     const int64_t hkv = cfg->n_kv_heads, g = cfg->q_per_kv, hq = hkv * g;
@@ -150,9 +150,10 @@ int layout(const pariskv_config* cfg, int32_t batch, int64_t n, const pariskv_bu
     L->score8 = take((size_t)rows * L->n_pad);
     L->chunk_sfx = take((size_t)rows * L->n_chunks * kSfx * 4);
     L->chunk_base = take((size_t)rows * L->n_chunks * 2 * 4);
-    L->thresh = take((size_t)rows * 4 * 4);
+    L->thresh = take((size_t)rows * 8 * 4);
     L->cand = take((size_t)rows * bud->n_cand * 4);
     L->cand_score = take((size_t)rows * bud->n_cand * 4);
+    L->stats = take((size_t)rows * kB * 2 * 4);
     L->total = off;
     return PARISKV_OK;
 }
@@ -270,7 +271,7 @@ using namespace pariskv;
 
 extern "C" {
 
-int32_t pariskv_abi_version(void) { return 2; }
+int32_t pariskv_abi_version(void) { return 3; }
 
 const char* pariskv_strerror(int code) {
     switch (code) {
@@ -530,7 +531,8 @@ static int retrieve_impl(const pariskv_config* cfg, const pariskv_index* index, 
     a.c_eff = L.c_eff;
     a.top_k = budget->top_k;
     a.flags = ((cfg->flags & PARISKV_NO_ROTATION) ? kFlagNoRotation : 0u) |
-              ((budget->flags & PARISKV_BINARY_COLLISIONS) ? kFlagBinary : 0u);
+              ((budget->flags & PARISKV_BINARY_COLLISIONS) ? kFlagBinary : 0u) |
+              ((budget->flags & PARISKV_EXACT_RECOUNT) ? kFlagRecount : 0u);
     for (int l = 0; l < kTierCount; ++l) {
         static const int64_t pct[kTierCount] = {5, 15, 30, 50, 75, 100};
         // ceil(pct * C_rho / 100) in integers; start ranks never exceed 2^31.
@@ -552,6 +554,7 @@ static int retrieve_impl(const pariskv_config* cfg, const pariskv_index* index, 
     a.thresh = reinterpret_cast<int32_t*>(ws + L.thresh);
     a.cand = reinterpret_cast<int32_t*>(ws + L.cand);
     a.cand_score = reinterpret_cast<float*>(ws + L.cand_score);
+    a.stats = reinterpret_cast<float*>(ws + L.stats);
     a.out_idx = out_idx;
     a.out_score = out_score;
     a.sb = pack_signs(cfg->rot_signs);

@@ -35,6 +35,7 @@ __global__ __launch_bounds__(kAtThreads) void attend_kernel(const __half* __rest
     const int seq = (int)(row / hq);
     const int h = (int)(row % hq);
     const int64_t kvrow0 = ((int64_t)seq * hkv + h / g) * kv_capacity;
+    const uint4 qv = attend_query_part(q + row * kD);
     // Stage the row's list so the row loads never wait on it (the host checked
     // that dense rows + k fit kMaxAttendRows).
     const int32_t* ir = idx + row * k;
@@ -52,7 +53,7 @@ __global__ __launch_bounds__(kAtThreads) void attend_kernel(const __half* __rest
     }
     __syncthreads();
     const int64_t wrow0 = win.win_capacity > 0 ? ((int64_t)seq * hkv + h / g) * win.win_capacity : 0;
-    attend_row(q + row * kD, K + kvrow0 * kD, V + kvrow0 * kD, kv_capacity, Kw + wrow0 * kD,
+    attend_row(qv, K + kvrow0 * kD, V + kvrow0 * kD, kv_capacity, Kw + wrow0 * kD,
                Vw + wrow0 * kD, win.win_capacity, s_idx, nd + k, scale, out + row * kD, s_sm);
 }
 

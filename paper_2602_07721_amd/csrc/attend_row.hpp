@@ -43,11 +43,18 @@ __device__ __forceinline__ void unpack8_half(const uint4 v, float* f) {
     }
 }
 
-// q: the head's D float16 values; K, V: the KV head's rows [kv_capacity][D];
-// Kw, Vw: its window-cache rows [win_capacity][D] (entries with kWinRow);
-// list: k entries in LDS (already synchronised); out: D floats.  Every thread
-// of the block must call it; it ends with the block synchronised.
-__device__ __forceinline__ void attend_row(const __half* __restrict__ q, const __half* __restrict__ K,
+// The 16 bytes of the head's float16 query that thread `tid` uses: dims
+// [8 (tid & 15), 8 (tid & 15) + 8).  Callers load it first, so its latency
+// overlaps their own work.
+__device__ __forceinline__ uint4 attend_query_part(const __half* q_row) {
+    return reinterpret_cast<const uint4*>(q_row)[threadIdx.x & 15];
+}
+
+// qv: this thread's query part (attend_query_part); K, V: the KV head's rows
+// [kv_capacity][D]; Kw, Vw: its window-cache rows [win_capacity][D] (entries
+// with kWinRow); list: k entries in LDS (already synchronised); out: D floats.
+// Every thread of the block must call it; it ends with the block synchronised.
+__device__ __forceinline__ void attend_row(uint4 qv, const __half* __restrict__ K,
                                            const __half* __restrict__ V, int64_t kv_capacity,
                                            const __half* __restrict__ Kw, const __half* __restrict__ Vw,
                                            int64_t win_capacity, const int32_t* list, int32_t k,
@@ -57,7 +64,7 @@ __device__ __forceinline__ void attend_row(const __half* __restrict__ q, const _
     const int l16 = tid & 15;
 
     float qf[8];
-    unpack8_half(reinterpret_cast<const uint4*>(q)[l16], qf);
+    unpack8_half(qv, qf);
 #pragma unroll
     for (int d = 0; d < 8; ++d) qf[d] *= scale;
 

@@ -101,12 +101,7 @@ __global__ __launch_bounds__(kGaThreads) void group_attend_kernel(
         first[e] = (v != kGaInvalid && (p == 0 || sg.row[p - 1] != v)) ? 1u : 0u;
         cnt += first[e];
     }
-    uint32_t incl = cnt;
-#pragma unroll
-    for (int d = 1; d < 64; d <<= 1) {
-        const uint32_t o = __shfl_up(incl, d, 64);
-        if (lane >= d) incl += o;
-    }
+    const uint32_t incl = wave_incl_sum(cnt);
     if (lane == 63) sg.wsum[wave] = incl;
     __syncthreads();
     uint32_t before = incl - cnt;

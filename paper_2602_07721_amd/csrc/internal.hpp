@@ -18,8 +18,9 @@ constexpr int kCentroids = 256;   // 2^m
 constexpr int kRec = 128;         // bytes per rerank record
 constexpr int kMaxScore = 96;     // 6 * B
 constexpr int kBins = kMaxScore + 1;
-constexpr int kSfx = kBins + 1;     // suffix histogram entries v = 0..97 (entry 97 is 0)
+constexpr int kSfx = kBins + 1;   // suffix histogram entries v = 0..97 (entry 97 is 0)
 constexpr int kChunk = 4096;      // keys per collision / selection chunk
+constexpr int kThreshRow = 8;     // int32 per query head in the thresh array
 constexpr int kTierCount = 6;
 
 // Stored form of a centroid id (the ids array holds slot(c)): bits 5..7 kept,
@@ -47,6 +48,21 @@ __device__ __forceinline__ uint32_t lane_xor(uint32_t v, int lm, int lane) {
         case 16: return (uint32_t)__builtin_amdgcn_ds_swizzle((int)v, 0x1F | (16 << 10));
         default: return (uint32_t)__builtin_amdgcn_ds_bpermute((lane ^ 32) << 2, (int)v);
     }
+}
+
+// Inclusive sum over the 64 lanes of a wave through DPP moves, without LDS: shifts
+// of 1, 2, 4 and 8 lanes inside each row of 16 lanes, then the total of row 0 into
+// row 1 and of row 2 into row 3 (row_bcast:15), then lane 31's running total into
+// rows 2 and 3 (row_bcast:31).  Lanes a move cannot reach add 0.  Every lane of the
+// wave must be active.
+__device__ __forceinline__ uint32_t wave_incl_sum(uint32_t v) {
+    v += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x111, 0xF, 0xF, false);  // row_shr:1
+    v += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x112, 0xF, 0xF, false);  // row_shr:2
+    v += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x114, 0xF, 0xF, false);  // row_shr:4
+    v += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x118, 0xF, 0xF, false);  // row_shr:8
+    v += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x142, 0xA, 0xF, false);  // row_bcast:15
+    v += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x143, 0xC, 0xF, false);  // row_bcast:31
+    return v;
 }
 
 // Byte k of x shifted left (right) by 2 in one SDWA instruction: the byte
@@ -109,6 +125,7 @@ hipError_t launch_encode(const void* keys, int64_t n_src, int64_t src_stride, in
 constexpr uint32_t kFlagNoRotation = 1u;     // R = I (encode and query transform)
 constexpr uint32_t kFlagNoAlpha = 2u;        // W_b = sqrt(S_b) (encode)
 constexpr uint32_t kFlagBinary = 1u << 8;    // admitted clusters score 1 (bonus tables)
+constexpr uint32_t kFlagRecount = 1u << 9;   // no score histogrammed: threshold by recount
 
 // List-entry flag of the attention body: the entry names a row of the window
 // cache (Sink + Local / Update Buffer kept on the GPU), not of the main cache.
@@ -145,7 +162,7 @@ struct RetrieveArgs {
     int64_t n, n_pad, n_chunks, capacity;
     int64_t n_cand, c_eff;   // row stride of cand / cand_score, and min(C, n)
     int32_t top_k;
-    uint32_t flags;  // kFlagNoRotation, kFlagBinary
+    uint32_t flags;  // kFlagNoRotation, kFlagBinary, kFlagRecount
     uint32_t cuts[kTierCount];
     // inputs
     const void* q;
@@ -161,6 +178,7 @@ struct RetrieveArgs {
     int32_t* thresh;
     int32_t* cand;
     float* cand_score;
+    float* stats;      // [rows][B][2] bonus moments (the histogram floor)
     // outputs
     int32_t* out_idx;
     float* out_score;

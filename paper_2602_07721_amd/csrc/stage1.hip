@@ -45,15 +45,6 @@ namespace {
 
 // ---------------------------------------------------------------- helpers
 
-__device__ __forceinline__ uint32_t wave_incl_scan_u32(uint32_t v, int lane) {
-#pragma unroll
-    for (int d = 1; d < 64; d <<= 1) {
-        uint32_t o = __shfl_up(v, d, 64);
-        if (lane >= d) v += o;
-    }
-    return v;
-}
-
 // Ranking the 256 centroids of a subspace.  Flipping every sign of a centroid
 // negates its proxy, so once the 128 centroids with bit 7 clear are sorted, the
 // other 128 (their complements c ^ 255, keys from the same values) come in the
@@ -140,6 +131,37 @@ __device__ __forceinline__ void merge_complements_desc(int64_t (&key)[4], int la
     }
     order_pair(key[0], key[1], ~0ull);  // j = 1
     order_pair(key[2], key[3], ~0ull);
+}
+
+// The histogram floor v_lo of a query head: the collision scan histograms only scores
+// S >= v_lo.  It is one below a normal-law estimate of the selection threshold with the
+// subspaces' bonus weights taken as independent: mean sum_b E[bonus_b], variance
+// sum_b Var[bonus_b] from the moments stats[b] = (sum_c count_c bonus_c, sum_c count_c
+// bonus_c^2), and the upper-tail quantile z of the selected fraction p = C_eff / n by the
+// rational approximation of Abramowitz & Stegun 26.2.23 (|error| < 4.5e-4).  Keys that
+// resemble the query tend to be admitted in many subspaces at once, which fattens the
+// upper tail, so the estimate usually lies below the true threshold; when it does not,
+// the threshold kernel recounts (the floor never changes a result).  Floor 1 counts every
+// nonzero score (for p >= 1/2, where little would be saved).  The scan and the threshold
+// kernel evaluate this same function on the same inputs.
+__device__ __forceinline__ uint32_t hist_floor(const float* st, int64_t n, int64_t c_eff, uint32_t flags) {
+    if (flags & kFlagRecount) return kBins;  // above every score: nothing is histogrammed
+    const float inv_n = 1.0f / (float)n;
+    const float p = (float)c_eff * inv_n;
+    if (!(p < 0.5f)) return 1u;
+    float mu = 0.0f, var = 0.0f;
+#pragma unroll
+    for (int b = 0; b < kB; ++b) {
+        const float m1 = st[2 * b] * inv_n, m2 = st[2 * b + 1] * inv_n;
+        mu += m1;
+        var += fmaxf(m2 - m1 * m1, 0.0f);
+    }
+    const float t = sqrtf(-2.0f * logf(p));
+    const float z = t - (2.515517f + t * (0.802853f + t * 0.010328f)) /
+                            (1.0f + t * (1.432788f + t * (0.189269f + t * 0.001308f)));
+    const float est = mu + z * sqrtf(var) - 1.0f;
+    if (!(est >= 1.0f)) return 1u;
+    return est >= (float)kMaxScore ? (uint32_t)kMaxScore : (uint32_t)est;
 }
 
 // ---------------------------------------------------------------- query + LUT
@@ -242,14 +264,15 @@ __global__ __launch_bounds__(kLutThreads) void query_lut_kernel(RetrieveArgs a) 
             cc[r] = s_cnt[sub][cid[r]];
         }
         const uint32_t t0 = cc[0] + cc[1], t1 = cc[2] + cc[3];
-        const uint32_t incl0 = wave_incl_scan_u32(t0, lane);
-        const uint32_t incl1 = wave_incl_scan_u32(t1, lane);
+        const uint32_t incl0 = wave_incl_sum(t0);
+        const uint32_t incl1 = wave_incl_sum(t1);
         const uint32_t half = __shfl(incl0, 63, 64);  // counts of the first 128 ranks
         uint32_t starts[4];
         starts[0] = incl0 - t0;
         starts[1] = starts[0] + cc[0];
         starts[2] = half + incl1 - t1;
         starts[3] = starts[2] + cc[2];
+        float m1 = 0.0f, m2 = 0.0f;  // sum of count * bonus and count * bonus^2 (an estimate's input)
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
             const uint32_t start = starts[r];
@@ -261,6 +284,18 @@ __global__ __launch_bounds__(kLutThreads) void query_lut_kernel(RetrieveArgs a) 
             if (a.flags & kFlagBinary) bonus = bonus ? 1u : 0u;
             // The table is indexed like the stored ids, by slot.
             if (bonus) atomicOr(&s_lut[sub][id_slot((uint32_t)cid[r])], bonus << (8 * slot));
+            m1 += (float)cc[r] * (float)bonus;
+            m2 += (float)cc[r] * (float)(bonus * bonus);
+        }
+#pragma unroll
+        for (int d = 1; d < 64; d <<= 1) {
+            m1 += __uint_as_float(lane_xor(__float_as_uint(m1), d, lane));
+            m2 += __uint_as_float(lane_xor(__float_as_uint(m2), d, lane));
+        }
+        if (lane == 0) {
+            float* st = a.stats + (row * kB + b) * 2;
+            st[0] = m1;
+            st[1] = m2;
         }
     }
     __syncthreads();
@@ -305,6 +340,7 @@ __device__ __forceinline__ void wave_suffix97(uint32_t lo, uint32_t hi, int lane
 __global__ __launch_bounds__(kColThreads) void collide_kernel(RetrieveArgs a) {
     __shared__ uint32_t s_lut[kB * kCentroids];
     __shared__ uint32_t s_hist[kHistCopies * 4 * kHistStride];
+    __shared__ uint32_t s_floor[4];
 
     const int tid = threadIdx.x;
     const int lane = tid & 63;
@@ -335,7 +371,16 @@ __global__ __launch_bounds__(kColThreads) void collide_kernel(RetrieveArgs a) {
     for (int i = tid; i < kB * kCentroids / 4; i += kColThreads)
         reinterpret_cast<uint4*>(s_lut)[i] = lsrc[i];
     for (int i = tid; i < kHistCopies * 4 * kHistStride; i += kColThreads) s_hist[i] = 0;
+    // Histogram floor of each head (a slot past the quad's last head scores 0: none).
+    if (tid < 4) s_floor[tid] = tid < nh ? hist_floor(a.stats + (row0 + tid) * (kB * 2), a.n, a.c_eff, a.flags)
+                                         : (uint32_t)kBins;
     __syncthreads();
+    uint32_t floor_h[4];
+#pragma unroll
+    for (int h = 0; h < 4; ++h) floor_h[h] = s_floor[h];
+    // The floors are the same in every chunk of a row; the first chunk records them
+    // for the threshold kernel.
+    if (chunk == 0 && tid < nh) a.thresh[(row0 + tid) * kThreshRow + 4] = (int32_t)s_floor[tid];
 
     const int64_t c0 = chunk * kChunk;
     const int64_t c1 = min(c0 + (int64_t)kChunk, a.n);
@@ -373,12 +418,13 @@ __global__ __launch_bounds__(kColThreads) void collide_kernel(RetrieveArgs a) {
                 acc += s_lut[b * kCentroids + ((ww[b >> 2] >> (8 * (b & 3))) & 0xffu)];
             const bool live = i < nkeys;
             acc = live ? acc : 0u;  // a key past the end scores 0 for every head
-            // Exact per-value LDS histogram of the nonzero scores.  Slots of the last
-            // quad without a head have an all-zero bonus table, so score 0.
+            // Exact per-value LDS histogram of the scores at or above the head's floor
+            // (at least 1).  Slots of the last quad without a head have an all-zero
+            // bonus table, so score 0, and floor 97.
 #pragma unroll
             for (int h = 0; h < 4; ++h) {
                 const uint32_t sh = (acc >> (8 * h)) & 0xffu;
-                if (sh != 0u) atomicAdd(hcopy + h * kHistStride + sh, 1u);
+                if (sh >= floor_h[h]) atomicAdd(hcopy + h * kHistStride + sh, 1u);
             }
             // A wave stores 64 consecutive score bytes of a head per instruction.
             const uint32_t off = live ? i : kOffsetOutOfRange;
@@ -390,7 +436,8 @@ __global__ __launch_bounds__(kColThreads) void collide_kernel(RetrieveArgs a) {
 
     __syncthreads();
 
-    // Per-chunk suffix histogram of every head: sfx[v] = #{keys in chunk : S >= v}, v = 0..97.
+    // Per-chunk suffix histogram of every head: sfx[v] = #{keys in chunk : S >= v} for
+    // v = 0 and v >= floor; #{S >= floor} for 0 < v < floor.
     if (wave < nh) {
         const int h = wave;
         // Exact count of each value v >= 1: lane holds v = lane and v = 64 + lane.
@@ -404,7 +451,7 @@ __global__ __launch_bounds__(kColThreads) void collide_kernel(RetrieveArgs a) {
         const uint32_t lo = count_of(lane);
         const uint32_t hi = count_of(64 + lane);
         uint32_t sl, sh;
-        wave_suffix97(lo, hi, lane, &sl, &sh);  // exact for v >= 1
+        wave_suffix97(lo, hi, lane, &sl, &sh);  // exact for v >= floor
         if (lane == 0) sl = (uint32_t)(c1 - c0);
         uint32_t* dst = a.chunk_sfx + ((row0 + h) * a.n_chunks + chunk) * kSfx;
         dst[lane] = sl;
@@ -418,14 +465,29 @@ __global__ __launch_bounds__(kColThreads) void collide_kernel(RetrieveArgs a) {
 constexpr int kThrThreads = 1024;  // one block per query head
 constexpr int kThrWaves = kThrThreads / 64;
 
+// theta = largest v with #{S >= v} >= C, from a whole-row suffix histogram held as
+// (lo: v = lane, hi: v = 64 + lane), and gt = #{S > theta}.  Suffix counts fall with v
+// and #{S >= 0} = n >= C.
+__device__ __forceinline__ void theta_of(uint32_t ttl, uint32_t tth, uint32_t C, int lane, int* theta,
+                                         uint32_t* gt) {
+    const uint64_t ok_lo = __ballot(ttl >= C);
+    const uint64_t ok_hi = __ballot(lane < kBins - 64 && tth >= C);
+    const int th = ok_hi ? 64 + (63 - __clzll(ok_hi)) : (63 - __clzll(ok_lo));
+    *gt = th + 1 < 64 ? __shfl(ttl, th + 1, 64) : __shfl(tth, th + 1 - 64, 64);
+    *theta = th;
+}
+
 __global__ __launch_bounds__(kThrThreads) void threshold_kernel(RetrieveArgs a) {
     __shared__ uint32_t s_part[kThrWaves][2][64];
     __shared__ uint32_t s_wtot[2][kThrWaves];
-    __shared__ int s_theta;
+    __shared__ uint32_t s_hist[kBins];
+    __shared__ int s_theta, s_recount;
     const int tid = threadIdx.x;
     const int lane = tid & 63, wave = tid >> 6;
     const int64_t row = blockIdx.x;
-    const uint32_t* sfx = a.chunk_sfx + row * a.n_chunks * kSfx;
+    uint32_t* sfx = a.chunk_sfx + row * a.n_chunks * kSfx;
+    int32_t* t = a.thresh + row * kThreshRow;
+    const uint32_t fl = wave == 0 ? (uint32_t)t[4] : 0u;  // the floor the scan used
     // Whole-row suffix histogram; lane holds v = lane and v = 64 + lane.  Wave w
     // sums chunks w, w + 16, ... with 4 independent loads in flight.
     uint32_t tl[4], th[4];
@@ -449,21 +511,91 @@ __global__ __launch_bounds__(kThrThreads) void threshold_kernel(RetrieveArgs a) 
         uint32_t ttl = 0, tth = 0;
 #pragma unroll
         for (int w = 0; w < kThrWaves; ++w) { ttl += s_part[w][0][lane]; tth += s_part[w][1][lane]; }
-        // theta = largest v with #{S >= v} >= C (suffix counts fall with v; #{S >= 0} = n >= C).
-        const uint64_t ok_lo = __ballot(ttl >= C);
-        const uint64_t ok_hi = __ballot(lane < kBins - 64 && tth >= C);
-        const int theta = ok_hi ? 64 + (63 - __clzll(ok_hi)) : (63 - __clzll(ok_lo));
-        const uint32_t gt = theta + 1 < 64 ? __shfl(ttl, theta + 1, 64) : __shfl(tth, theta + 1 - 64, 64);
+        // The counts are exact for v = 0 and v >= the floor the scan used (it left it in
+        // t[4]).  With #{S >= floor} >= C (or floor 1) theta is found among them;
+        // otherwise it lies below the floor and the row's scores are recounted.
+        const uint32_t at_floor = fl < 64 ? __shfl(ttl, (int)fl, 64) : __shfl(tth, (int)fl - 64, 64);
+        const int recount = fl > 1u && at_floor < C;
+        if (!recount) {
+            int theta;
+            uint32_t gt;
+            theta_of(ttl, tth, C, lane, &theta, &gt);
+            if (lane == 0) {
+                t[0] = theta;
+                t[1] = (int32_t)gt;
+                t[2] = (int32_t)(C - gt);
+                t[3] = (int32_t)C;
+                s_theta = theta;
+            }
+        }
         if (lane == 0) {
-            int32_t* t = a.thresh + row * 4;
-            t[0] = theta;
-            t[1] = (int32_t)gt;
-            t[2] = (int32_t)(C - gt);
-            t[3] = (int32_t)C;
-            s_theta = theta;
+            t[5] = recount;
+            t[6] = t[7] = 0;
+            s_recount = recount;
         }
     }
     __syncthreads();
+    if (s_recount) {
+        // Exact histogram of the row's stored scores, then theta from it.
+        for (int i = tid; i < kBins; i += kThrThreads) s_hist[i] = 0;
+        __syncthreads();
+        const uint8_t* srow = a.score8 + row * a.n_pad;
+        for (int64_t i = (int64_t)tid * 16; i < a.n; i += (int64_t)kThrThreads * 16) {
+            const uint4 w = *reinterpret_cast<const uint4*>(srow + i);  // i + 16 <= n_pad
+            const uint32_t ww[4] = {w.x, w.y, w.z, w.w};
+#pragma unroll
+            for (int j = 0; j < 16; ++j)
+                if (i + j < a.n) atomicAdd(&s_hist[(ww[j >> 2] >> (8 * (j & 3))) & 0xffu], 1u);
+        }
+        __syncthreads();
+        if (wave == 0) {
+            uint32_t sl, sh;
+            wave_suffix97(s_hist[lane], lane < kBins - 64 ? s_hist[64 + lane] : 0u, lane, &sl, &sh);
+            int theta;
+            uint32_t gt;
+            theta_of(sl, sh, C, lane, &theta, &gt);
+            if (lane == 0) {
+                t[0] = theta;
+                t[1] = (int32_t)gt;
+                t[2] = (int32_t)(C - gt);
+                t[3] = (int32_t)C;
+                s_theta = theta;
+            }
+        }
+        __syncthreads();
+        const int theta = s_theta;
+        // Each chunk's exact #{S >= theta} and #{S > theta}, written over its suffix
+        // entries theta and theta + 1 for the chunk bases below: wave w takes chunks
+        // w, w + 16, ..., 16 bytes per lane and step.
+        for (int64_t c = wave; c < a.n_chunks; c += kThrWaves) {
+            uint32_t ge = 0, g = 0;
+#pragma unroll
+            for (int q = 0; q < kChunk / (64 * 16); ++q) {
+                const int64_t i = c * kChunk + (int64_t)(q * 64 + lane) * 16;
+                if (i < a.n) {
+                    const uint4 w = *reinterpret_cast<const uint4*>(srow + i);
+                    const uint32_t ww[4] = {w.x, w.y, w.z, w.w};
+#pragma unroll
+                    for (int j = 0; j < 16; ++j) {
+                        const int v = (int)((ww[j >> 2] >> (8 * (j & 3))) & 0xffu);
+                        const bool in = i + j < a.n;
+                        ge += (in && v >= theta) ? 1u : 0u;
+                        g += (in && v > theta) ? 1u : 0u;
+                    }
+                }
+            }
+#pragma unroll
+            for (int d = 1; d < 64; d <<= 1) {
+                ge += __shfl_xor(ge, d, 64);
+                g += __shfl_xor(g, d, 64);
+            }
+            if (lane == 0) {
+                sfx[c * kSfx + theta] = ge;
+                sfx[c * kSfx + theta + 1] = g;
+            }
+        }
+        __syncthreads();
+    }
     const int theta = s_theta;
     // Keys with S > theta and S == theta in the chunks before each chunk: thread t
     // takes chunk cb + t; wave scans, then a scan of the wave totals.
@@ -475,8 +607,8 @@ __global__ __launch_bounds__(kThrThreads) void threshold_kernel(RetrieveArgs a) 
             g = sfx[c * kSfx + theta + 1];
             e = sfx[c * kSfx + theta] - g;
         }
-        const uint32_t ig = wave_incl_scan_u32(g, lane);
-        const uint32_t ie = wave_incl_scan_u32(e, lane);
+        const uint32_t ig = wave_incl_sum(g);
+        const uint32_t ie = wave_incl_sum(e);
         if (lane == 63) { s_wtot[0][wave] = ig; s_wtot[1][wave] = ie; }
         __syncthreads();
         uint32_t pg = 0, pe = 0, tg = 0, te = 0;

@@ -39,15 +39,6 @@ constexpr int kRrThreads = 256;           // one 4096-key chunk per block, 16 ke
 constexpr int kRrSlots = kRrThreads / 8;  // candidates reranked per block iteration
 constexpr int kRrUnroll = 4;              // records in flight per lane
 
-__device__ __forceinline__ uint32_t wave_incl_scan32(uint32_t v, int lane) {
-#pragma unroll
-    for (int d = 1; d < 64; d <<= 1) {
-        uint32_t o = __shfl_up(v, d, 64);
-        if (lane >= d) v += o;
-    }
-    return v;
-}
-
 // Compaction of one chunk's candidates (Stage I selection) fused with their
 // RSQ-IP rerank (Stage II).  The selected keys of a chunk hold consecutive
 // positions [P0, P0 + m) of the row's ascending candidate list, so the block
@@ -66,7 +57,7 @@ __global__ __launch_bounds__(kRrThreads) void compact_rerank_kernel(RetrieveArgs
     const int64_t grp = (int64_t)seq * a.hkv + hq / a.g;
 
     // Everything this block reads up front.
-    const int32_t* th = a.thresh + row * 4;
+    const int32_t* th = a.thresh + row * kThreshRow;
     const uint32_t theta = (uint32_t)th[0];
     const uint32_t quota = (uint32_t)th[2];
     const int32_t* cb = a.chunk_base + (row * a.n_chunks + chunk) * 2;
@@ -100,7 +91,7 @@ __global__ __launch_bounds__(kRrThreads) void compact_rerank_kernel(RetrieveArgs
     }
     // Packed (gt, eq) counts: each at most 4096 per chunk, 16 bits each.
     const uint32_t mine = (uint32_t)__popc(gmask) | ((uint32_t)__popc(emask) << 16);
-    const uint32_t incl = wave_incl_scan32(mine, lane);
+    const uint32_t incl = wave_incl_sum(mine);
     if (lane == 63) s_wsum[wave] = incl;
     __syncthreads();
     uint32_t pre = incl - mine, tot = 0;
@@ -198,30 +189,30 @@ __device__ __forceinline__ float key_float(uint32_t k) {
     return __uint_as_float(u);
 }
 
-// Shared by both top-k kernels: suffix scan of a histogram by wave 0 to find
-// the digit holding the need-th largest element.  Lane L owns digits
-// NB-1-L*PER .. NB-PER-L*PER (descending); writes s_digit / s_need.
+// Shared by both top-k kernels, run by one whole wave: the digit holding the
+// need-th largest element of a histogram of NB bins.  Lane L owns bins
+// NB-1-L*PER .. NB-PER-L*PER (descending); a scan of the lane totals finds the
+// lane whose bins hold the crossing, then PER lanes take its bins from the
+// largest down and a second scan finds the bin.  Writes s_digit and s_need (the
+// rank inside that bin).  Needs 1 <= need <= the histogram's total.
 template <int NB>
 __device__ __forceinline__ void find_digit(const uint32_t* hist, uint32_t need, int lane, uint32_t* s_digit,
                                            uint32_t* s_need) {
     constexpr int PER = NB / 64;
+    static_assert(PER >= 1 && PER <= 64, "bins per lane");
     const uint32_t* h = hist + NB - PER * (lane + 1);  // this lane's bins, ascending
     uint32_t tot = 0;
 #pragma unroll 8
     for (int r = 0; r < PER; ++r) tot += h[r];
-    const uint32_t incl = wave_incl_scan32(tot, lane);
-    uint32_t above = incl - tot;  // elements with a larger digit than this lane's bins
-    if (above < need && above + tot >= need) {
-        // Exactly one lane holds the crossing; walk its bins from the largest down.
-        for (int r = PER - 1; r >= 0; --r) {
-            const uint32_t c = h[r];
-            if (above + c >= need) {
-                *s_digit = (uint32_t)(NB - PER * (lane + 1) + r);
-                *s_need = need - above;
-                break;
-            }
-            above += c;
-        }
+    const uint32_t above = wave_incl_sum(tot) - tot;  // elements with a larger digit
+    const int L = (int)__builtin_ctzll(__ballot(above < need && above + tot >= need));
+    const uint32_t above_L = __shfl(above, L, 64);
+    const int bin = NB - PER * (L + 1) + (PER - 1 - lane);  // lane r < PER: L's bins, largest first
+    const uint32_t c = lane < PER ? hist[bin] : 0u;
+    const uint32_t ci = wave_incl_sum(c);
+    if (lane == (int)__builtin_ctzll(__ballot(lane < PER && above_L + ci >= need))) {
+        *s_digit = (uint32_t)bin;
+        *s_need = need - (above_L + ci - c);
     }
 }
 
@@ -254,6 +245,8 @@ __global__ __launch_bounds__(TH) void topk_lds_kernel(RetrieveArgs a) {
     __shared__ uint32_t s_mm[2][kWaves];
     __shared__ uint32_t s_digit, s_need, s_nsmall;
     __shared__ uint32_t s_small[64];
+    // With kAttend the winners' estimates wait here until the attention is done.
+    __shared__ float s_wsc[kAttend ? PARISKV_MAX_TOPK : 1];
 
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int64_t row = blockIdx.x;
@@ -263,53 +256,68 @@ __global__ __launch_bounds__(TH) void topk_lds_kernel(RetrieveArgs a) {
     const int32_t* cand = a.cand + row * a.n_cand;
     if (tid == 0) s_nsmall = 0;
 
-    // Coalesced staging of the estimates as order-preserving keys.  The arrays start
-    // 256-byte aligned and a row is n_cand entries long, so the 16-byte loads are taken
-    // only when n_cand is a multiple of 4 (every row start then 16-byte aligned).
-    const bool vec16 = (a.n_cand & 3) == 0;
-    for (int p4 = tid; p4 < kCap / 4; p4 += TH) {
-        const int p = 4 * p4;
-        uint4 kv = make_uint4(0, 0, 0, 0);
-        int4 iv = make_int4(-1, -1, -1, -1);
-        if (vec16 && p + 3 < C) {
-            const float4 f = reinterpret_cast<const float4*>(sc)[p4];
-            kv = make_uint4(order_key(f.x), order_key(f.y), order_key(f.z), order_key(f.w));
-            if (kStageIdx) iv = reinterpret_cast<const int4*>(cand)[p4];
-        } else {
-            uint32_t k4[4] = {0, 0, 0, 0};
-            int32_t i4[4] = {-1, -1, -1, -1};
-#pragma unroll
-            for (int q = 0; q < 4; ++q)
-                if (p + q < C) {
-                    k4[q] = order_key(sc[p + q]);
-                    if (kStageIdx) i4[q] = cand[p + q];
-                }
-            kv = make_uint4(k4[0], k4[1], k4[2], k4[3]);
-            iv = make_int4(i4[0], i4[1], i4[2], i4[3]);
-        }
-        reinterpret_cast<uint4*>(s_key)[p4] = kv;
-        if (kStageIdx) reinterpret_cast<int4*>(s_idx)[p4] = iv;
-    }
-    for (int i = tid; i < 2 * kNB; i += TH) (&s_hist[0][0])[i] = 0;
-    __syncthreads();
+    // With kAttend, this thread's part of the query, requested first.
+    const uint4 qv = kAttend ? attend_query_part(static_cast<const __half*>(a.q) + row * kD)
+                             : make_uint4(0, 0, 0, 0);
 
-    uint32_t key[EPT];
+    // Staging of the estimates as order-preserving keys (and of the candidate
+    // indices): every load of the thread is issued before the first LDS store, and
+    // the smallest and largest valid keys are reduced on the way.  The arrays start
+    // 256-byte aligned and a row is n_cand entries long, so 16-byte loads are taken
+    // when n_cand is a multiple of 4 (every row start then 16-byte aligned); slots
+    // past the row re-read its last 16 bytes and are masked.
     uint32_t kmin = 0xffffffffu, kmax = 0u;
+    if ((a.n_cand & 3) == 0) {
+        constexpr int kIt = kCap / 4 / TH;
+        const int nq = (int)(a.n_cand >> 2);
+        float4 f[kIt];
+        int4 ix[kIt];
 #pragma unroll
-    for (int e4 = 0; e4 < EPT / 4; ++e4) {
-        const uint4 kv = reinterpret_cast<const uint4*>(s_key)[tid * (EPT / 4) + e4];
-        key[4 * e4] = kv.x; key[4 * e4 + 1] = kv.y; key[4 * e4 + 2] = kv.z; key[4 * e4 + 3] = kv.w;
+        for (int it = 0; it < kIt; ++it) {
+            const int p4 = min(tid + it * TH, nq - 1);
+            f[it] = reinterpret_cast<const float4*>(sc)[p4];
+            if (kStageIdx) ix[it] = reinterpret_cast<const int4*>(cand)[p4];
+        }
+#pragma unroll
+        for (int it = 0; it < kIt; ++it) {
+            const int p = 4 * (tid + it * TH);
+            const float fq[4] = {f[it].x, f[it].y, f[it].z, f[it].w};
+            uint32_t k4[4];
+#pragma unroll
+            for (int q = 0; q < 4; ++q) {
+                k4[q] = p + q < C ? order_key(fq[q]) : 0u;  // valid keys are all > 0
+                if (k4[q] != 0u) { kmin = min(kmin, k4[q]); kmax = max(kmax, k4[q]); }
+            }
+            reinterpret_cast<uint4*>(s_key)[tid + it * TH] = make_uint4(k4[0], k4[1], k4[2], k4[3]);
+            if (kStageIdx)
+                reinterpret_cast<int4*>(s_idx)[tid + it * TH] =
+                    make_int4(p < C ? ix[it].x : -1, p + 1 < C ? ix[it].y : -1, p + 2 < C ? ix[it].z : -1,
+                              p + 3 < C ? ix[it].w : -1);
+        }
+    } else {
+        for (int p = tid; p < kCap; p += TH) {
+            const uint32_t k1 = p < C ? order_key(sc[p]) : 0u;
+            if (k1 != 0u) { kmin = min(kmin, k1); kmax = max(kmax, k1); }
+            s_key[p] = k1;
+            if (kStageIdx) s_idx[p] = p < C ? cand[p] : -1;
+        }
     }
-#pragma unroll
-    for (int e = 0; e < EPT; ++e)
-        if (key[e] != 0u) { kmin = min(kmin, key[e]); kmax = max(kmax, key[e]); }
 #pragma unroll
     for (int d = 1; d < 64; d <<= 1) {
         kmin = min(kmin, (uint32_t)__shfl_xor(kmin, d, 64));
         kmax = max(kmax, (uint32_t)__shfl_xor(kmax, d, 64));
     }
     if (lane == 0) { s_mm[0][wave] = kmin; s_mm[1][wave] = kmax; }
+    for (int i = tid; i < 2 * kNB; i += TH) (&s_hist[0][0])[i] = 0;
     __syncthreads();
+
+    // Each thread then owns EPT consecutive candidates.
+    uint32_t key[EPT];
+#pragma unroll
+    for (int e4 = 0; e4 < EPT / 4; ++e4) {
+        const uint4 kv = reinterpret_cast<const uint4*>(s_key)[tid * (EPT / 4) + e4];
+        key[4 * e4] = kv.x; key[4 * e4 + 1] = kv.y; key[4 * e4 + 2] = kv.z; key[4 * e4 + 3] = kv.w;
+    }
 #pragma unroll
     for (int w = 0; w < kWaves; ++w) {
         kmin = min(kmin, s_mm[0][w]);
@@ -396,7 +404,16 @@ __global__ __launch_bounds__(TH) void topk_lds_kernel(RetrieveArgs a) {
         ne += (key[e] == T && key[e] != 0u) ? 1u : 0u;
     }
     const uint32_t mine = ng | (ne << 16);
-    const uint32_t incl = wave_incl_scan32(mine, lane);
+    // This thread's candidate indices, read before they are needed.
+    int32_t widx[EPT];
+    if (kStageIdx) {
+#pragma unroll
+        for (int e4 = 0; e4 < EPT / 4; ++e4) {
+            const int4 v4 = reinterpret_cast<const int4*>(s_idx)[tid * (EPT / 4) + e4];
+            widx[4 * e4] = v4.x; widx[4 * e4 + 1] = v4.y; widx[4 * e4 + 2] = v4.z; widx[4 * e4 + 3] = v4.w;
+        }
+    }
+    const uint32_t incl = wave_incl_sum(mine);
     if (lane == 63) s_w[wave] = incl;
     __syncthreads();
     uint32_t pre = incl - mine;
@@ -408,7 +425,9 @@ __global__ __launch_bounds__(TH) void topk_lds_kernel(RetrieveArgs a) {
     float* os = a.out_score ? a.out_score + row * a.top_k : nullptr;
     // With kAttend the attention list in region B is Sink rows, then Local +
     // Update Buffer rows (nd in all), then the winners at their cache rows
-    // (retr_begin + key; the host checked they stay below dense_begin).
+    // (retr_begin + key; the host checked they stay below dense_begin), and the
+    // outputs are written after the attention, so that its first loads do not
+    // wait behind these stores.
     const int nd = kAttend ? (int)a.win.dense_rows() : 0;
 #pragma unroll
     for (int e = 0; e < EPT; ++e) {
@@ -421,15 +440,21 @@ __global__ __launch_bounds__(TH) void topk_lds_kernel(RetrieveArgs a) {
             ++eb;
         }
         if (p < (uint32_t)kk) {
-            const int32_t win = kStageIdx ? s_idx[tid * EPT + e] : cand[tid * EPT + e];
-            oi[p] = win;
-            if (os) os[p] = key_float(key[e]);
-            if (kAttend) s_win[nd + p] = (int32_t)(a.win.retr_begin + win);
+            const int32_t win = kStageIdx ? widx[e] : cand[tid * EPT + e];
+            if (kAttend) {
+                s_win[nd + p] = (int32_t)(a.win.retr_begin + win);
+                s_wsc[p] = key_float(key[e]);
+            } else {
+                oi[p] = win;
+                if (os) os[p] = key_float(key[e]);
+            }
         }
     }
-    for (int r = kk + tid; r < a.top_k; r += TH) {
-        oi[r] = -1;
-        if (os) os[r] = -__builtin_huge_valf();
+    if (!kAttend) {
+        for (int r = kk + tid; r < a.top_k; r += TH) {
+            oi[r] = -1;
+            if (os) os[r] = -__builtin_huge_valf();
+        }
     }
     if (kAttend) {
         // Attention over the dense rows and the kk winners (Eqs. approx_weight,
@@ -441,13 +466,18 @@ __global__ __launch_bounds__(TH) void topk_lds_kernel(RetrieveArgs a) {
         const int64_t kvrow0 = ((int64_t)seq * a.hkv + h / a.g) * a.kv_capacity;
         const bool wc = a.win.win_capacity > 0;
         const int64_t wrow0 = wc ? ((int64_t)seq * a.hkv + h / a.g) * a.win.win_capacity : kvrow0;
-        attend_row(static_cast<const __half*>(a.q) + row * kD,
-                   static_cast<const __half*>(a.K) + kvrow0 * kD,
+        attend_row(qv, static_cast<const __half*>(a.K) + kvrow0 * kD,
                    static_cast<const __half*>(a.V) + kvrow0 * kD, a.kv_capacity,
                    static_cast<const __half*>(wc ? a.Kw : a.K) + wrow0 * kD,
                    static_cast<const __half*>(wc ? a.Vw : a.V) + wrow0 * kD, a.win.win_capacity,
                    s_win, nd + kk, a.scale,
                    a.attn_out + row * kD, *reinterpret_cast<AttendScratch*>(s_raw));
+        // The winners in ascending key index, then the padding.
+        for (int r = tid; r < a.top_k; r += TH) {
+            const bool w = r < kk;
+            oi[r] = w ? (int32_t)((int64_t)s_win[nd + r] - a.win.retr_begin) : -1;
+            if (os) os[r] = w ? s_wsc[r] : -__builtin_huge_valf();
+        }
     }
 }
 
@@ -528,7 +558,7 @@ __global__ __launch_bounds__(TH) void topk_reg_kernel(RetrieveArgs a) {
         ne += (key[e] == T && key[e] != 0u) ? 1u : 0u;
     }
     const uint32_t mine = ng | (ne << 16);
-    const uint32_t incl = wave_incl_scan32(mine, lane);
+    const uint32_t incl = wave_incl_sum(mine);
     if (lane == 63) s_w[wave] = incl;
     __syncthreads();
     uint32_t pre = incl - mine;

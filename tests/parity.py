@@ -118,7 +118,7 @@ class GpuRun:
             zq=ws_array(ws, L["zq"], np.float32, (b, hq, 128)),
             lut=ws_array(ws, L["lut"], np.uint32, (b, hkv, L["quads"], 16, 256)),
             S=ws_array(ws, L["score8"], np.uint8, (b, hq, L["n_pad"])),
-            thresh=ws_array(ws, L["thresh"], np.int32, (b, hq, 4)),
+            thresh=ws_array(ws, L["thresh"], np.int32, (b, hq, 8)),
             cand=ws_array(ws, L["cand"], np.int32, (b, hq, self.budget.n_cand)),
             cand_score=ws_array(ws, L["cand_score"], np.float32, (b, hq, self.budget.n_cand)),
             idx=self.out_idx.cpu().numpy(),
@@ -172,7 +172,13 @@ def check_head(inter, seq, kvh, g, q_per_kv, q, oracle, signs, budget, n, rotate
     np.testing.assert_array_equal(inter["S"][seq, hq, :n].astype(np.int64), r["S"])
     C = min(budget.n_cand, n)
     theta, gt, quota = oret.selection_threshold(r["S"], budget.n_cand)
-    np.testing.assert_array_equal(inter["thresh"][seq, hq], [theta, gt, quota, C])
+    np.testing.assert_array_equal(inter["thresh"][seq, hq, :4], [theta, gt, quota, C])
+    # the histogram floor the scan used, and whether the threshold came from the recount:
+    # the recount runs exactly when the floor overshoots #{S >= floor} >= C
+    floor, recount = int(inter["thresh"][seq, hq, 4]), int(inter["thresh"][seq, hq, 5])
+    assert 1 <= floor <= 97 and recount == int(floor > 1 and np.sum(r["S"] >= floor) < C)
+    if budget.flags & pk.EXACT_RECOUNT:
+        assert floor == 97 and recount == 1
     np.testing.assert_array_equal(inter["cand"][seq, hq, :C], r["cand"])
     # RSQ-IP estimates
     at = abs_terms(q, codes[r["cand"]], W[r["cand"]], signs, rotate)

@@ -31,7 +31,7 @@ def test_every_declared_symbol_is_exported():
     L = pk.lib()
     for n in names:
         assert hasattr(L, n), n
-    assert L.pariskv_abi_version() == 2
+    assert L.pariskv_abi_version() == 3
 
 
 def test_error_strings():
@@ -113,7 +113,7 @@ def test_workspace_layout_is_consistent():
     assert lay["total"] == pk.retrieve_workspace_size(cfg, 2, 4000, b)
     assert lay["n_pad"] == 4032 and lay["n_chunks"] == 1 and lay["c_eff"] == 512 and lay["quads"] == 1
     offs = [lay[k] for k in ("zq", "lut", "score8", "chunk_sfx", "chunk_base", "thresh", "cand",
-                             "cand_score")]
+                             "cand_score", "stats")]
     assert offs == sorted(offs) and all(o % 256 == 0 for o in offs) and lay["total"] > offs[-1]
     assert lay["score8"] - lay["lut"] >= 2 * 8 * 1 * 16 * 256 * 4
     lay2 = pk.workspace_layout(_cfg(q_per_kv=6), 1, 100, pk.Budget(512, 1024, 64))
@@ -325,7 +325,8 @@ def test_variant_flag_validation():
     assert L.pariskv_retrieve_workspace(bad.c(), 1, 4000, b.c()) == 0
     assert _encode(bad, _index()) == pk.ERR_INVALID
     assert pk.retrieve_workspace_size(_cfg(flags=pk.NO_ROTATION | pk.NO_ALPHA_CORRECTION), 1, 4000, b) > 0
-    assert L.pariskv_retrieve_workspace(_cfg().c(), 1, 4000, pk.Budget(512, 1024, 64, flags=2).c()) == 0
+    assert L.pariskv_retrieve_workspace(_cfg().c(), 1, 4000, pk.Budget(512, 1024, 64, flags=4).c()) == 0
+    assert pk.retrieve_workspace_size(_cfg(), 1, 4000, pk.Budget(512, 1024, 64, flags=pk.EXACT_RECOUNT)) > 0
     assert pk.retrieve_workspace_size(_cfg(), 1, 4000, pk.Budget(512, 1024, 64, flags=pk.BINARY_COLLISIONS)) > 0
 
 

@@ -106,6 +106,36 @@ def test_edge_shapes(name, batch, hkv, G, n, bud):
     _full_check(wc, K, V, Q, signs, pk.Budget(*bud), capacity=n + 37)
 
 
+RECOUNT = [
+    # name, batch, hkv, G, n, (C, C_rho, k)
+    ("ragged_two_chunks", 1, 1, 4, 4099, (512, 1024, 64)),
+    ("g6_two_quads", 1, 2, 6, 5000, (400, 800, 50)),
+    ("k_odd_ragged", 1, 1, 2, 777, (333, 555, 77)),
+    ("many_chunks", 1, 1, 1, 300000, (4096, 8192, 256)),
+    ("rows32_xcd_ragged", 4, 8, 4, 5000, (512, 1024, 64)),
+]
+
+
+@pytest.mark.parametrize("name,batch,hkv,G,n,bud", RECOUNT, ids=[e[0] for e in RECOUNT])
+def test_exact_recount_path(name, batch, hkv, G, n, bud):
+    # With PARISKV_EXACT_RECOUNT the scan histograms nothing and every threshold comes
+    # from the recount over the stored scores: the oracle must still match in full,
+    # and the outputs must equal those of the ordinary call bit for bit.
+    print(f"case recount {name} batch={batch} hkv={hkv} G={G} n={n} budget={bud}", flush=True)
+    wc = workloads.Config(name, batch=batch, n_kv_heads=hkv, q_per_kv=G, n=n, n_cand=bud[0],
+                          n_collide=bud[1], top_k=bud[2], seed=101 + len(name))
+    K, V = workloads.layer_kv(wc)
+    Q, _ = workloads.layer_queries(wc, K)
+    signs = workloads.rotation_signs(wc.seed)
+    run, inter, _ = _full_check(wc, K, V, Q, signs, pk.Budget(*bud, flags=pk.EXACT_RECOUNT), capacity=n + 37)
+    assert np.all(inter["thresh"][..., 5] == 1)
+    plain = GpuRun(K, V, Q, signs, G, pk.Budget(*bud), SCALE, capacity=n + 37).retrieve()
+    pi = plain.intermediates()
+    for k in ("cand", "cand_score", "idx", "score"):
+        np.testing.assert_array_equal(inter[k].view(np.uint32), pi[k].view(np.uint32))
+    np.testing.assert_array_equal(inter["thresh"][..., :4], pi["thresh"][..., :4])
+
+
 def test_degenerate_keys_and_queries():
     # duplicates (ties in S and in the estimates), zero keys, a zero query,
     # and one giant cluster (positive multiples of one key).
@@ -308,8 +338,12 @@ def test_batch8_128k_sampled_at_full_size():
     assert np.all(np.diff(cand, axis=-1) > 0) and cand.min() >= 0 and cand.max() < wc.n
     S = inter["S"][:, :, :wc.n]
     th = inter["thresh"]
+    # every head's threshold comes from the floored histogram, none from the recount
+    print(f"histogram floors {np.unique(th[..., 4]).tolist()}, recounts {int(th[..., 5].sum())}", flush=True)
+    assert np.all(th[..., 5] == 0) and np.all(th[..., 4] > 1)
     for s in range(wc.batch):
         for hq in range(wc.n_q_heads):
+            assert np.sum(S[s, hq] >= th[s, hq, 4]) >= C
             sel = S[s, hq, cand[s, hq]]
             assert sel.min() >= th[s, hq, 0]
             assert np.sum(S[s, hq] > th[s, hq, 0]) == th[s, hq, 1]

@@ -205,7 +205,7 @@ def test_decode_loop_with_buffer_updates_matches_the_oracle():
             zq=ws_array(ws, lay["zq"], np.float32, (b, hkv * g, 128)),
             lut=ws_array(ws, lay["lut"], np.uint32, (b, hkv, lay["quads"], 16, 256)),
             S=ws_array(ws, lay["score8"], np.uint8, (b, hkv * g, lay["n_pad"])),
-            thresh=ws_array(ws, lay["thresh"], np.int32, (b, hkv * g, 4)),
+            thresh=ws_array(ws, lay["thresh"], np.int32, (b, hkv * g, 8)),
             cand=ws_array(ws, lay["cand"], np.int32, (b, hkv * g, budget.n_cand)),
             cand_score=ws_array(ws, lay["cand_score"], np.float32, (b, hkv * g, budget.n_cand)),
             idx=idx.cpu().numpy(), score=sc.cpu().numpy())
@@ -301,7 +301,7 @@ def test_fused_tiered_equals_separate_and_window_paths(n_cand, host):
         zq=ws_array(ws, lay["zq"], np.float32, (b, hkv * g, 128)),
         lut=ws_array(ws, lay["lut"], np.uint32, (b, hkv, lay["quads"], 16, 256)),
         S=ws_array(ws, lay["score8"], np.uint8, (b, hkv * g, lay["n_pad"])),
-        thresh=ws_array(ws, lay["thresh"], np.int32, (b, hkv * g, 4)),
+        thresh=ws_array(ws, lay["thresh"], np.int32, (b, hkv * g, 8)),
         cand=ws_array(ws, lay["cand"], np.int32, (b, hkv * g, budget.n_cand)),
         cand_score=ws_array(ws, lay["cand_score"], np.float32, (b, hkv * g, budget.n_cand)),
         idx=i1.cpu().numpy(), score=sc1.cpu().numpy())

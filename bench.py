@@ -47,8 +47,9 @@ def parse():
     ap.add_argument("--no-flush", action="store_true", help="keep caches warm between steps")
     ap.add_argument("--no-profile", action="store_true", help="no per-kernel events in the timed steps")
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--cpu-groups", type=int, default=8)
-    ap.add_argument("--cpu-steps", type=int, default=8)
+    ap.add_argument("--cpu-groups", type=int, default=64,
+                    help="(sequence, KV head) groups the oracle baseline samples, at most one per host core")
+    ap.add_argument("--cpu-steps", type=int, default=4)
     ap.add_argument("--separate", action="store_true",
                     help="run the step as pariskv_retrieve + pariskv_sparse_attend instead of the fused "
                          "pariskv_retrieve_attend")
@@ -65,8 +66,7 @@ def parse():
     ap.add_argument("--offload-steps", type=int, default=0,
                     help="also run the 1M-token offload setting (GPU window ring, Retrieval K/V in pinned "
                          "host memory, buffer updates offloaded on a second stream) for this many steps")
-    ap.add_argument("--copy-calibration", action="store_true",
-                    help="also run one plain 1 GiB device copy (for scaling HBM counters)")
+    ap.add_argument("--no-warm", action="store_true", help="skip the warm-cache loop")
     return ap.parse_args()
 
 
@@ -123,45 +123,75 @@ def measured_traffic(workload):
     return {}
 
 
-def cpu_baseline(wc, K, V, Qs, signs, budget, scale, groups, steps):
-    """Time the oracle's retrieve + attend on a bounded sample, scaled to a whole step."""
+def _oracle_worker(wname, seq, kvh, steps, start, results):
+    """Child process (spawned: no torch, no GPU): regenerate one (sequence, KV head)
+    group of a workload from its seeds, encode it with the oracle (prefill, untimed),
+    wait for the other workers, then time the oracle's retrieve + attend of the group's
+    query heads over `steps` decode steps, single-threaded."""
     import numpy as np
     from threadpoolctl import threadpool_limits
 
+    import workloads
     from oracle import attention as oatt
     from oracle import encode as oenc
     from oracle import quantizer as oq
     from oracle import retrieve as oret
 
+    wc = workloads.CONFIGS[wname]
+    signs = workloads.rotation_signs(wc.seed)
     tau, a, _ = oq.lloyd_max(8)
-    picks = [(s % wc.batch, (s * 3) % wc.n_kv_heads) for s in range(groups)]
-    index = {}
-    for (s, h) in picks:  # prefill, not part of a decode step: untimed
-        ids, codes, W = oenc.encode(K[s, h], signs, tau, a, 16)
-        index[(s, h)] = (ids, codes, W, oenc.cluster_counts(ids, 8))
+    K = workloads.head_keys(wc.seed, seq, kvh, wc.n)
+    V = workloads.head_values(wc.seed, seq, kvh, wc.n)
+    Qs = [workloads.needle_queries(K, wc.seed, seq, kvh, wc.q_per_kv, st)[0] for st in range(steps)]
+    scale = 1.0 / np.sqrt(wc.head_dim)
     with threadpool_limits(limits=1):
+        ids, codes, W = oenc.encode(K, signs, tau, a, 16)
+        cnt = oenc.cluster_counts(ids, 8)
+        start.wait()
         t0 = time.perf_counter()
         for st in range(steps):
-            Q = Qs[st]
-            for (s, h) in picks:
-                ids, codes, W, cnt = index[(s, h)]
-                for g in range(wc.q_per_kv):
-                    q = Q[s, h * wc.q_per_kv + g]
-                    r = oret.retrieve_head(q, ids, codes, W, cnt, signs, a, 16, budget.n_cand,
-                                           budget.n_collide, budget.top_k)
-                    oatt.sparse_attention(q, K[s, h], V[s, h], r["idx"], scale=scale)
-        el = time.perf_counter() - t0
-    per_group_step = el / (groups * steps)
+            for g in range(wc.q_per_kv):
+                q = Qs[st][g]
+                r = oret.retrieve_head(q, ids, codes, W, cnt, signs, a, 16, wc.n_cand, wc.n_collide, wc.top_k)
+                oatt.sparse_attention(q, K, V, r["idx"], scale=scale)
+        results.put(time.perf_counter() - t0)
+
+
+def cpu_baseline(wname, groups, steps):
+    """The oracle's retrieve + attend timed on the host cores: one spawned process per
+    sampled (sequence, KV head) group, all timed together after a common start, each
+    single-threaded.  Returns the whole-layer step time the cores sustain."""
+    import multiprocessing as mp
+
+    import workloads
+
+    wc = workloads.CONFIGS[wname]
+    cores = len(os.sched_getaffinity(0))
+    total = wc.batch * wc.n_kv_heads
+    groups = max(1, min(groups, cores, total))
+    picks = [((g * 3) % wc.batch, (g * 5) % wc.n_kv_heads) if total > groups else (g // wc.n_kv_heads,
+             g % wc.n_kv_heads) for g in range(groups)]
+    ctx = mp.get_context("spawn")
+    start = ctx.Barrier(groups)
+    results = ctx.Queue()
+    procs = [ctx.Process(target=_oracle_worker, args=(wname, s, h, steps, start, results)) for s, h in picks]
+    for p in procs:
+        p.start()
+    el = [results.get() for _ in procs]
+    for p in procs:
+        p.join()
+    per_group_step = float(sum(el)) / (groups * steps)  # seconds, one core busy
+    # `groups` cores work in parallel; a layer step is `total` group-steps.
+    value = per_group_step * total / groups * 1e6
     return {
-        "value": per_group_step * wc.batch * wc.n_kv_heads * 1e6,
+        "value": round(value, 1),
         "unit": "us/step/layer",
-        "cores": 1,
+        "cores": groups,
         "kind": "oracle",
-        "sample": (f"{groups} of {wc.batch * wc.n_kv_heads} (sequence, KV head) groups x "
-                   f"{wc.q_per_kv} query heads x {steps} steps of retrieve+attend "
-                   f"({el:.1f} s single-threaded NumPy float64), scaled x"
-                   f"{wc.batch * wc.n_kv_heads} to one whole step; host has "
-                   f"{len(os.sched_getaffinity(0))} cores available"),
+        "sample": (f"{wname}: {groups} of {total} (sequence, KV head) groups, one per core, each "
+                   f"single-threaded NumPy float64 retrieve+attend for its {wc.q_per_kv} query heads x "
+                   f"{steps} steps ({sum(el):.1f} s of CPU work, {max(el):.1f} s wall), scaled to all "
+                   f"{total} groups of a step on {groups} cores; host has {cores} cores"),
     }
 
 
@@ -694,6 +724,15 @@ def main():
               f"of a larger run would repeat the one-GPU figure.", file=sys.stderr)
         sys.exit(2)
 
+    # The oracle baselines run first, in spawned child processes, before this process
+    # touches the GPU.
+    cpu = cpu32 = None
+    if not args.no_cpu_baseline:
+        cpu = cpu_baseline(args.workload, args.cpu_groups, args.cpu_steps)
+        if args.workload == "batch8_128k":
+            cpu32 = cpu_baseline("layer32k", 8, args.cpu_steps)
+        print(f"[bench] oracle baselines done", file=sys.stderr, flush=True)
+
     import numpy as np
     import torch
 
@@ -786,12 +825,42 @@ def main():
     # themselves lengthen that loop's steps, so it does not set the value).
     step_ms, wall, _ = timed_loop(False)
     prof_step_ms, _, prof = timed_loop(not args.no_profile) if not args.no_profile else (None, None, {})
+    warm_ms = None
+    if not args.no_warm and not args.no_flush:
+        # The same steps back to back without the flush: the index and K/V rows that the
+        # previous step touched may still sit in the 256 MB Infinity Cache and the L2s.
+        flag = args.no_flush
+        args.no_flush = True
+        warm_ms, _, _ = timed_loop(False)
+        args.no_flush = flag
 
     # Needle hit rate on the last step (a sanity figure, not a parity check).
     _, needles = workloads.layer_queries(wc, K, step=total_steps - 1)
     idx_h = out_idx.cpu().numpy()
     hits = float(np.mean([needles[s, h] in set(idx_h[s, h].tolist())
                           for s in range(wc.batch) for h in range(hq)]))
+
+    # Achievable ceilings on this GPU: the library's reference streaming copy of 1 GiB
+    # (read + write) and streaming read of 1 GiB, best of 5 each.
+    def best_of(fn, reps=5):
+        best = None
+        for _ in range(reps):
+            c0, c1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            c0.record()
+            fn()
+            c1.record()
+            torch.cuda.synchronize()
+            t = c0.elapsed_time(c1) * 1e-3
+            best = t if best is None else min(best, t)
+        return best
+
+    src = torch.empty(1 << 30, dtype=torch.uint8, device=dev)
+    dst = torch.empty_like(src)
+    src.fill_(1)
+    torch.cuda.synchronize()
+    copy_gbs = 2 * src.numel() / best_of(lambda: pk.stream_copy(dst, src)) / 1e9
+    del src, dst
+    read_gbs = flush.numel() * 4 / best_of(lambda: pk.stream_read(flush, flush_sink)) / 1e9
 
     c_eff = min(wc.n_cand, wc.n)
     algo = algorithmic_bytes(wc, c_eff)
@@ -810,29 +879,24 @@ def main():
     roofline = None
     if dominant:
         kr = kernels[dominant]
+        tr = traffic.get(dominant)
         roofline = {"bound": "hbm", "kernel": dominant, "achieved": round(kr["GBps"], 1),
                     "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": round(kr["frac_hbm_peak"], 4),
-                    "traffic": traffic.get(dominant),
-                    "algorithmic_bytes": algo[dominant]}
+                    "traffic": tr,
+                    "algorithmic_bytes": algo[dominant],
+                    # the same kernel against the copy ceiling measured in this run, and its
+                    # measured HBM bytes (counters) per launch over the same duration
+                    "frac_copy_ceiling": round(kr["GBps"] / copy_gbs, 4),
+                    "traffic_frac_hbm_peak": (round(tr / (kr["avg_us"] * 1e-6) / 1e9 / HBM_PEAK_GBS, 4)
+                                              if tr else None)}
     for name, row in kernels.items():
+        if "GBps" in row:
+            row["frac_copy_ceiling"] = row["GBps"] / copy_gbs
         if name in traffic:
             row["hbm_traffic_bytes"] = traffic[name]
+            row["traffic_frac_hbm_peak"] = traffic[name] / (row["avg_us"] * 1e-6) / 1e9 / HBM_PEAK_GBS
     collide_gbs = kernels.get("collide", {}).get("GBps")
 
-    if args.copy_calibration:
-        src = torch.empty(1 << 30, dtype=torch.uint8, device=dev)
-        dst = torch.empty_like(src)
-        src.fill_(1)
-        torch.cuda.synchronize()
-        c0, c1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-        c0.record()
-        dst.copy_(src)
-        c1.record()
-        torch.cuda.synchronize()
-        copy_gbs = 2 * src.numel() / (c0.elapsed_time(c1) * 1e-3) / 1e9
-        del src, dst
-    else:
-        copy_gbs = None
 
     extras = {}
     if args.extras:
@@ -862,10 +926,6 @@ def main():
         torch.cuda.empty_cache()
         extras["offload"] = offload_run(pk, torch, np, workloads, dev, args.offload_steps)
 
-    cpu = None
-    if not args.no_cpu_baseline:
-        cpu = cpu_baseline(wc, K, V, Qs, signs, budget, scale, args.cpu_groups,
-                           min(args.cpu_steps, total_steps))
 
     mean_us = float(step_ms.mean() * 1e3)
     result = {
@@ -896,16 +956,22 @@ def main():
         "wall_ms_per_step_incl_flush": round(wall / args.steps * 1e3, 4),
         "profiled_loop_us_per_step": (round(float(prof_step_ms.mean() * 1e3), 2)
                                       if prof_step_ms is not None else None),
+        "warm_us": round(float(warm_ms.mean() * 1e3), 2) if warm_ms is not None else None,
+        "warm_p10_us": round(float(np.percentile(warm_ms, 10) * 1e3), 2) if warm_ms is not None else None,
+        "warm_p90_us": round(float(np.percentile(warm_ms, 90) * 1e3), 2) if warm_ms is not None else None,
         "code_scan_GBps": round(collide_gbs, 1) if collide_gbs else None,
         "code_scan_frac_hbm_peak": round(collide_gbs / HBM_PEAK_GBS, 4) if collide_gbs else None,
+        "code_scan_frac_copy_ceiling": round(collide_gbs / copy_gbs, 4) if collide_gbs else None,
         "roofline": roofline,
         "kernels": {k: {kk: (round(vv, 3) if isinstance(vv, float) else vv) for kk, vv in v.items()}
                     for k, v in sorted(kernels.items())},
         "encode": {"ms": round(enc_ms, 3), "keys_per_s": round(n_keys / (enc_ms * 1e-3), 1),
                    "GBps": round(n_keys * (256 + 144) / (enc_ms * 1e-3) / 1e9, 1)},
         "needle_hit_rate": round(hits, 4),
-        "copy_GBps": round(copy_gbs, 1) if copy_gbs else None,
+        "copy_GBps": round(copy_gbs, 1),
+        "read_GBps": round(read_gbs, 1),
         "cpu_baseline": cpu,
+        "cpu_baseline_layer32k": cpu32,
     }
     result.update(extras)
     print(json.dumps(result), flush=True)

@@ -264,8 +264,8 @@ int pariskv_workspace_layout(const pariskv_config* cfg, int32_t batch, int64_t n
  * by the number of keys preceding the cluster, and sums over subspaces.
  * Selection keeps the min(C, n) best scores, ties at the threshold in
  * ascending key index: theta is the largest v with #{S >= v} >= min(C, n).
- * The scan histograms only scores at or above a per-head floor v_lo, one
- * below a normal-law estimate of theta from the bonus moments (stats); when
+ * The scan histograms only scores at or above a per-head floor v_lo, the
+ * integer part of a normal-law estimate of theta from the bonus moments (stats); when
  * #{S >= v_lo} < min(C, n) the threshold is found by an exact recount over
  * the stored scores instead, so the result never depends on the floor.
  * Stage II estimates <k_i, q> for those candidates.
@@ -447,6 +447,17 @@ int pariskv_quantizer_table(int32_t m, double* tau, double* a);
  * values to host memory `out`, ready for pariskv_config.rot_signs.  Host only.
  * Errors: INVALID for D < 1 or a null `out`. */
 int pariskv_rotation_signs(uint64_t seed, int32_t D, int8_t* out);
+
+/* Reference streaming kernels for measurement (not part of the retrieval path):
+ * a plain copy of `bytes` from src to dst, and a plain read of `bytes` of src,
+ * both device memory, 16-byte aligned, bytes a multiple of 16.  They state the
+ * HBM bandwidth this GPU achieves for a pure stream, and scale HBM counters (a
+ * copy of known size moves exactly 2 x bytes).  The read folds the data into one
+ * word per thread and stores it to device `sink` (4 bytes) only if it equals
+ * `key`, so its loads cannot be removed.
+ * Errors: INVALID (NULL or misaligned pointers, bytes not a multiple of 16), HIP. */
+int pariskv_stream_copy(void* dst, const void* src, size_t bytes, void* stream);
+int pariskv_stream_read(const void* src, size_t bytes, uint32_t key, uint32_t* sink, void* stream);
 
 /* Per-kernel timing with HIP events attached to the kernel dispatches on the
  * launch stream.  The first kernel of a call is timed from its dispatch to its

@@ -23,7 +23,7 @@ __all__ = [
     "retrieve_attend_noalloc", "NOALLOC_SCRATCH_BYTES",
     "window_regions", "window_attend", "retrieve_window_attend", "tiered_attend", "retrieve_tiered_attend",
     "offload_rows", "window_slot", "group_attend", "quantizer_table", "rotation_signs",
-    "profile_enable", "profile_reset", "profile_read",
+    "profile_enable", "profile_reset", "profile_read", "stream_copy", "stream_read",
 ]
 
 LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libpariskv.so")
@@ -112,6 +112,8 @@ def lib():
         L.pariskv_group_attend.argtypes = [P(_Config), VP, VP, VP, I32, I64, VP, I32, I32, ctypes.c_float, VP,
                                            VP, VP]
         L.pariskv_offload_rows.argtypes = [VP, VP, I64, I64, VP, VP, I64, I64, I64, I32, I32, VP]
+        L.pariskv_stream_copy.argtypes = [VP, VP, SZ, VP]
+        L.pariskv_stream_read.argtypes = [VP, SZ, ctypes.c_uint32, VP, VP]
         L.pariskv_quantizer_table.argtypes = [I32, P(ctypes.c_double), P(ctypes.c_double)]
         L.pariskv_rotation_signs.argtypes = [ctypes.c_uint64, I32, P(ctypes.c_int8)]
         L.pariskv_profile_enable.argtypes = [I32]
@@ -557,6 +559,24 @@ def offload_rows(K_src, V_src, src_row, K_dst, V_dst, dst_row, t, stream=None):
             raise ValueError(f"{nm} must be device or pinned host memory")
     _check(lib().pariskv_offload_rows(ps[0], ps[1], src_cap, int(src_row), ps[2], ps[3], dst_cap, int(dst_row),
                                       int(t), b, hkv, _stream(stream)))
+
+
+def stream_copy(dst, src, stream=None):
+    """Reference streaming copy of src into dst (device tensors of equal byte size, a
+    multiple of 16): measurement only."""
+    nb = src.numel() * src.element_size()
+    if dst.numel() * dst.element_size() != nb:
+        raise ValueError("dst and src must hold the same number of bytes")
+    _check(lib().pariskv_stream_copy(_ptr(dst, "dst"), _ptr(src, "src"), nb, _stream(stream)))
+
+
+def stream_read(src, sink, key=0xFFFFFFFF, stream=None):
+    """Reference streaming read of src (a device tensor, multiple of 16 bytes); writes sink
+    (a 4-byte device tensor) only if the folded data equals key: measurement only."""
+    if sink.numel() * sink.element_size() < 4:
+        raise ValueError("sink needs 4 bytes")
+    _check(lib().pariskv_stream_read(_ptr(src, "src"), src.numel() * src.element_size(), key,
+                                     _ptr(sink, "sink"), _stream(stream)))
 
 
 def quantizer_table(m=8):

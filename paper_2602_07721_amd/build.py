@@ -34,7 +34,8 @@ HIP_FLAGS = [
 ]
 # Files whose float64 decision path is specified operation by operation.
 EXACT_FP = {"encode.hip", "stage1.hip"}
-HIP_SOURCES = ["api.hip", "encode.hip", "stage1.hip", "stage2.hip", "attend.hip", "group_attend.hip"]
+HIP_SOURCES = ["api.hip", "encode.hip", "stage1.hip", "stage2.hip", "attend.hip", "group_attend.hip",
+               "calib.hip"]
 CXX_SOURCES = ["quantizer.cpp"]
 
 

@@ -799,6 +799,22 @@ int pariskv_offload_rows(const void* K_src, const void* V_src, int64_t src_capac
     return PARISKV_OK;
 }
 
+int pariskv_stream_copy(void* dst, const void* src, size_t bytes, void* stream) {
+    prof_chain_start();
+    if (!dst || !src || !aligned16(dst) || !aligned16(src) || bytes % 16 != 0)
+        return fail(PARISKV_ERR_INVALID, "stream copy needs 16-byte aligned pointers and a multiple of 16 bytes");
+    const hipError_t e = launch_stream_copy(dst, src, bytes, static_cast<hipStream_t>(stream));
+    return e == hipSuccess ? PARISKV_OK : hip_fail(e, "stream_copy launch");
+}
+
+int pariskv_stream_read(const void* src, size_t bytes, uint32_t key, uint32_t* sink, void* stream) {
+    prof_chain_start();
+    if (!src || !sink || !aligned16(src) || (reinterpret_cast<uintptr_t>(sink) & 3u) != 0 || bytes % 16 != 0)
+        return fail(PARISKV_ERR_INVALID, "stream read needs aligned pointers and a multiple of 16 bytes");
+    const hipError_t e = launch_stream_read(src, bytes, key, sink, static_cast<hipStream_t>(stream));
+    return e == hipSuccess ? PARISKV_OK : hip_fail(e, "stream_read launch");
+}
+
 int pariskv_profile_enable(int32_t on) {
     std::lock_guard<std::mutex> lk(g_prof_mu);
     g_prof_on = on != 0;

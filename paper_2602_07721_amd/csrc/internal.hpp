@@ -222,6 +222,10 @@ hipError_t launch_group_attend(const void* q, const void* K, const void* V, int6
                                const int32_t* idx, int32_t k, int32_t batch, int32_t hkv, int32_t g,
                                float scale, float* out, int32_t* union_rows, hipStream_t s);
 
+// Reference streaming kernels (measurement only): a copy and a read of `bytes`.
+hipError_t launch_stream_copy(void* dst, const void* src, size_t bytes, hipStream_t s);
+hipError_t launch_stream_read(const void* src, size_t bytes, uint32_t key, uint32_t* sink, hipStream_t s);
+
 // Kernel-level profiling hooks (no-ops unless enabled).
 // Event pair for one kernel launch when profiling is on (nulls otherwise), to be
 // passed to hipExtLaunchKernelGGL so the timestamps are the dispatch's own.

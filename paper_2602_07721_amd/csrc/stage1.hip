@@ -134,7 +134,7 @@ __device__ __forceinline__ void merge_complements_desc(int64_t (&key)[4], int la
 }
 
 // The histogram floor v_lo of a query head: the collision scan histograms only scores
-// S >= v_lo.  It is one below a normal-law estimate of the selection threshold with the
+// S >= v_lo.  It is the integer part of a normal-law estimate of the selection threshold with the
 // subspaces' bonus weights taken as independent: mean sum_b E[bonus_b], variance
 // sum_b Var[bonus_b] from the moments stats[b] = (sum_c count_c bonus_c, sum_c count_c
 // bonus_c^2), and the upper-tail quantile z of the selected fraction p = C_eff / n by the
@@ -159,7 +159,7 @@ __device__ __forceinline__ uint32_t hist_floor(const float* st, int64_t n, int64
     const float t = sqrtf(-2.0f * logf(p));
     const float z = t - (2.515517f + t * (0.802853f + t * 0.010328f)) /
                             (1.0f + t * (1.432788f + t * (0.189269f + t * 0.001308f)));
-    const float est = mu + z * sqrtf(var) - 1.0f;
+    const float est = mu + z * sqrtf(var);
     if (!(est >= 1.0f)) return 1u;
     return est >= (float)kMaxScore ? (uint32_t)kMaxScore : (uint32_t)est;
 }
@@ -319,22 +319,15 @@ constexpr int kRawBufferWord3 = 0x00020000;
 constexpr uint32_t kOffsetOutOfRange = 0x80000000u;
 
 // Suffix sums of a 97-bin histogram held as (lo = bins 0..63 by lane, hi = bins
-// 64..96 by lane < 33): returns (sfx_lo, sfx_hi) with sfx[v] = sum_{u >= v} h[u].
+// 64..96 by lane < 33, 0 above): sfx[v] = sum_{u >= v} h[u], the total less the
+// exclusive prefix, from two DPP scans.  Returns (sfx_lo, sfx_hi).
 __device__ __forceinline__ void wave_suffix97(uint32_t lo, uint32_t hi, int lane, uint32_t* s_lo,
                                               uint32_t* s_hi) {
-#pragma unroll
-    for (int d = 1; d < 64; d <<= 1) {
-        const uint32_t o = __shfl_down(hi, d, 64);
-        if (lane + d < 64) hi += o;
-    }
-    const uint32_t tot_hi = __shfl(hi, 0, 64);
-#pragma unroll
-    for (int d = 1; d < 64; d <<= 1) {
-        const uint32_t o = __shfl_down(lo, d, 64);
-        if (lane + d < 64) lo += o;
-    }
-    *s_lo = lo + tot_hi;
-    *s_hi = hi;
+    const uint32_t ilo = wave_incl_sum(lo), ihi = wave_incl_sum(hi);
+    const uint32_t tlo = (uint32_t)__builtin_amdgcn_readlane((int)ilo, 63);
+    const uint32_t thi = (uint32_t)__builtin_amdgcn_readlane((int)ihi, 63);
+    *s_lo = thi + tlo - (ilo - lo);
+    *s_hi = thi - (ihi - hi);
 }
 
 __global__ __launch_bounds__(kColThreads) void collide_kernel(RetrieveArgs a) {

@@ -427,3 +427,12 @@ def test_binding_refuses_mismatched_tensors_before_any_launch():
         pk.tiered_attend(cfg, q, torch.zeros((1, 1, 16, 128), dtype=f16), K, K, K, idx, pk.Window(), 0.1)
     with pytest.raises(ValueError, match="V_dst must have shape"):
         pk.offload_rows(K, K, 0, K, K[:1, :1].contiguous(), 0, 4)
+
+
+def test_stream_kernels_validation():
+    L = pk.lib()
+    assert L.pariskv_stream_copy(ctypes.c_void_p(FAKE), ctypes.c_void_p(FAKE), 100, None) == pk.ERR_INVALID
+    assert L.pariskv_stream_copy(ctypes.c_void_p(FAKE + 4), ctypes.c_void_p(FAKE), 256, None) == pk.ERR_INVALID
+    assert L.pariskv_stream_copy(None, ctypes.c_void_p(FAKE), 256, None) == pk.ERR_INVALID
+    assert L.pariskv_stream_read(ctypes.c_void_p(FAKE), 100, 0, ctypes.c_void_p(FAKE), None) == pk.ERR_INVALID
+    assert L.pariskv_stream_read(ctypes.c_void_p(FAKE), 256, 0, None, None) == pk.ERR_INVALID

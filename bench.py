@@ -67,16 +67,20 @@ def parse():
                     help="also run the 1M-token offload setting (GPU window ring, Retrieval K/V in pinned "
                          "host memory, buffer updates offloaded on a second stream) for this many steps")
     ap.add_argument("--no-warm", action="store_true", help="skip the warm-cache loop")
+    ap.add_argument("--group-fetch", action="store_true",
+                    help="PARISKV_GROUP_FETCH: each quad of query heads fetches every distinct K/V row once")
     return ap.parse_args()
 
 
-def algorithmic_bytes(wc, c_eff):
-    """Bytes each kernel must move per launch (whole batch), by its definition."""
+def algorithmic_bytes(wc, c_eff, parts=1):
+    """Bytes each kernel must move per launch (whole batch), by its definition.  With a
+    two-pass top-k (parts > 1 slices per row) the final pass reads the slices' winners."""
     b, hkv, G, n, k = wc.batch, wc.n_kv_heads, wc.q_per_kv, wc.n, wc.top_k
     hq = hkv * G
     quads = (G + 3) // 4
     n_chunks = (n + 4095) // 4096
     C = c_eff
+    S = parts * k if parts > 1 else C  # entries the (final) top-k pass selects from
     return {
         # query heads (fp16) + counts read, bonus tables and z/D written
         "query_lut": b * hq * 128 * 2 + b * hkv * 16 * 256 * 4 + b * hkv * quads * 16 * 256 * 4
@@ -89,12 +93,15 @@ def algorithmic_bytes(wc, c_eff):
         # score bytes read, candidate index written, then per candidate the 128-byte record
         # gathered and its 4-byte estimate written
         "compact_rerank": b * hq * n + b * hq * C * (4 + 128 + 4),
-        # C estimates + C indices read, k indices + k scores written
-        "topk": b * hq * (C * 8 + k * 8),
+        # first pass of a two-pass top-k: C estimates + C indices read, k winners (index +
+        # estimate) written per 4096-candidate slice
+        "topk_part": b * hq * (C * 8 + parts * k * 8),
+        # S estimates + S indices read, k indices + k scores written
+        "topk": b * hq * (S * 8 + k * 8),
         # 256-byte K row + 256-byte V row + 4-byte index per selected key
         "attend": b * hq * k * (512 + 4),
         # the fused top-k + attention: both, minus the index re-read
-        "topk_attend": b * hq * (C * 8 + k * 8) + b * hq * k * 512,
+        "topk_attend": b * hq * (S * 8 + k * 8) + b * hq * k * 512,
     }
 
 
@@ -745,7 +752,7 @@ def main():
     pk.lib()
     wc = workloads.CONFIGS[args.workload]
     signs = workloads.rotation_signs(wc.seed)
-    budget = pk.Budget(wc.n_cand, wc.n_collide, wc.top_k)
+    budget = pk.Budget(wc.n_cand, wc.n_collide, wc.top_k, flags=pk.GROUP_FETCH if args.group_fetch else 0)
     scale = 1.0 / np.sqrt(wc.head_dim)
     total_steps = args.warmup + args.steps
 
@@ -863,7 +870,16 @@ def main():
     read_gbs = flush.numel() * 4 / best_of(lambda: pk.stream_read(flush, flush_sink)) / 1e9
 
     c_eff = min(wc.n_cand, wc.n)
-    algo = algorithmic_bytes(wc, c_eff)
+    algo = algorithmic_bytes(wc, c_eff, lay["topk_parts"])
+    fetch = None
+    if args.group_fetch:
+        # rows the last step's attention fetched, against the heads' own lists
+        quads = (wc.q_per_kv + 3) // 4
+        grows = int(ws[lay["group_rows"]:lay["group_rows"] + wc.batch * wc.n_kv_heads * quads * 4]
+                    .view(torch.int32).sum().item())
+        lists = int((out_idx >= 0).sum().item())
+        algo["group_attend"] = grows * 512 + wc.batch * hq * wc.top_k * 4
+        fetch = {"rows_fetched": grows, "rows_in_head_lists": lists, "fetch_ratio": round(grows / max(lists, 1), 4)}
     kernels = {}
     for name, (launches, ms) in prof.items():
         avg_ms = ms / max(1, launches)
@@ -970,6 +986,7 @@ def main():
         "needle_hit_rate": round(hits, 4),
         "copy_GBps": round(copy_gbs, 1),
         "read_GBps": round(read_gbs, 1),
+        "group_fetch": fetch,
         "cpu_baseline": cpu,
         "cpu_baseline_layer32k": cpu32,
     }

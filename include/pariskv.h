@@ -130,6 +130,17 @@ typedef struct pariskv_index {
  * scores (see pariskv_ws_layout.thresh).  Same outputs, slower; it exercises
  * the recount that otherwise runs only when the histogram floor is too high. */
 #define PARISKV_EXACT_RECOUNT 2
+/* For pariskv.budget.flags with pariskv_retrieve_attend (and its _noalloc form):
+ * GQA-group de-duplication of the fetch.  The attention of each quad of query
+ * heads sharing a KV head reads every distinct K/V row of their winner lists
+ * once (pariskv_group_attend) instead of once per head inside each head's
+ * top-k; worth it when the rows cross the host link (kv_host_mapped = 1) and the
+ * heads' lists overlap.  out then equals per-head attention up to float32
+ * rounding order (not bit for bit); out_idx / out_score are unchanged.  The
+ * distinct rows fetched per (sequence, KV head, quad) are left in the workspace
+ * (pariskv_ws_layout.group_rows).  Needs min(G, 4) * k <= PARISKV_MAX_ATTEND_ROWS;
+ * the window and tiered entry points refuse it (UNSUPPORTED). */
+#define PARISKV_GROUP_FETCH 4
 
 /* Retrieval budgets of Alg. 1: C = ceil(beta n), C_rho = ceil(rho n), k. */
 typedef struct pariskv_budget {
@@ -137,7 +148,7 @@ typedef struct pariskv_budget {
     int64_t n_collide; /* C_rho >= 1: keys covered by the admitted clusters   */
     int32_t top_k;     /* k, 1..min(C, PARISKV_MAX_TOPK)                      */
     int32_t flags;     /* PARISKV_BINARY_COLLISIONS (else the paper's tiers),
-                          PARISKV_EXACT_RECOUNT, or 0                          */
+                          PARISKV_EXACT_RECOUNT, PARISKV_GROUP_FETCH, or 0     */
 } pariskv_budget;
 
 /* Rows one query head attends at a decode step besides its retrieved keys
@@ -185,12 +196,21 @@ typedef struct pariskv_ws_layout {
     size_t stats;       /* float [batch][Hq][B][2]: per subspace, sum over the
                            clusters of count * bonus and of count * bonus^2 (the
                            moments that set the histogram floor v_lo)           */
+    size_t surv;        /* with topk_parts > 1: int32 [batch][Hq][topk_parts * k]
+                           then float [batch][Hq][topk_parts * k], the winners
+                           (index, estimate) of each 4096-candidate slice        */
+    size_t group_rows;  /* with PARISKV_GROUP_FETCH: int32 [batch][Hkv][quads],
+                           the distinct K/V rows the attention fetched           */
     int64_t n_pad;      /* row length of score8 (n rounded up to 64)             */
     int64_t n_chunks;   /* ceil(n / chunk_keys)                                  */
     int64_t chunk_keys; /* keys per selection chunk                              */
     int64_t c_eff;      /* min(n_cand, n)                                        */
     int32_t quads;      /* ceil(G / 4)                                           */
-    int32_t reserved;
+    int32_t topk_parts; /* 1, or the slices of the two-pass top-k: with fewer than
+                           256 rows (batch x Hq) and more than 8192 candidates,
+                           ceil(min(C, n) / 4096) blocks per row first keep the k
+                           best of their slice, then one block per row selects
+                           among those (the same winners as one pass)           */
 } pariskv_ws_layout;
 
 /* ------------------------------------------------------------ encoding */
@@ -279,8 +299,8 @@ int pariskv_retrieve(const pariskv_config* cfg, const pariskv_index* index,
  * winners, in one call: the same out_idx / out_score as pariskv_retrieve and
  * the same `out` as pariskv_sparse_attend(cfg, q, K, V, kv_host_mapped,
  * kv_capacity, out_idx, k, batch, scale, out) would give, bit for bit.  For
- * C <= 32768 the attention runs inside the top-k kernel over the winners it
- * holds (no second pass over out_idx); otherwise the two kernels run in turn.
+ * every C the attention runs inside the (final) top-k kernel over the winners
+ * it holds, with no second pass over out_idx.
  * Arguments as in those two functions.
  * Errors: those of pariskv_retrieve and of pariskv_sparse_attend. */
 int pariskv_retrieve_attend(const pariskv_config* cfg, const pariskv_index* index,
@@ -325,7 +345,7 @@ int pariskv_window_attend(const pariskv_config* cfg, const void* q, const void* 
 /* pariskv_retrieve over the Retrieval region (n index rows, the keys of cache
  * rows [win->retr_begin, win->retr_begin + n)) followed by
  * pariskv_window_attend over Sink + winners + Local/Buffer, in one call, with
- * the same outputs bit for bit.  For C <= 32768 the attention runs inside the
+ * the same outputs bit for bit.  The attention runs inside the
  * top-k kernel.  Also requires win->retr_begin + n <= win->dense_begin.
  * Errors: those of pariskv_retrieve and pariskv_window_attend. */
 int pariskv_retrieve_window_attend(const pariskv_config* cfg, const pariskv_index* index,
@@ -372,7 +392,7 @@ int pariskv_tiered_attend(const pariskv_config* cfg, const void* q, const void* 
                           void* stream);
 
 /* pariskv_retrieve followed by pariskv_tiered_attend, in one call, with the
- * same outputs bit for bit (attention inside the top-k kernel for C <= 32768).
+ * same outputs bit for bit (attention inside the top-k kernel).
  * Also requires win->retr_begin + n <= min(win->dense_begin, kv_capacity).
  * Errors: those of pariskv_retrieve and pariskv_tiered_attend. */
 int pariskv_retrieve_tiered_attend(const pariskv_config* cfg, const pariskv_index* index,
@@ -473,6 +493,8 @@ int pariskv_profile_read(int32_t max_entries, const char** names, int64_t* launc
 
 const char* pariskv_strerror(int code);
 const char* pariskv_last_error(void);
+/* Version of the structs and entry points declared here: 4 (pariskv_ws_layout
+ * with stats, surv, group_rows and topk_parts). */
 int32_t pariskv_abi_version(void);
 
 #ifdef __cplusplus

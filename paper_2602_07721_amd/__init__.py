@@ -27,6 +27,8 @@ __all__ = [
 ]
 
 LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libpariskv.so")
+# pariskv_abi_version() of the library this binding marshals for (struct layouts, entry points)
+ABI_VERSION = 4
 
 OK, ERR_INVALID, ERR_CAPACITY, ERR_WORKSPACE, ERR_HIP, ERR_UNSUPPORTED = 0, -1, -2, -3, -4, -5
 HEAD_DIM, SUBSPACES, CENTROIDS, REC_BYTES = 128, 16, 256, 128
@@ -36,6 +38,8 @@ NO_ROTATION, NO_ALPHA_CORRECTION = 1, 2
 BINARY_COLLISIONS = 1
 # Diagnostic Budget.flags bit: every selection threshold from the exact recount.
 EXACT_RECOUNT = 2
+# Budget.flags bit for retrieve_attend: GQA-group de-duplication of the K/V fetch.
+GROUP_FETCH = 4
 
 
 class PariskvError(RuntimeError):
@@ -68,9 +72,9 @@ class _Window(ctypes.Structure):
 class _Layout(ctypes.Structure):
     _fields_ = [(name, ctypes.c_size_t) for name in
                 ("total", "zq", "lut", "score8", "chunk_sfx", "chunk_base", "thresh", "cand",
-                 "cand_score", "stats")] + \
+                 "cand_score", "stats", "surv", "group_rows")] + \
                [(name, ctypes.c_int64) for name in ("n_pad", "n_chunks", "chunk_keys", "c_eff")] + \
-               [("quads", ctypes.c_int32), ("reserved", ctypes.c_int32)]
+               [("quads", ctypes.c_int32), ("topk_parts", ctypes.c_int32)]
 
 
 _lib = None
@@ -122,6 +126,9 @@ def lib():
         L.pariskv_strerror.argtypes = [ctypes.c_int]
         L.pariskv_last_error.restype = ctypes.c_char_p
         L.pariskv_abi_version.restype = I32
+        if L.pariskv_abi_version() != ABI_VERSION:
+            raise ImportError(f"{LIB_PATH} has ABI version {L.pariskv_abi_version()}, this binding expects "
+                              f"{ABI_VERSION}: rebuild the library")
         _lib = L
     return _lib
 

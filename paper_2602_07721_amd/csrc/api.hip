@@ -127,7 +127,7 @@ int layout(const pariskv_config* cfg, int32_t batch, int64_t n, const pariskv_bu
         return fail(PARISKV_ERR_INVALID, "top_k %d outside 1..n_cand", bud->top_k);
     if (bud->top_k > PARISKV_MAX_TOPK)
         return fail(PARISKV_ERR_UNSUPPORTED, "top_k %d above %d", bud->top_k, PARISKV_MAX_TOPK);
-    if (bud->flags & ~(PARISKV_BINARY_COLLISIONS | PARISKV_EXACT_RECOUNT))
+    if (bud->flags & ~(PARISKV_BINARY_COLLISIONS | PARISKV_EXACT_RECOUNT | PARISKV_GROUP_FETCH))
         return fail(PARISKV_ERR_INVALID, "unknown budget flags 0x%x", bud->flags);
 
     const int64_t hkv = cfg->n_kv_heads, g = cfg->q_per_kv, hq = hkv * g;
@@ -154,6 +154,9 @@ int layout(const pariskv_config* cfg, int32_t batch, int64_t n, const pariskv_bu
     L->cand = take((size_t)rows * bud->n_cand * 4);
     L->cand_score = take((size_t)rows * bud->n_cand * 4);
     L->stats = take((size_t)rows * kB * 2 * 4);
+    L->topk_parts = topk_parts(rows, L->c_eff, bud->top_k);
+    L->surv = take(L->topk_parts > 1 ? (size_t)rows * L->topk_parts * bud->top_k * 8 : 0);
+    L->group_rows = take((bud->flags & PARISKV_GROUP_FETCH) ? (size_t)batch * hkv * quads * 4 : 0);
     L->total = off;
     return PARISKV_OK;
 }
@@ -271,7 +274,7 @@ using namespace pariskv;
 
 extern "C" {
 
-int32_t pariskv_abi_version(void) { return 3; }
+int32_t pariskv_abi_version(void) { return 4; }
 
 const char* pariskv_strerror(int code) {
     switch (code) {
@@ -514,6 +517,15 @@ static int retrieve_impl(const pariskv_config* cfg, const pariskv_index* index, 
     const void* Vd = nullptr;
     if (att) {
         if ((rc = check_attend_args(*att)) != PARISKV_OK) return rc;
+        if (budget->flags & PARISKV_GROUP_FETCH) {
+            const AttendWindow& w = att->win;
+            if (w.sink || w.retr_begin || w.dense_begin || w.dense_end || w.win_capacity)
+                return fail(PARISKV_ERR_UNSUPPORTED, "PARISKV_GROUP_FETCH serves the plain retrieve + attend only");
+            const int64_t per = (int64_t)(cfg->q_per_kv < 4 ? cfg->q_per_kv : 4) * budget->top_k;
+            if (per > kMaxAttendRows)
+                return fail(PARISKV_ERR_UNSUPPORTED, "PARISKV_GROUP_FETCH: min(G, 4) * k = %lld above %d",
+                            (long long)per, kMaxAttendRows);
+        }
         if ((rc = device_kv(*att, &Kd, &Vd)) != PARISKV_OK) return rc;
     }
 
@@ -555,6 +567,9 @@ static int retrieve_impl(const pariskv_config* cfg, const pariskv_index* index, 
     a.cand = reinterpret_cast<int32_t*>(ws + L.cand);
     a.cand_score = reinterpret_cast<float*>(ws + L.cand_score);
     a.stats = reinterpret_cast<float*>(ws + L.stats);
+    a.topk_parts = L.topk_parts;
+    a.surv_idx = reinterpret_cast<int32_t*>(ws + L.surv);
+    a.surv_score = reinterpret_cast<float*>(ws + L.surv + (size_t)a.batch * a.hq * L.topk_parts * a.top_k * 4);
     a.out_idx = out_idx;
     a.out_score = out_score;
     a.sb = pack_signs(cfg->rot_signs);
@@ -579,15 +594,27 @@ static int retrieve_impl(const pariskv_config* cfg, const pariskv_index* index, 
                                             att->win, s);
         return ea == hipSuccess ? PARISKV_OK : hip_fail(ea, "attend launch");
     };
+    const bool group_fetch = att && (budget->flags & PARISKV_GROUP_FETCH);
+    // Attention per quad of heads over the union of their (ascending) winner lists.
+    auto attend_groups = [&]() -> int {
+        const hipError_t eg = launch_group_attend(q, Kd, Vd, att->kv_capacity, out_idx, budget->top_k, batch,
+                                                  a.hkv, a.g, att->scale, att->out,
+                                                  reinterpret_cast<int32_t*>(ws + L.group_rows), s);
+        return eg == hipSuccess ? PARISKV_OK : hip_fail(eg, "group_attend launch");
+    };
     if (n == 0) {
         e = launch_pad_outputs(a, s);
         if (e != hipSuccess) return hip_fail(e, "pad outputs");
-        return att ? attend_separately() : PARISKV_OK;
+        return !att ? PARISKV_OK : group_fetch ? attend_groups() : attend_separately();
     }
     if ((e = launch_query_lut(a, s)) != hipSuccess) return hip_fail(e, "query_lut launch");
     if ((e = launch_collide(a, s)) != hipSuccess) return hip_fail(e, "collide launch");
     if ((e = launch_threshold(a, s)) != hipSuccess) return hip_fail(e, "threshold launch");
     if ((e = launch_compact_rerank(a, s)) != hipSuccess) return hip_fail(e, "compact_rerank launch");
+    if (group_fetch) {
+        if ((e = launch_topk(a, s, false)) != hipSuccess) return hip_fail(e, "topk launch");
+        return attend_groups();
+    }
     bool fused = false;
     if ((e = launch_topk(a, s, att != nullptr, &fused)) != hipSuccess) return hip_fail(e, "topk launch");
     if (att && !fused) return attend_separately();

@@ -21,6 +21,19 @@ constexpr int kBins = kMaxScore + 1;
 constexpr int kSfx = kBins + 1;   // suffix histogram entries v = 0..97 (entry 97 is 0)
 constexpr int kChunk = 4096;      // keys per collision / selection chunk
 constexpr int kThreshRow = 8;     // int32 per query head in the thresh array
+constexpr int kTopkPart = 4096;   // candidates per block in the first of two top-k passes
+
+// Slices per row of the two-pass top-k: a first pass takes the top k of every
+// 4096-candidate slice in its own block, and the final pass selects among the slices'
+// winners (at most 16 slices x 2048 = 32768, which one block holds in LDS).  Used for
+// more than 32768 candidates per row, and for more than 8192 when fewer than 256 rows
+// (query heads x sequences) would leave most CUs idle; otherwise 1 (one pass, one
+// block per row).
+__host__ __device__ inline int32_t topk_parts(int64_t rows, int64_t c_eff, int32_t k) {
+    (void)k;
+    if (c_eff <= 8192 || (rows >= 256 && c_eff <= 32768)) return 1;
+    return (int32_t)((c_eff + kTopkPart - 1) / kTopkPart);
+}
 constexpr int kTierCount = 6;
 
 // Stored form of a centroid id (the ids array holds slot(c)): bits 5..7 kept,
@@ -179,6 +192,19 @@ struct RetrieveArgs {
     int32_t* cand;
     float* cand_score;
     float* stats;      // [rows][B][2] bonus moments (the histogram floor)
+    int32_t* surv_idx;  // [rows][topk_parts * top_k] survivors of the partial top-k pass
+    float* surv_score;
+    int32_t topk_parts; // 1, or the slices of a row the first of two top-k passes splits it into
+    // The list a top-k launch selects from (set by launch_topk): block b takes part
+    // b % tk_parts of row b / tk_parts, entries [p * tk_part_len, min((p + 1) *
+    // tk_part_len, tk_c)) of that row of tk_score / tk_idx (row stride tk_stride), and
+    // writes top_k entries at tk_out_idx / tk_out_score + b * top_k.
+    const float* tk_score;
+    const int32_t* tk_idx;
+    int64_t tk_stride, tk_c;
+    int32_t tk_parts, tk_part_len;
+    int32_t* tk_out_idx;
+    float* tk_out_score;
     // outputs
     int32_t* out_idx;
     float* out_score;

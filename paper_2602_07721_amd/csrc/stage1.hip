@@ -482,13 +482,15 @@ __global__ __launch_bounds__(kThrThreads) void threshold_kernel(RetrieveArgs a) 
     int32_t* t = a.thresh + row * kThreshRow;
     const uint32_t fl = wave == 0 ? (uint32_t)t[4] : 0u;  // the floor the scan used
     // Whole-row suffix histogram; lane holds v = lane and v = 64 + lane.  Wave w
-    // sums chunks w, w + 16, ... with 4 independent loads in flight.
-    uint32_t tl[4], th[4];
+    // sums chunks w, w + 16, ... with up to 16 chunks' loads in flight (256 chunks,
+    // a 1M-key row, in one round).
+    constexpr int kThrUnroll = 16;
+    uint32_t tl[kThrUnroll], th[kThrUnroll];
 #pragma unroll
-    for (int u = 0; u < 4; ++u) tl[u] = th[u] = 0;
-    for (int64_t c0 = wave; c0 < a.n_chunks; c0 += kThrWaves * 4) {
+    for (int u = 0; u < kThrUnroll; ++u) tl[u] = th[u] = 0;
+    for (int64_t c0 = wave; c0 < a.n_chunks; c0 += kThrWaves * kThrUnroll) {
 #pragma unroll
-        for (int u = 0; u < 4; ++u) {
+        for (int u = 0; u < kThrUnroll; ++u) {
             const int64_t c = c0 + kThrWaves * u;
             if (c < a.n_chunks) {
                 tl[u] += sfx[c * kSfx + lane];
@@ -496,8 +498,10 @@ __global__ __launch_bounds__(kThrThreads) void threshold_kernel(RetrieveArgs a) 
             }
         }
     }
-    s_part[wave][0][lane] = (tl[0] + tl[1]) + (tl[2] + tl[3]);
-    s_part[wave][1][lane] = (th[0] + th[1]) + (th[2] + th[3]);
+#pragma unroll
+    for (int u = 1; u < kThrUnroll; ++u) { tl[0] += tl[u]; th[0] += th[u]; }
+    s_part[wave][0][lane] = tl[0];
+    s_part[wave][1][lane] = th[0];
     __syncthreads();
     const uint32_t C = (uint32_t)a.c_eff;
     if (wave == 0) {

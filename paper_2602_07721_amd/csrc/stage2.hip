@@ -18,15 +18,16 @@
 // keeps the 16 query coordinates of its two subspaces in registers; the
 // signed level table (16 floats) lives in LDS.
 //
-// topk kernels: one block per query head; the k-th largest estimate is found
+// topk_lds_kernel: one block per list; the k-th largest estimate is found
 // exactly on order-preserving uint32 keys, ties at it taken in candidate
 // order, then an ordered compaction lists the winners in ascending key index
-// (candidate order) without a sort.  topk_lds_kernel (C <= 32768) stages the
-// keys in LDS, bins them linearly in value over [min, max] (the float bit
-// patterns crowd into a few exponent prefixes), and ranks the boundary bin by
-// brute force when it holds at most 64 keys, else by 11/11/10-bit radix passes
-// restricted to it.  topk_reg_kernel (larger C) keeps the keys in registers and
-// runs 8-bit radix passes from the top of the occupied key range.
+// (candidate order) without a sort.  The keys are staged in LDS, binned
+// linearly in value over [min, max] (the float bit patterns crowd into a few
+// exponent prefixes), and the boundary bin is ranked by brute force when it
+// holds at most 64 keys, else by 11/11/10-bit radix passes restricted to it.
+// A list is one query head's candidates (C <= 32768), or, in two passes, first
+// every 4096-candidate slice of a head and then the concatenated winners of its
+// slices (more than 32768 candidates, or more than 8192 for few heads).
 
 #include "attend_row.hpp"
 #include "internal.hpp"
@@ -36,6 +37,8 @@ namespace pariskv {
 namespace {
 
 constexpr int kRrThreads = 256;           // one 4096-key chunk per block, 16 keys per thread
+static_assert(kTopkPart >= PARISKV_MAX_TOPK, "a top-k slice holds at least k candidates");
+static_assert(PARISKV_MAX_CAND / kTopkPart * PARISKV_MAX_TOPK <= 1024 * 32, "the slices' winners fit one block");
 constexpr int kRrSlots = kRrThreads / 8;  // candidates reranked per block iteration
 constexpr int kRrUnroll = 4;              // records in flight per lane
 
@@ -249,11 +252,14 @@ __global__ __launch_bounds__(TH) void topk_lds_kernel(RetrieveArgs a) {
     __shared__ float s_wsc[kAttend ? PARISKV_MAX_TOPK : 1];
 
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-    const int64_t row = blockIdx.x;
-    const int C = (int)a.c_eff;
+    // This block's list: part blk % tk_parts of row blk / tk_parts (see RetrieveArgs).
+    const int64_t blk = blockIdx.x;
+    const int64_t row = blk / a.tk_parts;
+    const int64_t off = (blk % a.tk_parts) * (int64_t)a.tk_part_len;
+    const int C = (int)min((int64_t)a.tk_part_len, a.tk_c - off);
     const int kk = min(a.top_k, C);
-    const float* sc = a.cand_score + row * a.n_cand;
-    const int32_t* cand = a.cand + row * a.n_cand;
+    const float* sc = a.tk_score + row * a.tk_stride + off;
+    const int32_t* cand = a.tk_idx + row * a.tk_stride + off;
     if (tid == 0) s_nsmall = 0;
 
     // With kAttend, this thread's part of the query, requested first.
@@ -263,13 +269,13 @@ __global__ __launch_bounds__(TH) void topk_lds_kernel(RetrieveArgs a) {
     // Staging of the estimates as order-preserving keys (and of the candidate
     // indices): every load of the thread is issued before the first LDS store, and
     // the smallest and largest valid keys are reduced on the way.  The arrays start
-    // 256-byte aligned and a row is n_cand entries long, so 16-byte loads are taken
-    // when n_cand is a multiple of 4 (every row start then 16-byte aligned); slots
-    // past the row re-read its last 16 bytes and are masked.
+    // 256-byte aligned, so 16-byte loads are taken when the row stride and the part's
+    // offset are multiples of 4 (the list then starts 16-byte aligned); slots past
+    // the list re-read the row's last 16 bytes and are masked.
     uint32_t kmin = 0xffffffffu, kmax = 0u;
-    if ((a.n_cand & 3) == 0) {
+    if (((a.tk_stride | off) & 3) == 0) {
         constexpr int kIt = kCap / 4 / TH;
-        const int nq = (int)(a.n_cand >> 2);
+        const int nq = (int)((a.tk_stride - off) >> 2);
         float4 f[kIt];
         int4 ix[kIt];
 #pragma unroll
@@ -421,8 +427,8 @@ __global__ __launch_bounds__(TH) void topk_lds_kernel(RetrieveArgs a) {
     for (int w = 0; w < kWaves; ++w)
         if (w < wave) pre += s_w[w];
     uint32_t gb = pre & 0xffffu, eb = pre >> 16;
-    int32_t* oi = a.out_idx + row * a.top_k;
-    float* os = a.out_score ? a.out_score + row * a.top_k : nullptr;
+    int32_t* oi = a.tk_out_idx + blk * a.top_k;
+    float* os = a.tk_out_score ? a.tk_out_score + blk * a.top_k : nullptr;
     // With kAttend the attention list in region B is Sink rows, then Local +
     // Update Buffer rows (nd in all), then the winners at their cache rows
     // (retr_begin + key; the host checked they stay below dense_begin), and the
@@ -481,114 +487,6 @@ __global__ __launch_bounds__(TH) void topk_lds_kernel(RetrieveArgs a) {
     }
 }
 
-// Top-k for candidate lists too long for LDS: keys stay in registers, read
-// with a per-thread contiguous run.
-template <int TH, int EPT>
-__global__ __launch_bounds__(TH) void topk_reg_kernel(RetrieveArgs a) {
-    constexpr int kWaves = TH / 64;
-    __shared__ uint32_t s_hist[2][256];
-    __shared__ uint32_t s_w[kWaves];
-    __shared__ uint32_t s_mm[2][kWaves];
-    __shared__ uint32_t s_digit, s_need;
-
-    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-    const int64_t row = blockIdx.x;
-    const int C = (int)a.c_eff;
-    const int kk = min(a.top_k, C);
-    const float* sc = a.cand_score + row * a.n_cand;
-    const int32_t* cand = a.cand + row * a.n_cand;
-
-    uint32_t key[EPT];
-    uint32_t kmin = 0xffffffffu, kmax = 0u;
-#pragma unroll
-    for (int e = 0; e < EPT; ++e) {
-        const int p = tid * EPT + e;
-        key[e] = p < C ? order_key(sc[p]) : 0u;  // valid keys are all > 0
-        if (p < C) {
-            kmin = min(kmin, key[e]);
-            kmax = max(kmax, key[e]);
-        }
-    }
-    for (int i = tid; i < 512; i += TH) (&s_hist[0][0])[i] = 0;
-#pragma unroll
-    for (int d = 1; d < 64; d <<= 1) {
-        kmin = min(kmin, (uint32_t)__shfl_xor(kmin, d, 64));
-        kmax = max(kmax, (uint32_t)__shfl_xor(kmax, d, 64));
-    }
-    if (lane == 0) { s_mm[0][wave] = kmin; s_mm[1][wave] = kmax; }
-    __syncthreads();
-#pragma unroll
-    for (int w = 0; w < kWaves; ++w) {
-        kmin = min(kmin, s_mm[0][w]);
-        kmax = max(kmax, s_mm[1][w]);
-    }
-
-    const uint32_t range = kmax - kmin;
-    const int nbits = range ? 32 - __clz(range) : 0;
-    uint32_t prefix = 0, mask = 0, need = (uint32_t)kk;
-    int shift = nbits > 8 ? nbits - 8 : 0;
-#pragma unroll 1
-    for (int pass = 0; pass < 4 && nbits > 0; ++pass) {
-        uint32_t* hist = s_hist[pass & 1];
-#pragma unroll
-        for (int e = 0; e < EPT; ++e) {
-            const uint32_t u = key[e] - kmin;
-            if (key[e] != 0u && (u & mask) == prefix) atomicAdd(&hist[(u >> shift) & 255u], 1u);
-        }
-        __syncthreads();
-        if (wave == 0) {
-            find_digit<256>(hist, need, lane, &s_digit, &s_need);
-#pragma unroll
-            for (int r = 0; r < 4; ++r) s_hist[(pass + 1) & 1][4 * lane + r] = 0;
-        }
-        __syncthreads();
-        prefix |= s_digit << shift;
-        mask |= 255u << shift;
-        need = s_need;
-        if (shift == 0) break;
-        shift = shift > 8 ? shift - 8 : 0;
-    }
-    const uint32_t T = kmin + prefix;
-    const uint32_t quota = need;
-
-    uint32_t ng = 0, ne = 0;
-#pragma unroll
-    for (int e = 0; e < EPT; ++e) {
-        ng += (key[e] > T) ? 1u : 0u;
-        ne += (key[e] == T && key[e] != 0u) ? 1u : 0u;
-    }
-    const uint32_t mine = ng | (ne << 16);
-    const uint32_t incl = wave_incl_sum(mine);
-    if (lane == 63) s_w[wave] = incl;
-    __syncthreads();
-    uint32_t pre = incl - mine;
-#pragma unroll
-    for (int w = 0; w < kWaves; ++w)
-        if (w < wave) pre += s_w[w];
-    uint32_t gb = pre & 0xffffu, eb = pre >> 16;
-    int32_t* oi = a.out_idx + row * a.top_k;
-    float* os = a.out_score ? a.out_score + row * a.top_k : nullptr;
-#pragma unroll
-    for (int e = 0; e < EPT; ++e) {
-        uint32_t p = 0xffffffffu;
-        if (key[e] > T) {
-            p = gb + min(eb, quota);
-            ++gb;
-        } else if (key[e] == T && key[e] != 0u) {
-            if (eb < quota) p = gb + eb;
-            ++eb;
-        }
-        if (p < (uint32_t)kk) {
-            oi[p] = cand[tid * EPT + e];
-            if (os) os[p] = key_float(key[e]);
-        }
-    }
-    for (int r = kk + tid; r < a.top_k; r += TH) {
-        oi[r] = -1;
-        if (os) os[r] = -__builtin_huge_valf();
-    }
-}
-
 __global__ void pad_outputs_kernel(int32_t* out_idx, float* out_score, int64_t count) {
     const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
     if (i < count) {
@@ -606,11 +504,44 @@ hipError_t launch_compact_rerank(const RetrieveArgs& a, hipStream_t s) {
     return hipGetLastError();
 }
 
-hipError_t launch_topk(const RetrieveArgs& a, hipStream_t s, bool attend, bool* fused) {
-    const dim3 grid((unsigned)(a.batch * a.hq));
-    const int64_t C = a.c_eff;
-    if (fused) *fused = attend && C <= 1024 * 32;
-    const ProfEvents pe = prof_begin(attend && C <= 1024 * 32 ? "topk_attend" : "topk");
+hipError_t launch_topk(const RetrieveArgs& a0, hipStream_t s, bool attend, bool* fused) {
+    RetrieveArgs a = a0;
+    a.tk_score = a.cand_score;
+    a.tk_idx = a.cand;
+    a.tk_stride = a.n_cand;
+    a.tk_c = a.c_eff;
+    a.tk_parts = 1;
+    a.tk_part_len = (int32_t)a.c_eff;
+    a.tk_out_idx = a.out_idx;
+    a.tk_out_score = a.out_score;
+    const int64_t rows = (int64_t)a.batch * a.hq;
+    if (a.topk_parts > 1) {
+        // First pass: the k best of every 4096-candidate slice, in ascending key
+        // index.  Every winner of the row is among its slice's k best (fewer than k
+        // keys of its slice precede it), so the final pass over the slices' winners,
+        // concatenated in slice order, selects the same keys in the same order.
+        RetrieveArgs p = a;
+        p.tk_parts = a.topk_parts;
+        p.tk_part_len = kTopkPart;
+        p.tk_out_idx = a.surv_idx;
+        p.tk_out_score = a.surv_score;
+        const ProfEvents pp = prof_begin("topk_part");
+        hipExtLaunchKernelGGL((topk_lds_kernel<1024, 4, false>), dim3((unsigned)(rows * a.topk_parts)), dim3(1024),
+                              0, s, pp.start, pp.stop, 0, p);
+        const hipError_t e = hipGetLastError();
+        if (e != hipSuccess) return e;
+        a.tk_score = a.surv_score;
+        a.tk_idx = a.surv_idx;
+        a.tk_stride = (int64_t)a.topk_parts * a.top_k;
+        // only the last slice can hold fewer than k candidates (kTopkPart >= k)
+        const int64_t last = a.c_eff - (int64_t)(a.topk_parts - 1) * kTopkPart;
+        a.tk_c = (int64_t)(a.topk_parts - 1) * a.top_k + (last < a.top_k ? last : a.top_k);
+        a.tk_part_len = (int32_t)a.tk_c;
+    }
+    const dim3 grid((unsigned)rows);
+    const int64_t C = a.tk_c;
+    if (fused) *fused = attend;
+    const ProfEvents pe = prof_begin(attend ? "topk_attend" : "topk");
 #define PARISKV_TOPK_LDS(EPT)                                                                        \
     (attend ? hipExtLaunchKernelGGL((topk_lds_kernel<1024, EPT, true>), grid, dim3(1024), 0, s,       \
                                     pe.start, pe.stop, 0, a)                                          \
@@ -622,10 +553,8 @@ hipError_t launch_topk(const RetrieveArgs& a, hipStream_t s, bool attend, bool* 
         PARISKV_TOPK_LDS(8);
     else if (C <= 1024 * 16)
         PARISKV_TOPK_LDS(16);
-    else if (C <= 1024 * 32)
-        PARISKV_TOPK_LDS(32);
     else
-        hipExtLaunchKernelGGL((topk_reg_kernel<1024, 64>), grid, dim3(1024), 0, s, pe.start, pe.stop, 0, a);
+        PARISKV_TOPK_LDS(32);  // C <= 32768: at most 16 slices x 2048 winners after a first pass
 #undef PARISKV_TOPK_LDS
     return hipGetLastError();
 }

@@ -31,7 +31,7 @@ def test_every_declared_symbol_is_exported():
     L = pk.lib()
     for n in names:
         assert hasattr(L, n), n
-    assert L.pariskv_abi_version() == 3
+    assert L.pariskv_abi_version() == pk.ABI_VERSION == 4
 
 
 def test_error_strings():
@@ -325,7 +325,7 @@ def test_variant_flag_validation():
     assert L.pariskv_retrieve_workspace(bad.c(), 1, 4000, b.c()) == 0
     assert _encode(bad, _index()) == pk.ERR_INVALID
     assert pk.retrieve_workspace_size(_cfg(flags=pk.NO_ROTATION | pk.NO_ALPHA_CORRECTION), 1, 4000, b) > 0
-    assert L.pariskv_retrieve_workspace(_cfg().c(), 1, 4000, pk.Budget(512, 1024, 64, flags=4).c()) == 0
+    assert L.pariskv_retrieve_workspace(_cfg().c(), 1, 4000, pk.Budget(512, 1024, 64, flags=8).c()) == 0
     assert pk.retrieve_workspace_size(_cfg(), 1, 4000, pk.Budget(512, 1024, 64, flags=pk.EXACT_RECOUNT)) > 0
     assert pk.retrieve_workspace_size(_cfg(), 1, 4000, pk.Budget(512, 1024, 64, flags=pk.BINARY_COLLISIONS)) > 0
 
@@ -436,3 +436,26 @@ def test_stream_kernels_validation():
     assert L.pariskv_stream_copy(None, ctypes.c_void_p(FAKE), 256, None) == pk.ERR_INVALID
     assert L.pariskv_stream_read(ctypes.c_void_p(FAKE), 100, 0, ctypes.c_void_p(FAKE), None) == pk.ERR_INVALID
     assert L.pariskv_stream_read(ctypes.c_void_p(FAKE), 256, 0, None, None) == pk.ERR_INVALID
+
+
+def test_group_fetch_validation():
+    # PARISKV_GROUP_FETCH: plain retrieve + attend only, and min(G, 4) * k within one block's list
+    L = pk.lib()
+    cfg = _cfg()
+    ok = pk.Budget(512, 1024, 64, flags=pk.GROUP_FETCH)
+    lay = pk.workspace_layout(cfg, 1, 4000, ok)
+    assert lay["group_rows"] > 0 and lay["total"] >= lay["group_rows"] + 8 * 4
+    big = pk.Budget(8192, 16384, 2048, flags=pk.GROUP_FETCH)   # 4 x 2048 > 4096
+    need = pk.retrieve_workspace_size(cfg, 1, 4000, big)
+    rc = L.pariskv_retrieve_attend(cfg.c(), ctypes.byref(_index()), ctypes.c_void_p(FAKE), 4000, 1, big.c(),
+                                   ctypes.c_void_p(FAKE), None, ctypes.c_void_p(FAKE), ctypes.c_void_p(FAKE), 0,
+                                   4096, ctypes.c_float(0.1), ctypes.c_void_p(FAKE), ctypes.c_void_p(FAKE), need,
+                                   None)
+    assert rc == pk.ERR_UNSUPPORTED
+    win = pk.Window(16, 16, 3000, 3100)
+    need = pk.retrieve_workspace_size(cfg, 1, 2000, ok)
+    rc = L.pariskv_retrieve_window_attend(cfg.c(), ctypes.byref(_index()), ctypes.c_void_p(FAKE), 2000, 1, ok.c(),
+                                          ctypes.c_void_p(FAKE), None, ctypes.c_void_p(FAKE), ctypes.c_void_p(FAKE), 0,
+                                          4096, win.c(), ctypes.c_float(0.1), ctypes.c_void_p(FAKE),
+                                          ctypes.c_void_p(FAKE), need, None)
+    assert rc == pk.ERR_UNSUPPORTED

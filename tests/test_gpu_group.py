@@ -83,3 +83,53 @@ def test_group_attend_on_retrieval_output_and_empty_lists():
         check_attention(out[0, hq], Q[0, hq], K[0, hq // 4], V[0, hq // 4], ih[0, hq], SCALE)
     assert not out[0, 5].any() and not ref[0, 5].any()
     np.testing.assert_allclose(out, ref, rtol=0, atol=1e-5 * np.abs(ref).max())
+
+
+@pytest.mark.parametrize("g,n,bud,host", [(4, 9000, (700, 1500, 100), True), (6, 5000, (400, 800, 64), False),
+                                          (4, 40000, (10000, 20000, 512), True), (4, 0, (64, 128, 16), False)],
+                         ids=["g4_host", "g6_two_quads", "g4_two_pass_host", "n0"])
+def test_retrieve_attend_with_group_fetch(g, n, bud, host):
+    # PARISKV_GROUP_FETCH: the winners are those of the plain call bit for bit, each head's
+    # attention matches the float64 oracle over its own winners, and the rows fetched per
+    # quad are the union of the quad's winner lists.
+    b, hkv = 2, 2
+    wc = workloads.Config("gfetch", batch=b, n_kv_heads=hkv, q_per_kv=g, n=max(n, 1), n_cand=bud[0],
+                          n_collide=bud[1], top_k=bud[2], seed=53)
+    print(f"[group fetch] g {g} n {n} budget {bud} host {host}", flush=True)
+    K, V = workloads.layer_kv(wc)
+    Q, _ = workloads.layer_queries(wc, K)
+    cfg = pk.Config(hkv, g, max(n, 1), workloads.rotation_signs(53))
+    Kd, Qd = torch.from_numpy(K).cuda(), torch.from_numpy(Q).cuda()
+    index = pk.Index.empty(cfg, b)
+    pk.encode(cfg, index, Kd[:, :, :n].contiguous())
+    Ka, Va = torch.from_numpy(K), torch.from_numpy(V)
+    Ka, Va = (Ka.pin_memory(), Va.pin_memory()) if host else (Ka.cuda(), Va.cuda())
+    plain = pk.Budget(*bud)
+    grouped = pk.Budget(*bud, flags=pk.GROUP_FETCH)
+    s1 = torch.empty((b, hkv * g, bud[2]), dtype=torch.float32, device="cuda")
+    i1, _, o1, _ = pk.retrieve_attend(cfg, index, Qd, n, plain, Ka, Va, SCALE, out_score=s1, kv_host_mapped=host)
+    s2 = torch.empty_like(s1)
+    i2, _, o2, ws = pk.retrieve_attend(cfg, index, Qd, n, grouped, Ka, Va, SCALE, out_score=s2,
+                                       kv_host_mapped=host)
+    torch.cuda.synchronize()
+    np.testing.assert_array_equal(i1.cpu().numpy(), i2.cpu().numpy())
+    np.testing.assert_array_equal(s1.cpu().numpy().view(np.uint32), s2.cpu().numpy().view(np.uint32))
+    idx, out = i2.cpu().numpy(), o2.cpu().numpy()
+    lay = pk.workspace_layout(cfg, b, n, grouped)
+    quads = (g + 3) // 4
+    from parity import ws_array
+    un = ws_array(ws, lay["group_rows"], np.int32, (b, hkv, quads))
+    for s in range(b):
+        for h in range(hkv):
+            for qd in range(quads):
+                rows = set()
+                for hq in range(h * g + 4 * qd, h * g + min(g, 4 * qd + 4)):
+                    rows |= set(int(x) for x in idx[s, hq] if x >= 0)
+                assert un[s, h, qd] == len(rows), (s, h, qd)
+            for j in range(g):
+                hq = h * g + j
+                if n == 0:
+                    assert not out[s, hq].any()
+                else:
+                    check_attention(out[s, hq], Q[s, hq], K[s, h], V[s, h], idx[s, hq], SCALE)
+    np.testing.assert_allclose(out, o1.cpu().numpy(), rtol=0, atol=1e-5 * max(np.abs(out).max(), 1e-30))

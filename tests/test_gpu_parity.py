@@ -79,9 +79,9 @@ EDGE = [
     ("tiny_collide_budget", 1, 1, 4, 2000, (200, 1, 20)),
     ("collide_budget_above_n", 1, 1, 4, 2000, (200, 100000, 20)),
     ("k_odd_ragged", 1, 1, 2, 777, (333, 555, 77)),
-    ("big_C", 1, 1, 2, 40000, (10000, 20000, 300)),
-    ("huge_C", 1, 1, 1, 70000, (40000, 60000, 2048)),
-    ("C_20000", 1, 1, 2, 40000, (20000, 30000, 1000)),      # top-k staging 32 keys per thread
+    ("big_C", 1, 1, 2, 40000, (10000, 20000, 300)),         # two-pass top-k: 3 slices of 4096
+    ("huge_C", 1, 1, 1, 70000, (40000, 60000, 2048)),       # 10 slices, final pass over 20480 winners
+    ("C_20000", 1, 1, 2, 40000, (20000, 30000, 1000)),      # 5 slices, final pass over 5000
     ("many_chunks", 1, 1, 1, 300000, (4096, 8192, 256)),    # 74 chunks: multi-wave chunk prefix
     # fewer than 32 score rows (quads of query heads): the scan keeps its plain block order
     ("rows8_ragged", 1, 8, 4, 5000, (512, 1024, 64)),
@@ -134,6 +134,43 @@ def test_exact_recount_path(name, batch, hkv, G, n, bud):
     for k in ("cand", "cand_score", "idx", "score"):
         np.testing.assert_array_equal(inter[k].view(np.uint32), pi[k].view(np.uint32))
     np.testing.assert_array_equal(inter["thresh"][..., :4], pi["thresh"][..., :4])
+
+
+@pytest.mark.parametrize("n,bud", [(12000, (10000, 20000, 300)), (24000, (20000, 30000, 600))],
+                         ids=["C10000_16_per_thread", "C20000_32_per_thread"])
+def test_many_rows_one_pass_top_k(n, bud):
+    # 256 score rows (2 sequences x 32 KV heads x 4 query heads): candidate lists of
+    # 8193..32768 go through the one-pass top-k with 16 or 32 keys per thread.  Three
+    # whole groups through the oracle, invariants on every head.
+    wc = workloads.Config("rows256", batch=2, n_kv_heads=32, q_per_kv=4, n=n, n_cand=bud[0],
+                          n_collide=bud[1], top_k=bud[2], seed=131)
+    print(f"case many rows n={n} budget={bud}", flush=True)
+    K, V = workloads.layer_kv(wc, threads=16)
+    Q, _ = workloads.layer_queries(wc, K)
+    signs = workloads.rotation_signs(wc.seed)
+    budget = pk.Budget(*bud)
+    run = GpuRun(K, V, Q, signs, 4, budget, SCALE)
+    assert pk.workspace_layout(run.cfg, 2, n, budget)["topk_parts"] == 1
+    o_gpu = run.retrieve_attend()
+    inter = run.intermediates()
+    gids, grec, gcnt = run.host_index()
+    for s, h in ((0, 0), (1, 17), (1, 31)):
+        orc = oracle_group(K[s, h], signs)
+        check_index(gids[s, h], grec[s, h], gcnt[s, h], orc)
+        for g in range(4):
+            check_head(inter, s, h, g, 4, Q[s, h * 4 + g], orc, signs, budget, n)
+            check_attention(o_gpu[s, h * 4 + g], Q[s, h * 4 + g], K[s, h], V[s, h], inter["idx"][s, h * 4 + g], SCALE)
+    C = budget.n_cand
+    cand = inter["cand"][:, :, :C]
+    assert np.all(np.diff(cand, axis=-1) > 0) and np.all(np.diff(inter["idx"], axis=-1) > 0)
+    # every head's winners are among its candidates, with estimates no lower than any
+    # candidate left out (ties at the k-th estimate aside)
+    for c_row, i_row, e_row, s_row in zip(cand.reshape(-1, C), inter["idx"].reshape(-1, budget.top_k),
+                                          inter["cand_score"][:, :, :C].reshape(-1, C),
+                                          inter["score"].reshape(-1, budget.top_k)):
+        win = np.isin(c_row, i_row)
+        assert win.sum() == budget.top_k
+        assert e_row[~win].max() <= s_row.min()
 
 
 def test_degenerate_keys_and_queries():
@@ -418,7 +455,7 @@ def test_host1m_sampled_at_full_size():
     (20000, 4, (8192, 16384, 512), False),   # 8 per thread, fused (the bench shape per head)
     (40000, 2, (10000, 20000, 300), False),  # 16 per thread, fused
     (40000, 2, (20000, 30000, 1000), False), # 32 per thread, fused
-    (70000, 1, (40000, 60000, 2048), False), # register top-k: attention as its own kernel
+    (70000, 1, (40000, 60000, 2048), False), # two-pass top-k, attention in the final pass
     (0, 4, (64, 128, 16), False),            # empty cache: padding and zero outputs
     (9000, 4, (700, 1500, 100), True),       # K/V in pinned host memory
 ], ids=["C512", "C8192", "C10000", "C20000", "C40000", "n0", "host"])

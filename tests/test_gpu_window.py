@@ -96,7 +96,7 @@ def _index_over(cfg, Kd, row_begin, n):
 
 @pytest.mark.parametrize("n_cand,n,k", [(512, 6000, 64), (4096, 6000, 256), (10000, 20000, 512),
                                         (34000, 36000, 512), (512, 0, 64)],
-                         ids=["C512", "C4096", "C10000", "C34000_split", "n0"])
+                         ids=["C512", "C4096", "C10000", "C34000_two_pass", "n0"])
 def test_fused_window_equals_retrieve_then_window_attend(n_cand, n, k):
     b, hkv, g = 1, 2, 4
     sink, local, buf = 128, 512, 40
@@ -271,7 +271,7 @@ def test_tiered_attend_equals_window_attend_bit_for_bit(host):
 
 
 @pytest.mark.parametrize("n_cand,host", [(512, True), (4096, False), (34000, True)],
-                         ids=["C512_host", "C4096_hbm", "C34000_split_host"])
+                         ids=["C512_host", "C4096_hbm", "C34000_two_pass_host"])
 def test_fused_tiered_equals_separate_and_window_paths(n_cand, host):
     b, hkv, g, k = 1, 2, 4, 128
     sink, local, buf = 128, 512, 60

@@ -69,6 +69,8 @@ def parse():
     ap.add_argument("--no-warm", action="store_true", help="skip the warm-cache loop")
     ap.add_argument("--group-fetch", action="store_true",
                     help="PARISKV_GROUP_FETCH: each quad of query heads fetches every distinct K/V row once")
+    ap.add_argument("--group-share", type=int, default=0,
+                    help="query heads per KV group planted on one shared needle (overlapping winner lists)")
     return ap.parse_args()
 
 
@@ -758,7 +760,7 @@ def main():
 
     t_gen = time.perf_counter()
     K, V = workloads.layer_kv(wc, threads=16)
-    Qs = [workloads.layer_queries(wc, K, step=s)[0] for s in range(total_steps)]
+    Qs = [workloads.layer_queries(wc, K, step=s, shared=args.group_share)[0] for s in range(total_steps)]
     print(f"[bench] generated {wc.name} inputs in {time.perf_counter() - t_gen:.1f} s", file=sys.stderr,
           flush=True)
 
@@ -965,6 +967,8 @@ def main():
                          + ("K/V in pinned host memory read through host-mapped pointers, Q and index "
                             "in HBM" if args.kv_host else "all in HBM")),
             "caches": "flushed between steps" if not args.no_flush else "warm",
+            **({"group_share": args.group_share} if args.group_share > 1 else {}),
+            **({"group_fetch": True} if args.group_fetch else {}),
         },
         "p10_us": round(float(np.percentile(step_ms, 10) * 1e3), 2),
         "p50_us": round(float(np.percentile(step_ms, 50) * 1e3), 2),

@@ -201,6 +201,9 @@ typedef struct pariskv_ws_layout {
                            (index, estimate) of each 4096-candidate slice        */
     size_t group_rows;  /* with PARISKV_GROUP_FETCH: int32 [batch][Hkv][quads],
                            the distinct K/V rows the attention fetched           */
+    size_t group_part;  /* with PARISKV_GROUP_FETCH and group_splits > 1: float
+                           [batch][Hkv][quads][group_splits][4][132], each share's
+                           per-head max, sum, 2 unused, unnormalised output     */
     int64_t n_pad;      /* row length of score8 (n rounded up to 64)             */
     int64_t n_chunks;   /* ceil(n / chunk_keys)                                  */
     int64_t chunk_keys; /* keys per selection chunk                              */
@@ -211,6 +214,10 @@ typedef struct pariskv_ws_layout {
                            ceil(min(C, n) / 4096) blocks per row first keep the k
                            best of their slice, then one block per row selects
                            among those (the same winners as one pass)           */
+    int32_t group_splits; /* with PARISKV_GROUP_FETCH: blocks sharing the union of
+                           one (sequence, KV head, quad): about 256 blocks in all,
+                           at most 16, at most min(G, 4) * k / 256, at least 1;
+                           0 without the flag                                    */
 } pariskv_ws_layout;
 
 /* ------------------------------------------------------------ encoding */
@@ -494,7 +501,7 @@ int pariskv_profile_read(int32_t max_entries, const char** names, int64_t* launc
 const char* pariskv_strerror(int code);
 const char* pariskv_last_error(void);
 /* Version of the structs and entry points declared here: 4 (pariskv_ws_layout
- * with stats, surv, group_rows and topk_parts). */
+ * with stats, surv, group_rows, group_part, topk_parts and group_splits). */
 int32_t pariskv_abi_version(void);
 
 #ifdef __cplusplus

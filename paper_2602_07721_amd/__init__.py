@@ -72,9 +72,9 @@ class _Window(ctypes.Structure):
 class _Layout(ctypes.Structure):
     _fields_ = [(name, ctypes.c_size_t) for name in
                 ("total", "zq", "lut", "score8", "chunk_sfx", "chunk_base", "thresh", "cand",
-                 "cand_score", "stats", "surv", "group_rows")] + \
+                 "cand_score", "stats", "surv", "group_rows", "group_part")] + \
                [(name, ctypes.c_int64) for name in ("n_pad", "n_chunks", "chunk_keys", "c_eff")] + \
-               [("quads", ctypes.c_int32), ("topk_parts", ctypes.c_int32)]
+               [(name, ctypes.c_int32) for name in ("quads", "topk_parts", "group_splits")]
 
 
 _lib = None
@@ -406,7 +406,7 @@ def retrieve(cfg, index, q, n, budget, out_idx=None, out_score=None, workspace=N
 
 def retrieve_attend(cfg, index, q, n, budget, K, V, scale, out_idx=None, out_score=None, out=None,
                     workspace=None, kv_host_mapped=False, stream=None):
-    """retrieve + sparse_attend in one call (attention fused into the top-k when C <= 32768);
+    """retrieve + sparse_attend in one call (the attention runs inside the final top-k kernel);
     returns (idx, score, out, workspace)."""
     dev = []
     qp, batch = _q_arg(cfg, q, dev)

@@ -156,7 +156,10 @@ int layout(const pariskv_config* cfg, int32_t batch, int64_t n, const pariskv_bu
     L->stats = take((size_t)rows * kB * 2 * 4);
     L->topk_parts = topk_parts(rows, L->c_eff, bud->top_k);
     L->surv = take(L->topk_parts > 1 ? (size_t)rows * L->topk_parts * bud->top_k * 8 : 0);
-    L->group_rows = take((bud->flags & PARISKV_GROUP_FETCH) ? (size_t)batch * hkv * quads * 4 : 0);
+    const bool group_fetch = (bud->flags & PARISKV_GROUP_FETCH) != 0;
+    L->group_rows = take(group_fetch ? (size_t)batch * hkv * quads * 4 : 0);
+    L->group_splits = group_fetch ? group_splits((int64_t)batch * hkv * quads, (g < 4 ? g : 4) * (int64_t)bud->top_k) : 0;
+    L->group_part = take(group_fetch ? group_part_bytes((int64_t)batch * hkv * quads, L->group_splits) : 0);
     L->total = off;
     return PARISKV_OK;
 }
@@ -599,7 +602,8 @@ static int retrieve_impl(const pariskv_config* cfg, const pariskv_index* index, 
     auto attend_groups = [&]() -> int {
         const hipError_t eg = launch_group_attend(q, Kd, Vd, att->kv_capacity, out_idx, budget->top_k, batch,
                                                   a.hkv, a.g, att->scale, att->out,
-                                                  reinterpret_cast<int32_t*>(ws + L.group_rows), s);
+                                                  reinterpret_cast<int32_t*>(ws + L.group_rows), L.group_splits,
+                                                  reinterpret_cast<float*>(ws + L.group_part), s);
         return eg == hipSuccess ? PARISKV_OK : hip_fail(eg, "group_attend launch");
     };
     if (n == 0) {
@@ -781,7 +785,8 @@ int pariskv_group_attend(const pariskv_config* cfg, const void* q, const void* K
         Vd = p;
     }
     hipError_t e = launch_group_attend(q, Kd, Vd, kv_capacity, idx, k, batch, cfg->n_kv_heads,
-                                       cfg->q_per_kv, scale, out, union_rows, static_cast<hipStream_t>(stream));
+                                       cfg->q_per_kv, scale, out, union_rows, 1, nullptr,
+                                       static_cast<hipStream_t>(stream));
     if (e != hipSuccess) return hip_fail(e, "group_attend launch");
     return PARISKV_OK;
 }

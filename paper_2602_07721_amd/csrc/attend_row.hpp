@@ -43,6 +43,19 @@ __device__ __forceinline__ void unpack8_half(const uint4 v, float* f) {
     }
 }
 
+// Sum of x over the 16 lanes of each row of the wave, in every lane, through
+// DPP adds (no LDS): partners lane ^ 1 and lane ^ 2 (quad_perm), then the
+// mirrored lane in the half row and in the row.  After the quad steps the lanes
+// of a quad hold equal values, so the mirror partners add the same values as
+// partners lane ^ 4 and lane ^ 8 would: the xor butterfly's result, bit for bit.
+__device__ __forceinline__ float sum16(float x) {
+    x += __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(x), 0xB1, 0xF, 0xF, false));   // quad_perm 1,0,3,2
+    x += __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(x), 0x4E, 0xF, 0xF, false));   // quad_perm 2,3,0,1
+    x += __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(x), 0x141, 0xF, 0xF, false));  // row_half_mirror
+    x += __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(x), 0x140, 0xF, 0xF, false));  // row_mirror
+    return x;
+}
+
 // The 16 bytes of the head's float16 query that thread `tid` uses: dims
 // [8 (tid & 15), 8 (tid & 15) + 8).  Callers load it first, so its latency
 // overlaps their own work.
@@ -102,10 +115,7 @@ __device__ __forceinline__ void attend_row(uint4 qv, const __half* __restrict__ 
             dot[u] = d0;
         }
 #pragma unroll
-        for (int st = 1; st < 16; st <<= 1) {
-#pragma unroll
-            for (int u = 0; u < kAtUnroll; ++u) dot[u] += __shfl_xor(dot[u], st, 64);
-        }
+        for (int u = 0; u < kAtUnroll; ++u) dot[u] = sum16(dot[u]);
         float mn = m;
 #pragma unroll
         for (int u = 0; u < kAtUnroll; ++u)

@@ -18,9 +18,18 @@
 //   3. union: a block scan over "first of its row" flags numbers the distinct
 //      rows; each head ORs its bit into its row's mask;
 //   4. 32 slots of 16 lanes (lane l16 owns dims [8 l16, 8 l16 + 8)) walk the
-//      union, 4 rows in flight per lane; each K and V row segment is read once
-//      and feeds the online softmax of every head whose bit is set;
-//   5. per head, the 32 slot states are merged in LDS.
+//      block's share of the union, 8 rows in flight per lane; each K and V row
+//      segment is read once and feeds the online softmax of every head whose
+//      bit is set (one rescale per head per 8 rows);
+//   5. the 32 slot states of every head are merged in LDS.
+//
+// With few (sequence, KV head, quad) groups the union of each is split over
+// `splits` blocks (the grid's fastest index), so that enough workgroups keep
+// reads in flight -- over the host link above all.  Every split redoes steps
+// 1-3 (LDS work on 16 KiB of indices), walks its contiguous share of the union
+// rows and leaves its per-head state (running max, sum, unnormalised output)
+// in `part`; group_combine_kernel then merges the shares of each head as step 5
+// merges slots.  With one split the block writes `out` itself.
 
 #include "attend_row.hpp"
 
@@ -30,9 +39,11 @@ namespace {
 
 constexpr int kGaThreads = 512;  // 8 waves: room for 4 heads of state per lane
 constexpr int kGaSlots = kGaThreads / 16;
-constexpr int kGaUnroll = 4;
+constexpr int kGaUnroll = 8;  // K/V rows in flight per lane
 constexpr int kGaMaxEntries = 4096;  // G * k per quad staged in LDS
 constexpr int32_t kGaInvalid = 0x7fffffff;
+constexpr int kGaPart = 4 + kD;  // one head's share state: max, sum, 2 pad, output
+static_assert(kGaThreads == 4 * kD, "the slot merge gives one thread to every (head, dim)");
 
 struct GroupScratch {
     int32_t list[kGaMaxEntries];   // staged lists, then the union's rows
@@ -43,26 +54,23 @@ struct GroupScratch {
     uint32_t nunion;
 };
 
-// Number of entries of the ascending list a[0, n) below v (lower) or not above v (upper).
-__device__ __forceinline__ int rank_in(const int32_t* a, int n, int32_t v, bool upper) {
-    int lo = 0, hi = n;
-    while (lo < hi) {
-        const int mid = (lo + hi) >> 1;
-        const bool before = upper ? a[mid] <= v : a[mid] < v;
-        if (before) lo = mid + 1;
-        else hi = mid;
-    }
-    return lo;
-}
+// LDS for the final merge of the slot states, every head of the quad at once.
+struct GroupMerge {
+    float m[4][kGaSlots];
+    float l[4][kGaSlots];
+    float acc[4][kGaSlots][kD];
+};
 
 __global__ __launch_bounds__(kGaThreads) void group_attend_kernel(
     const __half* __restrict__ q, const __half* __restrict__ K, const __half* __restrict__ V,
     int64_t kv_capacity, const int32_t* __restrict__ idx, int32_t k, int32_t hkv, int32_t g,
-    int32_t quads, float scale, float* __restrict__ out, int32_t* __restrict__ union_rows) {
+    int32_t quads, float scale, float* __restrict__ out, int32_t* __restrict__ union_rows, int32_t splits,
+    float* __restrict__ part) {
     __shared__ GroupScratch sg;
-    __shared__ AttendScratch sa;
+    __shared__ GroupMerge gm;
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-    const int64_t blk = blockIdx.x;  // (seq * hkv + kvh) * quads + quad
+    const int64_t blk = blockIdx.x / splits;  // (seq * hkv + kvh) * quads + quad
+    const int split = (int)(blockIdx.x % splits);
     const int quad = (int)(blk % quads);
     const int64_t grp = blk / quads;  // seq * hkv + kvh
     const int seq = (int)(grp / hkv), kvh = (int)(grp % hkv);
@@ -78,20 +86,56 @@ __global__ __launch_bounds__(kGaThreads) void group_attend_kernel(
         sg.mask[r] = 0u;
     }
     __syncthreads();
-    // 2. merge by rank
-    for (int r = tid; r < ne; r += kGaThreads) {
-        const int h = r / k, j = r % k;
-        const int32_t v = sg.list[r];
-        int pos = j;
-        for (int o = 0; o < nh; ++o)
-            if (o != h) pos += rank_in(sg.list + o * k, k, v, o < h);
-        pos = min(pos, ne - 1);
-        sg.row[pos] = v;
-        sg.head[pos] = (uint8_t)h;
+    // 2. merge by rank.  Thread t places entries t + 512 e (e < kPer); the rank of an
+    // entry in list o is found by binary lifting (the largest prefix of list o whose
+    // entries come before it), the kPer searches of a thread interleaved step by step.
+    constexpr int kPer = kGaMaxEntries / kGaThreads;
+    {
+        int32_t v[kPer];
+        int hd[kPer], pos[kPer];
+#pragma unroll
+        for (int e = 0; e < kPer; ++e) {
+            const int r = tid + kGaThreads * e;
+            hd[e] = r < ne ? r / k : -1;
+            v[e] = r < ne ? sg.list[r] : kGaInvalid;
+            pos[e] = r < ne ? r % k : 0;
+        }
+        int top = 1;
+        while (2 * top <= k) top *= 2;
+        for (int o = 0; o < nh; ++o) {
+            const int32_t* a = sg.list + o * k;
+            int lo[kPer];
+            bool upper[kPer];  // ties: entries of lower heads first
+#pragma unroll
+            for (int e = 0; e < kPer; ++e) {
+                lo[e] = 0;
+                upper[e] = o < hd[e];
+            }
+            // branch-free steps: all kPer reads issued before any compare
+            for (int step = top; step > 0; step >>= 1) {
+                int32_t x[kPer];
+#pragma unroll
+                for (int e = 0; e < kPer; ++e) x[e] = a[min(lo[e] + step, k) - 1];
+#pragma unroll
+                for (int e = 0; e < kPer; ++e) {
+                    const bool take = (lo[e] + step <= k) & ((x[e] < v[e]) | (upper[e] & (x[e] == v[e])));
+                    lo[e] = take ? lo[e] + step : lo[e];
+                }
+            }
+#pragma unroll
+            for (int e = 0; e < kPer; ++e) pos[e] += o != hd[e] ? lo[e] : 0;
+        }
+#pragma unroll
+        for (int e = 0; e < kPer; ++e) {
+            if (hd[e] >= 0) {
+                const int p = min(pos[e], ne - 1);
+                sg.row[p] = v[e];
+                sg.head[p] = (uint8_t)hd[e];
+            }
+        }
     }
     __syncthreads();
     // 3. union: thread t owns merged entries [8t, 8t + 8)
-    constexpr int kPer = kGaMaxEntries / kGaThreads;
     uint32_t first[kPer];
     uint32_t cnt = 0;
 #pragma unroll
@@ -123,10 +167,12 @@ __global__ __launch_bounds__(kGaThreads) void group_attend_kernel(
     }
     if (tid == 0) {
         sg.nunion = total;
-        if (union_rows) union_rows[blk] = (int32_t)total;
+        if (union_rows && split == 0) union_rows[blk] = (int32_t)total;
     }
     __syncthreads();
-    const int U = (int)sg.nunion;
+    // this block's share [u_lo, u_hi) of the union rows
+    const int u_lo = (int)((int64_t)sg.nunion * split / splits);
+    const int U = (int)((int64_t)sg.nunion * (split + 1) / splits);
 
     // 4. attention over the union, every head of the quad at once
     const int slot = tid >> 4, l16 = tid & 15;
@@ -147,7 +193,7 @@ __global__ __launch_bounds__(kGaThreads) void group_attend_kernel(
 #pragma unroll
         for (int d = 0; d < 8; ++d) acc[h][d] = 0.f;
     }
-    for (int base = 0; base < U; base += kGaSlots * kGaUnroll) {
+    for (int base = u_lo; base < U; base += kGaSlots * kGaUnroll) {
         uint32_t msk[kGaUnroll];
         uint4 kc[kGaUnroll], vc[kGaUnroll];
 #pragma unroll
@@ -163,71 +209,164 @@ __global__ __launch_bounds__(kGaThreads) void group_attend_kernel(
                 vc[w] = reinterpret_cast<const uint4*>(V + off)[l16];
             }
         }
+        // scores of every row for every head of the quad
+        float dot[4][kGaUnroll];
 #pragma unroll
         for (int w = 0; w < kGaUnroll; ++w) {
-            float kf[8], vf[8];
+            float kf[8];
             unpack8_half(kc[w], kf);
-            unpack8_half(vc[w], vf);
 #pragma unroll
             for (int h = 0; h < 4; ++h) {
-                float dot = 0.f;
+                float d0 = 0.f;
 #pragma unroll
-                for (int d = 0; d < 8; ++d) dot += qf[h][d] * kf[d];
-#pragma unroll
-                for (int st = 1; st < 16; st <<= 1) dot += __shfl_xor(dot, st, 64);
-                if ((msk[w] >> h) & 1u) {
-                    const float mn = fmaxf(m[h], dot);
-                    const float corr = __expf(m[h] - mn);
-                    const float p = __expf(dot - mn);
-                    lsum[h] = lsum[h] * corr + p;
-#pragma unroll
-                    for (int d = 0; d < 8; ++d) acc[h][d] = acc[h][d] * corr + p * vf[d];
-                    m[h] = mn;
-                }
+                for (int d = 0; d < 8; ++d) d0 += qf[h][d] * kf[d];
+                dot[h][w] = sum16(d0);
             }
         }
-    }
-    // 5. merge the 32 slot states of each head
-    for (int h = 0; h < nh; ++h) {
-        if (l16 == 0) {
-            sa.m[slot] = m[h];
-            sa.l[slot] = lsum[h];
-        }
+        // one online-softmax update per head for the rows carrying its bit
 #pragma unroll
-        for (int d = 0; d < 8; ++d) sa.acc[slot][8 * l16 + d] = acc[h][d];
-        __syncthreads();
-        if (tid < kD) {
-            float M = -__builtin_huge_valf();
+        for (int h = 0; h < 4; ++h) {
+            float mn = m[h];
 #pragma unroll
-            for (int j = 0; j < kGaSlots; ++j) M = fmaxf(M, sa.m[j]);
-            float L = 0.f, O = 0.f;
-            if (M > -__builtin_huge_valf()) {
+            for (int w = 0; w < kGaUnroll; ++w)
+                if ((msk[w] >> h) & 1u) mn = fmaxf(mn, dot[h][w]);
+            if (mn > -__builtin_huge_valf()) {
+                const float corr = __expf(m[h] - mn);
+                lsum[h] *= corr;
 #pragma unroll
-                for (int j = 0; j < kGaSlots; ++j) {
-                    if (sa.l[j] > 0.f) {
-                        const float c = __expf(sa.m[j] - M);
-                        L += sa.l[j] * c;
-                        O += sa.acc[j][tid] * c;
+                for (int d = 0; d < 8; ++d) acc[h][d] *= corr;
+#pragma unroll
+                for (int w = 0; w < kGaUnroll; ++w) {
+                    if ((msk[w] >> h) & 1u) {
+                        const float p = __expf(dot[h][w] - mn);
+                        float vf[8];
+                        unpack8_half(vc[w], vf);
+                        lsum[h] += p;
+#pragma unroll
+                        for (int d = 0; d < 8; ++d) acc[h][d] += p * vf[d];
                     }
                 }
+                m[h] = mn;
             }
-            out[(row0 + h) * kD + tid] = L > 0.f ? O / L : 0.f;
         }
-        __syncthreads();
     }
+    // 5. merge the 32 slot states of each head: all states to LDS, one barrier, then
+    // thread (h, d) = (tid / 128, tid % 128) folds dim d of head h.
+#pragma unroll
+    for (int h = 0; h < 4; ++h) {
+        if (l16 == 0) {
+            gm.m[h][slot] = m[h];
+            gm.l[h][slot] = lsum[h];
+        }
+#pragma unroll
+        for (int d = 0; d < 8; ++d) gm.acc[h][slot][8 * l16 + d] = acc[h][d];
+    }
+    __syncthreads();
+    const int h = tid / kD, dd = tid % kD;
+    if (h < nh) {
+        float M = -__builtin_huge_valf();
+#pragma unroll
+        for (int j = 0; j < kGaSlots; ++j) M = fmaxf(M, gm.m[h][j]);
+        float L = 0.f, O = 0.f;
+        if (M > -__builtin_huge_valf()) {
+#pragma unroll
+            for (int j = 0; j < kGaSlots; ++j) {
+                if (gm.l[h][j] > 0.f) {
+                    const float c = __expf(gm.m[h][j] - M);
+                    L += gm.l[h][j] * c;
+                    O += gm.acc[h][j][dd] * c;
+                }
+            }
+        }
+        if (splits == 1) {
+            out[(row0 + h) * kD + dd] = L > 0.f ? O / L : 0.f;
+        } else {
+            float* ps = part + ((blk * splits + split) * 4 + h) * kGaPart;
+            if (dd == 0) {
+                ps[0] = M;
+                ps[1] = L;
+            }
+            ps[4 + dd] = O;
+        }
+    }
+}
+
+// One block of kD threads per (group block, head): merges the `splits` share
+// states of the head (thread d owns output dim d).
+__global__ __launch_bounds__(kD) void group_combine_kernel(const float* __restrict__ part, int32_t splits,
+                                                           int32_t hkv, int32_t g, int32_t quads,
+                                                           float* __restrict__ out) {
+    const int tid = threadIdx.x;
+    const int64_t blk = blockIdx.x >> 2;  // (seq * hkv + kvh) * quads + quad
+    const int h = (int)(blockIdx.x & 3);
+    const int quad = (int)(blk % quads);
+    if (h >= min(4, g - 4 * quad)) return;
+    const int64_t grp = blk / quads;
+    const int64_t row = (grp / hkv) * hkv * g + (grp % hkv) * g + 4 * quad + h;
+    const float* ps = part + (blk * splits * 4 + h) * kGaPart;
+    const int64_t stride = 4 * kGaPart;  // next share of the same head
+    // every share's state loaded at once (splits <= kGaMaxSplits)
+    float mj[kGaMaxSplits], lj[kGaMaxSplits], oj[kGaMaxSplits];
+#pragma unroll
+    for (int j = 0; j < kGaMaxSplits; ++j) {
+        lj[j] = 0.f;
+        mj[j] = oj[j] = 0.f;
+        if (j < splits) {
+            mj[j] = ps[j * stride];
+            lj[j] = ps[j * stride + 1];
+            oj[j] = ps[j * stride + 4 + tid];
+        }
+    }
+    float M = -__builtin_huge_valf();
+#pragma unroll
+    for (int j = 0; j < kGaMaxSplits; ++j)
+        if (lj[j] > 0.f) M = fmaxf(M, mj[j]);
+    float L = 0.f, O = 0.f;
+#pragma unroll
+    for (int j = 0; j < kGaMaxSplits; ++j) {
+        if (lj[j] > 0.f) {
+            const float c = __expf(mj[j] - M);
+            L += lj[j] * c;
+            O += oj[j] * c;
+        }
+    }
+    out[row * kD + tid] = L > 0.f ? O / L : 0.f;
 }
 
 }  // namespace
 
+int32_t group_splits(int64_t groups, int64_t per) {
+    if (groups >= 256) return 1;
+    int64_t s = (256 + groups - 1) / groups;
+    s = s < kGaMaxSplits ? s : kGaMaxSplits;
+    const int64_t by_rows = per / 256;  // at least 256 union rows of the worst case per share
+    s = s < by_rows ? s : by_rows;
+    return (int32_t)(s < 1 ? 1 : s);
+}
+
+size_t group_part_bytes(int64_t groups, int32_t splits) {
+    return splits > 1 ? (size_t)groups * splits * 4 * kGaPart * sizeof(float) : 0;
+}
+
 hipError_t launch_group_attend(const void* q, const void* K, const void* V, int64_t kv_capacity,
                                const int32_t* idx, int32_t k, int32_t batch, int32_t hkv, int32_t g,
-                               float scale, float* out, int32_t* union_rows, hipStream_t s) {
+                               float scale, float* out, int32_t* union_rows, int32_t splits, float* part,
+                               hipStream_t s) {
     const int32_t quads = (g + 3) / 4;
-    const ProfEvents pe = prof_begin("group_attend");
-    hipExtLaunchKernelGGL(group_attend_kernel, dim3((unsigned)((int64_t)batch * hkv * quads)),
-                          dim3(kGaThreads), 0, s, pe.start, pe.stop, 0, static_cast<const __half*>(q),
-                          static_cast<const __half*>(K), static_cast<const __half*>(V), kv_capacity, idx, k,
-                          hkv, g, quads, scale, out, union_rows);
+    const int64_t groups = (int64_t)batch * hkv * quads;
+    if (splits < 1 || splits > kGaMaxSplits || (splits > 1 && !part)) return hipErrorInvalidValue;
+    {
+        const ProfEvents pe = prof_begin("group_attend");
+        hipExtLaunchKernelGGL(group_attend_kernel, dim3((unsigned)(groups * splits)), dim3(kGaThreads), 0, s,
+                              pe.start, pe.stop, 0, static_cast<const __half*>(q), static_cast<const __half*>(K),
+                              static_cast<const __half*>(V), kv_capacity, idx, k, hkv, g, quads, scale, out,
+                              union_rows, splits, part);
+        const hipError_t e = hipGetLastError();
+        if (e != hipSuccess || splits == 1) return e;
+    }
+    const ProfEvents pe = prof_begin("group_combine");
+    hipExtLaunchKernelGGL(group_combine_kernel, dim3((unsigned)(groups * 4)), dim3(kD), 0, s, pe.start, pe.stop,
+                          0, static_cast<const float*>(part), splits, hkv, g, quads, out);
     return hipGetLastError();
 }
 

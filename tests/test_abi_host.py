@@ -113,8 +113,11 @@ def test_workspace_layout_is_consistent():
     assert lay["total"] == pk.retrieve_workspace_size(cfg, 2, 4000, b)
     assert lay["n_pad"] == 4032 and lay["n_chunks"] == 1 and lay["c_eff"] == 512 and lay["quads"] == 1
     offs = [lay[k] for k in ("zq", "lut", "score8", "chunk_sfx", "chunk_base", "thresh", "cand",
-                             "cand_score", "stats")]
-    assert offs == sorted(offs) and all(o % 256 == 0 for o in offs) and lay["total"] > offs[-1]
+                             "cand_score", "stats", "surv", "group_rows", "group_part")]
+    assert offs == sorted(offs) and all(o % 256 == 0 for o in offs) and lay["total"] >= offs[-1]
+    # the regions a plain call does not use are empty
+    assert lay["surv"] == lay["group_rows"] == lay["group_part"] == lay["total"]
+    assert lay["topk_parts"] == 1 and lay["group_splits"] == 0
     assert lay["score8"] - lay["lut"] >= 2 * 8 * 1 * 16 * 256 * 4
     lay2 = pk.workspace_layout(_cfg(q_per_kv=6), 1, 100, pk.Budget(512, 1024, 64))
     assert lay2["quads"] == 2 and lay2["c_eff"] == 100
@@ -326,6 +329,8 @@ def test_variant_flag_validation():
     assert _encode(bad, _index()) == pk.ERR_INVALID
     assert pk.retrieve_workspace_size(_cfg(flags=pk.NO_ROTATION | pk.NO_ALPHA_CORRECTION), 1, 4000, b) > 0
     assert L.pariskv_retrieve_workspace(_cfg().c(), 1, 4000, pk.Budget(512, 1024, 64, flags=8).c()) == 0
+    every = pk.BINARY_COLLISIONS | pk.EXACT_RECOUNT | pk.GROUP_FETCH
+    assert every == 7 and pk.retrieve_workspace_size(_cfg(), 1, 4000, pk.Budget(512, 1024, 64, flags=every)) > 0
     assert pk.retrieve_workspace_size(_cfg(), 1, 4000, pk.Budget(512, 1024, 64, flags=pk.EXACT_RECOUNT)) > 0
     assert pk.retrieve_workspace_size(_cfg(), 1, 4000, pk.Budget(512, 1024, 64, flags=pk.BINARY_COLLISIONS)) > 0
 
@@ -445,6 +450,21 @@ def test_group_fetch_validation():
     ok = pk.Budget(512, 1024, 64, flags=pk.GROUP_FETCH)
     lay = pk.workspace_layout(cfg, 1, 4000, ok)
     assert lay["group_rows"] > 0 and lay["total"] >= lay["group_rows"] + 8 * 4
+    # 8 quads with 4 x 64 entries each: one block per quad (a share needs >= 256 rows)
+    assert lay["group_splits"] == 1 and lay["group_part"] == lay["total"]
+    assert pk.workspace_layout(cfg, 1, 4000, pk.Budget(512, 1024, 64))["group_splits"] == 0
+    # the host1m shape: 8 quads of 4 x 1024 entries -> 16 shares each, states of 4 x 132 floats
+    h1m = pk.workspace_layout(pk.Config(8, 4, 1 << 20, workloads.rotation_signs(0)), 1, 1 << 20,
+                              pk.Budget(32768, 65536, 1024, flags=pk.GROUP_FETCH))
+    assert h1m["group_splits"] == 16 and h1m["group_part"] > h1m["group_rows"]
+    assert h1m["total"] - h1m["group_part"] == 8 * 16 * 4 * 132 * 4
+    # batch 8 of the same: 64 quads -> 4 shares each
+    b8 = pk.workspace_layout(pk.Config(8, 4, 1 << 17, workloads.rotation_signs(0)), 8, 1 << 17,
+                             pk.Budget(8192, 16384, 512, flags=pk.GROUP_FETCH))
+    assert b8["group_splits"] == 4
+    # G = 2: 2 x 64 entries per quad, too few to share
+    g2 = pk.workspace_layout(_cfg(q_per_kv=2), 1, 4000, ok)
+    assert g2["group_splits"] == 1
     big = pk.Budget(8192, 16384, 2048, flags=pk.GROUP_FETCH)   # 4 x 2048 > 4096
     need = pk.retrieve_workspace_size(cfg, 1, 4000, big)
     rc = L.pariskv_retrieve_attend(cfg.c(), ctypes.byref(_index()), ctypes.c_void_p(FAKE), 4000, 1, big.c(),

@@ -85,17 +85,20 @@ def test_group_attend_on_retrieval_output_and_empty_lists():
     np.testing.assert_allclose(out, ref, rtol=0, atol=1e-5 * np.abs(ref).max())
 
 
-@pytest.mark.parametrize("g,n,bud,host", [(4, 9000, (700, 1500, 100), True), (6, 5000, (400, 800, 64), False),
-                                          (4, 40000, (10000, 20000, 512), True), (4, 0, (64, 128, 16), False)],
-                         ids=["g4_host", "g6_two_quads", "g4_two_pass_host", "n0"])
-def test_retrieve_attend_with_group_fetch(g, n, bud, host):
+@pytest.mark.parametrize("g,n,bud,host,splits", [
+    (4, 9000, (700, 1500, 100), True, 1), (6, 5000, (400, 800, 64), False, 1),
+    (4, 40000, (10000, 20000, 512), True, 8), (6, 12000, (1500, 3000, 256), False, 4),
+    (4, 0, (64, 128, 16), False, 1), (4, 0, (600, 1200, 512), False, 8)],
+    ids=["g4_host", "g6_two_quads", "g4_two_pass_host_split8", "g6_two_quads_split4", "n0", "n0_split8"])
+def test_retrieve_attend_with_group_fetch(g, n, bud, host, splits):
     # PARISKV_GROUP_FETCH: the winners are those of the plain call bit for bit, each head's
     # attention matches the float64 oracle over its own winners, and the rows fetched per
-    # quad are the union of the quad's winner lists.
+    # quad are the union of the quad's winner lists.  With splits > 1 each quad's union is
+    # shared by that many blocks and their states merged by a second kernel.
     b, hkv = 2, 2
     wc = workloads.Config("gfetch", batch=b, n_kv_heads=hkv, q_per_kv=g, n=max(n, 1), n_cand=bud[0],
                           n_collide=bud[1], top_k=bud[2], seed=53)
-    print(f"[group fetch] g {g} n {n} budget {bud} host {host}", flush=True)
+    print(f"[group fetch] g {g} n {n} budget {bud} host {host} splits {splits}", flush=True)
     K, V = workloads.layer_kv(wc)
     Q, _ = workloads.layer_queries(wc, K)
     cfg = pk.Config(hkv, g, max(n, 1), workloads.rotation_signs(53))
@@ -116,6 +119,7 @@ def test_retrieve_attend_with_group_fetch(g, n, bud, host):
     np.testing.assert_array_equal(s1.cpu().numpy().view(np.uint32), s2.cpu().numpy().view(np.uint32))
     idx, out = i2.cpu().numpy(), o2.cpu().numpy()
     lay = pk.workspace_layout(cfg, b, n, grouped)
+    assert lay["group_splits"] == splits
     quads = (g + 3) // 4
     from parity import ws_array
     un = ws_array(ws, lay["group_rows"], np.int32, (b, hkv, quads))

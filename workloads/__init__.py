@@ -80,12 +80,16 @@ def head_values(seed, seq, kvh, n, D=D_DEFAULT):
     return r.standard_normal(size=(n, D), dtype=np.float32).astype(np.float16)
 
 
-def needle_queries(keys, seed, seq, kvh, n_queries, step=0):
-    """(q [n_queries, D] float16, needle index [n_queries]) planted on the given keys."""
+def needle_queries(keys, seed, seq, kvh, n_queries, step=0, shared=0):
+    """(q [n_queries, D] float16, needle index [n_queries]) planted on the given keys.
+    shared > 1: the first `shared` queries share the first query's needle (each with its
+    own noise), as query heads of one KV group that attend to the same key."""
     keys = np.asarray(keys)
     n, D = keys.shape
     r = _rng(_TAG_QUERY, seed, seq, kvh, step)
     needles = r.integers(0, n, size=n_queries)
+    if shared > 1:
+        needles[:shared] = needles[0]
     noise = r.standard_normal(size=(n_queries, D))
     q = keys[needles].astype(np.float64) + NEEDLE_NOISE * noise
     return q.astype(np.float16), needles
@@ -194,14 +198,15 @@ def layer_kv(cfg, seqs=None, heads=None, n=None, values=True, threads=8):
     return K, V
 
 
-def layer_queries(cfg, K, step=0):
-    """Needle queries Q [b][Hq][D] float16 and needle indices [b][Hq] for keys K [b][Hkv][n][D]."""
+def layer_queries(cfg, K, step=0, shared=0):
+    """Needle queries Q [b][Hq][D] float16 and needle indices [b][Hq] for keys K [b][Hkv][n][D]
+    (shared: query heads per KV group sharing one needle, see needle_queries)."""
     b, hkv, n, D = K.shape
     Q = np.empty((b, hkv * cfg.q_per_kv, D), dtype=np.float16)
     needles = np.empty((b, hkv * cfg.q_per_kv), dtype=np.int64)
     for s in range(b):
         for h in range(hkv):
-            q, nd = needle_queries(K[s, h], cfg.seed, s, h, cfg.q_per_kv, step)
+            q, nd = needle_queries(K[s, h], cfg.seed, s, h, cfg.q_per_kv, step, shared)
             Q[s, h * cfg.q_per_kv:(h + 1) * cfg.q_per_kv] = q
             needles[s, h * cfg.q_per_kv:(h + 1) * cfg.q_per_kv] = nd
     return Q, needles

@@ -470,10 +470,14 @@ __device__ __forceinline__ void theta_of(uint32_t ttl, uint32_t tth, uint32_t C,
     *theta = th;
 }
 
+// kThrUnroll: chunks per wave and load round, the smallest power of two with
+// 16 kThrUnroll >= n_chunks (at most 16: a 1M-key row in one round).
+template <int kThrUnroll>
 __global__ __launch_bounds__(kThrThreads) void threshold_kernel(RetrieveArgs a) {
     __shared__ uint32_t s_part[kThrWaves][2][64];
     __shared__ uint32_t s_wtot[2][kThrWaves];
     __shared__ uint32_t s_hist[kBins];
+    __shared__ uint32_t s_cg[kThrWaves * kThrUnroll][2];  // per chunk: #{S > theta}, #{S == theta}
     __shared__ int s_theta, s_recount;
     const int tid = threadIdx.x;
     const int lane = tid & 63, wave = tid >> 6;
@@ -482,26 +486,35 @@ __global__ __launch_bounds__(kThrThreads) void threshold_kernel(RetrieveArgs a) 
     int32_t* t = a.thresh + row * kThreshRow;
     const uint32_t fl = wave == 0 ? (uint32_t)t[4] : 0u;  // the floor the scan used
     // Whole-row suffix histogram; lane holds v = lane and v = 64 + lane.  Wave w
-    // sums chunks w, w + 16, ... with up to 16 chunks' loads in flight (256 chunks,
-    // a 1M-key row, in one round).
-    constexpr int kThrUnroll = 16;
+    // sums chunks w, w + 16, ... with kThrUnroll chunks' loads in flight.  With at
+    // most 16 kThrUnroll chunks that is one round, and each wave keeps its chunks'
+    // histograms (chunk w + 16 u in tl[u], th[u]) for the chunk bases below.
+    const bool one_round = a.n_chunks <= kThrWaves * kThrUnroll;
     uint32_t tl[kThrUnroll], th[kThrUnroll];
 #pragma unroll
     for (int u = 0; u < kThrUnroll; ++u) tl[u] = th[u] = 0;
     for (int64_t c0 = wave; c0 < a.n_chunks; c0 += kThrWaves * kThrUnroll) {
+        // Branch-free: every load is issued (clamped into the row) before the first
+        // wait, and the entries past the row or past v = 97 are masked afterwards.
+        uint32_t xl[kThrUnroll], xh[kThrUnroll];
 #pragma unroll
         for (int u = 0; u < kThrUnroll; ++u) {
-            const int64_t c = c0 + kThrWaves * u;
-            if (c < a.n_chunks) {
-                tl[u] += sfx[c * kSfx + lane];
-                if (lane < kSfx - 64) th[u] += sfx[c * kSfx + 64 + lane];
-            }
+            const int64_t c = min(c0 + kThrWaves * u, a.n_chunks - 1);
+            xl[u] = sfx[c * kSfx + lane];
+            xh[u] = sfx[c * kSfx + 64 + min(lane, kSfx - 65)];
+        }
+#pragma unroll
+        for (int u = 0; u < kThrUnroll; ++u) {
+            const bool in = c0 + kThrWaves * u < a.n_chunks;
+            tl[u] += in ? xl[u] : 0u;
+            th[u] += in && lane < kSfx - 64 ? xh[u] : 0u;
         }
     }
+    uint32_t sl = 0, sh = 0;
 #pragma unroll
-    for (int u = 1; u < kThrUnroll; ++u) { tl[0] += tl[u]; th[0] += th[u]; }
-    s_part[wave][0][lane] = tl[0];
-    s_part[wave][1][lane] = th[0];
+    for (int u = 0; u < kThrUnroll; ++u) { sl += tl[u]; sh += th[u]; }
+    s_part[wave][0][lane] = sl;
+    s_part[wave][1][lane] = sh;
     __syncthreads();
     const uint32_t C = (uint32_t)a.c_eff;
     if (wave == 0) {
@@ -594,6 +607,26 @@ __global__ __launch_bounds__(kThrThreads) void threshold_kernel(RetrieveArgs a) 
         __syncthreads();
     }
     const int theta = s_theta;
+    // Each chunk's #{S > theta} and #{S == theta}: from the registers of the one-round
+    // load (entries theta and theta + 1 of the chunk's suffix histogram), else (more
+    // chunks, or the recount's entries) from memory below.
+    const bool from_regs = one_round && !s_recount;
+    if (from_regs) {
+        const int th_s = __builtin_amdgcn_readfirstlane(theta);
+#pragma unroll
+        for (int u = 0; u < kThrUnroll; ++u) {
+            const int64_t c = wave + kThrWaves * u;
+            const uint32_t ge = th_s < 64 ? (uint32_t)__builtin_amdgcn_readlane((int)tl[u], th_s)
+                                          : (uint32_t)__builtin_amdgcn_readlane((int)th[u], th_s - 64);
+            const uint32_t g = th_s + 1 < 64 ? (uint32_t)__builtin_amdgcn_readlane((int)tl[u], th_s + 1)
+                                              : (uint32_t)__builtin_amdgcn_readlane((int)th[u], th_s + 1 - 64);
+            if (lane == 0 && c < a.n_chunks) {
+                s_cg[c][0] = g;
+                s_cg[c][1] = ge - g;
+            }
+        }
+        __syncthreads();
+    }
     // Keys with S > theta and S == theta in the chunks before each chunk: thread t
     // takes chunk cb + t; wave scans, then a scan of the wave totals.
     uint32_t carry_g = 0, carry_e = 0;
@@ -601,8 +634,13 @@ __global__ __launch_bounds__(kThrThreads) void threshold_kernel(RetrieveArgs a) 
         const int64_t c = cb + tid;
         uint32_t g = 0, e = 0;
         if (c < a.n_chunks) {
-            g = sfx[c * kSfx + theta + 1];
-            e = sfx[c * kSfx + theta] - g;
+            if (from_regs) {
+                g = s_cg[c][0];
+                e = s_cg[c][1];
+            } else {
+                g = sfx[c * kSfx + theta + 1];
+                e = sfx[c * kSfx + theta] - g;
+            }
         }
         const uint32_t ig = wave_incl_sum(g);
         const uint32_t ie = wave_incl_sum(e);
@@ -646,7 +684,15 @@ hipError_t launch_collide(const RetrieveArgs& a, hipStream_t s) {
 hipError_t launch_threshold(const RetrieveArgs& a, hipStream_t s) {
     const int64_t rows = (int64_t)a.batch * a.hq;
     const ProfEvents pe = prof_begin("threshold");
-    hipExtLaunchKernelGGL(threshold_kernel, dim3((unsigned)rows), dim3(kThrThreads), 0, s, pe.start, pe.stop, 0, a);
+    const dim3 grid((unsigned)rows), block(kThrThreads);
+    if (a.n_chunks <= kThrWaves * 2)
+        hipExtLaunchKernelGGL(threshold_kernel<2>, grid, block, 0, s, pe.start, pe.stop, 0, a);
+    else if (a.n_chunks <= kThrWaves * 4)
+        hipExtLaunchKernelGGL(threshold_kernel<4>, grid, block, 0, s, pe.start, pe.stop, 0, a);
+    else if (a.n_chunks <= kThrWaves * 8)
+        hipExtLaunchKernelGGL(threshold_kernel<8>, grid, block, 0, s, pe.start, pe.stop, 0, a);
+    else
+        hipExtLaunchKernelGGL(threshold_kernel<16>, grid, block, 0, s, pe.start, pe.stop, 0, a);
     return hipGetLastError();
 }
 

@@ -83,6 +83,11 @@ EDGE = [
     ("huge_C", 1, 1, 1, 70000, (40000, 60000, 2048)),       # 10 slices, final pass over 20480 winners
     ("C_20000", 1, 1, 2, 40000, (20000, 30000, 1000)),      # 5 slices, final pass over 5000
     ("many_chunks", 1, 1, 1, 300000, (4096, 8192, 256)),    # 74 chunks: multi-wave chunk prefix
+    # the threshold kernel loads 2, 4, 8 or 16 chunks per wave and round: 49 chunks take
+    # the 4-chunk form; past 256 chunks the 16-chunk form loops and re-reads the chunk
+    # counts at theta from memory
+    ("chunks_49", 1, 1, 2, 200000, (2048, 4096, 128)),
+    ("chunks_269_two_rounds", 1, 1, 1, 1100000, (8192, 16384, 256)),
     # fewer than 32 score rows (quads of query heads): the scan keeps its plain block order
     ("rows8_ragged", 1, 8, 4, 5000, (512, 1024, 64)),
     ("rows8_two_quads_ragged", 1, 4, 8, 4099, (300, 700, 40)),

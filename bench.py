@@ -638,7 +638,8 @@ def group_run(pk, torch, np, workloads, dev, drift_steps, reps=8):
     (K/V in pinned host memory), top-256 retrieved per query head, then attention per head
     (pariskv_sparse_attend) and per KV head over the union of its heads' lists
     (pariskv_group_attend), for planted-needle queries (a different needle per head) and for
-    queries drawn from the key law (the heads of a group ask similar questions)."""
+    queries drawn from the key law (the heads of a group ask similar questions); and the
+    whole retrieve + attend step with and without PARISKV_GROUP_FETCH."""
     wc = workloads.CONFIGS["drift"]
     signs = workloads.rotation_signs(wc.seed)
     n = wc.n + drift_steps
@@ -690,12 +691,34 @@ def group_run(pk, torch, np, workloads, dev, drift_steps, reps=8):
             times[label] = e0.elapsed_time(e1) * 1e3 / reps
         urows = int(un.sum().item())
         row_b = 2 * wc.head_dim * 2
+        # The whole step (pariskv_retrieve_attend) with the attention fused into the
+        # top-k, and with PARISKV_GROUP_FETCH (top-k, then the split group attention).
+        gbud = pk.Budget(C, 2 * C, wc.top_k, flags=pk.GROUP_FETCH)
+        for label, b_ in (("step_per_head", bud), ("step_group_fetch", gbud)):
+            ws = torch.empty(pk.retrieve_workspace_size(cfg, wc.batch, n, b_), dtype=torch.uint8, device=dev)
+            oi = torch.empty((wc.batch, hq, wc.top_k), dtype=torch.int32, device=dev)
+
+            def call():
+                pk.retrieve_attend(cfg, index, Qd, n, b_, Kh, Vh, scale, out_idx=oi, out=out, workspace=ws,
+                                   kv_host_mapped=True)
+            call()
+            torch.cuda.synchronize()
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record()
+            for _ in range(reps):
+                call()
+            e1.record()
+            torch.cuda.synchronize()
+            times[label] = e0.elapsed_time(e1) * 1e3 / reps
         res[name] = {"rows_per_head_lists": rows, "rows_fetched_by_group": urows,
                      "fetch_ratio": round(urows / rows, 4),
                      "us_per_head_attend": round(times["per_head"], 1),
                      "us_group_attend": round(times["group"], 1),
                      "host_link_GBps_per_head": round(rows * row_b / (times["per_head"] * 1e-6) / 1e9, 2),
-                     "host_link_GBps_group": round(urows * row_b / (times["group"] * 1e-6) / 1e9, 2)}
+                     "host_link_GBps_group": round(urows * row_b / (times["group"] * 1e-6) / 1e9, 2),
+                     "us_step_retrieve_attend": round(times["step_per_head"], 1),
+                     "us_step_retrieve_attend_group_fetch": round(times["step_group_fetch"], 1),
+                     "us_saved_per_step": round(times["step_per_head"] - times["step_group_fetch"], 1)}
     return {"workload": (f"drift keys ({wc.batch} seqs x {wc.n_kv_heads} KV heads x {wc.q_per_kv} query heads, "
                          f"n = {n}), K/V in pinned host memory, top-{wc.top_k} per head from C = {C}"),
             **res}

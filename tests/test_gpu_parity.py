@@ -320,6 +320,59 @@ def test_streaming_decode_steps_match_the_oracle():
     assert n_cur == wc.n
 
 
+def test_drift_decode_at_full_width_sampled():
+    # The drift workload at its own width (4 sequences x 8 KV heads x 4 query heads, a
+    # 32768-key prefill) after appends of 1, 255 and 256 drifted keys, retrieved and
+    # attended with the fused call and C = ceil(n/16): two whole groups through the
+    # oracle (grown index, Stage I/II, top-k, attention), invariants on every head.
+    wc = workloads.CONFIGS["drift"]
+    total = wc.extra["decode_steps"]
+    extra = 512
+    print("case drift full width", flush=True)
+    K0, V0 = workloads.layer_kv(wc, threads=16)
+    b, hkv, n0, D = K0.shape
+    K = np.empty((b, hkv, n0 + extra, D), np.float16)
+    V = np.empty_like(K)
+    K[:, :, :n0], V[:, :, :n0] = K0, V0
+    rng = np.random.default_rng(wc.seed)
+    for s_ in range(b):
+        for h in range(hkv):
+            K[s_, h, n0:] = workloads.drift_keys(wc.seed, s_, h, 0, extra, total)
+            V[s_, h, n0:] = rng.standard_normal((extra, D)).astype(np.float16)
+    signs = workloads.rotation_signs(wc.seed)
+    g = wc.q_per_kv
+    run = GpuRun(K0, None, np.zeros((b, hkv * g, D), np.float16), signs, g, pk.Budget(1, 1, 1), SCALE,
+                 capacity=n0 + extra)
+    n_cur = n0
+    for t in (1, 255, 256):
+        pk.append(run.cfg, run.index, torch.from_numpy(np.ascontiguousarray(K[:, :, n_cur:n_cur + t])).cuda(),
+                  n_cur)
+        n_cur += t
+    assert n_cur == n0 + extra
+    Q = np.stack([np.concatenate([workloads.drift_query(wc.seed, s_, h, extra, total, g) for h in range(hkv)])
+                  for s_ in range(b)])
+    C = -(-n_cur // 16)
+    budget = pk.Budget(C, 2 * C, wc.top_k)
+    run.Q = torch.from_numpy(Q).cuda()
+    run.budget, run.n = budget, n_cur
+    o_gpu = run.retrieve_attend(torch.from_numpy(K).cuda(), torch.from_numpy(V).cuda())
+    inter = run.intermediates()
+    gids, grec, gcnt = run.host_index()
+    cand = inter["cand"][:, :, :C]
+    assert np.all(np.diff(cand, axis=-1) > 0) and cand.min() >= 0 and cand.max() < n_cur
+    assert np.all(np.diff(inter["idx"], axis=-1) > 0)
+    assert np.all(gcnt.reshape(b, hkv, 16, 256).sum(axis=-1) == n_cur)
+    for s_, h in ((0, 2), (3, 7)):
+        print(f"case drift full width oracle group ({s_}, {h})", flush=True)
+        orc = oracle_group(K[s_, h, :n_cur], signs)
+        check_index(gids[s_, h], grec[s_, h], gcnt[s_, h], orc)
+        for gg in range(g):
+            hq = h * g + gg
+            check_head(inter, s_, h, gg, g, Q[s_, hq], orc, signs, budget, n_cur)
+            check_attention(o_gpu[s_, hq], Q[s_, hq], K[s_, h, :n_cur], V[s_, h, :n_cur], inter["idx"][s_, hq],
+                            SCALE)
+
+
 def test_host_mapped_attention_matches_hbm():
     cfg = workloads.CONFIGS["layer32k"]
     wc, K, V, Q, _, signs = _inputs(cfg, n=8192)

@@ -223,3 +223,34 @@ def test_needles_are_found():
         hits += needles[0, h] in r["idx"]
         assert retrieve.recall(r["idx"], ref) > 0.5
     assert hits == cfg.n_q_heads
+
+
+def test_exact_topk_brute_force_and_ties():
+    # exact_topk against a plain Python selection: scores summed term by term in float64,
+    # then repeatedly the largest remaining score, the lower index on ties
+    r = np.random.default_rng(5)
+    K = r.standard_normal((40, 6)).astype(np.float16)
+    K[7] = K[3]            # equal keys tie: the lower index comes first
+    K[20] = K[3]
+    q = r.standard_normal(6).astype(np.float16)
+    scores = [sum(float(K[i, j]) * float(q[j]) for j in range(6)) for i in range(40)]
+    left, want = list(range(40)), []
+    for _ in range(12):
+        best = max(left, key=lambda i: (scores[i], -i))
+        want.append(best)
+        left.remove(best)
+    got = [int(i) for i in retrieve.exact_topk(K, q, 12)]
+    assert got == want
+    if 3 in want:
+        assert want.index(3) < want.index(7) < want.index(20)
+    # k above n returns every key, best first
+    assert sorted(int(i) for i in retrieve.exact_topk(K, q, 100)) == list(range(40))
+
+
+def test_recall_counts_hits_over_the_reference():
+    assert retrieve.recall([4, 1, -1, -1], [1, 2, 3]) == pytest.approx(1 / 3)
+    assert retrieve.recall([3, 2, 1], [1, 2, 3]) == 1.0
+    assert retrieve.recall([3, 3, 3, -1], [3, 4]) == 0.5      # a repeated index counts once
+    assert retrieve.recall([-1, -1], [0, 1]) == 0.0            # padding is never a hit
+    assert retrieve.recall([5], []) == 0.0                     # empty reference
+    assert retrieve.recall(np.array([9, 8, 7], np.int32), np.array([7, 8, 9, 10])) == 0.75

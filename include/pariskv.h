@@ -138,8 +138,9 @@ typedef struct pariskv_index {
  * heads' lists overlap.  out then equals per-head attention up to float32
  * rounding order (not bit for bit); out_idx / out_score are unchanged.  The
  * distinct rows fetched per (sequence, KV head, quad) are left in the workspace
- * (pariskv_ws_layout.group_rows).  Needs min(G, 4) * k <= PARISKV_MAX_ATTEND_ROWS;
- * the window and tiered entry points refuse it (UNSUPPORTED). */
+ * (pariskv_ws_layout.group_rows).  Needs min(G, 4) * k <= PARISKV_MAX_ATTEND_ROWS
+ * and n <= 4194304 (64 key ranges of 65536); the window and tiered entry points
+ * refuse it (UNSUPPORTED). */
 #define PARISKV_GROUP_FETCH 4
 
 /* Retrieval budgets of Alg. 1: C = ceil(beta n), C_rho = ceil(rho n), k. */
@@ -203,7 +204,8 @@ typedef struct pariskv_ws_layout {
                            the distinct K/V rows the attention fetched           */
     size_t group_part;  /* with PARISKV_GROUP_FETCH and group_splits > 1: float
                            [batch][Hkv][quads][group_splits][4][132], each share's
-                           per-head max, sum, 2 unused, unnormalised output     */
+                           per-head max, sum, rows fetched (head 0, int32 bits),
+                           unused, unnormalised output                          */
     int64_t n_pad;      /* row length of score8 (n rounded up to 64)             */
     int64_t n_chunks;   /* ceil(n / chunk_keys)                                  */
     int64_t chunk_keys; /* keys per selection chunk                              */
@@ -214,10 +216,12 @@ typedef struct pariskv_ws_layout {
                            ceil(min(C, n) / 4096) blocks per row first keep the k
                            best of their slice, then one block per row selects
                            among those (the same winners as one pass)           */
-    int32_t group_splits; /* with PARISKV_GROUP_FETCH: blocks sharing the union of
-                           one (sequence, KV head, quad): about 256 blocks in all,
-                           at most 16, at most min(G, 4) * k / 256, at least 1;
-                           0 without the flag                                    */
+    int32_t group_splits; /* with PARISKV_GROUP_FETCH: blocks sharing one (sequence,
+                           KV head, quad), block s taking the winners in key range
+                           [s r, (s + 1) r), r = ceil(max(n, 1) / group_splits):
+                           about 256 blocks in all and at most min(G, 4) * k / 256,
+                           but at least ceil(n / 65536) (r <= 65536), at most 64,
+                           at least 1; 0 without the flag                        */
 } pariskv_ws_layout;
 
 /* ------------------------------------------------------------ encoding */

@@ -158,7 +158,7 @@ int layout(const pariskv_config* cfg, int32_t batch, int64_t n, const pariskv_bu
     L->surv = take(L->topk_parts > 1 ? (size_t)rows * L->topk_parts * bud->top_k * 8 : 0);
     const bool group_fetch = (bud->flags & PARISKV_GROUP_FETCH) != 0;
     L->group_rows = take(group_fetch ? (size_t)batch * hkv * quads * 4 : 0);
-    L->group_splits = group_fetch ? group_splits((int64_t)batch * hkv * quads, (g < 4 ? g : 4) * (int64_t)bud->top_k) : 0;
+    L->group_splits = group_fetch ? group_splits((int64_t)batch * hkv * quads, (g < 4 ? g : 4) * (int64_t)bud->top_k, n) : 0;
     L->group_part = take(group_fetch ? group_part_bytes((int64_t)batch * hkv * quads, L->group_splits) : 0);
     L->total = off;
     return PARISKV_OK;
@@ -528,6 +528,9 @@ static int retrieve_impl(const pariskv_config* cfg, const pariskv_index* index, 
             if (per > kMaxAttendRows)
                 return fail(PARISKV_ERR_UNSUPPORTED, "PARISKV_GROUP_FETCH: min(G, 4) * k = %lld above %d",
                             (long long)per, kMaxAttendRows);
+            if (n > kGaMaxSplits * kGaRangeKeys)
+                return fail(PARISKV_ERR_UNSUPPORTED, "PARISKV_GROUP_FETCH: n = %lld above %lld keys", (long long)n,
+                            (long long)(kGaMaxSplits * kGaRangeKeys));
         }
         if ((rc = device_kv(*att, &Kd, &Vd)) != PARISKV_OK) return rc;
     }
@@ -598,12 +601,14 @@ static int retrieve_impl(const pariskv_config* cfg, const pariskv_index* index, 
         return ea == hipSuccess ? PARISKV_OK : hip_fail(ea, "attend launch");
     };
     const bool group_fetch = att && (budget->flags & PARISKV_GROUP_FETCH);
-    // Attention per quad of heads over the union of their (ascending) winner lists.
+    // Attention per quad of heads over the union of their winner lists, share s of a
+    // quad taking the rows in [s * group_range, (s + 1) * group_range).
+    const int64_t group_range = group_fetch ? ((n > 0 ? n : 1) + L.group_splits - 1) / L.group_splits : 0;
     auto attend_groups = [&]() -> int {
         const hipError_t eg = launch_group_attend(q, Kd, Vd, att->kv_capacity, out_idx, budget->top_k, batch,
                                                   a.hkv, a.g, att->scale, att->out,
                                                   reinterpret_cast<int32_t*>(ws + L.group_rows), L.group_splits,
-                                                  reinterpret_cast<float*>(ws + L.group_part), s);
+                                                  group_range, reinterpret_cast<float*>(ws + L.group_part), s);
         return eg == hipSuccess ? PARISKV_OK : hip_fail(eg, "group_attend launch");
     };
     if (n == 0) {
@@ -784,8 +789,11 @@ int pariskv_group_attend(const pariskv_config* cfg, const void* q, const void* K
         if (e != hipSuccess) return hip_fail(e, "hipHostGetDevicePointer(V)");
         Vd = p;
     }
+    // One share per quad: the union by key bitmap over the whole cache when it spans at
+    // most kGaRangeKeys rows, else by merging the lists.
     hipError_t e = launch_group_attend(q, Kd, Vd, kv_capacity, idx, k, batch, cfg->n_kv_heads,
-                                       cfg->q_per_kv, scale, out, union_rows, 1, nullptr,
+                                       cfg->q_per_kv, scale, out, union_rows, 1,
+                                       kv_capacity <= kGaRangeKeys ? kv_capacity : 0, nullptr,
                                        static_cast<hipStream_t>(stream));
     if (e != hipSuccess) return hip_fail(e, "group_attend launch");
     return PARISKV_OK;

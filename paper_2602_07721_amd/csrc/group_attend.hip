@@ -6,30 +6,29 @@
 //   o_h = sum_{i in idx_h} softmax_i(scale <k_i, q_h>) v_i   for each head h,
 //   float16 in, float32 math -- the same value as the per-head attention.
 //
-// One block of 512 threads per (sequence, KV head, quad of query heads):
-//   1. the quad's lists (each ascending with -1 padding at its end, as the
-//      retrieval writes them) are staged in LDS, invalid entries as +inf;
-//   2. merge by rank: an entry's place in the merged order is its index plus,
-//      for every other list, the number of entries before it there (binary
-//      search; ties ordered by head), so the merged rows are ascending and
-//      equal rows adjacent.  Every place is below G * k whatever the input
-//      order, so unsorted lists give an unspecified result, never a stray
-//      access;
-//   3. union: a block scan over "first of its row" flags numbers the distinct
-//      rows; each head ORs its bit into its row's mask;
+// One block of 512 threads per (sequence, KV head, quad of query heads) and
+// share of it:
+//   1-3. the union of the quad's lists with each row's head mask, in one of two
+//      ways.  Key ranges (the retrieval path, and stand-alone calls over at most
+//      65536 cache rows): share s of `splits` takes the rows in
+//      [s * range, (s + 1) * range), range <= 65536; each head sets its rows'
+//      bits in a bitmap of the range, and a block scan over the OR of the four
+//      bitmaps numbers the distinct rows in ascending order.  Merge (larger
+//      stand-alone calls, one share): the lists (each ascending with -1 padding
+//      at its end, as the retrieval writes them) are staged in LDS, merged by
+//      rank (an entry's place is its index plus, for every other list, the
+//      number of entries before it there; ties ordered by head), and a block
+//      scan over "first of its row" flags numbers the distinct rows.  Unsorted
+//      lists give an unspecified result there, never a stray access;
 //   4. 32 slots of 16 lanes (lane l16 owns dims [8 l16, 8 l16 + 8)) walk the
-//      block's share of the union, 8 rows in flight per lane; each K and V row
-//      segment is read once and feeds the online softmax of every head whose
-//      bit is set (one rescale per head per 8 rows);
+//      share's union rows, 8 rows in flight per lane; each K and V row segment
+//      is read once and feeds the online softmax of every head whose bit is set
+//      (one rescale per head per 8 rows);
 //   5. the 32 slot states of every head are merged in LDS.
-//
-// With few (sequence, KV head, quad) groups the union of each is split over
-// `splits` blocks (the grid's fastest index), so that enough workgroups keep
-// reads in flight -- over the host link above all.  Every split redoes steps
-// 1-3 (LDS work on 16 KiB of indices), walks its contiguous share of the union
-// rows and leaves its per-head state (running max, sum, unnormalised output)
-// in `part`; group_combine_kernel then merges the shares of each head as step 5
-// merges slots.  With one split the block writes `out` itself.
+// With one share the block writes `out`; with several, each leaves its per-head
+// state (running max, sum, unnormalised output) and its row count in `part`,
+// and group_combine_kernel merges the shares of each head as step 5 merges
+// slots.
 
 #include "attend_row.hpp"
 
@@ -42,16 +41,22 @@ constexpr int kGaSlots = kGaThreads / 16;
 constexpr int kGaUnroll = 8;  // K/V rows in flight per lane
 constexpr int kGaMaxEntries = 4096;  // G * k per quad staged in LDS
 constexpr int32_t kGaInvalid = 0x7fffffff;
-constexpr int kGaPart = 4 + kD;  // one head's share state: max, sum, 2 pad, output
+constexpr int kGaPart = 4 + kD;  // one head's share state: max, sum, row count (head 0), pad, output
+constexpr int kGaRangeWords = kGaRangeKeys / 32;
 static_assert(kGaThreads == 4 * kD, "the slot merge gives one thread to every (head, dim)");
+static_assert(kGaRangeWords % kGaThreads == 0, "range words per thread");
 
 struct GroupScratch {
-    int32_t list[kGaMaxEntries];   // staged lists, then the union's rows
-    int32_t row[kGaMaxEntries];    // merged rows
-    uint8_t head[kGaMaxEntries];   // head of each merged entry
+    int32_t list[kGaMaxEntries];   // merge: staged lists; then the union's rows
     uint32_t mask[kGaMaxEntries];  // head mask of each union row
+    union {
+        struct {
+            int32_t row[kGaMaxEntries];  // merged rows
+            uint8_t head[kGaMaxEntries]; // head of each merged entry
+        } m;
+        uint32_t bits[4][kGaRangeWords];  // key ranges: each head's rows in the range
+    } u;
     uint32_t wsum[kGaThreads / 64];
-    uint32_t nunion;
 };
 
 // LDS for the final merge of the slot states, every head of the quad at once.
@@ -61,11 +66,28 @@ struct GroupMerge {
     float acc[4][kGaSlots][kD];
 };
 
+// Block scan of per-thread counts: (exclusive prefix of this thread, block total).
+__device__ __forceinline__ void block_count_scan(uint32_t cnt, uint32_t* wsum, uint32_t* before, uint32_t* total) {
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    const uint32_t incl = wave_incl_sum(cnt);
+    if (lane == 63) wsum[wave] = incl;
+    __syncthreads();
+    uint32_t b = incl - cnt, t = 0;
+#pragma unroll
+    for (int w = 0; w < kGaThreads / 64; ++w) {
+        if (w < wave) b += wsum[w];
+        t += wsum[w];
+    }
+    *before = b;
+    *total = t;
+}
+
+template <bool kRanges>
 __global__ __launch_bounds__(kGaThreads) void group_attend_kernel(
     const __half* __restrict__ q, const __half* __restrict__ K, const __half* __restrict__ V,
     int64_t kv_capacity, const int32_t* __restrict__ idx, int32_t k, int32_t hkv, int32_t g,
     int32_t quads, float scale, float* __restrict__ out, int32_t* __restrict__ union_rows, int32_t splits,
-    float* __restrict__ part) {
+    int64_t range, float* __restrict__ part) {
     __shared__ GroupScratch sg;
     __shared__ GroupMerge gm;
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
@@ -78,101 +100,135 @@ __global__ __launch_bounds__(kGaThreads) void group_attend_kernel(
     const int64_t row0 = (int64_t)seq * hkv * g + (int64_t)kvh * g + 4 * quad;  // first query head row
     const int ne = nh * k;  // entries of the quad (host checked <= kGaMaxEntries)
 
-    // 1. stage the lists; invalid entries sort last
-    for (int r = tid; r < ne; r += kGaThreads) {
-        const int32_t v = idx[(row0 + r / k) * k + r % k];
-        sg.list[r] = (v >= 0 && v < kv_capacity) ? v : kGaInvalid;
-        sg.row[r] = kGaInvalid;  // a place no entry lands on (unsorted input) stays empty
-        sg.mask[r] = 0u;
-    }
-    __syncthreads();
-    // 2. merge by rank.  Thread t places entries t + 512 e (e < kPer); the rank of an
-    // entry in list o is found by binary lifting (the largest prefix of list o whose
-    // entries come before it), the kPer searches of a thread interleaved step by step.
     constexpr int kPer = kGaMaxEntries / kGaThreads;
-    {
-        int32_t v[kPer];
-        int hd[kPer], pos[kPer];
-#pragma unroll
-        for (int e = 0; e < kPer; ++e) {
-            const int r = tid + kGaThreads * e;
-            hd[e] = r < ne ? r / k : -1;
-            v[e] = r < ne ? sg.list[r] : kGaInvalid;
-            pos[e] = r < ne ? r % k : 0;
+    int U;  // union rows of this share, in sg.list / sg.mask [0, U)
+    if constexpr (kRanges) {
+        // 1. each head's rows in [r0, r0 + range) as bits
+        const int64_t r0 = (int64_t)split * range;
+        for (int i = tid; i < 4 * kGaRangeWords; i += kGaThreads) (&sg.u.bits[0][0])[i] = 0u;
+        __syncthreads();
+        for (int r = tid; r < ne; r += kGaThreads) {
+            const int h = r / k;
+            const int32_t v = idx[(row0 + h) * k + r % k];
+            const int64_t d = (int64_t)v - r0;
+            if (v >= 0 && v < kv_capacity && d >= 0 && d < range)
+                atomicOr(&sg.u.bits[h][d >> 5], 1u << (d & 31));
         }
-        int top = 1;
-        while (2 * top <= k) top *= 2;
-        for (int o = 0; o < nh; ++o) {
-            const int32_t* a = sg.list + o * k;
-            int lo[kPer];
-            bool upper[kPer];  // ties: entries of lower heads first
+        __syncthreads();
+        // 2-3. thread t owns words [4t, 4t + 4) of the range; rows in ascending order
+        constexpr int kWords = kGaRangeWords / kGaThreads;
+        uint32_t uw[kWords];
+        uint32_t cnt = 0;
+#pragma unroll
+        for (int e = 0; e < kWords; ++e) {
+            const int w = kWords * tid + e;
+            uw[e] = sg.u.bits[0][w] | sg.u.bits[1][w] | sg.u.bits[2][w] | sg.u.bits[3][w];
+            cnt += (uint32_t)__popc(uw[e]);
+        }
+        uint32_t before, total;
+        block_count_scan(cnt, sg.wsum, &before, &total);
+        uint32_t u = before;
+#pragma unroll
+        for (int e = 0; e < kWords; ++e) {
+            const int w = kWords * tid + e;
+            for (uint32_t x = uw[e]; x; x &= x - 1u) {
+                const int bit = __builtin_ctz(x);
+                sg.list[u] = (int32_t)(r0 + 32 * w + bit);
+                sg.mask[u] = ((sg.u.bits[0][w] >> bit) & 1u) | (((sg.u.bits[1][w] >> bit) & 1u) << 1) |
+                             (((sg.u.bits[2][w] >> bit) & 1u) << 2) | (((sg.u.bits[3][w] >> bit) & 1u) << 3);
+                ++u;
+            }
+        }
+        U = (int)total;
+    } else {
+        // 1. stage the lists; invalid entries sort last
+        for (int r = tid; r < ne; r += kGaThreads) {
+            const int32_t v = idx[(row0 + r / k) * k + r % k];
+            sg.list[r] = (v >= 0 && v < kv_capacity) ? v : kGaInvalid;
+            sg.u.m.row[r] = kGaInvalid;  // a place no entry lands on (unsorted input) stays empty
+            sg.mask[r] = 0u;
+        }
+        __syncthreads();
+        // 2. merge by rank.  Thread t places entries t + 512 e (e < kPer); the rank of an
+        // entry in list o is found by binary lifting (the largest prefix of list o whose
+        // entries come before it), the kPer searches of a thread interleaved step by step.
+        {
+            int32_t v[kPer];
+            int hd[kPer], pos[kPer];
 #pragma unroll
             for (int e = 0; e < kPer; ++e) {
-                lo[e] = 0;
-                upper[e] = o < hd[e];
+                const int r = tid + kGaThreads * e;
+                hd[e] = r < ne ? r / k : -1;
+                v[e] = r < ne ? sg.list[r] : kGaInvalid;
+                pos[e] = r < ne ? r % k : 0;
             }
-            // branch-free steps: all kPer reads issued before any compare
-            for (int step = top; step > 0; step >>= 1) {
-                int32_t x[kPer];
-#pragma unroll
-                for (int e = 0; e < kPer; ++e) x[e] = a[min(lo[e] + step, k) - 1];
+            int top = 1;
+            while (2 * top <= k) top *= 2;
+            for (int o = 0; o < nh; ++o) {
+                const int32_t* a = sg.list + o * k;
+                int lo[kPer];
+                bool upper[kPer];  // ties: entries of lower heads first
 #pragma unroll
                 for (int e = 0; e < kPer; ++e) {
-                    const bool take = (lo[e] + step <= k) & ((x[e] < v[e]) | (upper[e] & (x[e] == v[e])));
-                    lo[e] = take ? lo[e] + step : lo[e];
+                    lo[e] = 0;
+                    upper[e] = o < hd[e];
+                }
+                // branch-free steps: all kPer reads issued before any compare
+                for (int step = top; step > 0; step >>= 1) {
+                    int32_t x[kPer];
+#pragma unroll
+                    for (int e = 0; e < kPer; ++e) x[e] = a[min(lo[e] + step, k) - 1];
+#pragma unroll
+                    for (int e = 0; e < kPer; ++e) {
+                        const bool take = (lo[e] + step <= k) & ((x[e] < v[e]) | (upper[e] & (x[e] == v[e])));
+                        lo[e] = take ? lo[e] + step : lo[e];
+                    }
+                }
+#pragma unroll
+                for (int e = 0; e < kPer; ++e) pos[e] += o != hd[e] ? lo[e] : 0;
+            }
+#pragma unroll
+            for (int e = 0; e < kPer; ++e) {
+                if (hd[e] >= 0) {
+                    const int p = min(pos[e], ne - 1);
+                    sg.u.m.row[p] = v[e];
+                    sg.u.m.head[p] = (uint8_t)hd[e];
                 }
             }
-#pragma unroll
-            for (int e = 0; e < kPer; ++e) pos[e] += o != hd[e] ? lo[e] : 0;
         }
+        __syncthreads();
+        // 3. union: thread t owns merged entries [8t, 8t + 8)
+        uint32_t first[kPer];
+        uint32_t cnt = 0;
 #pragma unroll
         for (int e = 0; e < kPer; ++e) {
-            if (hd[e] >= 0) {
-                const int p = min(pos[e], ne - 1);
-                sg.row[p] = v[e];
-                sg.head[p] = (uint8_t)hd[e];
-            }
+            const int p = kPer * tid + e;
+            const int32_t v = p < ne ? sg.u.m.row[p] : kGaInvalid;
+            first[e] = (v != kGaInvalid && (p == 0 || sg.u.m.row[p - 1] != v)) ? 1u : 0u;
+            cnt += first[e];
+        }
+        uint32_t before, total;
+        block_count_scan(cnt, sg.wsum, &before, &total);
+        // union row u keeps its row in list[u] (the staged lists are no longer read)
+        uint32_t u = before;
+#pragma unroll
+        for (int e = 0; e < kPer; ++e) {
+            const int p = kPer * tid + e;
+            if (first[e]) sg.list[u] = sg.u.m.row[p];
+            u += first[e];
+            // a duplicate belongs to the union row of the last first at or before it
+            if (p < ne && sg.u.m.row[p] != kGaInvalid) atomicOr(&sg.mask[u - 1], 1u << sg.u.m.head[p]);
+        }
+        U = (int)total;
+    }
+    if (tid == 0) {
+        if (splits == 1) {
+            if (union_rows) union_rows[blk] = U;
+        } else {
+            part[((blk * splits + split) * 4) * kGaPart + 2] = __int_as_float(U);  // head 0's count slot
         }
     }
     __syncthreads();
-    // 3. union: thread t owns merged entries [8t, 8t + 8)
-    uint32_t first[kPer];
-    uint32_t cnt = 0;
-#pragma unroll
-    for (int e = 0; e < kPer; ++e) {
-        const int p = kPer * tid + e;
-        const int32_t v = p < ne ? sg.row[p] : kGaInvalid;
-        first[e] = (v != kGaInvalid && (p == 0 || sg.row[p - 1] != v)) ? 1u : 0u;
-        cnt += first[e];
-    }
-    const uint32_t incl = wave_incl_sum(cnt);
-    if (lane == 63) sg.wsum[wave] = incl;
-    __syncthreads();
-    uint32_t before = incl - cnt;
-    uint32_t total = 0;
-#pragma unroll
-    for (int w = 0; w < kGaThreads / 64; ++w) {
-        if (w < wave) before += sg.wsum[w];
-        total += sg.wsum[w];
-    }
-    // union row u keeps its row in list[u] (the staged lists are no longer read)
-    uint32_t u = before;
-#pragma unroll
-    for (int e = 0; e < kPer; ++e) {
-        const int p = kPer * tid + e;
-        if (first[e]) sg.list[u] = sg.row[p];
-        u += first[e];
-        // a duplicate belongs to the union row of the last first at or before it
-        if (p < ne && sg.row[p] != kGaInvalid) atomicOr(&sg.mask[u - 1], 1u << sg.head[p]);
-    }
-    if (tid == 0) {
-        sg.nunion = total;
-        if (union_rows && split == 0) union_rows[blk] = (int32_t)total;
-    }
-    __syncthreads();
-    // this block's share [u_lo, u_hi) of the union rows
-    const int u_lo = (int)((int64_t)sg.nunion * split / splits);
-    const int U = (int)((int64_t)sg.nunion * (split + 1) / splits);
 
     // 4. attention over the union, every head of the quad at once
     const int slot = tid >> 4, l16 = tid & 15;
@@ -193,7 +249,7 @@ __global__ __launch_bounds__(kGaThreads) void group_attend_kernel(
 #pragma unroll
         for (int d = 0; d < 8; ++d) acc[h][d] = 0.f;
     }
-    for (int base = u_lo; base < U; base += kGaSlots * kGaUnroll) {
+    for (int base = 0; base < U; base += kGaSlots * kGaUnroll) {
         uint32_t msk[kGaUnroll];
         uint4 kc[kGaUnroll], vc[kGaUnroll];
 #pragma unroll
@@ -292,10 +348,12 @@ __global__ __launch_bounds__(kGaThreads) void group_attend_kernel(
 }
 
 // One block of kD threads per (group block, head): merges the `splits` share
-// states of the head (thread d owns output dim d).
+// states of the head (thread d owns output dim d); kMaxShares >= splits sizes
+// the registers that take every share's state at once.
+template <int kMaxShares>
 __global__ __launch_bounds__(kD) void group_combine_kernel(const float* __restrict__ part, int32_t splits,
                                                            int32_t hkv, int32_t g, int32_t quads,
-                                                           float* __restrict__ out) {
+                                                           float* __restrict__ out, int32_t* __restrict__ union_rows) {
     const int tid = threadIdx.x;
     const int64_t blk = blockIdx.x >> 2;  // (seq * hkv + kvh) * quads + quad
     const int h = (int)(blockIdx.x & 3);
@@ -305,10 +363,15 @@ __global__ __launch_bounds__(kD) void group_combine_kernel(const float* __restri
     const int64_t row = (grp / hkv) * hkv * g + (grp % hkv) * g + 4 * quad + h;
     const float* ps = part + (blk * splits * 4 + h) * kGaPart;
     const int64_t stride = 4 * kGaPart;  // next share of the same head
-    // every share's state loaded at once (splits <= kGaMaxSplits)
-    float mj[kGaMaxSplits], lj[kGaMaxSplits], oj[kGaMaxSplits];
+    if (h == 0 && tid == 0 && union_rows) {
+        int32_t rows = 0;
+        for (int j = 0; j < splits; ++j) rows += __float_as_int(ps[j * stride + 2]);
+        union_rows[blk] = rows;
+    }
+    // every share's state loaded at once (splits <= kMaxShares)
+    float mj[kMaxShares], lj[kMaxShares], oj[kMaxShares];
 #pragma unroll
-    for (int j = 0; j < kGaMaxSplits; ++j) {
+    for (int j = 0; j < kMaxShares; ++j) {
         lj[j] = 0.f;
         mj[j] = oj[j] = 0.f;
         if (j < splits) {
@@ -319,11 +382,11 @@ __global__ __launch_bounds__(kD) void group_combine_kernel(const float* __restri
     }
     float M = -__builtin_huge_valf();
 #pragma unroll
-    for (int j = 0; j < kGaMaxSplits; ++j)
+    for (int j = 0; j < kMaxShares; ++j)
         if (lj[j] > 0.f) M = fmaxf(M, mj[j]);
     float L = 0.f, O = 0.f;
 #pragma unroll
-    for (int j = 0; j < kGaMaxSplits; ++j) {
+    for (int j = 0; j < kMaxShares; ++j) {
         if (lj[j] > 0.f) {
             const float c = __expf(mj[j] - M);
             L += lj[j] * c;
@@ -335,12 +398,14 @@ __global__ __launch_bounds__(kD) void group_combine_kernel(const float* __restri
 
 }  // namespace
 
-int32_t group_splits(int64_t groups, int64_t per) {
-    if (groups >= 256) return 1;
-    int64_t s = (256 + groups - 1) / groups;
+int32_t group_splits(int64_t groups, int64_t per, int64_t n) {
+    int64_t s = groups >= 256 ? 1 : (256 + groups - 1) / groups;
     s = s < kGaMaxSplits ? s : kGaMaxSplits;
-    const int64_t by_rows = per / 256;  // at least 256 union rows of the worst case per share
+    const int64_t by_rows = per / 256;  // no more shares than 256-entry slices of the quad's lists
     s = s < by_rows ? s : by_rows;
+    const int64_t need = (n + kGaRangeKeys - 1) / kGaRangeKeys;  // key ranges of at most kGaRangeKeys
+    s = s > need ? s : need;
+    s = s < kGaMaxSplits ? s : kGaMaxSplits;
     return (int32_t)(s < 1 ? 1 : s);
 }
 
@@ -350,23 +415,35 @@ size_t group_part_bytes(int64_t groups, int32_t splits) {
 
 hipError_t launch_group_attend(const void* q, const void* K, const void* V, int64_t kv_capacity,
                                const int32_t* idx, int32_t k, int32_t batch, int32_t hkv, int32_t g,
-                               float scale, float* out, int32_t* union_rows, int32_t splits, float* part,
-                               hipStream_t s) {
+                               float scale, float* out, int32_t* union_rows, int32_t splits, int64_t range,
+                               float* part, hipStream_t s) {
     const int32_t quads = (g + 3) / 4;
     const int64_t groups = (int64_t)batch * hkv * quads;
-    if (splits < 1 || splits > kGaMaxSplits || (splits > 1 && !part)) return hipErrorInvalidValue;
+    const bool ranges = range >= 1 && range <= kGaRangeKeys;
+    if (splits < 1 || splits > kGaMaxSplits || (splits > 1 && (!part || !ranges))) return hipErrorInvalidValue;
     {
         const ProfEvents pe = prof_begin("group_attend");
-        hipExtLaunchKernelGGL(group_attend_kernel, dim3((unsigned)(groups * splits)), dim3(kGaThreads), 0, s,
-                              pe.start, pe.stop, 0, static_cast<const __half*>(q), static_cast<const __half*>(K),
-                              static_cast<const __half*>(V), kv_capacity, idx, k, hkv, g, quads, scale, out,
-                              union_rows, splits, part);
+        const dim3 grid((unsigned)(groups * splits)), block(kGaThreads);
+        const __half *qh = static_cast<const __half*>(q), *Kh = static_cast<const __half*>(K),
+                     *Vh = static_cast<const __half*>(V);
+        if (ranges)
+            hipExtLaunchKernelGGL(group_attend_kernel<true>, grid, block, 0, s, pe.start, pe.stop, 0, qh, Kh, Vh,
+                                  kv_capacity, idx, k, hkv, g, quads, scale, out, union_rows, splits, range, part);
+        else
+            hipExtLaunchKernelGGL(group_attend_kernel<false>, grid, block, 0, s, pe.start, pe.stop, 0, qh, Kh, Vh,
+                                  kv_capacity, idx, k, hkv, g, quads, scale, out, union_rows, splits, range, part);
         const hipError_t e = hipGetLastError();
         if (e != hipSuccess || splits == 1) return e;
     }
     const ProfEvents pe = prof_begin("group_combine");
-    hipExtLaunchKernelGGL(group_combine_kernel, dim3((unsigned)(groups * 4)), dim3(kD), 0, s, pe.start, pe.stop,
-                          0, static_cast<const float*>(part), splits, hkv, g, quads, out);
+    const dim3 cgrid((unsigned)(groups * 4)), cblock(kD);
+    const float* pc = part;
+    if (splits <= 16)
+        hipExtLaunchKernelGGL(group_combine_kernel<16>, cgrid, cblock, 0, s, pe.start, pe.stop, 0, pc, splits, hkv,
+                              g, quads, out, union_rows);
+    else
+        hipExtLaunchKernelGGL(group_combine_kernel<kGaMaxSplits>, cgrid, cblock, 0, s, pe.start, pe.stop, 0, pc,
+                              splits, hkv, g, quads, out, union_rows);
     return hipGetLastError();
 }
 

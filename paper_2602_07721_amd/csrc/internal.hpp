@@ -244,17 +244,20 @@ constexpr int kMaxAttendRows = 4096;
 // Attention of each quad of query heads sharing a KV head over the union of
 // their (ascending) lists, every distinct row fetched once; min(G, 4) * k must
 // not exceed kMaxAttendRows.  union_rows (nullable): [batch][Hkv][quads] sizes.
-// With splits > 1 each quad's union is shared by that many blocks, whose
-// states (group_part_bytes of `part`) a second kernel merges into out.
-constexpr int kGaMaxSplits = 16;
+// With 1 <= range <= kGaRangeKeys, share s of `splits` per quad takes the rows
+// in [s * range, (s + 1) * range) (rows past splits * range are dropped); with
+// splits > 1 a second kernel merges the shares' states (group_part_bytes of
+// `part`).  range = 0: one share per quad, the union by merging the lists.
+constexpr int kGaMaxSplits = 64;
+constexpr int64_t kGaRangeKeys = 65536;
 hipError_t launch_group_attend(const void* q, const void* K, const void* V, int64_t kv_capacity,
                                const int32_t* idx, int32_t k, int32_t batch, int32_t hkv, int32_t g,
-                               float scale, float* out, int32_t* union_rows, int32_t splits, float* part,
-                               hipStream_t s);
-// Blocks per quad for `groups` (sequence, KV head, quad) triples with at most
-// `per` = min(G, 4) * k entries each: enough for ~256 blocks, at most
-// kGaMaxSplits, and no more than per / 256.
-int32_t group_splits(int64_t groups, int64_t per);
+                               float scale, float* out, int32_t* union_rows, int32_t splits, int64_t range,
+                               float* part, hipStream_t s);
+// Shares per quad for `groups` (sequence, KV head, quad) triples with at most
+// `per` = min(G, 4) * k entries each over n keys: enough for ~256 blocks, no
+// more than per / 256, at least ceil(n / kGaRangeKeys), at most kGaMaxSplits.
+int32_t group_splits(int64_t groups, int64_t per, int64_t n);
 size_t group_part_bytes(int64_t groups, int32_t splits);
 
 // Reference streaming kernels (measurement only): a copy and a read of `bytes`.

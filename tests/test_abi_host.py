@@ -465,6 +465,21 @@ def test_group_fetch_validation():
     # G = 2: 2 x 64 entries per quad, too few to share
     g2 = pk.workspace_layout(_cfg(q_per_kv=2), 1, 4000, ok)
     assert g2["group_splits"] == 1
+    # key ranges of at most 65536: 1.1M keys need 17 shares even where 16 would do
+    big = pk.Config(8, 4, 1100000, workloads.rotation_signs(0))
+    assert pk.workspace_layout(big, 1, 1100000, pk.Budget(8192, 16384, 1024, flags=pk.GROUP_FETCH))[
+        "group_splits"] == 17
+    assert pk.workspace_layout(big, 1, 1100000, pk.Budget(8192, 16384, 16, flags=pk.GROUP_FETCH))[
+        "group_splits"] == 17
+    # beyond 64 ranges of 65536 keys the flag is refused
+    huge = pk.Config(1, 4, 5000000, workloads.rotation_signs(0))
+    hb = pk.Budget(8192, 16384, 64, flags=pk.GROUP_FETCH)
+    need = pk.retrieve_workspace_size(huge, 1, 4200000, hb)
+    rc = L.pariskv_retrieve_attend(huge.c(), ctypes.byref(_index()), ctypes.c_void_p(FAKE), 4200000, 1, hb.c(),
+                                   ctypes.c_void_p(FAKE), None, ctypes.c_void_p(FAKE), ctypes.c_void_p(FAKE), 0,
+                                   4200000, ctypes.c_float(0.1), ctypes.c_void_p(FAKE), ctypes.c_void_p(FAKE), need,
+                                   None)
+    assert rc == pk.ERR_UNSUPPORTED and "4194304" in L.pariskv_last_error().decode()
     big = pk.Budget(8192, 16384, 2048, flags=pk.GROUP_FETCH)   # 4 x 2048 > 4096
     need = pk.retrieve_workspace_size(cfg, 1, 4000, big)
     rc = L.pariskv_retrieve_attend(cfg.c(), ctypes.byref(_index()), ctypes.c_void_p(FAKE), 4000, 1, big.c(),

@@ -32,12 +32,16 @@ def _lists(b, hkv, g, k, cap, overlap, seed):
     return idx
 
 
-@pytest.mark.parametrize("g,k,overlap,host", [(4, 256, 0.6, False), (4, 1024, 0.3, False), (1, 512, 0.0, False),
-                                              (3, 300, 0.9, False), (6, 128, 0.5, False), (4, 256, 0.6, True)],
-                         ids=["g4", "g4_k1024", "g1", "g3_odd_k", "g6_two_quads", "g4_host"])
-def test_group_attend_matches_the_oracle_per_head(g, k, overlap, host):
-    b, hkv, cap = 2, 2, 5000
-    print(f"[group_attend] g {g} k {k} overlap {overlap} host {host}", flush=True)
+@pytest.mark.parametrize("g,k,overlap,host,cap", [
+    (4, 256, 0.6, False, 5000), (4, 1024, 0.3, False, 5000), (1, 512, 0.0, False, 5000),
+    (3, 300, 0.9, False, 5000), (6, 128, 0.5, False, 5000), (4, 256, 0.6, True, 5000),
+    (4, 512, 0.5, True, 70000), (6, 200, 0.7, False, 70000)],
+    ids=["g4", "g4_k1024", "g1", "g3_odd_k", "g6_two_quads", "g4_host", "g4_host_merge", "g6_merge"])
+def test_group_attend_matches_the_oracle_per_head(g, k, overlap, host, cap):
+    # Over at most 65536 cache rows the union is built as a key bitmap, above that by
+    # merging the sorted lists (the *_merge cases).
+    b, hkv = 2, 2
+    print(f"[group_attend] g {g} k {k} overlap {overlap} host {host} cap {cap}", flush=True)
     K = np.stack([np.stack([workloads.head_keys(51, s, h, cap) for h in range(hkv)]) for s in range(b)])
     V = np.stack([np.stack([workloads.head_values(51, s, h, cap) for h in range(hkv)]) for s in range(b)])
     Q = np.stack([np.concatenate([workloads.needle_queries(K[s, h], 51, s, h, g)[0] for h in range(hkv)])
@@ -88,13 +92,17 @@ def test_group_attend_on_retrieval_output_and_empty_lists():
 @pytest.mark.parametrize("g,n,bud,host,splits", [
     (4, 9000, (700, 1500, 100), True, 1), (6, 5000, (400, 800, 64), False, 1),
     (4, 40000, (10000, 20000, 512), True, 8), (6, 12000, (1500, 3000, 256), False, 4),
-    (4, 0, (64, 128, 16), False, 1), (4, 0, (600, 1200, 512), False, 8)],
-    ids=["g4_host", "g6_two_quads", "g4_two_pass_host_split8", "g6_two_quads_split4", "n0", "n0_split8"])
+    (4, 0, (64, 128, 16), False, 1), (4, 0, (600, 1200, 512), False, 8),
+    (4, 140000, (4096, 8192, 64), True, 3)],
+    ids=["g4_host", "g6_two_quads", "g4_two_pass_host_split8", "g6_two_quads_split4", "n0", "n0_split8",
+         "g4_three_key_ranges_host"])
 def test_retrieve_attend_with_group_fetch(g, n, bud, host, splits):
     # PARISKV_GROUP_FETCH: the winners are those of the plain call bit for bit, each head's
     # attention matches the float64 oracle over its own winners, and the rows fetched per
-    # quad are the union of the quad's winner lists.  With splits > 1 each quad's union is
-    # shared by that many blocks and their states merged by a second kernel.
+    # quad are the union of the quad's winner lists.  With splits > 1 each quad's winners
+    # are shared by that many blocks by key range (at most 65536 keys each, so 140000
+    # keys take 3 even where the block count alone would ask for 1) and their states
+    # merged by a second kernel.
     b, hkv = 2, 2
     wc = workloads.Config("gfetch", batch=b, n_kv_heads=hkv, q_per_kv=g, n=max(n, 1), n_cand=bud[0],
                           n_collide=bud[1], top_k=bud[2], seed=53)
@@ -137,3 +145,34 @@ def test_retrieve_attend_with_group_fetch(g, n, bud, host, splits):
                 else:
                     check_attention(out[s, hq], Q[s, hq], K[s, h], V[s, h], idx[s, hq], SCALE)
     np.testing.assert_allclose(out, o1.cpu().numpy(), rtol=0, atol=1e-5 * max(np.abs(out).max(), 1e-30))
+
+
+def test_group_fetch_over_more_than_16_key_ranges():
+    # 1.1M keys: 17 key ranges of at most 65536 per quad, so the combine kernel takes its
+    # form for more than 16 shares.  One KV head, K/V in pinned host memory.
+    b, hkv, g, n = 1, 1, 4, 1100000
+    wc = workloads.Config("gfetch17", batch=b, n_kv_heads=hkv, q_per_kv=g, n=n, n_cand=4096, n_collide=8192,
+                          top_k=64, seed=54)
+    print("[group fetch] 17 key ranges", flush=True)
+    K, V = workloads.layer_kv(wc, threads=16)
+    Q, _ = workloads.layer_queries(wc, K)
+    cfg = pk.Config(hkv, g, n, workloads.rotation_signs(54))
+    index = pk.Index.empty(cfg, b)
+    pk.encode(cfg, index, torch.from_numpy(K).cuda())
+    Kh, Vh = torch.from_numpy(K).pin_memory(), torch.from_numpy(V).pin_memory()
+    Qd = torch.from_numpy(Q).cuda()
+    grouped = pk.Budget(4096, 8192, 64, flags=pk.GROUP_FETCH)
+    lay = pk.workspace_layout(cfg, b, n, grouped)
+    assert lay["group_splits"] == 17
+    i1, _, o1, _ = pk.retrieve_attend(cfg, index, Qd, n, pk.Budget(4096, 8192, 64), Kh, Vh, SCALE,
+                                      kv_host_mapped=True)
+    i2, _, o2, ws = pk.retrieve_attend(cfg, index, Qd, n, grouped, Kh, Vh, SCALE, kv_host_mapped=True)
+    torch.cuda.synchronize()
+    np.testing.assert_array_equal(i1.cpu().numpy(), i2.cpu().numpy())
+    idx, out = i2.cpu().numpy(), o2.cpu().numpy()
+    from parity import ws_array
+    un = ws_array(ws, lay["group_rows"], np.int32, (b, hkv, 1))
+    assert un[0, 0, 0] == len(set(int(x) for x in idx[0].ravel() if x >= 0))
+    for hq in range(g):
+        check_attention(out[0, hq], Q[0, hq], K[0, 0], V[0, 0], idx[0, hq], SCALE)
+    np.testing.assert_allclose(out, o1.cpu().numpy(), rtol=0, atol=1e-5 * np.abs(out).max())

@@ -513,7 +513,7 @@ def beta_length_run(pk, torch, np, workloads, dev, lengths=(4096, 16384, 65536, 
     }
 
 
-def offload_run(pk, torch, np, workloads, dev, steps, sink=128, local=512, m=256):
+def offload_run(pk, torch, np, workloads, dev, steps, sink=128, local=512, m=256, group_fetch=False, share=0):
     """The offload setting at 1M tokens (Sec. "Buffer Update" with GPU->CPU offload; Sec.
     "On-Demand UVA Fetch"): Sink and Local + Update Buffer K/V in a GPU window ring, the
     Retrieval region's K/V in pinned host memory.  Each decode step writes the new token into
@@ -526,7 +526,7 @@ def offload_run(pk, torch, np, workloads, dev, steps, sink=128, local=512, m=256
     P = wc.n
     total = P + steps
     K, V = workloads.layer_kv(wc, n=total, threads=16)
-    Q = np.stack([workloads.layer_queries(wc, K[:, :, :P], step=t)[0] for t in range(steps)])
+    Q = np.stack([workloads.layer_queries(wc, K[:, :, :P], step=t, shared=share)[0] for t in range(steps)])
     Kh = torch.from_numpy(K).pin_memory()   # the offloaded cache (rows of Retrieval)
     Vh = torch.from_numpy(V).pin_memory()
     hq = wc.n_kv_heads * wc.q_per_kv
@@ -549,7 +549,7 @@ def offload_run(pk, torch, np, workloads, dev, steps, sink=128, local=512, m=256
     del Kd
     torch.cuda.empty_cache()
     Qd = torch.from_numpy(Q).to(dev)
-    budget = pk.Budget(wc.n_cand, wc.n_collide, wc.top_k)
+    budget = pk.Budget(wc.n_cand, wc.n_collide, wc.top_k, flags=pk.GROUP_FETCH if group_fetch else 0)
     scale = 1.0 / np.sqrt(wc.head_dim)
     ws = torch.empty(pk.retrieve_workspace_size(cfg, wc.batch, total, budget), dtype=torch.uint8, device=dev)
     out_idx = torch.empty((wc.batch, hq, wc.top_k), dtype=torch.int32, device=dev)
@@ -628,6 +628,8 @@ def offload_run(pk, torch, np, workloads, dev, steps, sink=128, local=512, m=256
                       "topk_attend_us": round(ta_us, 1) if ta_us else None,
                       "GBps_of_topk_attend": round(fetch_bytes / (ta_us * 1e-6) / 1e9, 2) if ta_us else None},
         "kernels_avg_us": {k: round(v[1] * 1e3 / max(1, v[0]), 1) for k, v in prof.items()},
+        "group_fetch": group_fetch,
+        "query_heads_per_needle": max(share, 1),
         "timing": ("HIP events on the main stream around each step (steps 1-8 left out); the offload "
                    "copies timed on their own stream"),
     }
@@ -965,7 +967,8 @@ def main():
         extras["group_dedup"] = group_run(pk, torch, np, workloads, dev, args.drift_steps)
     if args.offload_steps > 0:
         torch.cuda.empty_cache()
-        extras["offload"] = offload_run(pk, torch, np, workloads, dev, args.offload_steps)
+        extras["offload"] = offload_run(pk, torch, np, workloads, dev, args.offload_steps,
+                                        group_fetch=args.group_fetch, share=args.group_share)
 
 
     mean_us = float(step_ms.mean() * 1e3)

@@ -130,17 +130,19 @@ typedef struct pariskv_index {
  * scores (see pariskv_ws_layout.thresh).  Same outputs, slower; it exercises
  * the recount that otherwise runs only when the histogram floor is too high. */
 #define PARISKV_EXACT_RECOUNT 2
-/* For pariskv.budget.flags with pariskv_retrieve_attend (and its _noalloc form):
- * GQA-group de-duplication of the fetch.  The attention of each quad of query
- * heads sharing a KV head reads every distinct K/V row of their winner lists
- * once (pariskv_group_attend) instead of once per head inside each head's
- * top-k; worth it when the rows cross the host link (kv_host_mapped = 1) and the
- * heads' lists overlap.  out then equals per-head attention up to float32
- * rounding order (not bit for bit); out_idx / out_score are unchanged.  The
- * distinct rows fetched per (sequence, KV head, quad) are left in the workspace
- * (pariskv_ws_layout.group_rows).  Needs min(G, 4) * k <= PARISKV_MAX_ATTEND_ROWS
- * and n <= 4194304 (64 key ranges of 65536); the window and tiered entry points
- * refuse it (UNSUPPORTED). */
+/* For pariskv.budget.flags with pariskv_retrieve_attend (and its _noalloc form),
+ * pariskv_retrieve_window_attend and pariskv_retrieve_tiered_attend: GQA-group
+ * de-duplication of the fetch.  The attention of each quad of query heads
+ * sharing a KV head reads every distinct K/V row of their winner lists once
+ * (pariskv_group_attend), and the window's dense rows (Sink, Local / Update
+ * Buffer), which every head attends, once per quad, instead of once per head
+ * inside each head's top-k; worth it when the rows cross the host link
+ * (kv_host_mapped = 1) and the heads' lists overlap.  out then equals per-head
+ * attention up to float32 rounding order (not bit for bit); out_idx / out_score
+ * are unchanged.  The distinct winner rows fetched per (sequence, KV head,
+ * quad) are left in the workspace (pariskv_ws_layout.group_rows).  Needs
+ * min(G, 4) * k <= PARISKV_MAX_ATTEND_ROWS and n <= 4194304 (64 key ranges of
+ * 65536), else UNSUPPORTED. */
 #define PARISKV_GROUP_FETCH 4
 
 /* Retrieval budgets of Alg. 1: C = ceil(beta n), C_rho = ceil(rho n), k. */

@@ -521,9 +521,6 @@ static int retrieve_impl(const pariskv_config* cfg, const pariskv_index* index, 
     if (att) {
         if ((rc = check_attend_args(*att)) != PARISKV_OK) return rc;
         if (budget->flags & PARISKV_GROUP_FETCH) {
-            const AttendWindow& w = att->win;
-            if (w.sink || w.retr_begin || w.dense_begin || w.dense_end || w.win_capacity)
-                return fail(PARISKV_ERR_UNSUPPORTED, "PARISKV_GROUP_FETCH serves the plain retrieve + attend only");
             const int64_t per = (int64_t)(cfg->q_per_kv < 4 ? cfg->q_per_kv : 4) * budget->top_k;
             if (per > kMaxAttendRows)
                 return fail(PARISKV_ERR_UNSUPPORTED, "PARISKV_GROUP_FETCH: min(G, 4) * k = %lld above %d",
@@ -608,7 +605,8 @@ static int retrieve_impl(const pariskv_config* cfg, const pariskv_index* index, 
         const hipError_t eg = launch_group_attend(q, Kd, Vd, att->kv_capacity, out_idx, budget->top_k, batch,
                                                   a.hkv, a.g, att->scale, att->out,
                                                   reinterpret_cast<int32_t*>(ws + L.group_rows), L.group_splits,
-                                                  group_range, reinterpret_cast<float*>(ws + L.group_part), s);
+                                                  group_range, reinterpret_cast<float*>(ws + L.group_part),
+                                                  att->win, att->Kw, att->Vw, s);
         return eg == hipSuccess ? PARISKV_OK : hip_fail(eg, "group_attend launch");
     };
     if (n == 0) {
@@ -793,8 +791,8 @@ int pariskv_group_attend(const pariskv_config* cfg, const void* q, const void* K
     // most kGaRangeKeys rows, else by merging the lists.
     hipError_t e = launch_group_attend(q, Kd, Vd, kv_capacity, idx, k, batch, cfg->n_kv_heads,
                                        cfg->q_per_kv, scale, out, union_rows, 1,
-                                       kv_capacity <= kGaRangeKeys ? kv_capacity : 0, nullptr,
-                                       static_cast<hipStream_t>(stream));
+                                       kv_capacity <= kGaRangeKeys ? kv_capacity : 0, nullptr, AttendWindow{},
+                                       nullptr, nullptr, static_cast<hipStream_t>(stream));
     if (e != hipSuccess) return hip_fail(e, "group_attend launch");
     return PARISKV_OK;
 }

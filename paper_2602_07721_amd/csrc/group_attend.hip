@@ -21,9 +21,12 @@
 //      scan over "first of its row" flags numbers the distinct rows.  Unsorted
 //      lists give an unspecified result there, never a stray access;
 //   4. 32 slots of 16 lanes (lane l16 owns dims [8 l16, 8 l16 + 8)) walk the
-//      share's union rows, 8 rows in flight per lane; each K and V row segment
-//      is read once and feeds the online softmax of every head whose bit is set
-//      (one rescale per head per 8 rows);
+//      share's union rows, then its share of the window's dense rows (Sink,
+//      Local / Update Buffer: every head's list holds them, so they feed every
+//      head; dense position j goes to share j mod splits, read from the window
+//      cache or the main cache as the window says), 8 rows in flight per lane;
+//      each K and V row segment is read once and feeds the online softmax of
+//      every head whose bit is set (one rescale per head per 8 rows);
 //   5. the 32 slot states of every head are merged in LDS.
 // With one share the block writes `out`; with several, each leaves its per-head
 // state (running max, sum, unnormalised output) and its row count in `part`,
@@ -87,7 +90,8 @@ __global__ __launch_bounds__(kGaThreads) void group_attend_kernel(
     const __half* __restrict__ q, const __half* __restrict__ K, const __half* __restrict__ V,
     int64_t kv_capacity, const int32_t* __restrict__ idx, int32_t k, int32_t hkv, int32_t g,
     int32_t quads, float scale, float* __restrict__ out, int32_t* __restrict__ union_rows, int32_t splits,
-    int64_t range, float* __restrict__ part) {
+    int64_t range, float* __restrict__ part, AttendWindow win, const __half* __restrict__ Kw,
+    const __half* __restrict__ Vw) {
     __shared__ GroupScratch sg;
     __shared__ GroupMerge gm;
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
@@ -99,6 +103,8 @@ __global__ __launch_bounds__(kGaThreads) void group_attend_kernel(
     const int nh = min(4, g - 4 * quad);
     const int64_t row0 = (int64_t)seq * hkv * g + (int64_t)kvh * g + 4 * quad;  // first query head row
     const int ne = nh * k;  // entries of the quad (host checked <= kGaMaxEntries)
+    // list entry v names cache row retr_begin + v; entries past the cache are skipped
+    const int64_t v_end = kv_capacity - win.retr_begin;
 
     constexpr int kPer = kGaMaxEntries / kGaThreads;
     int U;  // union rows of this share, in sg.list / sg.mask [0, U)
@@ -111,7 +117,7 @@ __global__ __launch_bounds__(kGaThreads) void group_attend_kernel(
             const int h = r / k;
             const int32_t v = idx[(row0 + h) * k + r % k];
             const int64_t d = (int64_t)v - r0;
-            if (v >= 0 && v < kv_capacity && d >= 0 && d < range)
+            if (v >= 0 && v < v_end && d >= 0 && d < range)
                 atomicOr(&sg.u.bits[h][d >> 5], 1u << (d & 31));
         }
         __syncthreads();
@@ -144,7 +150,7 @@ __global__ __launch_bounds__(kGaThreads) void group_attend_kernel(
         // 1. stage the lists; invalid entries sort last
         for (int r = tid; r < ne; r += kGaThreads) {
             const int32_t v = idx[(row0 + r / k) * k + r % k];
-            sg.list[r] = (v >= 0 && v < kv_capacity) ? v : kGaInvalid;
+            sg.list[r] = (v >= 0 && v < v_end) ? v : kGaInvalid;
             sg.u.m.row[r] = kGaInvalid;  // a place no entry lands on (unsorted input) stays empty
             sg.mask[r] = 0u;
         }
@@ -233,6 +239,12 @@ __global__ __launch_bounds__(kGaThreads) void group_attend_kernel(
     // 4. attention over the union, every head of the quad at once
     const int slot = tid >> 4, l16 = tid & 15;
     const int64_t kvrow0 = grp * kv_capacity;
+    const int64_t wrow0 = grp * win.win_capacity;
+    // After the share's U union rows come its dense rows (Sink, Local / Update Buffer),
+    // attended by every head of the quad: dense position j = split + splits * i.
+    const int64_t nd = win.dense_rows();
+    const int Ut = U + (int)(nd > split ? (nd - split + splits - 1) / splits : 0);
+    const uint32_t all_heads = (1u << nh) - 1u;
     float qf[4][8];
 #pragma unroll
     for (int h = 0; h < 4; ++h) {
@@ -249,7 +261,7 @@ __global__ __launch_bounds__(kGaThreads) void group_attend_kernel(
 #pragma unroll
         for (int d = 0; d < 8; ++d) acc[h][d] = 0.f;
     }
-    for (int base = 0; base < U; base += kGaSlots * kGaUnroll) {
+    for (int base = 0; base < Ut; base += kGaSlots * kGaUnroll) {
         uint32_t msk[kGaUnroll];
         uint4 kc[kGaUnroll], vc[kGaUnroll];
 #pragma unroll
@@ -260,9 +272,16 @@ __global__ __launch_bounds__(kGaThreads) void group_attend_kernel(
             vc[w] = make_uint4(0, 0, 0, 0);
             if (r < U) {
                 msk[w] = sg.mask[r];
-                const int64_t off = (kvrow0 + sg.list[r]) * kD;
+                const int64_t off = (kvrow0 + win.retr_begin + sg.list[r]) * kD;
                 kc[w] = reinterpret_cast<const uint4*>(K + off)[l16];
                 vc[w] = reinterpret_cast<const uint4*>(V + off)[l16];
+            } else if (r < Ut) {
+                msk[w] = all_heads;
+                const int32_t e = win.dense_entry(split + (int64_t)splits * (r - U));
+                const bool in_win = (e & kWinRow) != 0;
+                const int64_t off = in_win ? (wrow0 + (e - kWinRow)) * kD : (kvrow0 + e) * kD;
+                kc[w] = reinterpret_cast<const uint4*>((in_win ? Kw : K) + off)[l16];
+                vc[w] = reinterpret_cast<const uint4*>((in_win ? Vw : V) + off)[l16];
             }
         }
         // scores of every row for every head of the quad
@@ -416,7 +435,8 @@ size_t group_part_bytes(int64_t groups, int32_t splits) {
 hipError_t launch_group_attend(const void* q, const void* K, const void* V, int64_t kv_capacity,
                                const int32_t* idx, int32_t k, int32_t batch, int32_t hkv, int32_t g,
                                float scale, float* out, int32_t* union_rows, int32_t splits, int64_t range,
-                               float* part, hipStream_t s) {
+                               float* part, const AttendWindow& win, const void* Kw, const void* Vw,
+                               hipStream_t s) {
     const int32_t quads = (g + 3) / 4;
     const int64_t groups = (int64_t)batch * hkv * quads;
     const bool ranges = range >= 1 && range <= kGaRangeKeys;
@@ -426,12 +446,15 @@ hipError_t launch_group_attend(const void* q, const void* K, const void* V, int6
         const dim3 grid((unsigned)(groups * splits)), block(kGaThreads);
         const __half *qh = static_cast<const __half*>(q), *Kh = static_cast<const __half*>(K),
                      *Vh = static_cast<const __half*>(V);
+        const __half *Kwh = static_cast<const __half*>(Kw), *Vwh = static_cast<const __half*>(Vw);
         if (ranges)
             hipExtLaunchKernelGGL(group_attend_kernel<true>, grid, block, 0, s, pe.start, pe.stop, 0, qh, Kh, Vh,
-                                  kv_capacity, idx, k, hkv, g, quads, scale, out, union_rows, splits, range, part);
+                                  kv_capacity, idx, k, hkv, g, quads, scale, out, union_rows, splits, range, part,
+                                  win, Kwh, Vwh);
         else
             hipExtLaunchKernelGGL(group_attend_kernel<false>, grid, block, 0, s, pe.start, pe.stop, 0, qh, Kh, Vh,
-                                  kv_capacity, idx, k, hkv, g, quads, scale, out, union_rows, splits, range, part);
+                                  kv_capacity, idx, k, hkv, g, quads, scale, out, union_rows, splits, range, part,
+                                  win, Kwh, Vwh);
         const hipError_t e = hipGetLastError();
         if (e != hipSuccess || splits == 1) return e;
     }

@@ -444,7 +444,7 @@ def test_stream_kernels_validation():
 
 
 def test_group_fetch_validation():
-    # PARISKV_GROUP_FETCH: plain retrieve + attend only, and min(G, 4) * k within one block's list
+    # PARISKV_GROUP_FETCH: min(G, 4) * k within one block's list, n within 64 key ranges
     L = pk.lib()
     cfg = _cfg()
     ok = pk.Budget(512, 1024, 64, flags=pk.GROUP_FETCH)
@@ -486,11 +486,4 @@ def test_group_fetch_validation():
                                    ctypes.c_void_p(FAKE), None, ctypes.c_void_p(FAKE), ctypes.c_void_p(FAKE), 0,
                                    4096, ctypes.c_float(0.1), ctypes.c_void_p(FAKE), ctypes.c_void_p(FAKE), need,
                                    None)
-    assert rc == pk.ERR_UNSUPPORTED
-    win = pk.Window(16, 16, 3000, 3100)
-    need = pk.retrieve_workspace_size(cfg, 1, 2000, ok)
-    rc = L.pariskv_retrieve_window_attend(cfg.c(), ctypes.byref(_index()), ctypes.c_void_p(FAKE), 2000, 1, ok.c(),
-                                          ctypes.c_void_p(FAKE), None, ctypes.c_void_p(FAKE), ctypes.c_void_p(FAKE), 0,
-                                          4096, win.c(), ctypes.c_float(0.1), ctypes.c_void_p(FAKE),
-                                          ctypes.c_void_p(FAKE), need, None)
     assert rc == pk.ERR_UNSUPPORTED

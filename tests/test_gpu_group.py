@@ -176,3 +176,51 @@ def test_group_fetch_over_more_than_16_key_ranges():
     for hq in range(g):
         check_attention(out[0, hq], Q[0, hq], K[0, 0], V[0, 0], idx[0, hq], SCALE)
     np.testing.assert_allclose(out, o1.cpu().numpy(), rtol=0, atol=1e-5 * np.abs(out).max())
+
+
+@pytest.mark.parametrize("tiered,host,splits_hint", [(True, True, "one share"), (True, True, "shares"),
+                                                     (False, False, "shares")],
+                         ids=["tiered_host", "tiered_host_shares", "window_hbm_shares"])
+def test_window_and_tiered_calls_with_group_fetch(tiered, host, splits_hint):
+    # The window's dense rows (Sink, Local / Update Buffer) are attended by every head of
+    # a quad, once per quad: retrieve_tiered_attend (dense rows from the GPU window ring,
+    # retrieval rows from host memory) and retrieve_window_attend (dense rows in the main
+    # cache) with PARISKV_GROUP_FETCH against the oracle's window attention per head, and
+    # the winners bit for bit those of the plain call.
+    from oracle import window as owin
+    from test_gpu_window import _cache, _close, _dense, _index_over, _queries, _window_cache
+    b, hkv, g = 1, 2, 4
+    k = 64 if splits_hint == "one share" else 512
+    sink, local, buf = 128, 512, 60
+    n = 9000
+    cap = sink + n + local + buf
+    win = pk.Window(sink, sink, sink + n, cap)
+    wcap = sink + local + 2 * 256
+    print(f"[group fetch window] tiered {tiered} host {host} k {k}", flush=True)
+    K, V = _cache(b, hkv, cap, seed=29)
+    Q = _queries(K, g, seed=29)
+    cfg = pk.Config(hkv, g, n, workloads.rotation_signs(29))
+    Kd, Vd, Qd = (torch.from_numpy(x).cuda() for x in (K, V, Q))
+    index = _index_over(cfg, Kd, sink, n)
+    Kr, Vr = (torch.from_numpy(x) for x in (K, V))
+    Kr, Vr = (Kr.pin_memory(), Vr.pin_memory()) if host else (Kd, Vd)
+    plain, grouped = pk.Budget(1024, 2048, k), pk.Budget(1024, 2048, k, flags=pk.GROUP_FETCH)
+    splits = pk.workspace_layout(cfg, b, n, grouped)["group_splits"]
+    assert (splits == 1) == (splits_hint == "one share")
+    if tiered:
+        Kw, Vw = (torch.from_numpy(x).cuda() for x in _window_cache(K, V, win, wcap))
+        call = lambda bud: pk.retrieve_tiered_attend(cfg, index, Qd, n, bud, Kw, Vw, Kr, Vr, win, SCALE,
+                                                     kv_host_mapped=host)
+    else:
+        call = lambda bud: pk.retrieve_window_attend(cfg, index, Qd, n, bud, Kr, Vr, win, SCALE,
+                                                     kv_host_mapped=host)
+    i1, _, o1, _ = call(plain)
+    i2, _, o2, _ = call(grouped)
+    torch.cuda.synchronize()
+    np.testing.assert_array_equal(i1.cpu().numpy(), i2.cpu().numpy())
+    idx, out = i2.cpu().numpy(), o2.cpu().numpy()
+    for hq in range(hkv * g):
+        retrieved = [sink + int(j) for j in idx[0, hq] if j >= 0]
+        want = owin.window_attention(Q[0, hq], K[0, hq // g], V[0, hq // g], _dense(win), retrieved, SCALE)
+        _close(out[0, hq], want, hq)
+    np.testing.assert_allclose(out, o1.cpu().numpy(), rtol=0, atol=1e-5 * np.abs(out).max())

@@ -266,7 +266,7 @@ __global__ __launch_bounds__(kLutThreads) void query_lut_kernel(RetrieveArgs a) 
         const uint32_t t0 = cc[0] + cc[1], t1 = cc[2] + cc[3];
         const uint32_t incl0 = wave_incl_sum(t0);
         const uint32_t incl1 = wave_incl_sum(t1);
-        const uint32_t half = __shfl(incl0, 63, 64);  // counts of the first 128 ranks
+        const uint32_t half = (uint32_t)__builtin_amdgcn_readlane((int)incl0, 63);  // counts of the first 128 ranks
         uint32_t starts[4];
         starts[0] = incl0 - t0;
         starts[1] = starts[0] + cc[0];
@@ -287,11 +287,8 @@ __global__ __launch_bounds__(kLutThreads) void query_lut_kernel(RetrieveArgs a) 
             m1 += (float)cc[r] * (float)bonus;
             m2 += (float)cc[r] * (float)(bonus * bonus);
         }
-#pragma unroll
-        for (int d = 1; d < 64; d <<= 1) {
-            m1 += __uint_as_float(lane_xor(__float_as_uint(m1), d, lane));
-            m2 += __uint_as_float(lane_xor(__float_as_uint(m2), d, lane));
-        }
+        m1 = wave_sum_f32(m1);
+        m2 = wave_sum_f32(m2);
         if (lane == 0) {
             float* st = a.stats + (row * kB + b) * 2;
             st[0] = m1;

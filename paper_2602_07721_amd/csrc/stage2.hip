@@ -308,11 +308,8 @@ __global__ __launch_bounds__(TH) void topk_lds_kernel(RetrieveArgs a) {
             if (kStageIdx) s_idx[p] = p < C ? cand[p] : -1;
         }
     }
-#pragma unroll
-    for (int d = 1; d < 64; d <<= 1) {
-        kmin = min(kmin, (uint32_t)__shfl_xor(kmin, d, 64));
-        kmax = max(kmax, (uint32_t)__shfl_xor(kmax, d, 64));
-    }
+    kmin = wave_min_u32(kmin);
+    kmax = wave_max_u32(kmax);
     if (lane == 0) { s_mm[0][wave] = kmin; s_mm[1][wave] = kmax; }
     for (int i = tid; i < 2 * kNB; i += TH) (&s_hist[0][0])[i] = 0;
     __syncthreads();

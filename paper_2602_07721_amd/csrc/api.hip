@@ -606,7 +606,7 @@ static int retrieve_impl(const pariskv_config* cfg, const pariskv_index* index, 
                                                   a.hkv, a.g, att->scale, att->out,
                                                   reinterpret_cast<int32_t*>(ws + L.group_rows), L.group_splits,
                                                   group_range, reinterpret_cast<float*>(ws + L.group_part),
-                                                  att->win, att->Kw, att->Vw, s);
+                                                  att->win, att->Kw, att->Vw, att->kv_host_mapped != 0, s);
         return eg == hipSuccess ? PARISKV_OK : hip_fail(eg, "group_attend launch");
     };
     if (n == 0) {
@@ -792,7 +792,7 @@ int pariskv_group_attend(const pariskv_config* cfg, const void* q, const void* K
     hipError_t e = launch_group_attend(q, Kd, Vd, kv_capacity, idx, k, batch, cfg->n_kv_heads,
                                        cfg->q_per_kv, scale, out, union_rows, 1,
                                        kv_capacity <= kGaRangeKeys ? kv_capacity : 0, nullptr, AttendWindow{},
-                                       nullptr, nullptr, static_cast<hipStream_t>(stream));
+                                       nullptr, nullptr, kv_host_mapped != 0, static_cast<hipStream_t>(stream));
     if (e != hipSuccess) return hip_fail(e, "group_attend launch");
     return PARISKV_OK;
 }

@@ -288,12 +288,13 @@ constexpr int kGaMaxSplits = 64;
 constexpr int64_t kGaRangeKeys = 65536;
 // win: the dense rows every head also attends and the retrieval rows' offset
 // (list entry v is cache row win.retr_begin + v), with the window cache Kw, Vw
-// when win.win_capacity > 0, as for launch_attend.
+// when win.win_capacity > 0, as for launch_attend.  host_kv: K and V are
+// host-mapped (the fetch then keeps fewer rows in flight).
 hipError_t launch_group_attend(const void* q, const void* K, const void* V, int64_t kv_capacity,
                                const int32_t* idx, int32_t k, int32_t batch, int32_t hkv, int32_t g,
                                float scale, float* out, int32_t* union_rows, int32_t splits, int64_t range,
                                float* part, const AttendWindow& win, const void* Kw, const void* Vw,
-                               hipStream_t s);
+                               bool host_kv, hipStream_t s);
 // Shares per quad for `groups` (sequence, KV head, quad) triples with at most
 // `per` = min(G, 4) * k entries each over n keys: enough for ~256 blocks, no
 // more than per / 256, at least ceil(n / kGaRangeKeys), at most kGaMaxSplits.

@@ -178,10 +178,10 @@ def test_group_fetch_over_more_than_16_key_ranges():
     np.testing.assert_allclose(out, o1.cpu().numpy(), rtol=0, atol=1e-5 * np.abs(out).max())
 
 
-@pytest.mark.parametrize("tiered,host,splits_hint", [(True, True, "one share"), (True, True, "shares"),
-                                                     (False, False, "shares")],
-                         ids=["tiered_host", "tiered_host_shares", "window_hbm_shares"])
-def test_window_and_tiered_calls_with_group_fetch(tiered, host, splits_hint):
+@pytest.mark.parametrize("tiered,host,splits_hint,n", [(True, True, "one share", 9000), (True, True, "shares", 9000),
+                                                       (False, False, "shares", 9000), (True, True, "shares", 0)],
+                         ids=["tiered_host", "tiered_host_shares", "window_hbm_shares", "tiered_n0_dense_only"])
+def test_window_and_tiered_calls_with_group_fetch(tiered, host, splits_hint, n):
     # The window's dense rows (Sink, Local / Update Buffer) are attended by every head of
     # a quad, once per quad: retrieve_tiered_attend (dense rows from the GPU window ring,
     # retrieval rows from host memory) and retrieve_window_attend (dense rows in the main
@@ -192,14 +192,13 @@ def test_window_and_tiered_calls_with_group_fetch(tiered, host, splits_hint):
     b, hkv, g = 1, 2, 4
     k = 64 if splits_hint == "one share" else 512
     sink, local, buf = 128, 512, 60
-    n = 9000
     cap = sink + n + local + buf
     win = pk.Window(sink, sink, sink + n, cap)
     wcap = sink + local + 2 * 256
     print(f"[group fetch window] tiered {tiered} host {host} k {k}", flush=True)
     K, V = _cache(b, hkv, cap, seed=29)
     Q = _queries(K, g, seed=29)
-    cfg = pk.Config(hkv, g, n, workloads.rotation_signs(29))
+    cfg = pk.Config(hkv, g, max(n, 1), workloads.rotation_signs(29))
     Kd, Vd, Qd = (torch.from_numpy(x).cuda() for x in (K, V, Q))
     index = _index_over(cfg, Kd, sink, n)
     Kr, Vr = (torch.from_numpy(x) for x in (K, V))

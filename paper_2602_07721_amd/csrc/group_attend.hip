@@ -4,7 +4,8 @@
 // Fetch": the fetched rows are what crosses the host link).
 //
 //   o_h = sum_{i in idx_h} softmax_i(scale <k_i, q_h>) v_i   for each head h,
-//   float16 in, float32 math -- the same value as the per-head attention.
+//   float16 in, float32 math -- the per-head attention's value up to the
+//   order of the float32 sums.
 //
 // One block of 512 threads per (sequence, KV head, quad of query heads) and
 // share of it:

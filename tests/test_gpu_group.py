@@ -93,9 +93,10 @@ def test_group_attend_on_retrieval_output_and_empty_lists():
     (4, 9000, (700, 1500, 100), True, 1), (6, 5000, (400, 800, 64), False, 1),
     (4, 40000, (10000, 20000, 512), True, 8), (6, 12000, (1500, 3000, 256), False, 4),
     (4, 0, (64, 128, 16), False, 1), (4, 0, (600, 1200, 512), False, 8),
-    (4, 140000, (4096, 8192, 64), True, 3)],
+    (4, 140000, (4096, 8192, 64), True, 3), (3, 9000, (700, 1500, 300), True, 3),
+    (1, 9000, (700, 1500, 300), False, 1)],
     ids=["g4_host", "g6_two_quads", "g4_two_pass_host_split8", "g6_two_quads_split4", "n0", "n0_split8",
-         "g4_three_key_ranges_host"])
+         "g4_three_key_ranges_host", "g3_host_split3", "g1"])
 def test_retrieve_attend_with_group_fetch(g, n, bud, host, splits):
     # PARISKV_GROUP_FETCH: the winners are those of the plain call bit for bit, each head's
     # attention matches the float64 oracle over its own winners, and the rows fetched per

@@ -190,9 +190,13 @@ __global__ __launch_bounds__(kLutThreads) void query_lut_kernel(RetrieveArgs a) 
     const bool live = hg < a.g;
     const int64_t row = (int64_t)seq * a.hq + kvh * a.g + hg;
 
-    // Cluster counts of the 4 subspaces.
+    // Cluster counts of the 4 subspaces, requested first and put in LDS after the
+    // transform; the sign word of this lane's coordinates picked without indexing.
     const uint32_t* cnt = a.counts + grp * (kB * kCentroids) + (4 * sg) * kCentroids;
-    (&s_cnt[0][0])[tid] = cnt[tid];
+    const uint32_t cval = cnt[tid];
+    const uint32_t sword = select_mask(0xFFFFFFFF00000000ull,
+                                       select_mask(0xFFFF0000FFFF0000ull, a.sb.w[3], a.sb.w[2]),
+                                       select_mask(0xFFFF0000FFFF0000ull, a.sb.w[1], a.sb.w[0]));
     (&s_lut[0][0])[tid] = 0u;
     // z = H (s (.) q) of the 4 heads exactly in float64: wave `slot` of subspace 0 takes
     // head `slot` in registers (coordinates 2 lane + r; stride-1 butterflies inside a
@@ -206,7 +210,7 @@ __global__ __launch_bounds__(kLutThreads) void query_lut_kernel(RetrieveArgs a) 
             const int zi = 2 * lane + r;
             double v = (double)__half2float(__ushort_as_half((unsigned short)(r ? qw >> 16 : qw & 0xffffu)));
             if (!rotate) v *= (double)kD;  // z = D q without the rotation (exact: D = 2^7)
-            else if ((a.sb.w[zi >> 5] >> (zi & 31)) & 1u) v = -v;
+            else if ((sword >> (zi & 31)) & 1u) v = -v;  // word zi / 32 = lane / 16
             z[r] = v;
         }
         if (rotate) {
@@ -235,6 +239,7 @@ __global__ __launch_bounds__(kLutThreads) void query_lut_kernel(RetrieveArgs a) 
             if (sg == 0) a.zq[row * kD + 2 * lane + r] = (float)(z[r] * (1.0 / kD));
         }
     }
+    (&s_cnt[0][0])[tid] = cval;
     __syncthreads();
 
     if (live) {
@@ -357,9 +362,15 @@ __global__ __launch_bounds__(kColThreads) void collide_kernel(RetrieveArgs a) {
     const int nh = min(4, a.g - 4 * quad);     // heads in this quad
     const int64_t row0 = (int64_t)seq * a.hq + kvh * a.g + 4 * quad;  // row of head 0 of the quad
 
-    const uint4* lsrc = reinterpret_cast<const uint4*>(a.lut + gq * (kB * kCentroids));
-    for (int i = tid; i < kB * kCentroids / 4; i += kColThreads)
-        reinterpret_cast<uint4*>(s_lut)[i] = lsrc[i];
+    // The bonus table: every load in flight before the first LDS store.
+    static_assert(kB * kCentroids / 4 == 4 * kColThreads, "four 16-byte table rows per thread");
+    const uint4* lsrc = reinterpret_cast<const uint4*>(a.lut + gq * (kB * kCentroids)) + tid;
+    const uint4 t0 = lsrc[0], t1 = lsrc[kColThreads], t2 = lsrc[2 * kColThreads], t3 = lsrc[3 * kColThreads];
+    uint4* ldst = reinterpret_cast<uint4*>(s_lut) + tid;
+    ldst[0] = t0;
+    ldst[kColThreads] = t1;
+    ldst[2 * kColThreads] = t2;
+    ldst[3 * kColThreads] = t3;
     for (int i = tid; i < kHistCopies * 4 * kHistStride; i += kColThreads) s_hist[i] = 0;
     // Histogram floor of each head (a slot past the quad's last head scores 0: none).
     if (tid < 4) s_floor[tid] = tid < nh ? hist_floor(a.stats + (row0 + tid) * (kB * 2), a.n, a.c_eff, a.flags)

@@ -18,16 +18,17 @@
 // keeps the 16 query coordinates of its two subspaces in registers; the
 // signed level table (16 floats) lives in LDS.
 //
-// topk_lds_kernel: one block per list; the k-th largest estimate is found
-// exactly on order-preserving uint32 keys, ties at it taken in candidate
-// order, then an ordered compaction lists the winners in ascending key index
-// (candidate order) without a sort.  The keys are staged in LDS, binned
-// linearly in value over [min, max] (the float bit patterns crowd into a few
-// exponent prefixes), and the boundary bin is ranked by brute force when it
-// holds at most 64 keys, else by 11/11/10-bit radix passes restricted to it.
-// A list is one query head's candidates (C <= 32768), or, in two passes, first
-// every 4096-candidate slice of a head and then the concatenated winners of its
-// slices (more than 32768 candidates, or more than 8192 for few heads).
+// topk_reg_kernel (at most 8 candidates per thread) and topk_lds_kernel (more):
+// one block per list; the k-th largest estimate is found exactly on
+// order-preserving uint32 keys, ties at it taken in candidate order, then an
+// ordered compaction lists the winners in ascending key index (candidate order)
+// without a sort.  The keys are held in registers (staged in LDS by the second
+// kernel), binned linearly in value over [min, max] (the float bit patterns
+// crowd into a few exponent prefixes), and the boundary bin is ranked by brute force when it holds
+// at most 64 keys, else by 11/11/10-bit radix passes restricted to it.  A list
+// is one query head's candidates (C <= 32768), or, in two passes, first every
+// 4096-candidate slice of a head and then the concatenated winners of its slices
+// (more than 32768 candidates, or more than 8192 for few heads).
 
 #include "attend_row.hpp"
 #include "internal.hpp"
@@ -41,6 +42,18 @@ static_assert(kTopkPart >= PARISKV_MAX_TOPK, "a top-k slice holds at least k can
 static_assert(PARISKV_MAX_CAND / kTopkPart * PARISKV_MAX_TOPK <= 1024 * 32, "the slices' winners fit one block");
 constexpr int kRrSlots = kRrThreads / 8;  // candidates reranked per block iteration
 constexpr int kRrUnroll = 4;              // records in flight per lane
+
+// Order-preserving uint32 key of a float (larger float, larger key; finite floats
+// map above 0) and back.
+__device__ __forceinline__ uint32_t order_key(float f) {
+    const uint32_t u = __float_as_uint(f);
+    return (u & 0x80000000u) ? ~u : (u | 0x80000000u);
+}
+
+__device__ __forceinline__ float key_float(uint32_t k) {
+    const uint32_t u = (k & 0x80000000u) ? (k & 0x7fffffffu) : ~k;
+    return __uint_as_float(u);
+}
 
 // Compaction of one chunk's candidates (Stage I selection) fused with their
 // RSQ-IP rerank (Stage II).  The selected keys of a chunk hold consecutive
@@ -182,15 +195,6 @@ __global__ __launch_bounds__(kRrThreads) void compact_rerank_kernel(RetrieveArgs
 
 // ---------------------------------------------------------------- top-k
 
-__device__ __forceinline__ uint32_t order_key(float f) {
-    const uint32_t u = __float_as_uint(f);
-    return (u & 0x80000000u) ? ~u : (u | 0x80000000u);
-}
-
-__device__ __forceinline__ float key_float(uint32_t k) {
-    const uint32_t u = (k & 0x80000000u) ? (k & 0x7fffffffu) : ~k;
-    return __uint_as_float(u);
-}
 
 // Shared by both top-k kernels, run by one whole wave: the digit holding the
 // need-th largest element of a histogram of NB bins.  Lane L owns bins
@@ -219,7 +223,7 @@ __device__ __forceinline__ void find_digit(const uint32_t* hist, uint32_t need, 
     }
 }
 
-// Top-k for C <= TH * EPT held in LDS.  Scores and candidate indices are staged
+// Top-k for C <= TH * EPT held in LDS (more than 8 candidates per thread).  Scores and candidate indices are staged
 // with coalesced 16-byte loads; each thread then owns EPT consecutive candidates.
 // Exact radix select with 11-bit digits taken from the top of the occupied
 // [min, max] key range, then an ordered compaction (ascending key index).
@@ -484,6 +488,270 @@ __global__ __launch_bounds__(TH) void topk_lds_kernel(RetrieveArgs a) {
     }
 }
 
+// Top-k for C <= TH * EPT <= 8192 candidates, held in registers: thread t owns the 4-candidate
+// groups at positions 4 (t + j TH) .. 4 (t + j TH) + 3 for j < EPT / 4, read with
+// coalesced 16-byte loads.  Exact selection on order-preserving uint32 keys: one
+// histogram pass with 2048 bins linear in the estimate over [min, max], then the
+// boundary bin ranked by brute force (at most 64 keys) or by 11/11/10-bit radix
+// passes restricted to it; ties at the k-th key taken in candidate order.  An ordered
+// compaction (a block scan per group of positions) then lists the winners in
+// ascending key index without a sort.
+template <int TH, int EPT, bool kAttend>
+__global__ __launch_bounds__(TH) void topk_reg_kernel(RetrieveArgs a) {
+    constexpr int kWaves = TH / 64;
+    constexpr int kIt = EPT / 4;   // 4-candidate groups per thread
+    constexpr int kNB = 2048;
+    // LDS: region A = the attention's per-slot state (kAttend), region B = two
+    // histograms, whose place the attention list takes once they are done.
+    constexpr size_t kA = kAttend ? sizeof(AttendScratch) : 0;
+    constexpr size_t kBytes = kA + 2 * kNB * 4;
+    static_assert(!kAttend || 2 * kNB * 4 >= kMaxAttendRows * 4, "the attention list fits in region B");
+    static_assert(EPT % 4 == 0 && EPT <= 8, "whole 4-candidate groups, few enough to stay in registers");
+    __shared__ __align__(16) unsigned char s_raw[kBytes];
+    uint32_t (*s_hist)[kNB] = reinterpret_cast<uint32_t (*)[kNB]>(s_raw + kA);
+    int32_t* s_win = reinterpret_cast<int32_t*>(s_raw + kA);
+    __shared__ uint32_t s_w[kIt][kWaves];
+    __shared__ uint32_t s_mm[2][kWaves];
+    __shared__ uint32_t s_digit, s_need, s_nsmall;
+    __shared__ uint32_t s_small[64];
+    // With kAttend the winners' estimates wait here until the attention is done.
+    __shared__ float s_wsc[kAttend ? PARISKV_MAX_TOPK : 1];
+
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    // This block's list: part blk % tk_parts of row blk / tk_parts (see RetrieveArgs).
+    const int64_t blk = blockIdx.x;
+    const int64_t row = blk / a.tk_parts;
+    const int64_t off = (blk % a.tk_parts) * (int64_t)a.tk_part_len;
+    const int C = (int)min((int64_t)a.tk_part_len, a.tk_c - off);
+    const int kk = min(a.top_k, C);
+    const float* sc = a.tk_score + row * a.tk_stride + off;
+    const int32_t* cand = a.tk_idx + row * a.tk_stride + off;
+    if (tid == 0) s_nsmall = 0;
+
+    // With kAttend, this thread's part of the query, requested first.
+    const uint4 qv = kAttend ? attend_query_part(static_cast<const __half*>(a.q) + row * kD)
+                             : make_uint4(0, 0, 0, 0);
+    uint32_t kmin = 0xffffffffu, kmax = 0u;
+
+    // The estimates as keys (0 past the list; valid keys are all > 0) and the
+    // candidate indices.  The arrays start 256-byte aligned, so 16-byte loads are
+    // taken when the row stride and the part's offset are multiples of 4 (the list
+    // then starts 16-byte aligned); groups past the list re-read the row's last 16
+    // bytes and are masked.  Otherwise every candidate is read on its own.
+    uint32_t key[EPT];
+    int32_t widx[EPT];
+    if (((a.tk_stride | off) & 3) == 0) {
+        const int nq = (int)((a.tk_stride - off) >> 2);
+        float4 f[kIt];
+        int4 ix[kIt];
+#pragma unroll
+        for (int it = 0; it < kIt; ++it) {
+            const int p4 = min(tid + it * TH, nq - 1);
+            f[it] = reinterpret_cast<const float4*>(sc)[p4];
+            ix[it] = reinterpret_cast<const int4*>(cand)[p4];
+        }
+#pragma unroll
+        for (int it = 0; it < kIt; ++it) {
+            const int p = 4 * (tid + it * TH);
+            key[4 * it] = p < C ? order_key(f[it].x) : 0u;
+            key[4 * it + 1] = p + 1 < C ? order_key(f[it].y) : 0u;
+            key[4 * it + 2] = p + 2 < C ? order_key(f[it].z) : 0u;
+            key[4 * it + 3] = p + 3 < C ? order_key(f[it].w) : 0u;
+            widx[4 * it] = ix[it].x;
+            widx[4 * it + 1] = ix[it].y;
+            widx[4 * it + 2] = ix[it].z;
+            widx[4 * it + 3] = ix[it].w;
+        }
+    } else {
+#pragma unroll
+        for (int e = 0; e < EPT; ++e) {
+            const int p = 4 * (tid + (e >> 2) * TH) + (e & 3);
+            key[e] = p < C ? order_key(sc[p]) : 0u;
+            widx[e] = p < C ? cand[p] : -1;
+        }
+    }
+    for (int i = tid; i < 2 * kNB; i += TH) (&s_hist[0][0])[i] = 0;
+#pragma unroll
+    for (int e = 0; e < EPT; ++e)
+        if (key[e] != 0u) { kmin = min(kmin, key[e]); kmax = max(kmax, key[e]); }
+    kmin = wave_min_u32(kmin);
+    kmax = wave_max_u32(kmax);
+    if (lane == 0) { s_mm[0][wave] = kmin; s_mm[1][wave] = kmax; }
+    __syncthreads();
+#pragma unroll
+    for (int w = 0; w < kWaves; ++w) {
+        kmin = min(kmin, s_mm[0][w]);
+        kmax = max(kmax, s_mm[1][w]);
+    }
+
+    // Pass 0: 2048 bins linear in the score over [min, max].  The float bit
+    // patterns of the scores are concentrated in few sign/exponent prefixes, so
+    // value-linear bins spread the counts (and the atomics) far better.  The bin
+    // index is a non-decreasing function of the score, so the keys of a higher
+    // bin are all larger.
+    const float fmin = key_float(kmin), fmax = key_float(kmax);
+    const float frange = fmax - fmin;
+    float inv = frange > 0.0f ? (float)kNB / frange : 0.0f;
+    if (!(inv < 1e30f)) inv = 0.0f;  // a range that under- or overflows: one bin
+    auto bin_of = [&](uint32_t k) -> uint32_t {
+        return (uint32_t)fminf((float)(kNB - 1), (key_float(k) - fmin) * inv);
+    };
+#pragma unroll
+    for (int e = 0; e < EPT; ++e)
+        if (key[e] != 0u) atomicAdd(&s_hist[0][bin_of(key[e])], 1u);
+    __syncthreads();
+    if (wave == 0) find_digit<kNB>(s_hist[0], (uint32_t)kk, lane, &s_digit, &s_need);
+    __syncthreads();
+    const uint32_t bsel = s_digit;       // bin holding the kk-th largest key
+    uint32_t need = s_need;              // its rank (from the top) inside that bin
+    const uint32_t in_bin = s_hist[0][bsel];
+    uint32_t T, quota;
+    if (in_bin <= 64) {
+        // Few keys in the bin: gather them and rank them by brute force in one wave.
+#pragma unroll
+        for (int e = 0; e < EPT; ++e)
+            if (key[e] != 0u && bin_of(key[e]) == bsel) s_small[atomicAdd(&s_nsmall, 1u)] = key[e];
+        __syncthreads();
+        if (wave == 0) {
+            const uint32_t kl = lane < (int)in_bin ? s_small[lane] : 0u;
+            uint32_t gt = 0, eq = 0;
+            for (uint32_t j = 0; j < in_bin; ++j) {
+                const uint32_t kj = s_small[j];
+                gt += kj > kl ? 1u : 0u;
+                eq += kj == kl ? 1u : 0u;
+            }
+            const bool hit = lane < (int)in_bin && gt < need && need <= gt + eq;
+            const uint64_t hits = __ballot(hit);
+            if (hit && lane == __builtin_ctzll(hits)) {
+                s_digit = kl;
+                s_need = need - gt;
+            }
+        }
+        __syncthreads();
+        T = s_digit;
+        quota = s_need;
+    } else {
+        // Exact radix select on the full key restricted to the bin: 11, 11, 10 bits.
+        uint32_t prefix = 0, mask = 0;
+        int shift = 21;
+#pragma unroll 1
+        for (int pass = 1; pass <= 3; ++pass) {
+            uint32_t* hist = s_hist[pass & 1];
+#pragma unroll
+            for (int e = 0; e < EPT; ++e)
+                if (key[e] != 0u && (key[e] & mask) == prefix && bin_of(key[e]) == bsel)
+                    atomicAdd(&hist[(key[e] >> shift) & (kNB - 1)], 1u);
+            __syncthreads();
+            if (wave == 0) find_digit<kNB>(hist, need, lane, &s_digit, &s_need);
+            // The other buffer was read in the previous pass; clear it for the next one.
+            for (int i = tid; i < kNB; i += TH) s_hist[(pass + 1) & 1][i] = 0;
+            __syncthreads();
+            prefix |= s_digit << shift;
+            mask |= (uint32_t)(kNB - 1) << shift;
+            need = s_need;
+            shift = shift >= 11 ? shift - 11 : 0;
+        }
+        T = prefix;     // the kk-th largest key value
+        quota = need;   // how many keys equal to T are taken (lowest indices)
+    }
+
+    // Ordered compaction: an element's output slot is (#keys > T before it) +
+    // min(#keys == T before it, quota), which lists the winners by ascending index.
+    // Positions run group by group (j), thread by thread inside a group, so the
+    // counts before an element are the earlier groups' totals plus a block scan of
+    // this group (counts > T in the low 16 bits, == T in the high 16).
+    uint32_t pre[kIt];
+#pragma unroll
+    for (int it = 0; it < kIt; ++it) {
+        uint32_t mine = 0;
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+            const uint32_t k1 = key[4 * it + q];
+            mine += (k1 > T) ? 1u : (k1 == T && k1 != 0u) ? 0x10000u : 0u;
+        }
+        const uint32_t incl = wave_incl_sum(mine);
+        if (lane == 63) s_w[it][wave] = incl;
+        pre[it] = incl - mine;
+    }
+    __syncthreads();
+    uint32_t before_groups = 0;
+#pragma unroll
+    for (int it = 0; it < kIt; ++it) {
+        uint32_t tot = 0, earlier = 0;
+#pragma unroll
+        for (int w = 0; w < kWaves; ++w) {
+            const uint32_t x = s_w[it][w];
+            if (w < wave) earlier += x;
+            tot += x;
+        }
+        pre[it] += before_groups + earlier;
+        before_groups += tot;
+    }
+    int32_t* oi = a.tk_out_idx + blk * a.top_k;
+    float* os = a.tk_out_score ? a.tk_out_score + blk * a.top_k : nullptr;
+    // With kAttend the attention list in region B is Sink rows, then Local +
+    // Update Buffer rows (nd in all), then the winners at their cache rows
+    // (retr_begin + key; the host checked they stay below dense_begin), and the
+    // outputs are written after the attention, so that its first loads do not
+    // wait behind these stores.
+    const int nd = kAttend ? (int)a.win.dense_rows() : 0;
+#pragma unroll
+    for (int it = 0; it < kIt; ++it) {
+        uint32_t gb = pre[it] & 0xffffu, eb = pre[it] >> 16;
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+            const int e = 4 * it + q;
+            uint32_t p = 0xffffffffu;
+            if (key[e] > T) {
+                p = gb + min(eb, quota);
+                ++gb;
+            } else if (key[e] == T && key[e] != 0u) {
+                if (eb < quota) p = gb + eb;
+                ++eb;
+            }
+            if (p < (uint32_t)kk) {
+                const int32_t win = widx[e];
+                if (kAttend) {
+                    s_win[nd + p] = (int32_t)(a.win.retr_begin + win);
+                    s_wsc[p] = key_float(key[e]);
+                } else {
+                    oi[p] = win;
+                    if (os) os[p] = key_float(key[e]);
+                }
+            }
+        }
+    }
+    if (!kAttend) {
+        for (int r = kk + tid; r < a.top_k; r += TH) {
+            oi[r] = -1;
+            if (os) os[r] = -__builtin_huge_valf();
+        }
+    }
+    if (kAttend) {
+        // Attention over the dense rows and the kk winners (Eqs. approx_weight,
+        // approx_output), from LDS.  Region B is free once the compaction runs.
+        for (int r = tid; r < nd; r += TH) s_win[r] = a.win.dense_entry(r);
+        __syncthreads();
+        const int seq = (int)(row / a.hq);
+        const int h = (int)(row % a.hq);
+        const int64_t kvrow0 = ((int64_t)seq * a.hkv + h / a.g) * a.kv_capacity;
+        const bool wc = a.win.win_capacity > 0;
+        const int64_t wrow0 = wc ? ((int64_t)seq * a.hkv + h / a.g) * a.win.win_capacity : kvrow0;
+        attend_row(qv, static_cast<const __half*>(a.K) + kvrow0 * kD,
+                   static_cast<const __half*>(a.V) + kvrow0 * kD, a.kv_capacity,
+                   static_cast<const __half*>(wc ? a.Kw : a.K) + wrow0 * kD,
+                   static_cast<const __half*>(wc ? a.Vw : a.V) + wrow0 * kD, a.win.win_capacity,
+                   s_win, nd + kk, a.scale,
+                   a.attn_out + row * kD, *reinterpret_cast<AttendScratch*>(s_raw));
+        // The winners in ascending key index, then the padding.
+        for (int r = tid; r < a.top_k; r += TH) {
+            const bool w = r < kk;
+            oi[r] = w ? (int32_t)((int64_t)s_win[nd + r] - a.win.retr_begin) : -1;
+            if (os) os[r] = w ? s_wsc[r] : -__builtin_huge_valf();
+        }
+    }
+}
+
 __global__ void pad_outputs_kernel(int32_t* out_idx, float* out_score, int64_t count) {
     const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
     if (i < count) {
@@ -523,7 +791,7 @@ hipError_t launch_topk(const RetrieveArgs& a0, hipStream_t s, bool attend, bool*
         p.tk_out_idx = a.surv_idx;
         p.tk_out_score = a.surv_score;
         const ProfEvents pp = prof_begin("topk_part");
-        hipExtLaunchKernelGGL((topk_lds_kernel<1024, 4, false>), dim3((unsigned)(rows * a.topk_parts)), dim3(1024),
+        hipExtLaunchKernelGGL((topk_reg_kernel<1024, 4, false>), dim3((unsigned)(rows * a.topk_parts)), dim3(1024),
                               0, s, pp.start, pp.stop, 0, p);
         const hipError_t e = hipGetLastError();
         if (e != hipSuccess) return e;
@@ -539,20 +807,26 @@ hipError_t launch_topk(const RetrieveArgs& a0, hipStream_t s, bool attend, bool*
     const int64_t C = a.tk_c;
     if (fused) *fused = attend;
     const ProfEvents pe = prof_begin(attend ? "topk_attend" : "topk");
+#define PARISKV_TOPK_REG(EPT)                                                                        \
+    (attend ? hipExtLaunchKernelGGL((topk_reg_kernel<1024, EPT, true>), grid, dim3(1024), 0, s,       \
+                                    pe.start, pe.stop, 0, a)                                          \
+            : hipExtLaunchKernelGGL((topk_reg_kernel<1024, EPT, false>), grid, dim3(1024), 0, s,      \
+                                    pe.start, pe.stop, 0, a))
 #define PARISKV_TOPK_LDS(EPT)                                                                        \
     (attend ? hipExtLaunchKernelGGL((topk_lds_kernel<1024, EPT, true>), grid, dim3(1024), 0, s,       \
                                     pe.start, pe.stop, 0, a)                                          \
             : hipExtLaunchKernelGGL((topk_lds_kernel<1024, EPT, false>), grid, dim3(1024), 0, s,      \
                                     pe.start, pe.stop, 0, a))
     if (C <= 1024 * 4)
-        PARISKV_TOPK_LDS(4);
+        PARISKV_TOPK_REG(4);
     else if (C <= 1024 * 8)
-        PARISKV_TOPK_LDS(8);
+        PARISKV_TOPK_REG(8);
     else if (C <= 1024 * 16)
         PARISKV_TOPK_LDS(16);
     else
         PARISKV_TOPK_LDS(32);  // C <= 32768: at most 16 slices x 2048 winners after a first pass
 #undef PARISKV_TOPK_LDS
+#undef PARISKV_TOPK_REG
     return hipGetLastError();
 }
 

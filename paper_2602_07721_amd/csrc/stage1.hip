@@ -486,13 +486,13 @@ __global__ __launch_bounds__(kThrThreads) void threshold_kernel(RetrieveArgs a) 
     __shared__ uint32_t s_wtot[2][kThrWaves];
     __shared__ uint32_t s_hist[kBins];
     __shared__ uint32_t s_cg[kThrWaves * kThrUnroll][2];  // per chunk: #{S > theta}, #{S == theta}
-    __shared__ int s_theta, s_recount;
+    __shared__ int s_theta;
     const int tid = threadIdx.x;
     const int lane = tid & 63, wave = tid >> 6;
     const int64_t row = blockIdx.x;
     uint32_t* sfx = a.chunk_sfx + row * a.n_chunks * kSfx;
     int32_t* t = a.thresh + row * kThreshRow;
-    const uint32_t fl = wave == 0 ? (uint32_t)t[4] : 0u;  // the floor the scan used
+    const uint32_t fl = (uint32_t)t[4];  // the floor the scan used
     // Whole-row suffix histogram; lane holds v = lane and v = 64 + lane.  Wave w
     // sums chunks w, w + 16, ... with kThrUnroll chunks' loads in flight.  With at
     // most 16 kThrUnroll chunks that is one round, and each wave keeps its chunks'
@@ -525,35 +525,33 @@ __global__ __launch_bounds__(kThrThreads) void threshold_kernel(RetrieveArgs a) 
     s_part[wave][1][lane] = sh;
     __syncthreads();
     const uint32_t C = (uint32_t)a.c_eff;
-    if (wave == 0) {
-        uint32_t ttl = 0, tth = 0;
+    // Every wave sums the wave totals and derives the same theta, so no second barrier
+    // hands it out.
+    uint32_t ttl = 0, tth = 0;
 #pragma unroll
-        for (int w = 0; w < kThrWaves; ++w) { ttl += s_part[w][0][lane]; tth += s_part[w][1][lane]; }
-        // The counts are exact for v = 0 and v >= the floor the scan used (it left it in
-        // t[4]).  With #{S >= floor} >= C (or floor 1) theta is found among them;
-        // otherwise it lies below the floor and the row's scores are recounted.
-        const uint32_t at_floor = fl < 64 ? __shfl(ttl, (int)fl, 64) : __shfl(tth, (int)fl - 64, 64);
-        const int recount = fl > 1u && at_floor < C;
-        if (!recount) {
-            int theta;
-            uint32_t gt;
-            theta_of(ttl, tth, C, lane, &theta, &gt);
-            if (lane == 0) {
-                t[0] = theta;
-                t[1] = (int32_t)gt;
-                t[2] = (int32_t)(C - gt);
-                t[3] = (int32_t)C;
-                s_theta = theta;
-            }
-        }
-        if (lane == 0) {
-            t[5] = recount;
-            t[6] = t[7] = 0;
-            s_recount = recount;
+    for (int w = 0; w < kThrWaves; ++w) { ttl += s_part[w][0][lane]; tth += s_part[w][1][lane]; }
+    // The counts are exact for v = 0 and v >= the floor the scan used (it left it in
+    // t[4]).  With #{S >= floor} >= C (or floor 1) theta is found among them;
+    // otherwise it lies below the floor and the row's scores are recounted.
+    const uint32_t at_floor = fl < 64 ? __shfl(ttl, (int)fl, 64) : __shfl(tth, (int)fl - 64, 64);
+    const int recount = fl > 1u && at_floor < C;
+    int theta_w = 0;
+    if (!recount) {
+        uint32_t gt;
+        theta_of(ttl, tth, C, lane, &theta_w, &gt);
+        if (tid == 0) {
+            t[0] = theta_w;
+            t[1] = (int32_t)gt;
+            t[2] = (int32_t)(C - gt);
+            t[3] = (int32_t)C;
         }
     }
-    __syncthreads();
-    if (s_recount) {
+    if (tid == 0) {
+        t[5] = recount;
+        t[6] = t[7] = 0;
+        s_theta = theta_w;
+    }
+    if (recount) {
         // Exact histogram of the row's stored scores, then theta from it.
         for (int i = tid; i < kBins; i += kThrThreads) s_hist[i] = 0;
         __syncthreads();
@@ -614,11 +612,11 @@ __global__ __launch_bounds__(kThrThreads) void threshold_kernel(RetrieveArgs a) 
         }
         __syncthreads();
     }
-    const int theta = s_theta;
+    const int theta = recount ? s_theta : theta_w;  // the recount hands it out in s_theta
     // Each chunk's #{S > theta} and #{S == theta}: from the registers of the one-round
     // load (entries theta and theta + 1 of the chunk's suffix histogram), else (more
     // chunks, or the recount's entries) from memory below.
-    const bool from_regs = one_round && !s_recount;
+    const bool from_regs = one_round && !recount;
     if (from_regs) {
         const int th_s = __builtin_amdgcn_readfirstlane(theta);
 #pragma unroll
@@ -635,8 +633,22 @@ __global__ __launch_bounds__(kThrThreads) void threshold_kernel(RetrieveArgs a) 
         }
         __syncthreads();
     }
-    // Keys with S > theta and S == theta in the chunks before each chunk: thread t
-    // takes chunk cb + t; wave scans, then a scan of the wave totals.
+    // Keys with S > theta and S == theta in the chunks before each chunk.  Up to 64
+    // chunks from the registers: one scan in wave 0.
+    if (from_regs && a.n_chunks <= 64) {
+        if (wave == 0) {
+            const bool in = lane < a.n_chunks;
+            const uint32_t g = in ? s_cg[lane][0] : 0u, e = in ? s_cg[lane][1] : 0u;
+            const uint32_t ig = wave_incl_sum(g), ie = wave_incl_sum(e);
+            if (in) {
+                int32_t* cbp = a.chunk_base + (row * a.n_chunks + lane) * 2;
+                cbp[0] = (int32_t)(ig - g);
+                cbp[1] = (int32_t)(ie - e);
+            }
+        }
+        return;
+    }
+    // Otherwise thread t takes chunk cb + t; wave scans, then a scan of the wave totals.
     uint32_t carry_g = 0, carry_e = 0;
     for (int64_t cb = 0; cb < a.n_chunks; cb += kThrThreads) {
         const int64_t c = cb + tid;

@@ -607,29 +607,23 @@ __global__ __launch_bounds__(TH) void topk_reg_kernel(RetrieveArgs a) {
     const uint32_t in_bin = s_hist[0][bsel];
     uint32_t T, quota;
     if (in_bin <= 64) {
-        // Few keys in the bin: gather them and rank them by brute force in one wave.
+        // Few keys in the bin: gather them, then every wave ranks them by brute force
+        // (the same result in each, so no second barrier hands it out).
 #pragma unroll
         for (int e = 0; e < EPT; ++e)
             if (key[e] != 0u && bin_of(key[e]) == bsel) s_small[atomicAdd(&s_nsmall, 1u)] = key[e];
         __syncthreads();
-        if (wave == 0) {
-            const uint32_t kl = lane < (int)in_bin ? s_small[lane] : 0u;
-            uint32_t gt = 0, eq = 0;
-            for (uint32_t j = 0; j < in_bin; ++j) {
-                const uint32_t kj = s_small[j];
-                gt += kj > kl ? 1u : 0u;
-                eq += kj == kl ? 1u : 0u;
-            }
-            const bool hit = lane < (int)in_bin && gt < need && need <= gt + eq;
-            const uint64_t hits = __ballot(hit);
-            if (hit && lane == __builtin_ctzll(hits)) {
-                s_digit = kl;
-                s_need = need - gt;
-            }
+        const uint32_t kl = lane < (int)in_bin ? s_small[lane] : 0u;
+        uint32_t gt = 0, eq = 0;
+        for (uint32_t j = 0; j < in_bin; ++j) {
+            const uint32_t kj = s_small[j];
+            gt += kj > kl ? 1u : 0u;
+            eq += kj == kl ? 1u : 0u;
         }
-        __syncthreads();
-        T = s_digit;
-        quota = s_need;
+        const bool hit = lane < (int)in_bin && gt < need && need <= gt + eq;
+        const int first = (int)__builtin_ctzll(__ballot(hit));  // some key of the bin has rank need
+        T = (uint32_t)__builtin_amdgcn_readlane((int)kl, first);
+        quota = need - (uint32_t)__builtin_amdgcn_readlane((int)gt, first);
     } else {
         // Exact radix select on the full key restricted to the bin: 11, 11, 10 bits.
         uint32_t prefix = 0, mask = 0;

@@ -8,7 +8,9 @@
 // V row is one 256-byte contiguous read by 16 lanes.  Slot s takes list
 // entries s, s + 64, ...; every lane keeps 8 K and 8 V row segments in flight.
 // Each slot keeps an online-softmax state (running max, sum, 8 accumulators
-// per lane); the 64 states are merged in LDS at the end.
+// per lane).  At the end the 4 slots of a wave merge by two butterfly steps
+// across its rows of 16 lanes (partners lane ^ 16, then lane ^ 32), and the 16
+// wave states merge in LDS.
 //
 // Rows come from one of two caches: a list entry with kWinRow set names row
 // (entry - kWinRow) of the window cache (Kw, Vw, win_capacity: Sink and Local /
@@ -25,13 +27,14 @@ namespace pariskv {
 
 constexpr int kAtThreads = 1024;
 constexpr int kAtGroups = kAtThreads / 16;  // concurrent key slots per block
+constexpr int kAtWaves = kAtThreads / 64;   // slot states left after the in-wave merge
 constexpr int kAtUnroll = 8;                // K/V rows in flight per lane
 
-// LDS the row needs beyond the key list: running max, sum and accumulators per slot.
+// LDS the row needs beyond the key list: running max, sum and accumulators per wave.
 struct AttendScratch {
-    float m[kAtGroups];
-    float l[kAtGroups];
-    float acc[kAtGroups][kD];
+    float m[kAtWaves];
+    float l[kAtWaves];
+    float acc[kAtWaves][kD];
 };
 
 __device__ __forceinline__ void unpack8_half(const uint4 v, float* f) {
@@ -140,21 +143,42 @@ __device__ __forceinline__ void attend_row(uint4 qv, const __half* __restrict__ 
         }
     }
 
-    if (l16 == 0) {
-        sm.m[grp16] = m;
-        sm.l[grp16] = lsum;
-    }
+    // The wave's 4 slot states (rows of 16 lanes holding the same dims) into one.
+    const int lane = tid & 63;
 #pragma unroll
-    for (int d = 0; d < 8; ++d) sm.acc[grp16][8 * l16 + d] = acc[d];
+    for (int step = 16; step <= 32; step <<= 1) {
+        const float mp = __uint_as_float(lane_xor(__float_as_uint(m), step, lane));
+        const float lp = __uint_as_float(lane_xor(__float_as_uint(lsum), step, lane));
+        float ap[8];
+#pragma unroll
+        for (int d = 0; d < 8; ++d) ap[d] = __uint_as_float(lane_xor(__float_as_uint(acc[d]), step, lane));
+        const float mn = fmaxf(m, mp);
+        if (mn > -__builtin_huge_valf()) {
+            const float c0 = __expf(m - mn), c1 = __expf(mp - mn);
+            lsum = lsum * c0 + lp * c1;
+#pragma unroll
+            for (int d = 0; d < 8; ++d) acc[d] = acc[d] * c0 + ap[d] * c1;
+        }
+        m = mn;
+    }
+    const int wave = tid >> 6;
+    if (lane < 16) {
+        if (l16 == 0) {
+            sm.m[wave] = m;
+            sm.l[wave] = lsum;
+        }
+#pragma unroll
+        for (int d = 0; d < 8; ++d) sm.acc[wave][8 * l16 + d] = acc[d];
+    }
     __syncthreads();
     if (tid < kD) {
         float M = -__builtin_huge_valf();
 #pragma unroll
-        for (int j = 0; j < kAtGroups; ++j) M = fmaxf(M, sm.m[j]);
+        for (int j = 0; j < kAtWaves; ++j) M = fmaxf(M, sm.m[j]);
         float L = 0.f, O = 0.f;
         if (M > -__builtin_huge_valf()) {
 #pragma unroll
-            for (int j = 0; j < kAtGroups; ++j) {
+            for (int j = 0; j < kAtWaves; ++j) {
                 if (sm.l[j] > 0.f) {
                     const float c = __expf(sm.m[j] - M);
                     L += sm.l[j] * c;

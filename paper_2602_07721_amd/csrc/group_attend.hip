@@ -29,7 +29,8 @@
 //      over the host link, 4 from HBM; each K and V row segment is read once
 //      and feeds the online softmax of every head whose bit is set (one rescale
 //      per head per batch of rows in flight);
-//   5. the 32 slot states of every head are merged in LDS.
+//   5. the 32 slot states of every head are merged: the 4 of a wave by lane
+//      exchanges, then the 8 wave states in LDS.
 // With one share the block writes `out`; with several, each leaves its per-head
 // state (running max, sum, unnormalised output) and its row count in `part`,
 // and group_combine_kernel merges the shares of each head as step 5 merges
@@ -43,6 +44,7 @@ namespace {
 
 constexpr int kGaThreads = 512;  // 8 waves: room for 4 heads of state per lane
 constexpr int kGaSlots = kGaThreads / 16;
+constexpr int kGaWaves = kGaThreads / 64;  // slot states per head left after the in-wave merge
 constexpr int kGaMaxEntries = 4096;  // G * k per quad staged in LDS
 constexpr int32_t kGaInvalid = 0x7fffffff;
 constexpr int kGaPart = 4 + kD;  // one head's share state: max, sum, row count (head 0), pad, output
@@ -63,11 +65,11 @@ struct GroupScratch {
     uint32_t wsum[kGaThreads / 64];
 };
 
-// LDS for the final merge of the slot states, every head of the quad at once.
+// LDS for the final merge of the wave states, every head of the quad at once.
 struct GroupMerge {
-    float m[4][kGaSlots];
-    float l[4][kGaSlots];
-    float acc[4][kGaSlots][kD];
+    float m[4][kGaWaves];
+    float l[4][kGaWaves];
+    float acc[4][kGaWaves][kD];
 };
 
 // Block scan of per-thread counts: (exclusive prefix of this thread, block total).
@@ -329,27 +331,50 @@ __global__ __launch_bounds__(kGaThreads) void group_attend_kernel(
             }
         }
     }
-    // 5. merge the 32 slot states of each head: all states to LDS, one barrier, then
-    // thread (h, d) = (tid / 128, tid % 128) folds dim d of head h.
+    // 5. merge the 32 slot states of each head: the 4 slots of a wave (its rows of 16
+    // lanes hold the same dims) by two butterfly steps across rows (partners lane ^ 16,
+    // then lane ^ 32), the 8 wave states in LDS behind one barrier, where thread
+    // (h, d) = (tid / 128, tid % 128) folds dim d of head h.
 #pragma unroll
-    for (int h = 0; h < 4; ++h) {
-        if (l16 == 0) {
-            gm.m[h][slot] = m[h];
-            gm.l[h][slot] = lsum[h];
+    for (int step = 16; step <= 32; step <<= 1) {
+#pragma unroll
+        for (int h = 0; h < 4; ++h) {
+            const float mp = __uint_as_float(lane_xor(__float_as_uint(m[h]), step, lane));
+            const float lp = __uint_as_float(lane_xor(__float_as_uint(lsum[h]), step, lane));
+            float ap[8];
+#pragma unroll
+            for (int d = 0; d < 8; ++d) ap[d] = __uint_as_float(lane_xor(__float_as_uint(acc[h][d]), step, lane));
+            const float mn = fmaxf(m[h], mp);
+            if (mn > -__builtin_huge_valf()) {
+                const float c0 = __expf(m[h] - mn), c1 = __expf(mp - mn);
+                lsum[h] = lsum[h] * c0 + lp * c1;
+#pragma unroll
+                for (int d = 0; d < 8; ++d) acc[h][d] = acc[h][d] * c0 + ap[d] * c1;
+            }
+            m[h] = mn;
         }
+    }
+    if (lane < 16) {
 #pragma unroll
-        for (int d = 0; d < 8; ++d) gm.acc[h][slot][8 * l16 + d] = acc[h][d];
+        for (int h = 0; h < 4; ++h) {
+            if (l16 == 0) {
+                gm.m[h][wave] = m[h];
+                gm.l[h][wave] = lsum[h];
+            }
+#pragma unroll
+            for (int d = 0; d < 8; ++d) gm.acc[h][wave][8 * l16 + d] = acc[h][d];
+        }
     }
     __syncthreads();
     const int h = tid / kD, dd = tid % kD;
     if (h < nh) {
         float M = -__builtin_huge_valf();
 #pragma unroll
-        for (int j = 0; j < kGaSlots; ++j) M = fmaxf(M, gm.m[h][j]);
+        for (int j = 0; j < kGaWaves; ++j) M = fmaxf(M, gm.m[h][j]);
         float L = 0.f, O = 0.f;
         if (M > -__builtin_huge_valf()) {
 #pragma unroll
-            for (int j = 0; j < kGaSlots; ++j) {
+            for (int j = 0; j < kGaWaves; ++j) {
                 if (gm.l[h][j] > 0.f) {
                     const float c = __expf(gm.m[h][j] - M);
                     L += gm.l[h][j] * c;

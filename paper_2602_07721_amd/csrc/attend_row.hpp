@@ -10,7 +10,7 @@
 // Each slot keeps an online-softmax state (running max, sum, 8 accumulators
 // per lane).  At the end the 4 slots of a wave merge by two butterfly steps
 // across its rows of 16 lanes (partners lane ^ 16, then lane ^ 32), and the 16
-// wave states merge in LDS.
+// wave states merge through LDS, 8 threads per dimension.
 //
 // Rows come from one of two caches: a list entry with kWinRow set names row
 // (entry - kWinRow) of the window cache (Kw, Vw, win_capacity: Sink and Local /
@@ -171,22 +171,31 @@ __device__ __forceinline__ void attend_row(uint4 qv, const __half* __restrict__ 
         for (int d = 0; d < 8; ++d) sm.acc[wave][8 * l16 + d] = acc[d];
     }
     __syncthreads();
-    if (tid < kD) {
+    {
+        // Every thread: dim d of 2 of the 16 wave states, then a sum over the 8 threads
+        // of the dim (lanes 8 d' + part) by lane exchanges.  An empty state (m = -inf,
+        // l = 0, acc = 0) is scaled by exp(-inf) = 0, so it needs no test.
+        static_assert(kAtThreads == 8 * kD && kAtWaves == 16, "8 threads per dim, 2 states each");
+        const int d = tid >> 3, part = tid & 7;
         float M = -__builtin_huge_valf();
 #pragma unroll
         for (int j = 0; j < kAtWaves; ++j) M = fmaxf(M, sm.m[j]);
         float L = 0.f, O = 0.f;
         if (M > -__builtin_huge_valf()) {
 #pragma unroll
-            for (int j = 0; j < kAtWaves; ++j) {
-                if (sm.l[j] > 0.f) {
-                    const float c = __expf(sm.m[j] - M);
-                    L += sm.l[j] * c;
-                    O += sm.acc[j][tid] * c;
-                }
+            for (int r = 0; r < 2; ++r) {
+                const int j = 2 * part + r;
+                const float c = __expf(sm.m[j] - M);
+                L += sm.l[j] * c;
+                O += sm.acc[j][d] * c;
             }
         }
-        out[tid] = L > 0.f ? O / L : 0.f;
+#pragma unroll
+        for (int x = 1; x < 8; x <<= 1) {
+            L += __uint_as_float(lane_xor(__float_as_uint(L), x, lane));
+            O += __uint_as_float(lane_xor(__float_as_uint(O), x, lane));
+        }
+        if (part == 0) out[d] = L > 0.f ? O / L : 0.f;
     }
     __syncthreads();
 }

@@ -373,13 +373,12 @@ __global__ __launch_bounds__(kGaThreads) void group_attend_kernel(
         for (int j = 0; j < kGaWaves; ++j) M = fmaxf(M, gm.m[h][j]);
         float L = 0.f, O = 0.f;
         if (M > -__builtin_huge_valf()) {
+            // An empty state (m = -inf, l = 0, acc = 0) is scaled by exp(-inf) = 0.
 #pragma unroll
             for (int j = 0; j < kGaWaves; ++j) {
-                if (gm.l[h][j] > 0.f) {
-                    const float c = __expf(gm.m[h][j] - M);
-                    L += gm.l[h][j] * c;
-                    O += gm.acc[h][j][dd] * c;
-                }
+                const float c = __expf(gm.m[h][j] - M);
+                L += gm.l[h][j] * c;
+                O += gm.acc[h][j][dd] * c;
             }
         }
         if (splits == 1) {

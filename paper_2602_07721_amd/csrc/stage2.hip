@@ -516,6 +516,7 @@ __global__ __launch_bounds__(TH) void topk_reg_kernel(RetrieveArgs a) {
     __shared__ uint32_t s_small[64];
     // With kAttend the winners' estimates wait here until the attention is done.
     __shared__ float s_wsc[kAttend ? PARISKV_MAX_TOPK : 1];
+    __shared__ int32_t s_dump[kAttend ? TH : 1];  // a word per thread for non-winners' stores
 
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     // This block's list: part blk % tk_parts of row blk / tk_parts (see RetrieveArgs).
@@ -668,19 +669,21 @@ __global__ __launch_bounds__(TH) void topk_reg_kernel(RetrieveArgs a) {
         pre[it] = incl - mine;
     }
     __syncthreads();
+    // The waves' totals of each group: lane w < 16 takes wave w's, one wave scan, and
+    // the prefix before this wave read from lane wave - 1 (the group total from 15).
+    static_assert(kWaves == 16, "one lane per wave in the scan of the wave totals");
     uint32_t before_groups = 0;
 #pragma unroll
     for (int it = 0; it < kIt; ++it) {
-        uint32_t tot = 0, earlier = 0;
-#pragma unroll
-        for (int w = 0; w < kWaves; ++w) {
-            const uint32_t x = s_w[it][w];
-            if (w < wave) earlier += x;
-            tot += x;
-        }
+        const uint32_t x = lane < kWaves ? s_w[it][lane] : 0u;
+        const uint32_t ix = wave_incl_sum(x);
+        const int wv = __builtin_amdgcn_readfirstlane(wave);
+        const uint32_t earlier = wv > 0 ? (uint32_t)__builtin_amdgcn_readlane((int)ix, wv - 1) : 0u;
+        const uint32_t tot = (uint32_t)__builtin_amdgcn_readlane((int)ix, kWaves - 1);
         pre[it] += before_groups + earlier;
         before_groups += tot;
     }
+    const int32_t retr0 = (int32_t)a.win.retr_begin;  // below kv_capacity <= 2^30 - 1 (host-checked)
     int32_t* oi = a.tk_out_idx + blk * a.top_k;
     float* os = a.tk_out_score ? a.tk_out_score + blk * a.top_k : nullptr;
     // With kAttend the attention list in region B is Sink rows, then Local +
@@ -695,23 +698,21 @@ __global__ __launch_bounds__(TH) void topk_reg_kernel(RetrieveArgs a) {
 #pragma unroll
         for (int q = 0; q < 4; ++q) {
             const int e = 4 * it + q;
-            uint32_t p = 0xffffffffu;
-            if (key[e] > T) {
-                p = gb + min(eb, quota);
-                ++gb;
-            } else if (key[e] == T && key[e] != 0u) {
-                if (eb < quota) p = gb + eb;
-                ++eb;
-            }
-            if (p < (uint32_t)kk) {
-                const int32_t win = widx[e];
-                if (kAttend) {
-                    s_win[nd + p] = (int32_t)(a.win.retr_begin + win);
-                    s_wsc[p] = key_float(key[e]);
-                } else {
-                    oi[p] = win;
-                    if (os) os[p] = key_float(key[e]);
-                }
+            const bool gt = key[e] > T;
+            const bool eq = key[e] == T && key[e] != 0u;
+            const uint32_t p = gt ? gb + min(eb, quota) : (eq && eb < quota) ? gb + eb : 0xffffffffu;
+            gb += gt ? 1u : 0u;
+            eb += eq ? 1u : 0u;
+            if (kAttend) {
+                // Branch-free: a key that does not win writes this thread's own dump word.
+                const bool w = p < (uint32_t)kk;
+                int32_t* dw = w ? &s_win[nd + p] : &s_dump[tid];
+                float* ds = w ? &s_wsc[p] : reinterpret_cast<float*>(&s_dump[tid]);
+                *dw = retr0 + widx[e];
+                *ds = key_float(key[e]);
+            } else if (p < (uint32_t)kk) {
+                oi[p] = widx[e];
+                if (os) os[p] = key_float(key[e]);
             }
         }
     }

@@ -10,9 +10,10 @@
 //                      float64 by a register FWHT in one wave per head
 //                      (written as z/D float for the rerank), the 256
 //                      centroids ranked by the exact proxy sum_j +-z_j (ties:
-//                      lower id) by a 64-bit bitonic sort of the 128 with bit 7
-//                      clear and a merge with their complements, in registers,
-//                      cluster counts prefix-summed in that order, and the tier
+//                      lower id) by a 64-bit bitonic sort, in registers, of the
+//                      128 pair representatives (of c and c ^ 255 the one with
+//                      the larger proxy), cluster counts prefix-summed in that
+//                      order, and the tier
 //                      bonus of each cluster placed in byte `slot` of a packed
 //                      word (4 query heads of a KV head share one uint32) at the
 //                      entry of the stored id form slot(c), assembled in LDS and
@@ -46,11 +47,11 @@ namespace {
 // ---------------------------------------------------------------- helpers
 
 // Ranking the 256 centroids of a subspace.  Flipping every sign of a centroid
-// negates its proxy, so once the 128 centroids with bit 7 clear are sorted, the
-// other 128 (their complements c ^ 255, keys from the same values) come in the
-// reverse order, and the two halves form one bitonic sequence: a 128-key sort
-// and one bitonic merge replace a 256-key sort (22 stages' worth of
-// compare-exchanges on 2 or 4 keys per lane instead of 36 on 4).
+// negates its proxy, so the pairs {c, c ^ 255} hold proxies p and -p: sorting the
+// member with the larger proxy of each pair (128 keys, 2 per lane) ranks the upper
+// half, and the other members take the lower half in the reverse order.  One
+// 128-key sort replaces a 256-key sort (28 stages of compare-exchanges on 2 keys
+// per lane instead of 36 on 4).
 //
 // Each compare-exchange is one 64-bit compare into a lane mask, a scalar XOR with
 // the stage's direction pattern, and two v_cndmask; partners 1 or 2 lanes away come
@@ -84,7 +85,7 @@ __device__ __forceinline__ void order_pair(int64_t& x, int64_t& y, uint64_t desc
 
 // Bitonic sort of the 128 keys key[0..1] of every lane (element e = 2 lane + r),
 // descending.  Bit b >= 1 of e is bit b - 1 of the lane.
-__device__ __forceinline__ void sort128_desc(int64_t (&key)[4], int lane) {
+__device__ __forceinline__ void sort128_desc(int64_t (&key)[2], int lane) {
 #pragma unroll
     for (int k = 2; k <= 128; k <<= 1) {
 #pragma unroll
@@ -103,34 +104,6 @@ __device__ __forceinline__ void sort128_desc(int64_t (&key)[4], int lane) {
             }
         }
     }
-}
-
-// The key of centroid c ^ 255 from the key of c: proxy negated, id complemented
-// (keys are proxy * 256 + (255 - id)).
-__device__ __forceinline__ int64_t complement_key(int64_t k) {
-    const int64_t low = k & 255;
-    return -(k >> 8) * 256 + (255 - low);
-}
-
-// key[0..1] hold the sorted first half (positions 2 lane + r), key[2..3] get the
-// complements (positions 128 + 2 lane + r - 2, ascending); the bitonic merge leaves
-// all 256 keys descending in those positions.
-__device__ __forceinline__ void merge_complements_desc(int64_t (&key)[4], int lane) {
-    key[2] = complement_key(key[0]);
-    key[3] = complement_key(key[1]);
-    order_pair(key[0], key[2], ~0ull);  // j = 128: the half below keeps the larger key
-    order_pair(key[1], key[3], ~0ull);
-#pragma unroll
-    for (int j = 64; j >= 2; j >>= 1) {
-        const uint64_t keep_max = ~lane_bit(log2i(j) - 1);  // position bit log2 j clear
-#pragma unroll
-        for (int r = 0; r < 4; ++r) {
-            const uint32_t lo = (uint32_t)key[r], hi = (uint32_t)((uint64_t)key[r] >> 32);
-            key[r] = exchange(key[r], lane_xor(lo, j >> 1, lane), lane_xor(hi, j >> 1, lane), keep_max);
-        }
-    }
-    order_pair(key[0], key[1], ~0ull);  // j = 1
-    order_pair(key[2], key[3], ~0ull);
 }
 
 // The histogram floor v_lo of a query head: the collision scan histograms only scores
@@ -246,37 +219,50 @@ __global__ __launch_bounds__(kLutThreads) void query_lut_kernel(RetrieveArgs a) 
         double zb[8];
 #pragma unroll
         for (int j = 0; j < 8; ++j) zb[j] = s_z[slot][8 * b + j];
-        int64_t key[4];
+        // Each pair {c, c ^ 255} (c with bit 7 clear) has proxies p and -p.  Its
+        // representative is the member with the larger proxy (c when p = 0, the lower
+        // id); sorting the 128 representatives by (|p| desc, id asc) ranks them 0..127,
+        // and the other members follow in the reverse order: the one of the
+        // representative at position i has rank 255 - i (proxy -|p| desc, and for
+        // equal |p| the representatives' id order reverses under c ^ 255).
+        int64_t key[2];
 #pragma unroll
         for (int r = 0; r < 2; ++r) {
-            const int c = 2 * lane + r;  // the centroids with bit 7 clear
+            const int c = 2 * lane + r;
             double p = 0.0;
 #pragma unroll
             for (int j = 0; j < 8; ++j) p = ((c >> j) & 1) ? __dsub_rn(p, zb[j]) : __dadd_rn(p, zb[j]);
             // p is an exact multiple of 2^-24 with |p| < 2^26: exact as an integer.
             const int64_t pi = (int64_t)(p * 16777216.0);
-            key[r] = pi * 256 + (255 - c);  // descending key: proxy desc, then id asc
+            const bool neg = pi < 0;
+            const int rep = neg ? c ^ 255 : c;
+            key[r] = (neg ? -pi : pi) * 256 + (255 - rep);  // descending key: |proxy| desc, then id asc
         }
         sort128_desc(key, lane);
-        merge_complements_desc(key, lane);
-        // Exclusive prefix of cluster counts in rank order -> start rank P(c).  Ranks
-        // 2 lane + r (r = 0, 1) and 128 + 2 lane + r - 2 (r = 2, 3).
+        // Representatives at positions 2 lane + r (r = 0, 1), ranks 2 lane + r; the
+        // other members at ranks 255 - (2 lane + r).  Exclusive prefix of cluster
+        // counts in rank order -> start rank P(c): the representatives' by a wave scan,
+        // the other members' as everything before rank 128 plus the members of the
+        // positions after theirs (the total less an inclusive scan).
         uint32_t cc[4];
         int cid[4];
 #pragma unroll
-        for (int r = 0; r < 4; ++r) {
+        for (int r = 0; r < 2; ++r) {
             cid[r] = 255 - (int)(key[r] & 255);
-            cc[r] = s_cnt[sub][cid[r]];
+            cid[2 + r] = cid[r] ^ 255;
         }
+#pragma unroll
+        for (int r = 0; r < 4; ++r) cc[r] = s_cnt[sub][cid[r]];
         const uint32_t t0 = cc[0] + cc[1], t1 = cc[2] + cc[3];
         const uint32_t incl0 = wave_incl_sum(t0);
         const uint32_t incl1 = wave_incl_sum(t1);
-        const uint32_t half = (uint32_t)__builtin_amdgcn_readlane((int)incl0, 63);  // counts of the first 128 ranks
+        const uint32_t half = (uint32_t)__builtin_amdgcn_readlane((int)incl0, 63);  // counts of ranks 0..127
+        const uint32_t tot1 = (uint32_t)__builtin_amdgcn_readlane((int)incl1, 63);
         uint32_t starts[4];
         starts[0] = incl0 - t0;
         starts[1] = starts[0] + cc[0];
-        starts[2] = half + incl1 - t1;
-        starts[3] = starts[2] + cc[2];
+        starts[2] = half + tot1 - (incl1 - t1 + cc[2]);
+        starts[3] = half + tot1 - incl1;
         float m1 = 0.0f, m2 = 0.0f;  // sum of count * bonus and count * bonus^2 (an estimate's input)
 #pragma unroll
         for (int r = 0; r < 4; ++r) {

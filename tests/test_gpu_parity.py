@@ -87,6 +87,8 @@ EDGE = [
     # the 4-chunk form; past 256 chunks the 16-chunk form loops and re-reads the chunk
     # counts at theta from memory
     ("chunks_49", 1, 1, 2, 200000, (2048, 4096, 128)),
+    # 64 chunks, the most whose bases one wave scans from the loaded registers
+    ("chunks_64_ragged", 1, 1, 1, 262000, (4096, 8192, 256)),
     ("chunks_269_two_rounds", 1, 1, 1, 1100000, (8192, 16384, 256)),
     # fewer than 32 score rows (quads of query heads): the scan keeps its plain block order
     ("rows8_ragged", 1, 8, 4, 5000, (512, 1024, 64)),

@@ -88,6 +88,34 @@ def test_proxy_ranking_matches_paper_proxy():
             assert np.all(np.diff(p_paper[o]) <= 1e-12)
 
 
+
+def test_cluster_order_from_pair_representatives():
+    # The query kernel ranks the 256 centroids of a subspace from one sort of 128 keys:
+    # flipping every sign of centroid c gives c ^ 255 with the negated proxy, so of each
+    # pair the member with the larger proxy (c itself when the proxy is 0) sorted by
+    # (|proxy| desc, id asc) takes ranks 0..127 and its partner rank 255 - i.  That
+    # order must be the oracle's (proxy desc, ties by the lower id), ties included.
+    rng = np.random.default_rng(17)
+    for trial in range(400):
+        kind = trial % 4
+        if kind == 0:
+            zb = rng.standard_normal(8)
+        elif kind == 1:
+            zb = rng.integers(-2, 3, size=8).astype(np.float64)   # many exact ties and zeros
+        elif kind == 2:
+            zb = np.zeros(8)
+            zb[rng.integers(0, 8)] = 1.0                          # half the proxies equal
+        else:
+            zb = np.zeros(8)                                      # every proxy 0
+        prox = retrieve.centroid_proxy(zb)
+        np.testing.assert_array_equal(prox[np.arange(256) ^ 255], -prox)
+        reps = sorted((-abs(prox[c]), c ^ 255 if prox[c] < 0 else c) for c in range(128))
+        rank = np.empty(256, dtype=np.int64)
+        for i, (_, rep) in enumerate(reps):
+            rank[rep] = i
+            rank[rep ^ 255] = 255 - i
+        np.testing.assert_array_equal(np.argsort(rank), retrieve.cluster_order(prox))
+
 # ---------------------------------------------------------------- selection
 
 def test_hand_worked_selection():

@@ -171,11 +171,13 @@ __global__ __launch_bounds__(kLutThreads) void query_lut_kernel(RetrieveArgs a) 
                                        select_mask(0xFFFF0000FFFF0000ull, a.sb.w[3], a.sb.w[2]),
                                        select_mask(0xFFFF0000FFFF0000ull, a.sb.w[1], a.sb.w[0]));
     (&s_lut[0][0])[tid] = 0u;
-    // z = H (s (.) q) of the 4 heads exactly in float64: wave `slot` of subspace 0 takes
-    // head `slot` in registers (coordinates 2 lane + r; stride-1 butterflies inside a
-    // lane, the others across lanes) and leaves it in LDS for the other three waves.
+    // z = H (s (.) q) of the 4 heads exactly in float64: the wave of head `slot` and
+    // subspace `slot` takes it in registers (coordinates 2 lane + r; stride-1 butterflies
+    // inside a lane, the others across lanes) and leaves it in LDS for the other three
+    // waves.  Waves w = 4 slot + sub go to SIMD w mod 4, so the 4 transforms run on 4
+    // different SIMDs.
     const bool rotate = !(a.flags & kFlagNoRotation);
-    if (sub == 0 && live) {
+    if (sub == slot && live) {
         const uint32_t qw = reinterpret_cast<const uint32_t*>(static_cast<const __half*>(a.q) + row * kD)[lane];
         double z[2];
 #pragma unroll

@@ -8,10 +8,13 @@
 // where v_b has coordinates sign * a[t] decoded from the 4-bit codes.  The
 // query side z/D arrives as float from the query kernel.
 //
-// compact_rerank_kernel: one block per (query head, 4096-key chunk).  It
-// selects the chunk's candidates (all S > theta, then S == theta in ascending
-// key order while the row's quota lasts), which occupy consecutive positions
-// of the row's candidate list, writes them, and scores them at once: 8 lanes
+// compact_rerank_kernel: one block of 128 threads per (query head, 4096-key
+// chunk), 32 keys per thread, so that 16 blocks share a CU and their selection
+// phases hide under each other's gathers.  It selects the chunk's candidates
+// (all S > theta, then S == theta in ascending key order while the row's quota
+// lasts), which occupy consecutive positions of the row's candidate list,
+// writes them (and keeps them in LDS as 16-bit offsets in the chunk), and
+// scores them at once: 8 lanes
 // per candidate, lane l reads the 16-byte chunk l of the 128-byte record
 // (codes of subspaces 2l, 2l+1 and their W), so one candidate is one fully
 // used 128-byte line and a wave reads 8 lines per load instruction.  Lane l
@@ -37,7 +40,7 @@ namespace pariskv {
 
 namespace {
 
-constexpr int kRrThreads = 256;           // one 4096-key chunk per block, 16 keys per thread
+constexpr int kRrThreads = 128;           // one 4096-key chunk per block, 32 keys per thread
 static_assert(kTopkPart >= PARISKV_MAX_TOPK, "a top-k slice holds at least k candidates");
 static_assert(PARISKV_MAX_CAND / kTopkPart * PARISKV_MAX_TOPK <= 1024 * 32, "the slices' winners fit one block");
 constexpr int kRrSlots = kRrThreads / 8;  // candidates reranked per block iteration
@@ -60,9 +63,12 @@ __device__ __forceinline__ float key_float(uint32_t k) {
 // positions [P0, P0 + m) of the row's ascending candidate list, so the block
 // writes them to `cand`, keeps them in LDS and scores them right away.
 __global__ __launch_bounds__(kRrThreads) void compact_rerank_kernel(RetrieveArgs a) {
+    constexpr int kKpt = kChunk / kRrThreads;  // keys per thread
+    static_assert(kKpt % 16 == 0 && kKpt <= 32, "whole 16-byte score loads, one 32-bit mask");
     __shared__ float s_tab[16];
     __shared__ uint32_t s_wsum[kRrThreads / 64];
-    __shared__ int32_t s_list[kChunk];
+    // The selected keys as offsets in the chunk (2 bytes each, so 16 blocks fit a CU).
+    __shared__ uint16_t s_list[kChunk];
 
     const int tid = threadIdx.x;
     const int lane = tid & 63, wave = tid >> 6;
@@ -78,9 +84,15 @@ __global__ __launch_bounds__(kRrThreads) void compact_rerank_kernel(RetrieveArgs
     const uint32_t quota = (uint32_t)th[2];
     const int32_t* cb = a.chunk_base + (row * a.n_chunks + chunk) * 2;
     const uint32_t base_g = (uint32_t)cb[0], base_e = (uint32_t)cb[1];
-    const int64_t i0 = chunk * kChunk + 16 * tid;
-    uint4 sw = make_uint4(0, 0, 0, 0);
-    if (i0 < a.n) sw = *reinterpret_cast<const uint4*>(a.score8 + row * a.n_pad + i0);
+    // This thread's kKpt keys; score rows are padded to a multiple of 64 bytes, so a
+    // load that starts before n stays inside the row.
+    const int64_t i0 = chunk * kChunk + kKpt * tid;
+    uint4 sw[kKpt / 16];
+#pragma unroll
+    for (int u = 0; u < kKpt / 16; ++u) {
+        sw[u] = make_uint4(0, 0, 0, 0);
+        if (i0 + 16 * u < a.n) sw[u] = *reinterpret_cast<const uint4*>(a.score8 + row * a.n_pad + i0 + 16 * u);
+    }
     const int l = tid & 7;
     float z[16];
     {
@@ -96,9 +108,16 @@ __global__ __launch_bounds__(kRrThreads) void compact_rerank_kernel(RetrieveArgs
     // ---- compaction: all S > theta, and S == theta while the row's quota lasts.
     uint32_t gmask = 0, emask = 0;
     {
-        const uint32_t ww[4] = {sw.x, sw.y, sw.z, sw.w};
+        uint32_t ww[kKpt / 4];
 #pragma unroll
-        for (int j = 0; j < 16; ++j) {
+        for (int u = 0; u < kKpt / 16; ++u) {
+            ww[4 * u] = sw[u].x;
+            ww[4 * u + 1] = sw[u].y;
+            ww[4 * u + 2] = sw[u].z;
+            ww[4 * u + 3] = sw[u].w;
+        }
+#pragma unroll
+        for (int j = 0; j < kKpt; ++j) {
             const uint32_t sv = (ww[j >> 2] >> (8 * (j & 3))) & 0xffu;
             const bool in = i0 + j < a.n;
             gmask |= (in && sv > theta ? 1u : 0u) << j;
@@ -119,7 +138,7 @@ __global__ __launch_bounds__(kRrThreads) void compact_rerank_kernel(RetrieveArgs
     }
     const uint32_t P0 = base_g + min(base_e, quota);
     const uint32_t m = (tot & 0xffffu) + (min(base_e + (tot >> 16), quota) - min(base_e, quota));
-    const uint32_t gb = base_g + (pre & 0xffffu);  // S > theta keys before this thread's 16
+    const uint32_t gb = base_g + (pre & 0xffffu);  // S > theta keys before this thread's keys
     const uint32_t eb = base_e + (pre >> 16);      // S == theta keys before them
     int32_t* cand = a.cand + row * a.n_cand;
     const uint32_t c_eff = (uint32_t)a.c_eff;
@@ -138,7 +157,7 @@ __global__ __launch_bounds__(kRrThreads) void compact_rerank_kernel(RetrieveArgs
         if (p < c_eff) {
             const int32_t key = (int32_t)i0 + j;
             cand[p] = key;
-            s_list[p - P0] = key;
+            s_list[p - P0] = (uint16_t)(kKpt * tid + j);
         }
     }
     __syncthreads();
@@ -157,7 +176,7 @@ __global__ __launch_bounds__(kRrThreads) void compact_rerank_kernel(RetrieveArgs
         for (int u = 0; u < kRrUnroll; ++u) {
             // Past the end, re-read the last candidate; its result is not stored.
             const uint32_t ci = min(it + u * kRrSlots + slot, m - 1u);
-            rc[u] = rec[(uint64_t)(uint32_t)s_list[ci] * (kRec / 16) + l];
+            rc[u] = rec[((uint64_t)chunk * kChunk + s_list[ci]) * (kRec / 16) + l];
         }
 #pragma unroll
         for (int u = 0; u < kRrUnroll; ++u) {

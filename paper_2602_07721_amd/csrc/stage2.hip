@@ -8,9 +8,11 @@
 // where v_b has coordinates sign * a[t] decoded from the 4-bit codes.  The
 // query side z/D arrives as float from the query kernel.
 //
-// compact_rerank_kernel: one block of 128 threads per (query head, 4096-key
-// chunk), 32 keys per thread, so that 16 blocks share a CU and their selection
-// phases hide under each other's gathers.  It selects the chunk's candidates
+// compact_rerank_kernel: one block per (query head, 4096-key chunk).  Large
+// grids take blocks of 128 threads (32 keys per thread), so that 16 blocks
+// share a CU and their selection phases hide under each other's gathers; a
+// grid that fits the chip in one round of 256-thread blocks takes those (16
+// keys per thread), which halves each block's serial work.  It selects the chunk's candidates
 // (all S > theta, then S == theta in ascending key order while the row's quota
 // lasts), which occupy consecutive positions of the row's candidate list,
 // writes them (and keeps them in LDS as 16-bit offsets in the chunk), and
@@ -40,11 +42,12 @@ namespace pariskv {
 
 namespace {
 
-constexpr int kRrThreads = 128;           // one 4096-key chunk per block, 32 keys per thread
+// One 4096-key chunk per block: 128 threads for large grids, 256 for grids of at
+// most kRrWideGrid blocks (8 such blocks per CU on 256 CUs: one round).
+constexpr int kRrWideGrid = 2048;
 static_assert(kTopkPart >= PARISKV_MAX_TOPK, "a top-k slice holds at least k candidates");
 static_assert(PARISKV_MAX_CAND / kTopkPart * PARISKV_MAX_TOPK <= 1024 * 32, "the slices' winners fit one block");
-constexpr int kRrSlots = kRrThreads / 8;  // candidates reranked per block iteration
-constexpr int kRrUnroll = 4;              // records in flight per lane
+constexpr int kRrUnroll = 4;  // records in flight per lane
 
 // Order-preserving uint32 key of a float (larger float, larger key; finite floats
 // map above 0) and back.
@@ -62,8 +65,10 @@ __device__ __forceinline__ float key_float(uint32_t k) {
 // RSQ-IP rerank (Stage II).  The selected keys of a chunk hold consecutive
 // positions [P0, P0 + m) of the row's ascending candidate list, so the block
 // writes them to `cand`, keeps them in LDS and scores them right away.
+template <int kRrThreads>
 __global__ __launch_bounds__(kRrThreads) void compact_rerank_kernel(RetrieveArgs a) {
-    constexpr int kKpt = kChunk / kRrThreads;  // keys per thread
+    constexpr int kKpt = kChunk / kRrThreads;   // keys per thread
+    constexpr int kRrSlots = kRrThreads / 8;    // candidates reranked per block iteration
     static_assert(kKpt % 16 == 0 && kKpt <= 32, "whole 16-byte score loads, one 32-bit mask");
     __shared__ float s_tab[16];
     __shared__ uint32_t s_wsum[kRrThreads / 64];
@@ -778,8 +783,11 @@ __global__ void pad_outputs_kernel(int32_t* out_idx, float* out_score, int64_t c
 
 hipError_t launch_compact_rerank(const RetrieveArgs& a, hipStream_t s) {
     const ProfEvents pe = prof_begin("compact_rerank");
-    hipExtLaunchKernelGGL(compact_rerank_kernel, dim3((unsigned)a.n_chunks, (unsigned)(a.batch * a.hq)),
-                       dim3(kRrThreads), 0, s, pe.start, pe.stop, 0, a);
+    const dim3 grid((unsigned)a.n_chunks, (unsigned)(a.batch * a.hq));
+    if ((int64_t)a.n_chunks * a.batch * a.hq <= kRrWideGrid)
+        hipExtLaunchKernelGGL(compact_rerank_kernel<256>, grid, dim3(256), 0, s, pe.start, pe.stop, 0, a);
+    else
+        hipExtLaunchKernelGGL(compact_rerank_kernel<128>, grid, dim3(128), 0, s, pe.start, pe.stop, 0, a);
     return hipGetLastError();
 }
 

@@ -17,6 +17,11 @@
 // Update Buffer kept on the GPU), any other entry >= 0 a row of the main cache
 // (K, V, kv_capacity: the retrieval rows, in HBM or in host memory).  Entries
 // past their cache's capacity, and negative entries (-1 padding), are skipped.
+//
+// A caller that already holds some rows in LDS passes prow (LDS rows of 32
+// uint4: K then V) and lists such a row as entry -2 - (LDS row); it is read from
+// LDS, the same bytes in the same order, so the result does not depend on which
+// rows were held.  Without prow every negative entry is skipped.
 #pragma once
 
 #include <hip/hip_fp16.h>
@@ -74,7 +79,8 @@ __device__ __forceinline__ void attend_row(uint4 qv, const __half* __restrict__ 
                                            const __half* __restrict__ V, int64_t kv_capacity,
                                            const __half* __restrict__ Kw, const __half* __restrict__ Vw,
                                            int64_t win_capacity, const int32_t* list, int32_t k,
-                                           float scale, float* __restrict__ out, AttendScratch& sm) {
+                                           float scale, float* __restrict__ out, AttendScratch& sm,
+                                           const uint4* prow = nullptr) {
     const int tid = threadIdx.x;
     const int grp16 = tid >> 4;  // key slot 0 .. kAtGroups-1
     const int l16 = tid & 15;
@@ -101,6 +107,8 @@ __device__ __forceinline__ void attend_row(uint4 qv, const __half* __restrict__ 
             if (rowi >= (win ? win_capacity : kv_capacity)) key[u] = -1;
             kc[u] = make_uint4(0, 0, 0, 0);
             vc[u] = make_uint4(0, 0, 0, 0);
+            // A held row (entry <= -2 with prow) is read from LDS where it is used.
+            if (prow == nullptr && key[u] < 0) key[u] = -1;
             if (key[u] >= 0) {
                 const int64_t off = rowi * kD;
                 kc[u] = reinterpret_cast<const uint4*>((win ? Kw : K) + off)[l16];
@@ -110,6 +118,10 @@ __device__ __forceinline__ void attend_row(uint4 qv, const __half* __restrict__ 
         float dot[kAtUnroll];
 #pragma unroll
         for (int u = 0; u < kAtUnroll; ++u) {
+            if (prow != nullptr && key[u] <= -2) {
+                kc[u] = prow[32 * (-2 - key[u]) + l16];
+                vc[u] = prow[32 * (-2 - key[u]) + 16 + l16];
+            }
             float kf[8];
             unpack8_half(kc[u], kf);
             float d0 = 0.f;
@@ -122,7 +134,7 @@ __device__ __forceinline__ void attend_row(uint4 qv, const __half* __restrict__ 
         float mn = m;
 #pragma unroll
         for (int u = 0; u < kAtUnroll; ++u)
-            if (key[u] >= 0) mn = fmaxf(mn, dot[u]);
+            if (key[u] != -1) mn = fmaxf(mn, dot[u]);
         if (mn > -__builtin_huge_valf()) {
             const float corr = __expf(m - mn);
             lsum *= corr;
@@ -130,7 +142,7 @@ __device__ __forceinline__ void attend_row(uint4 qv, const __half* __restrict__ 
             for (int d = 0; d < 8; ++d) acc[d] *= corr;
 #pragma unroll
             for (int u = 0; u < kAtUnroll; ++u) {
-                if (key[u] >= 0) {
+                if (key[u] != -1) {
                     const float p = __expf(dot[u] - mn);
                     float vf[8];
                     unpack8_half(vc[u], vf);

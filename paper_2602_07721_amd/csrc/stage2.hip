@@ -33,7 +33,11 @@
 // at most 64 keys, else by 11/11/10-bit radix passes restricted to it.  A list
 // is one query head's candidates (C <= 32768), or, in two passes, first every
 // 4096-candidate slice of a head and then the concatenated winners of its slices
-// (more than 32768 candidates, or more than 8192 for few heads).
+// (more than 32768 candidates, or more than 8192 for few heads).  With the
+// attention fused (topk_reg_kernel), keys in bins above the boundary bin win
+// whatever the rest of the selection finds, so once that bin is known each wave
+// requests the K/V rows of up to 8 of them; those gathers run while the
+// selection finishes, the rows wait in LDS, and the attention reads them there.
 
 #include "attend_row.hpp"
 #include "internal.hpp"
@@ -541,6 +545,11 @@ __global__ __launch_bounds__(TH) void topk_reg_kernel(RetrieveArgs a) {
     // With kAttend the winners' estimates wait here until the attention is done.
     __shared__ float s_wsc[kAttend ? PARISKV_MAX_TOPK : 1];
     __shared__ int32_t s_dump[kAttend ? TH : 1];  // a word per thread for non-winners' stores
+    // With kAttend: K/V rows of up to kPf sure winners per wave, requested as soon as
+    // the boundary bin is known (see below), and their cache rows.
+    constexpr int kPf = 8;
+    __shared__ uint4 s_prow[kAttend ? kWaves * kPf * 32 : 1];
+    __shared__ __align__(16) int32_t s_pfrow[kAttend ? kWaves : 1][kPf];
 
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     // This block's list: part blk % tk_parts of row blk / tk_parts (see RetrieveArgs).
@@ -630,6 +639,61 @@ __global__ __launch_bounds__(TH) void topk_reg_kernel(RetrieveArgs a) {
     const uint32_t bsel = s_digit;       // bin holding the kk-th largest key
     uint32_t need = s_need;              // its rank (from the top) inside that bin
     const uint32_t in_bin = s_hist[0][bsel];
+    const int32_t retr0 = (int32_t)a.win.retr_begin;  // below kv_capacity <= 2^30 - 1 (host-checked)
+    // KV group of the row: row = seq hq + h with hq = hkv g, so seq hkv + h / g = row / g.
+    const int64_t kvrow0 = kAttend ? (int64_t)((int)row / a.g) * a.kv_capacity : 0;
+
+    // With kAttend: a key in a bin above bsel wins whatever the rest of the selection
+    // finds.  Each lane offers the first such key among its first kPfKeys, and each
+    // wave requests the K/V rows of the first kPf lanes that offer one into registers
+    // now, so that these gathers overlap the rest of the selection (a barrier does not
+    // wait for them); they go to LDS just before the attention, which reads them from
+    // there (listed as -2 - LDS row).  The bin test is the bin's own arithmetic: the
+    // bin is the truncated (f - fmin) inv, so bin > bsel iff that product >= bsel + 1.
+    constexpr int kPfKeys = EPT < 4 ? EPT : 4;
+    static_assert(kPf == 2 || kPf == 4 || kPf == 8, "up to four row loads per lane, in named registers");
+    uint4 pf0 = make_uint4(0, 0, 0, 0), pf1 = pf0, pf2 = pf0, pf3 = pf0;
+    int npf = 0, pf_e = -1, pf_slot = 0;  // this lane's held key (index e, or -1) and its LDS row
+    if (kAttend) {
+        const float edge = (float)(bsel + 1);
+        const uint32_t cap = (uint32_t)a.kv_capacity;
+        int e1 = -1;
+        int32_t r1 = 0;
+#pragma unroll
+        for (int e = kPfKeys - 1; e >= 0; --e) {
+            const int32_t rowi = retr0 + widx[e];
+            const bool sure = key[e] != 0u && (key_float(key[e]) - fmin) * inv >= edge && (uint32_t)rowi < cap;
+            e1 = sure ? e : e1;
+            r1 = sure ? rowi : r1;
+        }
+        const uint64_t m = __ballot(e1 >= 0);
+        const int pos = (int)__builtin_amdgcn_mbcnt_hi((uint32_t)(m >> 32), __builtin_amdgcn_mbcnt_lo((uint32_t)m, 0u));
+        npf = min(kPf, (int)__popcll(m));
+        if (e1 >= 0 && pos < kPf) {
+            s_pfrow[wave][kPf / 2 * (pos & 1) + (pos >> 1)] = r1;
+            pf_e = e1;
+            pf_slot = wave * kPf + pos;
+        }
+        // The wave reads back its own LDS words (in order, no barrier needed).  Load u:
+        // lanes 0-31 take row 2u (K in lanes 0-15, V in 16-31), lanes 32-63 row 2u + 1;
+        // row w sits at word kPf/2 (w % 2) + w / 2, so a lane's ids are one read.  The
+        // loads are unconditional (a missing row reads the group's row 0 and is not
+        // used): branches around them made the compiler wait for their data early.
+        const uint4* kv = reinterpret_cast<const uint4*>(static_cast<const __half*>((lane & 16) ? a.V : a.K) +
+                                                         kvrow0 * kD) + (lane & 15);
+        const int hi = lane >> 5;
+        const int32_t* idp = &s_pfrow[wave][kPf / 2 * hi];
+        int4 ids = make_int4(0, 0, 0, 0);
+        if constexpr (kPf == 8) ids = *reinterpret_cast<const int4*>(idp);
+        if constexpr (kPf == 4) { const int2 t = *reinterpret_cast<const int2*>(idp); ids.x = t.x; ids.y = t.y; }
+        if constexpr (kPf == 2) ids.x = idp[0];
+        pf0 = kv[(int64_t)(hi < npf ? ids.x : 0) * (kD / 8)];
+        if constexpr (kPf >= 4) pf1 = kv[(int64_t)(2 + hi < npf ? ids.y : 0) * (kD / 8)];
+        if constexpr (kPf >= 8) {
+            pf2 = kv[(int64_t)(4 + hi < npf ? ids.z : 0) * (kD / 8)];
+            pf3 = kv[(int64_t)(6 + hi < npf ? ids.w : 0) * (kD / 8)];
+        }
+    }
     uint32_t T, quota;
     if (in_bin <= 64) {
         // Few keys in the bin: gather them, then every wave ranks them by brute force
@@ -707,7 +771,6 @@ __global__ __launch_bounds__(TH) void topk_reg_kernel(RetrieveArgs a) {
         pre[it] += before_groups + earlier;
         before_groups += tot;
     }
-    const int32_t retr0 = (int32_t)a.win.retr_begin;  // below kv_capacity <= 2^30 - 1 (host-checked)
     int32_t* oi = a.tk_out_idx + blk * a.top_k;
     float* os = a.tk_out_score ? a.tk_out_score + blk * a.top_k : nullptr;
     // With kAttend the attention list in region B is Sink rows, then Local +
@@ -732,7 +795,7 @@ __global__ __launch_bounds__(TH) void topk_reg_kernel(RetrieveArgs a) {
                 const bool w = p < (uint32_t)kk;
                 int32_t* dw = w ? &s_win[nd + p] : &s_dump[tid];
                 float* ds = w ? &s_wsc[p] : reinterpret_cast<float*>(&s_dump[tid]);
-                *dw = retr0 + widx[e];
+                *dw = e == pf_e ? -2 - pf_slot : retr0 + widx[e];
                 *ds = key_float(key[e]);
             } else if (p < (uint32_t)kk) {
                 oi[p] = widx[e];
@@ -750,22 +813,37 @@ __global__ __launch_bounds__(TH) void topk_reg_kernel(RetrieveArgs a) {
         // Attention over the dense rows and the kk winners (Eqs. approx_weight,
         // approx_output), from LDS.  Region B is free once the compaction runs.
         for (int r = tid; r < nd; r += TH) s_win[r] = a.win.dense_entry(r);
+        {
+            uint4* dst = s_prow + 32 * (wave * kPf + (lane >> 5)) + (lane & 31);
+            const int hi = lane >> 5;
+            // Unconditional: rows past npf are never listed, and a store on every
+            // path keeps the compiler's view of the loads settled from here on.
+            dst[0] = pf0;
+            if constexpr (kPf >= 4) dst[2 * 32] = pf1;
+            if constexpr (kPf >= 8) {
+                dst[4 * 32] = pf2;
+                dst[6 * 32] = pf3;
+            }
+        }
         __syncthreads();
-        const int seq = (int)(row / a.hq);
-        const int h = (int)(row % a.hq);
-        const int64_t kvrow0 = ((int64_t)seq * a.hkv + h / a.g) * a.kv_capacity;
         const bool wc = a.win.win_capacity > 0;
-        const int64_t wrow0 = wc ? ((int64_t)seq * a.hkv + h / a.g) * a.win.win_capacity : kvrow0;
+        const int64_t wrow0 = wc ? (int64_t)((int)row / a.g) * a.win.win_capacity : kvrow0;
         attend_row(qv, static_cast<const __half*>(a.K) + kvrow0 * kD,
                    static_cast<const __half*>(a.V) + kvrow0 * kD, a.kv_capacity,
                    static_cast<const __half*>(wc ? a.Kw : a.K) + wrow0 * kD,
                    static_cast<const __half*>(wc ? a.Vw : a.V) + wrow0 * kD, a.win.win_capacity,
                    s_win, nd + kk, a.scale,
-                   a.attn_out + row * kD, *reinterpret_cast<AttendScratch*>(s_raw));
-        // The winners in ascending key index, then the padding.
+                   a.attn_out + row * kD, *reinterpret_cast<AttendScratch*>(s_raw), s_prow);
+        // The winners in ascending key index (a held row's from its prefetch record),
+        // then the padding.
         for (int r = tid; r < a.top_k; r += TH) {
             const bool w = r < kk;
-            oi[r] = w ? (int32_t)((int64_t)s_win[nd + r] - a.win.retr_begin) : -1;
+            int32_t v = w ? s_win[nd + r] : 0;
+            if (v <= -2) {
+                const int slot = -2 - v, pos = slot % kPf;
+                v = s_pfrow[slot / kPf][kPf / 2 * (pos & 1) + (pos >> 1)];
+            }
+            oi[r] = w ? (int32_t)((int64_t)v - a.win.retr_begin) : -1;
             if (os) os[r] = w ? s_wsc[r] : -__builtin_huge_valf();
         }
     }

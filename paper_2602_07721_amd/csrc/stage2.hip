@@ -676,23 +676,17 @@ __global__ __launch_bounds__(TH) void topk_reg_kernel(RetrieveArgs a) {
         }
         // The wave reads back its own LDS words (in order, no barrier needed).  Load u:
         // lanes 0-31 take row 2u (K in lanes 0-15, V in 16-31), lanes 32-63 row 2u + 1;
-        // row w sits at word kPf/2 (w % 2) + w / 2, so a lane's ids are one read.  The
-        // loads are unconditional (a missing row reads the group's row 0 and is not
-        // used): branches around them made the compiler wait for their data early.
+        // row w sits at word kPf/2 (w % 2) + w / 2, so a lane's ids are consecutive.
+        // Loads 0 and 1 go out now, 2 and 3 just before the winner list is built
+        // (four at once stalled the waves at issue).  The loads are unconditional (a
+        // missing row reads the group's row 0 and is not used): branches around them
+        // made the compiler wait for their data early.
         const uint4* kv = reinterpret_cast<const uint4*>(static_cast<const __half*>((lane & 16) ? a.V : a.K) +
                                                          kvrow0 * kD) + (lane & 15);
         const int hi = lane >> 5;
         const int32_t* idp = &s_pfrow[wave][kPf / 2 * hi];
-        int4 ids = make_int4(0, 0, 0, 0);
-        if constexpr (kPf == 8) ids = *reinterpret_cast<const int4*>(idp);
-        if constexpr (kPf == 4) { const int2 t = *reinterpret_cast<const int2*>(idp); ids.x = t.x; ids.y = t.y; }
-        if constexpr (kPf == 2) ids.x = idp[0];
-        pf0 = kv[(int64_t)(hi < npf ? ids.x : 0) * (kD / 8)];
-        if constexpr (kPf >= 4) pf1 = kv[(int64_t)(2 + hi < npf ? ids.y : 0) * (kD / 8)];
-        if constexpr (kPf >= 8) {
-            pf2 = kv[(int64_t)(4 + hi < npf ? ids.z : 0) * (kD / 8)];
-            pf3 = kv[(int64_t)(6 + hi < npf ? ids.w : 0) * (kD / 8)];
-        }
+        pf0 = kv[(int64_t)(hi < npf ? idp[0] : 0) * (kD / 8)];
+        if constexpr (kPf >= 4) pf1 = kv[(int64_t)(2 + hi < npf ? idp[1] : 0) * (kD / 8)];
     }
     uint32_t T, quota;
     if (in_bin <= 64) {
@@ -779,6 +773,15 @@ __global__ __launch_bounds__(TH) void topk_reg_kernel(RetrieveArgs a) {
     // outputs are written after the attention, so that its first loads do not
     // wait behind these stores.
     const int nd = kAttend ? (int)a.win.dense_rows() : 0;
+    if constexpr (kAttend && kPf >= 8) {
+        // Prefetch loads 2 and 3 (see above).
+        const uint4* kv = reinterpret_cast<const uint4*>(static_cast<const __half*>((lane & 16) ? a.V : a.K) +
+                                                         kvrow0 * kD) + (lane & 15);
+        const int hi = lane >> 5;
+        const int2 t = *reinterpret_cast<const int2*>(&s_pfrow[wave][kPf / 2 * hi + 2]);
+        pf2 = kv[(int64_t)(4 + hi < npf ? t.x : 0) * (kD / 8)];
+        pf3 = kv[(int64_t)(6 + hi < npf ? t.y : 0) * (kD / 8)];
+    }
 #pragma unroll
     for (int it = 0; it < kIt; ++it) {
         uint32_t gb = pre[it] & 0xffffu, eb = pre[it] >> 16;

@@ -36,7 +36,7 @@
 // (more than 32768 candidates, or more than 8192 for few heads).  With the
 // attention fused (topk_reg_kernel), keys in bins above the boundary bin win
 // whatever the rest of the selection finds, so once that bin is known each wave
-// requests the K/V rows of up to 8 of them; those gathers run while the
+// requests the K/V rows of up to 12 of them; those gathers run while the
 // selection finishes, the rows wait in LDS, and the attention reads them there.
 
 #include "attend_row.hpp"
@@ -547,7 +547,7 @@ __global__ __launch_bounds__(TH) void topk_reg_kernel(RetrieveArgs a) {
     __shared__ int32_t s_dump[kAttend ? TH : 1];  // a word per thread for non-winners' stores
     // With kAttend: K/V rows of up to kPf sure winners per wave, requested as soon as
     // the boundary bin is known (see below), and their cache rows.
-    constexpr int kPf = 8;
+    constexpr int kPf = 12;
     __shared__ uint4 s_prow[kAttend ? kWaves * kPf * 32 : 1];
     __shared__ __align__(16) int32_t s_pfrow[kAttend ? kWaves : 1][kPf];
 
@@ -651,8 +651,8 @@ __global__ __launch_bounds__(TH) void topk_reg_kernel(RetrieveArgs a) {
     // there (listed as -2 - LDS row).  The bin test is the bin's own arithmetic: the
     // bin is the truncated (f - fmin) inv, so bin > bsel iff that product >= bsel + 1.
     constexpr int kPfKeys = EPT < 4 ? EPT : 4;
-    static_assert(kPf == 2 || kPf == 4 || kPf == 8, "up to four row loads per lane, in named registers");
-    uint4 pf0 = make_uint4(0, 0, 0, 0), pf1 = pf0, pf2 = pf0, pf3 = pf0;
+    static_assert(kPf == 12, "six row loads per lane, in named registers");
+    uint4 pf0 = make_uint4(0, 0, 0, 0), pf1 = pf0, pf2 = pf0, pf3 = pf0, pf4 = pf0, pf5 = pf0;
     int npf = 0, pf_e = -1, pf_slot = 0;  // this lane's held key (index e, or -1) and its LDS row
     if (kAttend) {
         const float edge = (float)(bsel + 1);
@@ -677,8 +677,8 @@ __global__ __launch_bounds__(TH) void topk_reg_kernel(RetrieveArgs a) {
         // The wave reads back its own LDS words (in order, no barrier needed).  Load u:
         // lanes 0-31 take row 2u (K in lanes 0-15, V in 16-31), lanes 32-63 row 2u + 1;
         // row w sits at word kPf/2 (w % 2) + w / 2, so a lane's ids are consecutive.
-        // Loads 0 and 1 go out now, 2 and 3 just before the winner list is built
-        // (four at once stalled the waves at issue).  The loads are unconditional (a
+        // Loads 0 and 1 go out now, 2 and 3 before the compaction scan, 4 and 5 before
+        // the winner list is built (more at once stalled the waves at issue).  The loads are unconditional (a
         // missing row reads the group's row 0 and is not used): branches around them
         // made the compiler wait for their data early.
         const uint4* kv = reinterpret_cast<const uint4*>(static_cast<const __half*>((lane & 16) ? a.V : a.K) +
@@ -686,7 +686,7 @@ __global__ __launch_bounds__(TH) void topk_reg_kernel(RetrieveArgs a) {
         const int hi = lane >> 5;
         const int32_t* idp = &s_pfrow[wave][kPf / 2 * hi];
         pf0 = kv[(int64_t)(hi < npf ? idp[0] : 0) * (kD / 8)];
-        if constexpr (kPf >= 4) pf1 = kv[(int64_t)(2 + hi < npf ? idp[1] : 0) * (kD / 8)];
+        pf1 = kv[(int64_t)(2 + hi < npf ? idp[1] : 0) * (kD / 8)];
     }
     uint32_t T, quota;
     if (in_bin <= 64) {
@@ -732,6 +732,15 @@ __global__ __launch_bounds__(TH) void topk_reg_kernel(RetrieveArgs a) {
         quota = need;   // how many keys equal to T are taken (lowest indices)
     }
 
+    if constexpr (kAttend) {
+        // Prefetch loads 2 and 3 (see above).
+        const uint4* kv = reinterpret_cast<const uint4*>(static_cast<const __half*>((lane & 16) ? a.V : a.K) +
+                                                         kvrow0 * kD) + (lane & 15);
+        const int hi = lane >> 5;
+        const int2 t = *reinterpret_cast<const int2*>(&s_pfrow[wave][kPf / 2 * hi + 2]);
+        pf2 = kv[(int64_t)(4 + hi < npf ? t.x : 0) * (kD / 8)];
+        pf3 = kv[(int64_t)(6 + hi < npf ? t.y : 0) * (kD / 8)];
+    }
     // Ordered compaction: an element's output slot is (#keys > T before it) +
     // min(#keys == T before it, quota), which lists the winners by ascending index.
     // Positions run group by group (j), thread by thread inside a group, so the
@@ -773,14 +782,14 @@ __global__ __launch_bounds__(TH) void topk_reg_kernel(RetrieveArgs a) {
     // outputs are written after the attention, so that its first loads do not
     // wait behind these stores.
     const int nd = kAttend ? (int)a.win.dense_rows() : 0;
-    if constexpr (kAttend && kPf >= 8) {
-        // Prefetch loads 2 and 3 (see above).
+    if constexpr (kAttend) {
+        // Prefetch loads 4 and 5 (see above).
         const uint4* kv = reinterpret_cast<const uint4*>(static_cast<const __half*>((lane & 16) ? a.V : a.K) +
                                                          kvrow0 * kD) + (lane & 15);
         const int hi = lane >> 5;
-        const int2 t = *reinterpret_cast<const int2*>(&s_pfrow[wave][kPf / 2 * hi + 2]);
-        pf2 = kv[(int64_t)(4 + hi < npf ? t.x : 0) * (kD / 8)];
-        pf3 = kv[(int64_t)(6 + hi < npf ? t.y : 0) * (kD / 8)];
+        const int2 t = *reinterpret_cast<const int2*>(&s_pfrow[wave][kPf / 2 * hi + 4]);
+        pf4 = kv[(int64_t)(8 + hi < npf ? t.x : 0) * (kD / 8)];
+        pf5 = kv[(int64_t)(10 + hi < npf ? t.y : 0) * (kD / 8)];
     }
 #pragma unroll
     for (int it = 0; it < kIt; ++it) {
@@ -822,11 +831,11 @@ __global__ __launch_bounds__(TH) void topk_reg_kernel(RetrieveArgs a) {
             // Unconditional: rows past npf are never listed, and a store on every
             // path keeps the compiler's view of the loads settled from here on.
             dst[0] = pf0;
-            if constexpr (kPf >= 4) dst[2 * 32] = pf1;
-            if constexpr (kPf >= 8) {
-                dst[4 * 32] = pf2;
-                dst[6 * 32] = pf3;
-            }
+            dst[2 * 32] = pf1;
+            dst[4 * 32] = pf2;
+            dst[6 * 32] = pf3;
+            dst[8 * 32] = pf4;
+            dst[10 * 32] = pf5;
         }
         __syncthreads();
         const bool wc = a.win.win_capacity > 0;

@@ -562,9 +562,6 @@ __global__ __launch_bounds__(TH) void topk_reg_kernel(RetrieveArgs a) {
     const int32_t* cand = a.tk_idx + row * a.tk_stride + off;
     if (tid == 0) s_nsmall = 0;
 
-    // With kAttend, this thread's part of the query, requested first.
-    const uint4 qv = kAttend ? attend_query_part(static_cast<const __half*>(a.q) + row * kD)
-                             : make_uint4(0, 0, 0, 0);
     uint32_t kmin = 0xffffffffu, kmax = 0u;
 
     // The estimates as keys (0 past the list; valid keys are all > 0) and the
@@ -579,11 +576,16 @@ __global__ __launch_bounds__(TH) void topk_reg_kernel(RetrieveArgs a) {
         float4 f[kIt];
         int4 ix[kIt];
 #pragma unroll
-        for (int it = 0; it < kIt; ++it) {
-            const int p4 = min(tid + it * TH, nq - 1);
-            f[it] = reinterpret_cast<const float4*>(sc)[p4];
-            ix[it] = reinterpret_cast<const int4*>(cand)[p4];
-        }
+        for (int it = 0; it < kIt; ++it)
+            f[it] = reinterpret_cast<const float4*>(sc)[min(tid + it * TH, nq - 1)];
+#pragma unroll
+        for (int it = 0; it < kIt; ++it)
+            ix[it] = reinterpret_cast<const int4*>(cand)[min(tid + it * TH, nq - 1)];
+        // The estimates are needed first (the indices only after the digit search):
+        // an empty asm that reads them keeps each 16-byte load whole and makes the
+        // one wait here cover just them.
+#pragma unroll
+        for (int it = 0; it < kIt; ++it) asm volatile("" ::"v"(f[it].x), "v"(f[it].y), "v"(f[it].z), "v"(f[it].w));
 #pragma unroll
         for (int it = 0; it < kIt; ++it) {
             const int p = 4 * (tid + it * TH);
@@ -604,6 +606,9 @@ __global__ __launch_bounds__(TH) void topk_reg_kernel(RetrieveArgs a) {
             widx[e] = p < C ? cand[p] : -1;
         }
     }
+    // With kAttend, this thread's part of the query (needed only by the attention).
+    const uint4 qv = kAttend ? attend_query_part(static_cast<const __half*>(a.q) + row * kD)
+                             : make_uint4(0, 0, 0, 0);
     for (int i = tid; i < 2 * kNB; i += TH) (&s_hist[0][0])[i] = 0;
 #pragma unroll
     for (int e = 0; e < EPT; ++e)

@@ -683,9 +683,10 @@ __global__ __launch_bounds__(TH) void topk_reg_kernel(RetrieveArgs a) {
         // lanes 0-31 take row 2u (K in lanes 0-15, V in 16-31), lanes 32-63 row 2u + 1;
         // row w sits at word kPf/2 (w % 2) + w / 2, so a lane's ids are consecutive.
         // Loads 0 and 1 go out now, 2 and 3 before the compaction scan, 4 and 5 before
-        // the winner list is built (more at once stalled the waves at issue).  The loads are unconditional (a
-        // missing row reads the group's row 0 and is not used): branches around them
-        // made the compiler wait for their data early.
+        // the winner list is built (more at once stalled the waves at issue).  The
+        // loads are unconditional: a missing row reads the group's row 0 (there is
+        // one, kv_capacity >= 1 is checked on the host) and is not used; branches
+        // around them made the compiler wait for their data early.
         const uint4* kv = reinterpret_cast<const uint4*>(static_cast<const __half*>((lane & 16) ? a.V : a.K) +
                                                          kvrow0 * kD) + (lane & 15);
         const int hi = lane >> 5;
